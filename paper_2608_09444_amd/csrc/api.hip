@@ -1,0 +1,365 @@
+// libcdb C ABI: argument validation, packed-weight and workspace layouts, and
+// the launch sequences of the three stage calls.
+#include <string.h>
+
+#include "cdb_internal.h"
+
+namespace cdb {
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+bool desc_supported(const cdb_model_desc& d) {
+    if (d.d <= 0 || d.n_heads <= 0 || d.head_dim <= 0 || d.d_ff <= 0 || d.vocab <= 0) return false;
+    if (d.n_prelude < 0 || d.n_core < 1 || d.n_coda < 0 || d.r_max < 1 || d.r_max > 64) return false;
+    if (d.d % 32 || d.d_ff % 32 || d.vocab % 16 || d.n_heads * d.head_dim != d.d) return false;
+    if (d.head_dim != 64 && d.head_dim != 96 && d.head_dim != 128) return false;
+    if (d.page_tokens != kPage) return false;
+    if (d.injection != 0 && d.injection != 1) return false;
+    if (d.exit_kind != 0 && d.exit_kind != 1) return false;
+    return true;
+}
+
+bool weight_layout(const cdb_model_desc& d, WeightLayout* w) {
+    if (!desc_supported(d)) return false;
+    const size_t D = d.d, F = d.d_ff, V = d.vocab;
+    size_t off = 0;
+    w->qkv = off;
+    off = align256(off + 3 * D * D * 2);
+    w->o = off;
+    off = align256(off + D * D * 2);
+    w->gu = off;
+    off = align256(off + 2 * F * D * 2);
+    w->down = off;
+    off = align256(off + D * F * 2);
+    w->layer_stride = off;
+    off = w->layer_stride * (size_t)(d.n_prelude + d.n_core + d.n_coda);
+    w->adapter = off;
+    if (d.injection) off = align256(off + D * 2 * D * 2);
+    w->lm_head = off;
+    off = align256(off + V * D * 2);
+    w->embed = off;
+    off = align256(off + V * D * 2);
+    w->w_exit = off;
+    off = align256(off + D * 2);
+    w->total = off;
+    return true;
+}
+
+// The four per-layer GEMMs and the adapter / LM head, with their split counts.
+struct ModelGemms {
+    GemmShape qkv, o, gu, down, adapter, lm;
+};
+static ModelGemms model_gemms(const cdb_model_desc& d) {
+    ModelGemms g;
+    g.qkv = gemm_shape(3 * d.d, d.d);
+    g.o = gemm_shape(d.d, d.d);
+    g.gu = gemm_shape(2 * d.d_ff, d.d);
+    g.down = gemm_shape(d.d, d.d_ff);
+    g.adapter = gemm_shape(d.d, 2 * d.d);
+    g.lm = gemm_shape(d.vocab, d.d);
+    return g;
+}
+
+WsLayout ws_layout(const cdb_model_desc& d, int rows) {
+    WsLayout L;
+    const size_t D = d.d, F = d.d_ff, M = rows;
+    const ModelGemms g = model_gemms(d);
+    size_t part = 0;
+    const GemmShape all[6] = {g.qkv, g.o, g.gu, g.down, g.adapter, g.lm};
+    for (const GemmShape& s : all)
+        if (s.S > 1 && (size_t)s.S * s.N > part) part = (size_t)s.S * s.N;
+    size_t off = 0;
+    L.err = off;
+    off = 256;
+    L.counters = off;
+    off = align256(off + (size_t)kCounters * 4);
+    L.h = off;
+    off = align256(off + M * D * 4);
+    L.h_in = off;
+    off = align256(off + M * D * 4);
+    L.q = off;
+    off = align256(off + M * D * 4);
+    L.x = off;
+    off = align256(off + M * 2 * D * 2);
+    L.act = off;
+    off = align256(off + M * F * 2);
+    L.part = off;
+    off = align256(off + part * M * 4);
+    L.total = off;
+    return L;
+}
+
+// Everything a stage call needs, resolved once per call.
+struct Ctx {
+    const cdb_model_desc* md;
+    const unsigned char* wb;
+    WeightLayout wl;
+    ModelGemms gm;
+    unsigned char* ws;
+    WsLayout L;
+    int* err;
+    int* counters;
+    float* h;
+    float* h_in;
+    float* q;
+    uint16_t* x;
+    uint16_t* act;
+    float* part;
+};
+
+static Ctx make_ctx(const cdb_model* model, void* ws, int rows) {
+    Ctx c;
+    c.md = &model->desc;
+    c.wb = static_cast<const unsigned char*>(model->packed);
+    weight_layout(model->desc, &c.wl);
+    c.gm = model_gemms(model->desc);
+    c.ws = static_cast<unsigned char*>(ws);
+    c.L = ws_layout(model->desc, rows);
+    c.err = reinterpret_cast<int*>(c.ws + c.L.err);
+    c.counters = reinterpret_cast<int*>(c.ws + c.L.counters);
+    c.h = reinterpret_cast<float*>(c.ws + c.L.h);
+    c.h_in = reinterpret_cast<float*>(c.ws + c.L.h_in);
+    c.q = reinterpret_cast<float*>(c.ws + c.L.q);
+    c.x = reinterpret_cast<uint16_t*>(c.ws + c.L.x);
+    c.act = reinterpret_cast<uint16_t*>(c.ws + c.L.act);
+    c.part = reinterpret_cast<float*>(c.ws + c.L.part);
+    return c;
+}
+
+static const uint16_t* wptr(const Ctx& c, size_t off) { return reinterpret_cast<const uint16_t*>(c.wb + off); }
+
+#define HIPCHK(x)                                  \
+    do {                                           \
+        if ((x) != hipSuccess) return CDB_ERR_HIP; \
+    } while (0)
+
+// Run `count` transformer layers (global index first..) of one stage over the
+// rows in ctx.h, with K/V in `kv`.
+static cdb_status run_layers(const Ctx& c, int first, int count, KvTarget kv, const cdb_rows& r, hipStream_t st) {
+    const cdb_model_desc& d = *c.md;
+    const int M = r.n_rows;
+    for (int l = 0; l < count; ++l) {
+        const size_t lb = (size_t)(first + l) * c.wl.layer_stride;
+        kv.layer = l;
+        EpiArgs ea{};
+        ea.seq = r.seq;
+        ea.pos = r.pos;
+        ea.H = d.n_heads;
+        ea.hd = d.head_dim;
+        ea.rope_base = d.rope_base;
+        ea.err = c.err;
+        ea.kv = kv;
+        ea.q = c.q;
+        // attention half
+        HIPCHK(launch_rmsnorm(c.h, M, d.d, d.rms_eps, c.x, d.d, st));
+        HIPCHK(launch_gemm(EPI_QKV, c.x, d.d, wptr(c, lb + c.wl.qkv), M, c.gm.qkv, c.part, c.counters, ea, st));
+        HIPCHK(launch_attention(c.q, kv, r.seq, r.pos, M, d.n_heads, d.head_dim, c.x, c.err, st));
+        ea.out = c.h;
+        ea.ld_out = d.d;
+        HIPCHK(launch_gemm(EPI_RESID, c.x, d.d, wptr(c, lb + c.wl.o), M, c.gm.o, c.part, c.counters, ea, st));
+        // MLP half
+        HIPCHK(launch_rmsnorm(c.h, M, d.d, d.rms_eps, c.x, d.d, st));
+        ea.act = c.act;
+        ea.ld_act = d.d_ff;
+        HIPCHK(launch_gemm(EPI_SWIGLU, c.x, d.d, wptr(c, lb + c.wl.gu), M, c.gm.gu, c.part, c.counters, ea, st));
+        HIPCHK(launch_gemm(EPI_RESID, c.act, d.d_ff, wptr(c, lb + c.wl.down), M, c.gm.down, c.part, c.counters, ea,
+                           st));
+    }
+    return CDB_OK;
+}
+
+static KvTarget stage_target(const cdb_model_desc& d, const cdb_kv& kv, int stage) {
+    KvTarget t{};
+    t.page_table = kv.page_table;
+    t.max_seqs = kv.max_seqs;
+    t.max_pages = kv.max_pages;
+    t.n_planes = d.r_max + 2;
+    if (stage == 0) {
+        t.pool = static_cast<uint16_t*>(kv.pre_pool);
+        t.n_pages = kv.pre_pages;
+        t.n_layers = d.n_prelude;
+        t.plane_fixed = 0;
+    } else if (stage == 1) {
+        t.pool = static_cast<uint16_t*>(kv.core_pool);
+        t.n_pages = kv.core_pages;
+        t.n_layers = d.n_core;
+        t.plane_fixed = -1;
+    } else {
+        t.pool = static_cast<uint16_t*>(kv.coda_pool);
+        t.n_pages = kv.coda_pages;
+        t.n_layers = d.n_coda;
+        t.plane_fixed = d.r_max + 1;
+    }
+    return t;
+}
+
+static cdb_status check_common(const cdb_model* model, const cdb_kv* kv, const cdb_state* state, const cdb_rows* rows,
+                               void* ws, size_t ws_bytes, int stage) {
+    if (!model || !kv || !state || !rows || !ws || !model->packed || !state->h) return CDB_ERR_INVALID_ARG;
+    const cdb_model_desc& d = model->desc;
+    if (!desc_supported(d)) return CDB_ERR_UNSUPPORTED;
+    if (rows->n_rows < 0 || state->n_slots < 0 || kv->max_seqs < 0 || kv->max_pages < 0) return CDB_ERR_INVALID_ARG;
+    if (rows->n_rows > kMaxRows) return CDB_ERR_CAPACITY;
+    if (rows->n_rows > 0 && (!rows->slot || !rows->seq || !rows->pos)) return CDB_ERR_INVALID_ARG;
+    if (ws_bytes < ws_layout(d, rows->n_rows).total) return CDB_ERR_CAPACITY;
+    const int layers = stage == 0 ? d.n_prelude : (stage == 1 ? d.n_core : d.n_coda);
+    if (layers > 0) {
+        void* pool = stage == 0 ? kv->pre_pool : (stage == 1 ? kv->core_pool : kv->coda_pool);
+        const int np = stage == 0 ? kv->pre_pages : (stage == 1 ? kv->core_pages : kv->coda_pages);
+        if (!pool || np < 0 || !kv->page_table) return CDB_ERR_INVALID_ARG;
+    }
+    return CDB_OK;
+}
+
+}  // namespace cdb
+
+using namespace cdb;
+
+extern "C" {
+
+size_t cdb_packed_weight_bytes(const cdb_model_desc* desc) {
+    WeightLayout w;
+    if (!desc || !weight_layout(*desc, &w)) return 0;
+    return w.total;
+}
+
+cdb_status cdb_pack_weights(const cdb_model_desc* desc, const cdb_plain_weights* w, void* packed, size_t bytes,
+                            hipStream_t st) {
+    if (!desc || !w || !packed) return CDB_ERR_INVALID_ARG;
+    WeightLayout L;
+    if (!weight_layout(*desc, &L)) return CDB_ERR_UNSUPPORTED;
+    if (bytes < L.total) return CDB_ERR_CAPACITY;
+    const cdb_model_desc& d = *desc;
+    const int nl = d.n_prelude + d.n_core + d.n_coda;
+    if (!w->embed || !w->lm_head || !w->w_exit || (nl > 0 && !w->layer) || (d.injection && !w->adapter))
+        return CDB_ERR_INVALID_ARG;
+    for (int i = 0; i < 7 * nl; ++i)
+        if (!w->layer[i]) return CDB_ERR_INVALID_ARG;
+    unsigned char* b = static_cast<unsigned char*>(packed);
+    auto P = [&](size_t off) { return reinterpret_cast<uint16_t*>(b + off); };
+    auto S = [&](const void* p) { return static_cast<const uint16_t*>(p); };
+    for (int l = 0; l < nl; ++l) {
+        const void* const* t = w->layer + 7 * l;
+        const size_t lb = (size_t)l * L.layer_stride;
+        HIPCHK(launch_pack(PACK_QKV, S(t[0]), S(t[1]), S(t[2]), 3 * d.d, d.d, d.head_dim, P(lb + L.qkv), st));
+        HIPCHK(launch_pack(PACK_PLAIN, S(t[3]), nullptr, nullptr, d.d, d.d, 0, P(lb + L.o), st));
+        HIPCHK(launch_pack(PACK_GU, S(t[4]), S(t[5]), nullptr, 2 * d.d_ff, d.d, 0, P(lb + L.gu), st));
+        HIPCHK(launch_pack(PACK_PLAIN, S(t[6]), nullptr, nullptr, d.d, d.d_ff, 0, P(lb + L.down), st));
+    }
+    if (d.injection) HIPCHK(launch_pack(PACK_PLAIN, S(w->adapter), nullptr, nullptr, d.d, 2 * d.d, 0, P(L.adapter), st));
+    HIPCHK(launch_pack(PACK_PLAIN, S(w->lm_head), nullptr, nullptr, d.vocab, d.d, 0, P(L.lm_head), st));
+    HIPCHK(launch_copy_bf16(S(w->embed), (size_t)d.vocab * d.d, P(L.embed), st));
+    HIPCHK(launch_copy_bf16(S(w->w_exit), (size_t)d.d, P(L.w_exit), st));
+    return CDB_OK;
+}
+
+size_t cdb_workspace_bytes(const cdb_model_desc* desc, int32_t max_rows) {
+    if (!desc || !desc_supported(*desc) || max_rows < 0 || max_rows > kMaxRows) return 0;
+    return ws_layout(*desc, max_rows).total;
+}
+
+cdb_status cdb_workspace_init(void* ws, size_t ws_bytes, hipStream_t st) {
+    if (!ws) return CDB_ERR_INVALID_ARG;
+    if (ws_bytes < 256 + (size_t)kCounters * 4) return CDB_ERR_CAPACITY;
+    unsigned char* b = static_cast<unsigned char*>(ws);
+    HIPCHK(launch_ws_init(reinterpret_cast<int*>(b), reinterpret_cast<int*>(b + 256), kCounters, st));
+    return CDB_OK;
+}
+
+cdb_status cdb_boundary_prelude(const cdb_model* model, const cdb_kv* kv, const cdb_state* state, const cdb_rows* rows,
+                                const int32_t* tokens, void* ws, size_t ws_bytes, hipStream_t st) {
+    cdb_status s = check_common(model, kv, state, rows, ws, ws_bytes, 0);
+    if (s != CDB_OK) return s;
+    const cdb_model_desc& d = model->desc;
+    if (rows->n_rows > 0 && !tokens) return CDB_ERR_INVALID_ARG;
+    if (d.injection && !state->e) return CDB_ERR_INVALID_ARG;
+    if (rows->n_rows == 0) return CDB_OK;
+    Ctx c = make_ctx(model, ws, rows->n_rows);
+    HIPCHK(launch_embed(d, wptr(c, c.wl.embed), tokens, *rows, *kv, state->n_slots, c.h, c.err, st));
+    s = run_layers(c, 0, d.n_prelude, stage_target(d, *kv, 0), *rows, st);
+    if (s != CDB_OK) return s;
+    HIPCHK(launch_store_state(rows->n_rows, d.d, state->n_slots, rows->slot, c.h, state->h,
+                              d.injection ? state->e : nullptr, st));
+    return CDB_OK;
+}
+
+cdb_status cdb_loop_step(const cdb_model* model, const cdb_kv* kv, const cdb_state* state, const cdb_rows* rows,
+                         const cdb_step_out* out, void* ws, size_t ws_bytes, hipStream_t st) {
+    cdb_status s = check_common(model, kv, state, rows, ws, ws_bytes, 1);
+    if (s != CDB_OK) return s;
+    const cdb_model_desc& d = model->desc;
+    if (!out || !out->exit_score || !out->exit_mask || !out->cont || !out->exited || !out->counts)
+        return CDB_ERR_INVALID_ARG;
+    if (rows->n_rows > 0 && (!rows->c || !rows->depth)) return CDB_ERR_INVALID_ARG;
+    if (d.injection && !state->e) return CDB_ERR_INVALID_ARG;
+    const int M = rows->n_rows;
+    Ctx c = make_ctx(model, ws, M);
+    if (M > 0) {
+        HIPCHK(launch_gather(d, *state, *rows, *kv, c.h, c.h_in, d.injection ? c.x : nullptr, c.err, st));
+        if (d.injection) {
+            EpiArgs ea{};
+            ea.out = c.h;
+            ea.ld_out = d.d;
+            ea.err = c.err;
+            HIPCHK(launch_gemm(EPI_STORE, c.x, 2 * d.d, wptr(c, c.wl.adapter), M, c.gm.adapter, c.part, c.counters, ea,
+                               st));
+        }
+        KvTarget t = stage_target(d, *kv, 1);
+        t.c_row = rows->c;
+        s = run_layers(c, d.n_prelude, d.n_core, t, *rows, st);
+        if (s != CDB_OK) return s;
+        HIPCHK(launch_exit(d, *rows, c.h, c.h_in, wptr(c, c.wl.w_exit), state->h, state->n_slots, *out, st));
+    }
+    HIPCHK(launch_compact(M, out->exit_mask, out->cont, out->exited, out->counts, st));
+    if (M > 0) HIPCHK(launch_copy_on_exit(d, *kv, *rows, out->exited, out->counts, c.err, st));
+    return CDB_OK;
+}
+
+cdb_status cdb_boundary_coda(const cdb_model* model, const cdb_kv* kv, const cdb_state* state, const cdb_rows* rows,
+                             float* logits, int32_t* next_ids, void* ws, size_t ws_bytes, hipStream_t st) {
+    cdb_status s = check_common(model, kv, state, rows, ws, ws_bytes, 2);
+    if (s != CDB_OK) return s;
+    const cdb_model_desc& d = model->desc;
+    if (!logits || !next_ids) return CDB_ERR_INVALID_ARG;
+    const int M = rows->n_rows;
+    if (M == 0) return CDB_OK;
+    Ctx c = make_ctx(model, ws, M);
+    HIPCHK(launch_load_state(M, d.d, rows->slot, state->h, state->n_slots, c.h, c.err, st));
+    s = run_layers(c, d.n_prelude + d.n_core, d.n_coda, stage_target(d, *kv, 2), *rows, st);
+    if (s != CDB_OK) return s;
+    HIPCHK(launch_rmsnorm(c.h, M, d.d, d.rms_eps, c.x, d.d, st));
+    EpiArgs ea{};
+    ea.out = logits;
+    ea.ld_out = d.vocab;
+    ea.err = c.err;
+    HIPCHK(launch_gemm(EPI_STORE, c.x, d.d, wptr(c, c.wl.lm_head), M, c.gm.lm, c.part, c.counters, ea, st));
+    HIPCHK(launch_argmax(M, d.vocab, logits, next_ids, st));
+    return CDB_OK;
+}
+
+cdb_status cdb_read_device_error(void* ws, hipStream_t st, int32_t* code) {
+    if (!ws || !code) return CDB_ERR_INVALID_ARG;
+    int32_t v = 0;
+    if (hipMemcpyAsync(&v, ws, 4, hipMemcpyDeviceToHost, st) != hipSuccess) return CDB_ERR_HIP;
+    if (hipStreamSynchronize(st) != hipSuccess) return CDB_ERR_HIP;
+    *code = v;
+    if (v != 0) {
+        int* err = static_cast<int*>(ws);
+        if (launch_ws_init(err, err + 64, 0, st) != hipSuccess) return CDB_ERR_HIP;
+        if (hipStreamSynchronize(st) != hipSuccess) return CDB_ERR_HIP;
+    }
+    return CDB_OK;
+}
+
+const char* cdb_status_str(cdb_status s) {
+    switch (s) {
+        case CDB_OK: return "ok";
+        case CDB_ERR_INVALID_ARG: return "invalid argument";
+        case CDB_ERR_CAPACITY: return "capacity exceeded";
+        case CDB_ERR_HIP: return "HIP error";
+        case CDB_ERR_UNSUPPORTED: return "unsupported shape";
+    }
+    return "unknown status";
+}
+
+}  // extern "C"

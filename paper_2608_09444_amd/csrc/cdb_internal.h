@@ -1,0 +1,113 @@
+// Internal declarations shared by the libcdb translation units (device helpers,
+// packed-weight layout, workspace layout, kernel launchers).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/libcdb.h"
+
+namespace cdb {
+
+constexpr int kPage = 16;       // tokens per KV page
+constexpr int kMaxRows = 256;   // rows per stage call (workspace and GEMM limit)
+constexpr int kCounters = 16384;
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------- bf16 helpers
+__device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
+__device__ __forceinline__ float bflo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bfhi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+// fp32 -> bf16, round to nearest even (finite inputs; NaN stays NaN)
+__device__ __forceinline__ uint16_t f2bf(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7f800000u) == 0x7f800000u) return (uint16_t)((u >> 16) | ((u & 0xffffu) ? 0x40u : 0u));
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+// First sticky error wins.
+__device__ __forceinline__ void set_err(int* err, int code) { atomicCAS(err, 0, code); }
+
+// ---------------------------------------------------------------- GEMM epilogues
+enum Epi : int { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_STORE = 3 };
+
+// Where a stage's K/V lives and which rows write it.
+struct KvTarget {
+    uint16_t* pool;  // stage pool
+    int n_pages;     // pages in that pool
+    int layer;       // layer index inside the stage
+    int n_layers;    // layers per page of that stage
+    const int32_t* page_table;
+    int max_seqs, max_pages, n_planes;  // n_planes = r_max + 2
+    const int32_t* c_row;               // plane = c_row[m] + 1 when non-null
+    int plane_fixed;                    // otherwise this plane
+};
+
+struct EpiArgs {
+    float* out;     // RESID: h (read-modify-write); STORE: destination
+    int ld_out;
+    uint16_t* act;  // SWIGLU output [M][F]
+    int ld_act;
+    float* q;       // QKV: q after RoPE [M][d]
+    KvTarget kv;
+    const int32_t* seq;
+    const int32_t* pos;
+    int H, hd;
+    float rope_base;
+    int* err;
+};
+
+struct GemmShape {
+    int N, K, S;  // packed output columns, reduction length, K splits
+};
+
+// ---------------------------------------------------------------- layouts
+struct WeightLayout {
+    size_t qkv, o, gu, down;  // byte offsets of layer 0's tensors
+    size_t layer_stride;      // bytes per layer
+    size_t adapter, lm_head, embed, w_exit, total;
+};
+bool weight_layout(const cdb_model_desc& d, WeightLayout* out);
+
+struct WsLayout {
+    size_t err, counters, h, h_in, q, x, act, part, total;
+};
+WsLayout ws_layout(const cdb_model_desc& d, int rows);
+
+GemmShape gemm_shape(int N, int K);
+bool desc_supported(const cdb_model_desc& d);
+
+// ---------------------------------------------------------------- launchers
+hipError_t launch_gemm(int epi, const uint16_t* X, int ldx, const uint16_t* Wp, int M, GemmShape g, float* part,
+                       int* counters, const EpiArgs& ea, hipStream_t st);
+hipError_t launch_attention(const float* q, const KvTarget& kv, const int32_t* seq, const int32_t* pos, int M,
+                            int H, int hd, uint16_t* out, int* err, hipStream_t st);
+hipError_t launch_rmsnorm(const float* h, int M, int d, float eps, uint16_t* out, int ldo, hipStream_t st);
+hipError_t launch_gather(const cdb_model_desc& md, const cdb_state& s, const cdb_rows& r, const cdb_kv& kv,
+                         float* h, float* h_in, uint16_t* xcat, int* err, hipStream_t st);
+hipError_t launch_embed(const cdb_model_desc& md, const uint16_t* embed, const int32_t* tokens, const cdb_rows& r,
+                        const cdb_kv& kv, int n_slots, float* h, int* err, hipStream_t st);
+hipError_t launch_store_state(int M, int d, int n_slots, const int32_t* slot, const float* h, float* state_h,
+                              float* state_e, hipStream_t st);
+hipError_t launch_load_state(int M, int d, const int32_t* slot, const float* state_h, int n_slots, float* h,
+                             int* err, hipStream_t st);
+hipError_t launch_exit(const cdb_model_desc& md, const cdb_rows& r, const float* h, const float* h_in,
+                       const uint16_t* w_exit, float* state_h, int n_slots, const cdb_step_out& o, hipStream_t st);
+hipError_t launch_compact(int M, const uint8_t* mask, int32_t* cont, int32_t* exited, int32_t* counts,
+                          hipStream_t st);
+hipError_t launch_copy_on_exit(const cdb_model_desc& md, const cdb_kv& kv, const cdb_rows& r,
+                               const int32_t* exited, const int32_t* counts, int* err, hipStream_t st);
+hipError_t launch_argmax(int M, int V, const float* logits, int32_t* ids, hipStream_t st);
+hipError_t launch_pack(int kind, const uint16_t* a, const uint16_t* b, const uint16_t* c, int N, int K, int hd,
+                       uint16_t* dst, hipStream_t st);
+hipError_t launch_copy_bf16(const uint16_t* src, size_t n, uint16_t* dst, hipStream_t st);
+hipError_t launch_ws_init(int* err, int* counters, int n, hipStream_t st);
+
+enum PackKind : int { PACK_PLAIN = 0, PACK_QKV = 1, PACK_GU = 2 };
+
+}  // namespace cdb

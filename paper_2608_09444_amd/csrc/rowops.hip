@@ -1,0 +1,415 @@
+// Row-wise kernels of the stage calls: gather and validation, RMSNorm, embedding,
+// state write-back, exit score and decision, stable compaction, copy-on-exit,
+// argmax, weight packing and workspace initialisation.  All are bandwidth- or
+// latency-bound; accesses are 16-byte coalesced where the data allows.
+#include "cdb_internal.h"
+
+namespace cdb {
+
+// Block-wide fp32 sum for 256 threads (4 waves); result broadcast to all.
+__device__ __forceinline__ float block_sum(float v, float* red) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    const int w = threadIdx.x >> 6;
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) red[w] = v;
+    __syncthreads();
+    return red[0] + red[1] + red[2] + red[3];
+}
+
+// ------------------------------------------------------------------ gather
+// h[i] = state.h[slot[i]]; h_in[i] = h[i] (exit score of the L2 criterion);
+// xcat[i] = bf16([h; e]) for the input-injection adapter.  Validates the row.
+__global__ __launch_bounds__(256) void k_gather(int d, int r_max, int n_slots, int max_seqs, int max_pos,
+                                                const int32_t* __restrict__ slot, const int32_t* __restrict__ seq,
+                                                const int32_t* __restrict__ pos, const int32_t* __restrict__ c,
+                                                const int32_t* __restrict__ depth, const float* __restrict__ sh,
+                                                const float* __restrict__ se, float* __restrict__ h,
+                                                float* __restrict__ h_in, uint16_t* __restrict__ xcat, int* err) {
+    const int i = blockIdx.x;
+    const int sl = slot[i];
+    if (threadIdx.x == 0) {
+        if (depth[i] < 1 || depth[i] > r_max || c[i] < 0 || c[i] >= depth[i]) set_err(err, CDB_DEV_BAD_DEPTH);
+        if (sl < 0 || sl >= n_slots || seq[i] < 0 || seq[i] >= max_seqs || pos[i] < 0 || pos[i] >= max_pos)
+            set_err(err, CDB_DEV_BAD_INDEX);
+    }
+    const bool ok = sl >= 0 && sl < n_slots;
+    for (int k = threadIdx.x * 4; k < d; k += 256 * 4) {
+        float4 v = ok ? *reinterpret_cast<const float4*>(sh + (size_t)sl * d + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+        *reinterpret_cast<float4*>(h + (size_t)i * d + k) = v;
+        *reinterpret_cast<float4*>(h_in + (size_t)i * d + k) = v;
+        if (xcat) {
+            float4 e = ok ? *reinterpret_cast<const float4*>(se + (size_t)sl * d + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+            uint16_t* x = xcat + (size_t)i * 2 * d;
+            x[k] = f2bf(v.x); x[k + 1] = f2bf(v.y); x[k + 2] = f2bf(v.z); x[k + 3] = f2bf(v.w);
+            x[d + k] = f2bf(e.x); x[d + k + 1] = f2bf(e.y); x[d + k + 2] = f2bf(e.z); x[d + k + 3] = f2bf(e.w);
+        }
+    }
+}
+
+// h[i] = state.h[slot[i]] (coda input)
+__global__ __launch_bounds__(256) void k_load_state(int d, int n_slots, const int32_t* __restrict__ slot,
+                                                    const float* __restrict__ sh, float* __restrict__ h, int* err) {
+    const int i = blockIdx.x;
+    const int sl = slot[i];
+    const bool ok = sl >= 0 && sl < n_slots;
+    if (!ok && threadIdx.x == 0) set_err(err, CDB_DEV_BAD_INDEX);
+    for (int k = threadIdx.x * 4; k < d; k += 1024)
+        *reinterpret_cast<float4*>(h + (size_t)i * d + k) =
+            ok ? *reinterpret_cast<const float4*>(sh + (size_t)sl * d + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+}
+
+// ------------------------------------------------------------------ RMSNorm
+// out[i] = bf16(h[i] / sqrt(mean(h[i]^2) + eps)), unit gains
+__global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ h, int d, float eps,
+                                                 uint16_t* __restrict__ out, int ldo) {
+    __shared__ float red[4];
+    const int i = blockIdx.x;
+    const float* x = h + (size_t)i * d;
+    float ss = 0.f;
+    for (int k = threadIdx.x * 4; k < d; k += 1024) {
+        const float4 v = *reinterpret_cast<const float4*>(x + k);
+        ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+    }
+    ss = block_sum(ss, red);
+    const float inv = 1.0f / sqrtf(ss / d + eps);
+    uint16_t* o = out + (size_t)i * ldo;
+    for (int k = threadIdx.x * 4; k < d; k += 1024) {
+        const float4 v = *reinterpret_cast<const float4*>(x + k);
+        uint2 pk;
+        pk.x = (uint32_t)f2bf(v.x * inv) | ((uint32_t)f2bf(v.y * inv) << 16);
+        pk.y = (uint32_t)f2bf(v.z * inv) | ((uint32_t)f2bf(v.w * inv) << 16);
+        *reinterpret_cast<uint2*>(o + k) = pk;
+    }
+}
+
+// ------------------------------------------------------------------ embedding
+__global__ __launch_bounds__(256) void k_embed(int d, int vocab, int n_slots, int max_seqs, int max_pos,
+                                               const uint16_t* __restrict__ E, const int32_t* __restrict__ tok,
+                                               const int32_t* __restrict__ slot, const int32_t* __restrict__ seq,
+                                               const int32_t* __restrict__ pos, float* __restrict__ h, int* err) {
+    const int i = blockIdx.x;
+    const int t = tok[i];
+    const bool ok = t >= 0 && t < vocab;
+    if (threadIdx.x == 0 && (!ok || slot[i] < 0 || slot[i] >= n_slots || seq[i] < 0 || seq[i] >= max_seqs ||
+                             pos[i] < 0 || pos[i] >= max_pos))
+        set_err(err, CDB_DEV_BAD_INDEX);
+    for (int k = threadIdx.x * 4; k < d; k += 1024) {
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (ok) {
+            const uint2 w = *reinterpret_cast<const uint2*>(E + (size_t)t * d + k);
+            v = make_float4(bflo(w.x), bfhi(w.x), bflo(w.y), bfhi(w.y));
+        }
+        *reinterpret_cast<float4*>(h + (size_t)i * d + k) = v;
+    }
+}
+
+__global__ __launch_bounds__(256) void k_store_state(int d, int n_slots, const int32_t* __restrict__ slot,
+                                                     const float* __restrict__ h, float* __restrict__ sh,
+                                                     float* __restrict__ se) {
+    const int i = blockIdx.x;
+    const int sl = slot[i];
+    if (sl < 0 || sl >= n_slots) return;
+    for (int k = threadIdx.x * 4; k < d; k += 1024) {
+        const float4 v = *reinterpret_cast<const float4*>(h + (size_t)i * d + k);
+        *reinterpret_cast<float4*>(sh + (size_t)sl * d + k) = v;
+        if (se) *reinterpret_cast<float4*>(se + (size_t)sl * d + k) = v;
+    }
+}
+
+// ------------------------------------------------------------------ exit
+// score: sigmoid(w_exit . RMSNorm(h)) or ||h - h_in||_2; exit = (c + 1 == depth);
+// state.h[slot] = h.
+__global__ __launch_bounds__(256) void k_exit(int d, float eps, int exit_kind, int r_max, int n_slots,
+                                              const int32_t* __restrict__ slot, const int32_t* __restrict__ c,
+                                              const int32_t* __restrict__ depth, const float* __restrict__ h,
+                                              const float* __restrict__ h_in, const uint16_t* __restrict__ w_exit,
+                                              float* __restrict__ sh, float* __restrict__ score,
+                                              uint8_t* __restrict__ mask) {
+    __shared__ float red[4];
+    const int i = blockIdx.x;
+    const float* x = h + (size_t)i * d;
+    const float* x0 = h_in + (size_t)i * d;
+    float a = 0.f, b = 0.f;
+    for (int k = threadIdx.x * 4; k < d; k += 1024) {
+        const float4 v = *reinterpret_cast<const float4*>(x + k);
+        if (exit_kind == 1) {
+            const float4 u = *reinterpret_cast<const float4*>(x0 + k);
+            const float dx = v.x - u.x, dy = v.y - u.y, dz = v.z - u.z, dw = v.w - u.w;
+            a += dx * dx + dy * dy + dz * dz + dw * dw;
+        } else {
+            const uint2 w = *reinterpret_cast<const uint2*>(w_exit + k);
+            a += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+            b += v.x * bflo(w.x) + v.y * bfhi(w.x) + v.z * bflo(w.y) + v.w * bfhi(w.y);
+        }
+    }
+    a = block_sum(a, red);
+    b = block_sum(b, red);
+    const int sl = slot[i];
+    if (threadIdx.x == 0) {
+        float sc;
+        if (exit_kind == 1) {
+            sc = sqrtf(a);
+        } else {
+            const float z = b / sqrtf(a / d + eps);
+            sc = 1.0f / (1.0f + __expf(-z));
+        }
+        score[i] = sc;
+        const bool valid = depth[i] >= 1 && depth[i] <= r_max && c[i] >= 0 && c[i] < depth[i];
+        mask[i] = (uint8_t)(valid && c[i] + 1 == depth[i]);
+    }
+    if (sl >= 0 && sl < n_slots)
+        for (int k = threadIdx.x * 4; k < d; k += 1024)
+            *reinterpret_cast<float4*>(sh + (size_t)sl * d + k) = *reinterpret_cast<const float4*>(x + k);
+}
+
+// Stable partition of the batch into continuing and exiting rows (one
+// workgroup; blocked scan over chunks of 256 rows).
+__global__ __launch_bounds__(256) void k_compact(int M, const uint8_t* __restrict__ mask, int32_t* __restrict__ cont,
+                                                 int32_t* __restrict__ exited, int32_t* __restrict__ counts) {
+    __shared__ int s_scan[256];
+    __shared__ int s_base;
+    if (threadIdx.x == 0) s_base = 0;
+    __syncthreads();
+    for (int b0 = 0; b0 < M; b0 += 256) {
+        const int i = b0 + threadIdx.x;
+        const int e = i < M ? (int)mask[i] : 0;
+        s_scan[threadIdx.x] = e;
+        __syncthreads();
+        for (int o = 1; o < 256; o <<= 1) {
+            const int v = threadIdx.x >= o ? s_scan[threadIdx.x - o] : 0;
+            __syncthreads();
+            s_scan[threadIdx.x] += v;
+            __syncthreads();
+        }
+        const int incl = s_scan[threadIdx.x];
+        const int base = s_base;
+        if (i < M) {
+            const int ex_before = base + incl - e;  // exits before row i
+            if (e)
+                exited[ex_before] = i;
+            else
+                cont[i - ex_before] = i;
+        }
+        __syncthreads();
+        if (threadIdx.x == 255) s_base = base + incl;
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        counts[0] = M - s_base;
+        counts[1] = s_base;
+    }
+}
+
+// Last-exited cache: for each exiting row (depth < r_max), copy its K/V at pos
+// from plane depth to planes depth+1..r_max, for the core layer blockIdx.y.
+__global__ __launch_bounds__(256) void k_copy_on_exit(int H, int hd, int r_max, KvTarget kv,
+                                                      const int32_t* __restrict__ seq, const int32_t* __restrict__ pos,
+                                                      const int32_t* __restrict__ depth,
+                                                      const int32_t* __restrict__ exited,
+                                                      const int32_t* __restrict__ counts, int* err) {
+    const int j = blockIdx.x;
+    if (j >= counts[1]) return;
+    const int i = exited[j];
+    const int dep = depth[i];
+    if (dep >= r_max || dep < 1) return;
+    const int sq = seq[i], ps = pos[i], pg = ps / kPage;
+    const int l = blockIdx.y;
+    if (sq < 0 || sq >= kv.max_seqs || pg < 0 || pg >= kv.max_pages) {
+        if (threadIdx.x == 0) set_err(err, CDB_DEV_BAD_INDEX);
+        return;
+    }
+    const int32_t* pt = kv.page_table + (size_t)sq * kv.n_planes * kv.max_pages;
+    const int src = pt[(size_t)dep * kv.max_pages + pg];
+    if (src < 0 || src >= kv.n_pages) {
+        if (threadIdx.x == 0) set_err(err, CDB_DEV_UNMAPPED_PAGE);
+        return;
+    }
+    const size_t page_elems = (size_t)kv.n_layers * 2 * H * kPage * hd;
+    const int vec_per_head = hd / 8;  // 16-byte vectors per (kv, head) entry
+    const int nvec = 2 * H * vec_per_head;
+    for (int pl = dep + 1; pl <= r_max; ++pl) {
+        const int dst = pt[(size_t)pl * kv.max_pages + pg];
+        if (dst < 0 || dst >= kv.n_pages) {
+            if (threadIdx.x == 0) set_err(err, CDB_DEV_UNMAPPED_PAGE);
+            continue;
+        }
+        if (dst == src) continue;
+        for (int v = threadIdx.x; v < nvec; v += 256) {
+            const int kvh = v / vec_per_head, e = v - kvh * vec_per_head;  // kvh = kv*H + head
+            const size_t off = (((size_t)l * 2 * H + kvh) * kPage + (ps % kPage)) * hd + e * 8;
+            *reinterpret_cast<uint4*>(kv.pool + (size_t)dst * page_elems + off) =
+                *reinterpret_cast<const uint4*>(kv.pool + (size_t)src * page_elems + off);
+        }
+    }
+}
+
+// ------------------------------------------------------------------ argmax
+__global__ __launch_bounds__(256) void k_argmax(int V, const float* __restrict__ logits, int32_t* __restrict__ ids) {
+    __shared__ float sv[256];
+    __shared__ int si[256];
+    const int i = blockIdx.x;
+    const float* x = logits + (size_t)i * V;
+    float bv = -INFINITY;
+    int bi = 0x7fffffff;
+    for (int k = threadIdx.x; k < V; k += 256) {
+        const float v = x[k];
+        if (v > bv) {  // k increases, so ties keep the lower index
+            bv = v;
+            bi = k;
+        }
+    }
+    sv[threadIdx.x] = bv;
+    si[threadIdx.x] = bi;
+    __syncthreads();
+    for (int o = 128; o > 0; o >>= 1) {
+        if (threadIdx.x < o) {
+            const float v2 = sv[threadIdx.x + o];
+            const int i2 = si[threadIdx.x + o];
+            if (v2 > sv[threadIdx.x] || (v2 == sv[threadIdx.x] && i2 < si[threadIdx.x])) {
+                sv[threadIdx.x] = v2;
+                si[threadIdx.x] = i2;
+            }
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) ids[i] = si[0] == 0x7fffffff ? 0 : si[0];
+}
+
+// ------------------------------------------------------------------ packing
+// dst tile (nt, kt), lane l, element e  <-  row r(nt*16 + l%16), column kt*32 + 8*(l/16) + e
+__global__ __launch_bounds__(256) void k_pack(int kind, const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
+                                              const uint16_t* __restrict__ Cm, int N, int K, int hd, int H,
+                                              uint16_t* __restrict__ dst) {
+    const size_t KT = K / 32;
+    const size_t total = (size_t)(N / 16) * KT * 64;
+    for (size_t t = (size_t)blockIdx.x * 256 + threadIdx.x; t < total; t += (size_t)gridDim.x * 256) {
+        const int lane = (int)(t & 63);
+        const size_t tile = t >> 6;
+        const int nt = (int)(tile / KT), kt = (int)(tile % KT);
+        const int p = nt * 16 + (lane & 15);
+        const int k = kt * 32 + 8 * (lane >> 4);
+        const uint16_t* src;
+        int row;
+        if (kind == PACK_QKV) {
+            const int g = p >> 5, w = p & 31, half = w >> 4, jj = w & 15;
+            const int gph = hd >> 5, hg = H * gph;
+            const int part = g / hg, rem = g - part * hg;
+            const int head = rem / gph, gi = rem - head * gph;
+            row = head * hd + gi * 16 + jj + half * (hd >> 1);
+            src = part == 0 ? A : (part == 1 ? B : Cm);
+        } else if (kind == PACK_GU) {
+            const int g = p >> 5, half = (p >> 4) & 1;
+            row = g * 16 + (p & 15);
+            src = half ? B : A;
+        } else {
+            row = p;
+            src = A;
+        }
+        *reinterpret_cast<uint4*>(dst + t * 8) = *reinterpret_cast<const uint4*>(src + (size_t)row * K + k);
+    }
+}
+
+__global__ void k_copy16(const uint16_t* __restrict__ s, size_t n, uint16_t* __restrict__ d) {
+    for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256) d[i] = s[i];
+}
+
+__global__ void k_ws_init(int* err, int* counters, int n) {
+    for (int i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) counters[i] = 0;
+    if (blockIdx.x == 0 && threadIdx.x == 0) *err = 0;
+}
+
+// ------------------------------------------------------------------ launchers
+static int page_cap(const cdb_kv& kv) { return kv.max_pages * kPage; }
+
+hipError_t launch_gather(const cdb_model_desc& md, const cdb_state& s, const cdb_rows& r, const cdb_kv& kv, float* h,
+                         float* h_in, uint16_t* xcat, int* err, hipStream_t st) {
+    if (r.n_rows <= 0) return hipSuccess;
+    k_gather<<<r.n_rows, 256, 0, st>>>(md.d, md.r_max, s.n_slots, kv.max_seqs, page_cap(kv), r.slot, r.seq, r.pos, r.c,
+                                        r.depth, s.h, s.e, h, h_in, xcat, err);
+    return hipGetLastError();
+}
+
+hipError_t launch_load_state(int M, int d, const int32_t* slot, const float* state_h, int n_slots, float* h, int* err,
+                             hipStream_t st) {
+    if (M <= 0) return hipSuccess;
+    k_load_state<<<M, 256, 0, st>>>(d, n_slots, slot, state_h, h, err);
+    return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm(const float* h, int M, int d, float eps, uint16_t* out, int ldo, hipStream_t st) {
+    if (M <= 0) return hipSuccess;
+    k_rmsnorm<<<M, 256, 0, st>>>(h, d, eps, out, ldo);
+    return hipGetLastError();
+}
+
+hipError_t launch_embed(const cdb_model_desc& md, const uint16_t* embed, const int32_t* tokens, const cdb_rows& r,
+                        const cdb_kv& kv, int n_slots, float* h, int* err, hipStream_t st) {
+    if (r.n_rows <= 0) return hipSuccess;
+    k_embed<<<r.n_rows, 256, 0, st>>>(md.d, md.vocab, n_slots, kv.max_seqs, page_cap(kv), embed, tokens, r.slot, r.seq,
+                                       r.pos, h, err);
+    return hipGetLastError();
+}
+
+hipError_t launch_store_state(int M, int d, int n_slots, const int32_t* slot, const float* h, float* state_h,
+                              float* state_e, hipStream_t st) {
+    // out-of-range slots were reported by the embed kernel and are skipped here
+    if (M <= 0) return hipSuccess;
+    k_store_state<<<M, 256, 0, st>>>(d, n_slots, slot, h, state_h, state_e);
+    return hipGetLastError();
+}
+
+hipError_t launch_exit(const cdb_model_desc& md, const cdb_rows& r, const float* h, const float* h_in,
+                       const uint16_t* w_exit, float* state_h, int n_slots, const cdb_step_out& o, hipStream_t st) {
+    if (r.n_rows <= 0) return hipSuccess;
+    k_exit<<<r.n_rows, 256, 0, st>>>(md.d, md.rms_eps, md.exit_kind, md.r_max, n_slots, r.slot, r.c, r.depth, h,
+                                      h_in, w_exit, state_h, o.exit_score, o.exit_mask);
+    return hipGetLastError();
+}
+
+hipError_t launch_compact(int M, const uint8_t* mask, int32_t* cont, int32_t* exited, int32_t* counts, hipStream_t st) {
+    k_compact<<<1, 256, 0, st>>>(M, mask, cont, exited, counts);
+    return hipGetLastError();
+}
+
+hipError_t launch_copy_on_exit(const cdb_model_desc& md, const cdb_kv& kv, const cdb_rows& r, const int32_t* exited,
+                               const int32_t* counts, int* err, hipStream_t st) {
+    if (r.n_rows <= 0 || md.n_core <= 0) return hipSuccess;
+    KvTarget t{};
+    t.pool = static_cast<uint16_t*>(kv.core_pool);
+    t.n_pages = kv.core_pages;
+    t.n_layers = md.n_core;
+    t.page_table = kv.page_table;
+    t.max_seqs = kv.max_seqs;
+    t.max_pages = kv.max_pages;
+    t.n_planes = md.r_max + 2;
+    dim3 grid(r.n_rows, md.n_core);
+    k_copy_on_exit<<<grid, 256, 0, st>>>(md.n_heads, md.head_dim, md.r_max, t, r.seq, r.pos, r.depth, exited, counts,
+                                         err);
+    return hipGetLastError();
+}
+
+hipError_t launch_argmax(int M, int V, const float* logits, int32_t* ids, hipStream_t st) {
+    if (M <= 0) return hipSuccess;
+    k_argmax<<<M, 256, 0, st>>>(V, logits, ids);
+    return hipGetLastError();
+}
+
+hipError_t launch_pack(int kind, const uint16_t* a, const uint16_t* b, const uint16_t* c, int N, int K, int hd,
+                       uint16_t* dst, hipStream_t st) {
+    const int H = hd > 0 ? (N / 3) / hd : 0;
+    k_pack<<<2048, 256, 0, st>>>(kind, a, b, c, N, K, hd, H, dst);
+    return hipGetLastError();
+}
+
+hipError_t launch_copy_bf16(const uint16_t* src, size_t n, uint16_t* dst, hipStream_t st) {
+    k_copy16<<<1024, 256, 0, st>>>(src, n, dst);
+    return hipGetLastError();
+}
+
+hipError_t launch_ws_init(int* err, int* counters, int n, hipStream_t st) {
+    k_ws_init<<<64, 256, 0, st>>>(err, counters, n);
+    return hipGetLastError();
+}
+
+}  // namespace cdb
