@@ -1,0 +1,247 @@
+"""Benchmark: mixed-depth loop-step throughput of continuous depth batching.
+
+One step = one cdb_loop_step over a mixed-depth decode batch of the
+Ouro-1.4B-shaped looped LM (d 2048, 16 heads x 128, SwiGLU 5632, 24 core
+layers, r_max 4, 16-token pages, depth-indexed KV per (sequence, loop, layer)).
+The batch is 64 rows, one per sequence, as it stands mid-decode in refill mode:
+positions drawn from the decode range of a 512-token prompt + 256 decode
+tokens, exit depths from the categorical {1: .3, 2: .3, 3: .2, 4: .2}
+size-biased by work items, loop indices below the depth.  Weights are seeded
+random N(0, 0.02) in bf16; KV contents and states are random; everything is
+resident in HBM before timing starts.
+
+Prints one JSON line: loop-step rows (tokens) per second, ms per step, the
+roofline of the dominant kernel (paged attention, HBM-bound) and the CPU
+oracle's rate on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def setup(shape, w, n_rows, pos_lo, pos_hi, seed_stream=7):
+    import numpy as np
+    import torch
+
+    import cdbgen
+    import paper_2608_09444_amd as cdb
+    dm = cdb.DeviceModel(shape, w)
+    rows_np = cdbgen.decode_snapshot(n_rows, cdbgen.OURO_DEPTHS, shape.r_max, pos_lo, pos_hi, stream=seed_stream)
+    max_pages = cdbgen.pages_for(pos_hi + 1)
+    n_pages = n_rows * max_pages * shape.r_max
+    kv = cdb.PagedKV(shape, n_rows, max_pages, 0, n_pages, 0, fill="random")
+    g = torch.Generator(device="cuda")
+    g.manual_seed(1234)
+    kv.core.normal_(0.0, 1.0, generator=g)
+    pt = np.arange(n_pages, dtype=np.int32).reshape(n_rows, max_pages, shape.r_max).transpose(0, 2, 1)
+    full = np.full((n_rows, shape.r_max + 2, max_pages), -1, np.int32)
+    full[:, 1:shape.r_max + 1, :] = pt
+    kv.page_table.copy_(torch.from_numpy(full))
+    state = cdb.State(shape, n_rows)
+    state.h.normal_(0.0, 1.0, generator=g)
+    rows = cdb.Rows(rows_np["slot"], rows_np["seq"], rows_np["pos"], rows_np["c"], rows_np["depth"])
+    out = cdb.StepOut(n_rows)
+    ws = cdb.Workspace(dm.desc, n_rows)
+    torch.cuda.synchronize()
+    return dm, kv, state, rows, rows_np, out, ws
+
+
+def attention_bytes(shape, pos):
+    """Algorithmic bytes of one paged-attention launch (one layer): K and V of
+    every visible position of each row, q in (fp32) and the output (bf16)."""
+    import numpy as np
+    ctx = np.asarray(pos, dtype=np.int64) + 1
+    return int(ctx.sum()) * 2 * shape.d * 2 + len(ctx) * shape.d * (4 + 2)
+
+
+def step_bytes(shape, rows_np):
+    """Algorithmic bytes of one loop step: core weights once, every layer's K/V
+    over the visible context, the new K/V entries, copy-on-exit traffic, and the
+    row states in and out."""
+    import numpy as np
+    import cdbgen
+    pc = cdbgen.param_counts(shape)
+    w = pc["core"] * 2 + shape.d * 2
+    kv_tok = shape.n_core * 2 * shape.d * 2
+    ctx = rows_np["pos"].astype(np.int64) + 1
+    ex = rows_np["c"] + 1 == rows_np["depth"]
+    copies = int(((shape.r_max - rows_np["depth"]) * ex).sum())
+    n = len(ctx)
+    return w + int(ctx.sum()) * kv_tok + n * kv_tok + copies * 2 * kv_tok + n * shape.d * 4 * 2
+
+
+def step_flops(shape, rows_np):
+    import numpy as np
+    import cdbgen
+    n = len(rows_np["pos"])
+    ctx = rows_np["pos"].astype(np.int64) + 1
+    return 2 * n * cdbgen.param_counts(shape)["core"] + 4 * shape.n_core * shape.d * int(ctx.sum())
+
+
+def time_attention(shape, kv, rows, n_rows, launches):
+    """Average duration of the paged-attention kernel on the loop-step batch,
+    timed with events on the stream it is launched on."""
+    import torch
+    import paper_2608_09444_amd as cdb
+    q = torch.randn((n_rows, shape.d), dtype=torch.float32, device="cuda")
+    o = torch.empty((n_rows, shape.d), dtype=torch.bfloat16, device="cuda")
+    ws = torch.zeros(256, dtype=torch.uint8, device="cuda")
+    desc = cdb.make_desc(shape)
+    st = torch.cuda.current_stream()
+    for i in range(5):
+        cdb.cdb_paged_attention(desc, kv.c, rows.c, 1, i % shape.n_core, q, o, ws)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(st)
+    for i in range(launches):
+        cdb.cdb_paged_attention(desc, kv.c, rows.c, 1, i % shape.n_core, q, o, ws)
+    e1.record(st)
+    e1.synchronize()
+    return e0.elapsed_time(e1) / launches
+
+
+def cpu_baseline(shape, w, rows_np, n_sample, threads):
+    """The CPU oracle's loop step on `n_sample` rows of the same batch (same
+    positions, depths, loop indices; seeded random KV and state)."""
+    import numpy as np
+    os.environ["OMP_NUM_THREADS"] = str(threads)
+    import cdbgen
+    import oracle
+    m = oracle.Model(shape, w, bf16_storage=True)
+    idx = np.arange(n_sample)
+    pos = rows_np["pos"][idx]
+    pages = [cdbgen.pages_for(int(p) + 1) for p in pos]
+    maxp = max(pages)
+    # the row's plane over its whole context, plus the page at pos of every
+    # deeper plane (copy-on-exit destinations)
+    need = sum(pages) + sum(shape.r_max - int(rows_np["c"][i]) - 1 for i in idx)
+    paged = oracle.Paged(shape, n_sample, maxp, 0, need, 0)
+    nxt = 0
+    for i in range(n_sample):
+        plane = int(rows_np["c"][i]) + 1
+        for pg in range(pages[i]):
+            paged.page_table[i, plane, pg] = nxt
+            nxt += 1
+        for pl in range(plane + 1, shape.r_max + 1):
+            paged.page_table[i, pl, pages[i] - 1] = nxt
+            nxt += 1
+    kvbits = cdbgen.random_kv_bf16(paged.core.shape, seed=5)
+    paged.core[...] = cdbgen.bf16_to_f32(kvbits)
+    del kvbits
+    h = cdbgen.random_state(n_sample, shape.d, seed=6).astype(np.float64)
+    slot = idx.astype(np.int32)
+    t0 = time.perf_counter()
+    oracle.loop_step(m, paged, h, None, slot, slot, pos, rows_np["c"][idx], rows_np["depth"][idx])
+    dt = time.perf_counter() - t0
+    return {"value": n_sample / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{n_sample} of the {len(rows_np['pos'])} rows of the timed batch (same positions, loop "
+                      f"indices and depths; seeded random KV/state), one loop step, {dt:.1f}s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--cpu-sample", type=int, default=4, help="rows in the CPU-oracle sample (0 = skip)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: the loop step shards by sequence with no exchange between GPUs, "
+              "and this build runs and reports the single-GPU path (use --gpus 1).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import cdbgen
+    import paper_2608_09444_amd as cdb
+    shape = cdbgen.OURO
+    n_rows, pos_lo, pos_hi = 64, 512, 767
+    log("setup")
+    t0 = time.time()
+    w = cdbgen.model_weights(shape)
+    log(f"weights drawn in {time.time() - t0:.1f}s")
+    dm, kv, state, rows, rows_np, out, ws = setup(shape, w, n_rows, pos_lo, pos_hi)
+    st = torch.cuda.current_stream()
+
+    def step():
+        cdb.cdb_loop_step(dm.model, kv.c, state.c, rows.c, out.c, ws.buf)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    code = cdb.cdb_read_device_error(ws.buf)
+    if code != 0:
+        raise RuntimeError(f"device error {code} during warmup")
+    log(f"timing {args.steps} steps")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(st)
+    for _ in range(args.steps):
+        step()
+    e1.record(st)
+    e1.synchronize()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    value = n_rows / (ms * 1e-3)
+    sb = step_bytes(shape, rows_np)
+    log(f"{ms:.3f} ms/step, {value:.0f} rows/s, step bytes {sb / 1e9:.2f} GB -> {sb / (ms * 1e-3) / 1e9:.0f} GB/s")
+
+    attn_ms = time_attention(shape, kv, rows, n_rows, args.steps * shape.n_core)
+    ab = attention_bytes(shape, rows_np["pos"])
+    attn_gbs = ab / (attn_ms * 1e-3) / 1e9
+    log(f"attention {attn_ms * 1e3:.1f} us/launch, {ab / 1e6:.1f} MB -> {attn_gbs:.0f} GB/s")
+
+    cpu = None
+    if args.cpu_sample > 0:
+        threads = min(16, os.cpu_count() or 1)
+        log(f"cpu baseline on {args.cpu_sample} rows, {threads} threads")
+        cpu = cpu_baseline(shape, w, rows_np, args.cpu_sample, threads)
+
+    res = {
+        "metric": "mixed-depth loop-step tokens/s (Ouro-1.4B-shaped, bs=64); % HBM/MFMA roofline",
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "ouro-1.4b-shaped looped LM, mixed-depth decode loop step: 64 rows at positions "
+                               "U[512,767] (prompt 512 + decode 256), depths categorical {1:.3,2:.3,3:.2,4:.2}",
+                   "rows": n_rows, "d": shape.d, "heads": shape.n_heads, "head_dim": shape.head_dim,
+                   "d_ff": shape.d_ff, "core_layers": shape.n_core, "r_max": shape.r_max,
+                   "mean_context": float(np.mean(rows_np["pos"] + 1)),
+                   "exits_per_step": int((rows_np["c"] + 1 == rows_np["depth"]).sum())},
+        "roofline": {"bound": "hbm", "kernel": "k_attn<128> (paged decode attention, one layer)",
+                     "achieved": round(attn_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(attn_gbs / HBM_PEAK_GBS, 4), "traffic": None},
+        "step_roofline": {"bound": "hbm", "algorithmic_bytes": sb, "achieved": round(sb / (ms * 1e-3) / 1e9, 1),
+                          "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                          "frac": round(sb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                          "flops": step_flops(shape, rows_np)},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

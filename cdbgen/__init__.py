@@ -18,6 +18,7 @@ from __future__ import annotations
 
 import dataclasses
 import math
+import os
 from typing import Dict, List, Optional
 
 import numpy as np
@@ -104,11 +105,49 @@ def bf16_to_f32(bits: np.ndarray) -> np.ndarray:
     return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
 
 
+_BLOCK = 1 << 20  # elements per independently seeded block
+_POOL = None
+
+
+def _pool():
+    global _POOL
+    if _POOL is None:
+        from concurrent.futures import ThreadPoolExecutor
+        _POOL = ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1))
+    return _POOL
+
+
+def normal_bf16_many(specs) -> List[np.ndarray]:
+    """Several N(0, std) tensors, drawn in fp32 and stored as bf16 bits.  Each
+    spec is (shape, std, seed, *stream).  A tensor's flat array is cut into
+    blocks of 2^20 elements, block b drawn from stream (seed, *stream, b), so the
+    values do not depend on how many threads draw them."""
+    outs, tasks = [], []
+    for spec in specs:
+        shape, std, seed, stream = spec[0], spec[1], spec[2], tuple(spec[3:])
+        n = int(np.prod(shape))
+        out = np.empty(n, dtype=np.uint16)
+        outs.append(out.reshape(shape))
+        for b in range((n + _BLOCK - 1) // _BLOCK):
+            tasks.append((out, n, b, std, seed, stream))
+
+    def fill(t):
+        out, n, b, std, seed, stream = t
+        lo, hi = b * _BLOCK, min(n, (b + 1) * _BLOCK)
+        x = _rng(seed, *stream, b).standard_normal(size=hi - lo, dtype=np.float32)
+        x *= np.float32(std)
+        out[lo:hi] = bf16_bits(x)
+
+    if len(tasks) <= 1:
+        for t in tasks:
+            fill(t)
+    else:
+        list(_pool().map(fill, tasks))
+    return outs
+
+
 def normal_bf16(shape, std: float, seed: int, *stream: int) -> np.ndarray:
-    g = _rng(seed, *stream)
-    x = g.standard_normal(size=shape, dtype=np.float32)
-    x *= np.float32(std)
-    return bf16_bits(x)
+    return normal_bf16_many([(shape, std, seed, *stream)])[0]
 
 
 # ------------------------------------------------------------------ weights
@@ -124,21 +163,24 @@ def layer_shapes(s: ModelShape) -> Dict[str, tuple]:
 def layer_weights(s: ModelShape, layer: int, seed: int = WEIGHT_SEED, std: float = 0.02) -> Dict[str, np.ndarray]:
     """Weights of one transformer layer (index over prelude, core, coda), as
     row-major [out][in] bf16 bit arrays."""
-    out = {}
-    for j, (name, shp) in enumerate(layer_shapes(s).items()):
-        out[name] = normal_bf16(shp, std, seed, 4 + 7 * layer + j)
-    return out
+    names = list(layer_shapes(s))
+    arrs = normal_bf16_many([(shp, std, seed, 4 + 7 * layer + j) for j, shp in enumerate(layer_shapes(s).values())])
+    return dict(zip(names, arrs))
 
 
 def model_weights(s: ModelShape, seed: int = WEIGHT_SEED, std: float = 0.02) -> Dict[str, object]:
     """All weights of a model, N(0, std) drawn in fp32, stored as bf16 bits."""
-    w: Dict[str, object] = {
-        "embed": normal_bf16((s.vocab, s.d), std, seed, 0),
-        "lm_head": normal_bf16((s.vocab, s.d), std, seed, 1),
-        "w_exit": normal_bf16((s.d,), std, seed, 2),
-        "adapter": normal_bf16((s.d, 2 * s.d), std, seed, 3) if s.injection else None,
-        "layers": [layer_weights(s, L, seed, std) for L in range(s.n_layers)],
-    }
+    specs = [((s.vocab, s.d), std, seed, 0), ((s.vocab, s.d), std, seed, 1), ((s.d,), std, seed, 2)]
+    if s.injection:
+        specs.append(((s.d, 2 * s.d), std, seed, 3))
+    names = list(layer_shapes(s))
+    for L in range(s.n_layers):
+        specs += [(shp, std, seed, 4 + 7 * L + j) for j, shp in enumerate(layer_shapes(s).values())]
+    arrs = normal_bf16_many(specs)
+    w: Dict[str, object] = {"embed": arrs[0], "lm_head": arrs[1], "w_exit": arrs[2],
+                            "adapter": arrs[3] if s.injection else None}
+    k = 4 if s.injection else 3
+    w["layers"] = [dict(zip(names, arrs[k + 7 * L: k + 7 * L + 7])) for L in range(s.n_layers)]
     return w
 
 

@@ -66,7 +66,7 @@ enum {
 /* Model shape.  Layer split prelude-core-coda (Section 2): n_prelude, n_core,
  * n_coda transformer layers; the core is iterated up to r_max times.
  * Supported: d % 32 == 0, n_heads * head_dim == d, head_dim in {64, 96, 128},
- * d_ff % 32 == 0, vocab % 16 == 0, page_tokens == 16, 1 <= r_max <= 64. */
+ * d_ff % 32 == 0, vocab % 32 == 0, page_tokens == 16, 1 <= r_max <= 64. */
 typedef struct {
     int32_t d, n_heads, head_dim, d_ff, vocab;
     int32_t n_prelude, n_core, n_coda, r_max;
@@ -163,8 +163,8 @@ typedef struct {
 /* Workspace (device scratch) needed for calls with up to max_rows rows. */
 size_t cdb_workspace_bytes(const cdb_model_desc* desc, int32_t max_rows);
 
-/* Clears the workspace's error code and internal counters (a kernel, not a
- * memset).  Call once after allocating a workspace. */
+/* Clears the workspace's error code (a kernel, not a memset).  Call once after
+ * allocating a workspace. */
 cdb_status cdb_workspace_init(void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Prelude stage (Section 4.1; Eq. 1 h^(0) = P(x_t)): h = E[tokens[i]], then the
@@ -196,6 +196,17 @@ cdb_status cdb_loop_step(const cdb_model* model, const cdb_kv* kv, const cdb_sta
 cdb_status cdb_boundary_coda(const cdb_model* model, const cdb_kv* kv, const cdb_state* state,
                              const cdb_rows* rows, float* logits, int32_t* next_ids, void* ws, size_t ws_bytes,
                              hipStream_t stream);
+
+/* Paged decode attention of one layer, alone (the operation every layer of the
+ * stage calls runs after writing its K/V; Section 4.2): for row i and head h,
+ *   out[i][h*hd + :] = softmax_s(q[i][h*hd + :] . K_s / sqrt(hd)) V_s
+ * over positions s = 0..pos[i] of sequence seq[i] in the row's plane of stage
+ * `stage` (0 prelude, 1 core -> plane c[i] + 1, 2 coda), layer `layer` of that
+ * stage.  q: device fp32 [n_rows][d] (after RoPE); out: device bf16
+ * [n_rows][d].  Reads the cache only. */
+cdb_status cdb_paged_attention(const cdb_model_desc* desc, const cdb_kv* kv, const cdb_rows* rows, int32_t stage,
+                               int32_t layer, const float* q, void* out, void* ws, size_t ws_bytes,
+                               hipStream_t stream);
 
 /* Reads (and clears) the workspace's sticky device error code.  Synchronises
  * `stream`; not for the hot path. */

@@ -20,8 +20,8 @@ PAGE_TOKENS = 16
 MAX_ROWS = 256
 
 EXPORTED = ("cdb_packed_weight_bytes", "cdb_pack_weights", "cdb_workspace_bytes", "cdb_workspace_init",
-            "cdb_boundary_prelude", "cdb_loop_step", "cdb_boundary_coda", "cdb_read_device_error",
-            "cdb_status_str")
+            "cdb_boundary_prelude", "cdb_loop_step", "cdb_boundary_coda", "cdb_paged_attention",
+            "cdb_read_device_error", "cdb_status_str")
 
 
 class CdbError(RuntimeError):
@@ -85,11 +85,12 @@ def lib() -> C.CDLL:
         L.cdb_boundary_prelude.argtypes = [P, P, P, P, P, P, S, P]
         L.cdb_loop_step.argtypes = [P, P, P, P, P, P, S, P]
         L.cdb_boundary_coda.argtypes = [P, P, P, P, P, P, P, S, P]
+        L.cdb_paged_attention.argtypes = [P, P, P, I, I, P, P, P, S, P]
         L.cdb_read_device_error.argtypes = [P, P, P]
         L.cdb_status_str.argtypes = [C.c_int]
         L.cdb_status_str.restype = C.c_char_p
         for f in ("cdb_pack_weights", "cdb_workspace_init", "cdb_boundary_prelude", "cdb_loop_step",
-                  "cdb_boundary_coda", "cdb_read_device_error"):
+                  "cdb_boundary_coda", "cdb_paged_attention", "cdb_read_device_error"):
             getattr(L, f).restype = C.c_int
         _lib = L
     return _lib
@@ -157,6 +158,13 @@ def cdb_boundary_coda(model: cdb_model, kv: cdb_kv, state: cdb_state, rows: cdb_
     _check("cdb_boundary_coda", lib().cdb_boundary_coda(C.byref(model), C.byref(kv), C.byref(state), C.byref(rows),
                                                         _ptr(logits), _ptr(next_ids), _ptr(ws), ws.numel(),
                                                         _stream(stream)))
+
+
+def cdb_paged_attention(desc: cdb_model_desc, kv: cdb_kv, rows: cdb_rows, stage: int, layer: int, q, out, ws,
+                        stream=None):
+    _check("cdb_paged_attention", lib().cdb_paged_attention(C.byref(desc), C.byref(kv), C.byref(rows), stage, layer,
+                                                            _ptr(q), _ptr(out), _ptr(ws), ws.numel(),
+                                                            _stream(stream)))
 
 
 def cdb_read_device_error(ws, stream=None) -> int:

@@ -11,7 +11,7 @@ static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 bool desc_supported(const cdb_model_desc& d) {
     if (d.d <= 0 || d.n_heads <= 0 || d.head_dim <= 0 || d.d_ff <= 0 || d.vocab <= 0) return false;
     if (d.n_prelude < 0 || d.n_core < 1 || d.n_coda < 0 || d.r_max < 1 || d.r_max > 64) return false;
-    if (d.d % 32 || d.d_ff % 32 || d.vocab % 16 || d.n_heads * d.head_dim != d.d) return false;
+    if (d.d % 32 || d.d_ff % 32 || d.vocab % 32 || d.n_heads * d.head_dim != d.d) return false;
     if (d.head_dim != 64 && d.head_dim != 96 && d.head_dim != 128) return false;
     if (d.page_tokens != kPage) return false;
     if (d.injection != 0 && d.injection != 1) return false;
@@ -51,28 +51,23 @@ struct ModelGemms {
 };
 static ModelGemms model_gemms(const cdb_model_desc& d) {
     ModelGemms g;
-    g.qkv = gemm_shape(3 * d.d, d.d);
-    g.o = gemm_shape(d.d, d.d);
-    g.gu = gemm_shape(2 * d.d_ff, d.d);
-    g.down = gemm_shape(d.d, d.d_ff);
-    g.adapter = gemm_shape(d.d, 2 * d.d);
-    g.lm = gemm_shape(d.vocab, d.d);
+    g.qkv = gemm_shape(3 * d.d, d.d, EPI_QKV);
+    g.o = gemm_shape(d.d, d.d, EPI_PARTIAL);
+    g.gu = gemm_shape(2 * d.d_ff, d.d, EPI_SWIGLU);
+    g.down = gemm_shape(d.d, d.d_ff, EPI_PARTIAL);
+    g.adapter = gemm_shape(d.d, 2 * d.d, EPI_STORE);
+    g.lm = gemm_shape(d.vocab, d.d, EPI_STORE);
     return g;
 }
 
 WsLayout ws_layout(const cdb_model_desc& d, int rows) {
     WsLayout L;
-    const size_t D = d.d, F = d.d_ff, M = rows;
+    const size_t D = d.d, F = d.d_ff, M = rows, M32 = round32(rows);
     const ModelGemms g = model_gemms(d);
-    size_t part = 0;
-    const GemmShape all[6] = {g.qkv, g.o, g.gu, g.down, g.adapter, g.lm};
-    for (const GemmShape& s : all)
-        if (s.S > 1 && (size_t)s.S * s.N > part) part = (size_t)s.S * s.N;
+    const size_t part = (size_t)(g.o.S > g.down.S ? g.o.S : g.down.S) * D;  // split-K partials of O / down
     size_t off = 0;
     L.err = off;
     off = 256;
-    L.counters = off;
-    off = align256(off + (size_t)kCounters * 4);
     L.h = off;
     off = align256(off + M * D * 4);
     L.h_in = off;
@@ -80,9 +75,9 @@ WsLayout ws_layout(const cdb_model_desc& d, int rows) {
     L.q = off;
     off = align256(off + M * D * 4);
     L.x = off;
-    off = align256(off + M * 2 * D * 2);
+    off = align256(off + M32 * 2 * D * 2);
     L.act = off;
-    off = align256(off + M * F * 2);
+    off = align256(off + M32 * F * 2);
     L.part = off;
     off = align256(off + part * M * 4);
     L.total = off;
@@ -98,7 +93,6 @@ struct Ctx {
     unsigned char* ws;
     WsLayout L;
     int* err;
-    int* counters;
     float* h;
     float* h_in;
     float* q;
@@ -116,7 +110,6 @@ static Ctx make_ctx(const cdb_model* model, void* ws, int rows) {
     c.ws = static_cast<unsigned char*>(ws);
     c.L = ws_layout(model->desc, rows);
     c.err = reinterpret_cast<int*>(c.ws + c.L.err);
-    c.counters = reinterpret_cast<int*>(c.ws + c.L.counters);
     c.h = reinterpret_cast<float*>(c.ws + c.L.h);
     c.h_in = reinterpret_cast<float*>(c.ws + c.L.h_in);
     c.q = reinterpret_cast<float*>(c.ws + c.L.q);
@@ -134,10 +127,13 @@ static const uint16_t* wptr(const Ctx& c, size_t off) { return reinterpret_cast<
     } while (0)
 
 // Run `count` transformer layers (global index first..) of one stage over the
-// rows in ctx.h, with K/V in `kv`.
-static cdb_status run_layers(const Ctx& c, int first, int count, KvTarget kv, const cdb_rows& r, hipStream_t st) {
+// rows in ctx.h, with K/V in `kv`.  On return ctx.h holds the stage output and
+// ctx.x its RMSNorm when `norm_out` is set.
+static cdb_status run_layers(const Ctx& c, int first, int count, KvTarget kv, const cdb_rows& r, bool norm_out,
+                             hipStream_t st) {
     const cdb_model_desc& d = *c.md;
     const int M = r.n_rows;
+    int pending = 0;  // split-K partials of the previous down projection not yet added to h
     for (int l = 0; l < count; ++l) {
         const size_t lb = (size_t)(first + l) * c.wl.layer_stride;
         kv.layer = l;
@@ -150,21 +146,21 @@ static cdb_status run_layers(const Ctx& c, int first, int count, KvTarget kv, co
         ea.err = c.err;
         ea.kv = kv;
         ea.q = c.q;
-        // attention half
-        HIPCHK(launch_rmsnorm(c.h, M, d.d, d.rms_eps, c.x, d.d, st));
-        HIPCHK(launch_gemm(EPI_QKV, c.x, d.d, wptr(c, lb + c.wl.qkv), M, c.gm.qkv, c.part, c.counters, ea, st));
-        HIPCHK(launch_attention(c.q, kv, r.seq, r.pos, M, d.n_heads, d.head_dim, c.x, c.err, st));
-        ea.out = c.h;
-        ea.ld_out = d.d;
-        HIPCHK(launch_gemm(EPI_RESID, c.x, d.d, wptr(c, lb + c.wl.o), M, c.gm.o, c.part, c.counters, ea, st));
-        // MLP half
-        HIPCHK(launch_rmsnorm(c.h, M, d.d, d.rms_eps, c.x, d.d, st));
         ea.act = c.act;
         ea.ld_act = d.d_ff;
-        HIPCHK(launch_gemm(EPI_SWIGLU, c.x, d.d, wptr(c, lb + c.wl.gu), M, c.gm.gu, c.part, c.counters, ea, st));
-        HIPCHK(launch_gemm(EPI_RESID, c.act, d.d_ff, wptr(c, lb + c.wl.down), M, c.gm.down, c.part, c.counters, ea,
-                           st));
+        // attention half: h += down partials; x = RMSNorm(h); q/k/v + RoPE + K/V write
+        HIPCHK(launch_resid_norm(c.h, c.part, pending, M, d.d, d.rms_eps, c.x, st));
+        HIPCHK(launch_gemm(EPI_QKV, c.x, wptr(c, lb + c.wl.qkv), M, c.gm.qkv, c.part, ea, st));
+        HIPCHK(launch_attention(c.q, kv, r.seq, r.pos, M, d.n_heads, d.head_dim, c.x, c.err, st));
+        HIPCHK(launch_gemm(EPI_PARTIAL, c.x, wptr(c, lb + c.wl.o), M, c.gm.o, c.part, ea, st));
+        // MLP half: h += O partials; x = RMSNorm(h); act = SwiGLU; down partials
+        HIPCHK(launch_resid_norm(c.h, c.part, c.gm.o.S, M, d.d, d.rms_eps, c.x, st));
+        HIPCHK(launch_gemm(EPI_SWIGLU, c.x, wptr(c, lb + c.wl.gu), M, c.gm.gu, c.part, ea, st));
+        HIPCHK(launch_gemm(EPI_PARTIAL, c.act, wptr(c, lb + c.wl.down), M, c.gm.down, c.part, ea, st));
+        pending = c.gm.down.S;
     }
+    if (pending || norm_out)
+        HIPCHK(launch_resid_norm(c.h, c.part, pending, M, d.d, d.rms_eps, norm_out ? c.x : nullptr, st));
     return CDB_OK;
 }
 
@@ -260,9 +256,8 @@ size_t cdb_workspace_bytes(const cdb_model_desc* desc, int32_t max_rows) {
 
 cdb_status cdb_workspace_init(void* ws, size_t ws_bytes, hipStream_t st) {
     if (!ws) return CDB_ERR_INVALID_ARG;
-    if (ws_bytes < 256 + (size_t)kCounters * 4) return CDB_ERR_CAPACITY;
-    unsigned char* b = static_cast<unsigned char*>(ws);
-    HIPCHK(launch_ws_init(reinterpret_cast<int*>(b), reinterpret_cast<int*>(b + 256), kCounters, st));
+    if (ws_bytes < 256) return CDB_ERR_CAPACITY;
+    HIPCHK(launch_ws_init(static_cast<int*>(ws), st));
     return CDB_OK;
 }
 
@@ -276,7 +271,7 @@ cdb_status cdb_boundary_prelude(const cdb_model* model, const cdb_kv* kv, const 
     if (rows->n_rows == 0) return CDB_OK;
     Ctx c = make_ctx(model, ws, rows->n_rows);
     HIPCHK(launch_embed(d, wptr(c, c.wl.embed), tokens, *rows, *kv, state->n_slots, c.h, c.err, st));
-    s = run_layers(c, 0, d.n_prelude, stage_target(d, *kv, 0), *rows, st);
+    s = run_layers(c, 0, d.n_prelude, stage_target(d, *kv, 0), *rows, false, st);
     if (s != CDB_OK) return s;
     HIPCHK(launch_store_state(rows->n_rows, d.d, state->n_slots, rows->slot, c.h, state->h,
                               d.injection ? state->e : nullptr, st));
@@ -301,12 +296,11 @@ cdb_status cdb_loop_step(const cdb_model* model, const cdb_kv* kv, const cdb_sta
             ea.out = c.h;
             ea.ld_out = d.d;
             ea.err = c.err;
-            HIPCHK(launch_gemm(EPI_STORE, c.x, 2 * d.d, wptr(c, c.wl.adapter), M, c.gm.adapter, c.part, c.counters, ea,
-                               st));
+            HIPCHK(launch_gemm(EPI_STORE, c.x, wptr(c, c.wl.adapter), M, c.gm.adapter, c.part, ea, st));
         }
         KvTarget t = stage_target(d, *kv, 1);
         t.c_row = rows->c;
-        s = run_layers(c, d.n_prelude, d.n_core, t, *rows, st);
+        s = run_layers(c, d.n_prelude, d.n_core, t, *rows, false, st);
         if (s != CDB_OK) return s;
         HIPCHK(launch_exit(d, *rows, c.h, c.h_in, wptr(c, c.wl.w_exit), state->h, state->n_slots, *out, st));
     }
@@ -325,15 +319,35 @@ cdb_status cdb_boundary_coda(const cdb_model* model, const cdb_kv* kv, const cdb
     if (M == 0) return CDB_OK;
     Ctx c = make_ctx(model, ws, M);
     HIPCHK(launch_load_state(M, d.d, rows->slot, state->h, state->n_slots, c.h, c.err, st));
-    s = run_layers(c, d.n_prelude + d.n_core, d.n_coda, stage_target(d, *kv, 2), *rows, st);
+    s = run_layers(c, d.n_prelude + d.n_core, d.n_coda, stage_target(d, *kv, 2), *rows, true, st);
     if (s != CDB_OK) return s;
-    HIPCHK(launch_rmsnorm(c.h, M, d.d, d.rms_eps, c.x, d.d, st));
     EpiArgs ea{};
     ea.out = logits;
     ea.ld_out = d.vocab;
     ea.err = c.err;
-    HIPCHK(launch_gemm(EPI_STORE, c.x, d.d, wptr(c, c.wl.lm_head), M, c.gm.lm, c.part, c.counters, ea, st));
+    HIPCHK(launch_gemm(EPI_STORE, c.x, wptr(c, c.wl.lm_head), M, c.gm.lm, c.part, ea, st));
     HIPCHK(launch_argmax(M, d.vocab, logits, next_ids, st));
+    return CDB_OK;
+}
+
+cdb_status cdb_paged_attention(const cdb_model_desc* desc, const cdb_kv* kv, const cdb_rows* rows, int32_t stage,
+                               int32_t layer, const float* q, void* out, void* ws, size_t ws_bytes, hipStream_t st) {
+    if (!desc || !kv || !rows || !q || !out || !ws) return CDB_ERR_INVALID_ARG;
+    const cdb_model_desc& d = *desc;
+    if (!desc_supported(d)) return CDB_ERR_UNSUPPORTED;
+    if (stage < 0 || stage > 2 || rows->n_rows < 0) return CDB_ERR_INVALID_ARG;
+    const int layers = stage == 0 ? d.n_prelude : (stage == 1 ? d.n_core : d.n_coda);
+    if (layer < 0 || layer >= layers) return CDB_ERR_INVALID_ARG;
+    if (rows->n_rows > kMaxRows) return CDB_ERR_CAPACITY;
+    if (ws_bytes < 256) return CDB_ERR_CAPACITY;
+    if (rows->n_rows == 0) return CDB_OK;
+    if (!rows->seq || !rows->pos || (stage == 1 && !rows->c) || !kv->page_table) return CDB_ERR_INVALID_ARG;
+    KvTarget t = stage_target(d, *kv, stage);
+    if (!t.pool) return CDB_ERR_INVALID_ARG;
+    t.layer = layer;
+    if (stage == 1) t.c_row = rows->c;
+    HIPCHK(launch_attention(q, t, rows->seq, rows->pos, rows->n_rows, d.n_heads, d.head_dim,
+                            static_cast<uint16_t*>(out), static_cast<int*>(ws), st));
     return CDB_OK;
 }
 
@@ -345,7 +359,7 @@ cdb_status cdb_read_device_error(void* ws, hipStream_t st, int32_t* code) {
     *code = v;
     if (v != 0) {
         int* err = static_cast<int*>(ws);
-        if (launch_ws_init(err, err + 64, 0, st) != hipSuccess) return CDB_ERR_HIP;
+        if (launch_ws_init(err, st) != hipSuccess) return CDB_ERR_HIP;
         if (hipStreamSynchronize(st) != hipSuccess) return CDB_ERR_HIP;
     }
     return CDB_OK;

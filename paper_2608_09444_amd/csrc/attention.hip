@@ -12,7 +12,8 @@
 // DPP (quad_perm, half_mirror, mirror), and each row keeps its own online
 // softmax over the tokens it owns, so no cross-row traffic happens per page.
 // A workgroup of 4 waves takes one (row, head); wave w takes pages w, w+4, ...
-// The 16 partial (max, sum, acc) states are merged through LDS at the end.
+// The 16 partial (max, sum, acc) states are merged through LDS at the end; the
+// output is written in the fragment layout the output projection reads.
 #include "cdb_internal.h"
 
 namespace cdb {
@@ -139,7 +140,7 @@ __global__ __launch_bounds__(256) void k_attn(const float* __restrict__ q, KvTar
             num += w * s_acc[i][tid];
             den += w * s_l[i];
         }
-        out[(size_t)m * d + head * HD + tid] = f2bf(den > 0.f ? num / den : 0.f);
+        out[frag_index(m, head * HD + tid, d)] = f2bf(den > 0.f ? num / den : 0.f);
     }
 }
 

@@ -12,7 +12,6 @@ namespace cdb {
 
 constexpr int kPage = 16;       // tokens per KV page
 constexpr int kMaxRows = 256;   // rows per stage call (workspace and GEMM limit)
-constexpr int kCounters = 16384;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
@@ -30,11 +29,21 @@ __device__ __forceinline__ uint16_t f2bf(float f) {
     return (uint16_t)(u >> 16);
 }
 
+// Activations that feed a GEMM are stored in the B-operand fragment order of
+// v_mfma_f32_32x32x16_bf16 ("fragment layout"): element (m, k) of an [M][K]
+// matrix sits in 1 KiB tile (m/32, k/16), lane m%32 + 32*((k%16)/8), slot k%8,
+// tiles ordered row-tile-major.  A wave then fetches one operand with a single
+// contiguous 1 KiB load.  Buffers hold a multiple of 32 rows.
+__host__ __device__ __forceinline__ size_t frag_index(int m, int k, int K) {
+    return ((((size_t)(m >> 5) * (K >> 4) + (k >> 4)) * 64 + (m & 31) + 32 * ((k & 15) >> 3)) << 3) + (k & 7);
+}
+__host__ __device__ __forceinline__ int round32(int m) { return (m + 31) & ~31; }
+
 // First sticky error wins.
 __device__ __forceinline__ void set_err(int* err, int code) { atomicCAS(err, 0, code); }
 
 // ---------------------------------------------------------------- GEMM epilogues
-enum Epi : int { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_STORE = 3 };
+enum Epi : int { EPI_QKV = 0, EPI_PARTIAL = 1, EPI_SWIGLU = 2, EPI_STORE = 3 };
 
 // Where a stage's K/V lives and which rows write it.
 struct KvTarget {
@@ -49,10 +58,10 @@ struct KvTarget {
 };
 
 struct EpiArgs {
-    float* out;     // RESID: h (read-modify-write); STORE: destination
+    float* out;     // STORE: destination
     int ld_out;
-    uint16_t* act;  // SWIGLU output [M][F]
-    int ld_act;
+    uint16_t* act;  // SWIGLU output, fragment layout [M][F]
+    int ld_act;     // F
     float* q;       // QKV: q after RoPE [M][d]
     KvTarget kv;
     const int32_t* seq;
@@ -63,7 +72,7 @@ struct EpiArgs {
 };
 
 struct GemmShape {
-    int N, K, S;  // packed output columns, reduction length, K splits
+    int N, K, S, KW;  // packed output columns, reduction length, K splits over workgroups, waves per workgroup
 };
 
 // ---------------------------------------------------------------- layouts
@@ -75,19 +84,22 @@ struct WeightLayout {
 bool weight_layout(const cdb_model_desc& d, WeightLayout* out);
 
 struct WsLayout {
-    size_t err, counters, h, h_in, q, x, act, part, total;
+    size_t err, h, h_in, q, x, act, part, total;
 };
 WsLayout ws_layout(const cdb_model_desc& d, int rows);
 
-GemmShape gemm_shape(int N, int K);
+GemmShape gemm_shape(int N, int K, int epi);
 bool desc_supported(const cdb_model_desc& d);
 
 // ---------------------------------------------------------------- launchers
-hipError_t launch_gemm(int epi, const uint16_t* X, int ldx, const uint16_t* Wp, int M, GemmShape g, float* part,
-                       int* counters, const EpiArgs& ea, hipStream_t st);
+hipError_t launch_gemm(int epi, const uint16_t* X, const uint16_t* Wp, int M, GemmShape g, float* part,
+                       const EpiArgs& ea, hipStream_t st);
 hipError_t launch_attention(const float* q, const KvTarget& kv, const int32_t* seq, const int32_t* pos, int M,
                             int H, int hd, uint16_t* out, int* err, hipStream_t st);
-hipError_t launch_rmsnorm(const float* h, int M, int d, float eps, uint16_t* out, int ldo, hipStream_t st);
+// h[i] += sum over s < S of part[s][i] (split order), then, when out is set,
+// out = bf16(RMSNorm(h)) in fragment layout.
+hipError_t launch_resid_norm(float* h, const float* part, int S, int M, int d, float eps, uint16_t* out,
+                             hipStream_t st);
 hipError_t launch_gather(const cdb_model_desc& md, const cdb_state& s, const cdb_rows& r, const cdb_kv& kv,
                          float* h, float* h_in, uint16_t* xcat, int* err, hipStream_t st);
 hipError_t launch_embed(const cdb_model_desc& md, const uint16_t* embed, const int32_t* tokens, const cdb_rows& r,
@@ -106,7 +118,7 @@ hipError_t launch_argmax(int M, int V, const float* logits, int32_t* ids, hipStr
 hipError_t launch_pack(int kind, const uint16_t* a, const uint16_t* b, const uint16_t* c, int N, int K, int hd,
                        uint16_t* dst, hipStream_t st);
 hipError_t launch_copy_bf16(const uint16_t* src, size_t n, uint16_t* dst, hipStream_t st);
-hipError_t launch_ws_init(int* err, int* counters, int n, hipStream_t st);
+hipError_t launch_ws_init(int* err, hipStream_t st);
 
 enum PackKind : int { PACK_PLAIN = 0, PACK_QKV = 1, PACK_GU = 2 };
 

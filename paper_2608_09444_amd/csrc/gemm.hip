@@ -3,253 +3,222 @@
 // HBM exactly once per call.
 //
 // Design (gfx950):
-//  * W is pre-packed into 16x32 MFMA operand tiles (1 KiB each) in lane order,
-//    so one global_load_dwordx4 per lane fetches a full A operand of
-//    v_mfma_f32_16x16x32_bf16, perfectly coalesced.  Tiles of one 16-column
-//    stripe are contiguous along K.
-//  * A workgroup of 4 waves owns 64 output columns (one 16-column stripe per
-//    wave) and one K split.  The wave loads all its W tiles of the split into
-//    registers up front (<= 16 tiles in flight), then runs over the rows in
-//    chunks of 64: the chunk of X is staged in LDS once and read as the B
-//    operand by all four waves.
-//  * K splits are combined deterministically: each split writes fp32 partial
-//    sums, and the last workgroup of a column tile to arrive (device-scope
-//    counter) adds the partials in split order 0..S-1 and runs the fused
-//    epilogue.  The split count depends on (N, K) only, so a row's result does
-//    not depend on which other rows share the batch.
-//  * Epilogues: q/k/v with RoPE and the K/V page write; residual add into the
-//    fp32 stream; SwiGLU; plain store (adapter, LM head).
+//  * W is pre-packed into 32x16 operand tiles of v_mfma_f32_32x32x16_bf16 in
+//    lane order (1 KiB each), so one 16-byte load per lane fetches a whole A
+//    operand, coalesced; the tiles of one 32-column stripe are contiguous
+//    along K.  A 32-wide stripe halves the activation (B operand) traffic per
+//    weight byte compared with a 16-wide one.
+//  * A workgroup owns one 32-column stripe and one K split; its KW waves split
+//    that K range further.  Each wave issues the loads of (up to 16) weight
+//    tiles up front, and streams the activation fragments (L2-resident) two
+//    steps ahead.  The KW partial tiles are summed in LDS in wave order.
+//  * No reduction crosses workgroups inside the kernel.  Stripes whose K is
+//    split over S workgroups write fp32 partial tiles; the row kernel that
+//    runs next (residual add + RMSNorm) adds them in split order.  Every
+//    reduction order depends on (N, K) only, so a row's result does not depend
+//    on which other rows share the batch.
+//  * Epilogues: q/k/v with RoPE and the K/V page write (a 32-column group is
+//    16 first-half and the 16 matching second-half dims of one head), SwiGLU (a
+//    group is 16 gate and the 16 matching up columns), plain fp32 store, and
+//    the split-K partial store.
 #include "cdb_internal.h"
 
 namespace cdb {
 
-constexpr int kWaves = 4;
-constexpr int kTileN = 64;    // output columns per workgroup
-constexpr int kChunkM = 64;   // rows per LDS chunk
-constexpr int kMaxKt = 16;    // 32-wide K tiles per split held in registers
-constexpr int kFtileLd = kTileN + 4;
+typedef float floatx16 __attribute__((ext_vector_type(16)));
 
-__device__ __forceinline__ void epilogue(int epi, const float* ft, int m0, int M, int n_base, int N,
-                                         const EpiArgs& ea) {
-    const int tid = threadIdx.x;
-    const int nl = tid & 63;
-    const int p = n_base + nl;
-    if (p >= N) return;
-    for (int r = tid >> 6; r < kChunkM; r += 4) {
-        const int m = m0 + r;
-        if (m >= M) break;
-        const float val = ft[r * kFtileLd + nl];
-        if (epi == EPI_RESID) {
-            ea.out[(size_t)m * ea.ld_out + p] += val;
-        } else if (epi == EPI_STORE) {
-            ea.out[(size_t)m * ea.ld_out + p] = val;
-        } else if (epi == EPI_SWIGLU) {
-            // packed order: groups of 32 columns = 16 gate columns then the 16
-            // matching up columns
-            if (p & 16) continue;
-            const float g = val, u = ft[r * kFtileLd + (nl ^ 16)];
-            const int f = (p >> 5) * 16 + (p & 15);
-            const float s = g / (1.0f + __expf(-g));
-            ea.act[(size_t)m * ea.ld_act + f] = f2bf(s * u);
-        } else {  // EPI_QKV
-            // packed order: groups of 32 columns per (part, head, 16 pairs):
-            // 16 first-half dims j then the 16 second-half dims j + hd/2
-            const int g = p >> 5, w = p & 31, half = w >> 4, jj = w & 15;
-            const int gph = ea.hd >> 5;  // groups per head
-            const int hg = ea.H * gph;
-            const int part = g / hg, rem = g - part * hg;
-            const int head = rem / gph, gi = rem - head * gph;
-            const int j = gi * 16 + jj;
-            const int dim = j + half * (ea.hd >> 1);
-            float outv = val;
-            if (part < 2) {
-                const float partner = ft[r * kFtileLd + (nl ^ 16)];
-                const double ang = (double)ea.pos[m] * pow((double)ea.rope_base, -2.0 * j / ea.hd);
-                double sn, cs;
-                sincos(ang, &sn, &cs);
-                const float c = (float)cs, s = (float)sn;
-                const float xf = half ? partner : val, xs = half ? val : partner;
-                outv = half ? (xs * c + xf * s) : (xf * c - xs * s);
-            }
-            if (part == 0) {
-                ea.q[(size_t)m * (ea.H * ea.hd) + head * ea.hd + dim] = outv;
-            } else {
-                const KvTarget& kv = ea.kv;
-                const int sq = ea.seq[m], ps = ea.pos[m];
-                const int plane = kv.c_row ? kv.c_row[m] + 1 : kv.plane_fixed;
-                const int pg = ps / kPage;
-                int pid = -1;
-                if (sq >= 0 && sq < kv.max_seqs && pg >= 0 && pg < kv.max_pages && plane >= 0 && plane < kv.n_planes)
-                    pid = kv.page_table[((size_t)sq * kv.n_planes + plane) * kv.max_pages + pg];
-                if (pid < 0 || pid >= kv.n_pages) {
-                    set_err(ea.err, CDB_DEV_UNMAPPED_PAGE);
-                    continue;
-                }
-                const size_t page_elems = (size_t)kv.n_layers * 2 * ea.H * kPage * ea.hd;
-                const size_t off = (size_t)pid * page_elems +
-                                   ((((size_t)kv.layer * 2 + (part - 1)) * ea.H + head) * kPage + (ps % kPage)) * ea.hd +
-                                   dim;
-                kv.pool[off] = f2bf(outv);
-            }
+constexpr int kMaxKw = 8;     // waves per workgroup (2 per SIMD, so 256 registers each)
+
+struct GemmArgs {
+    const uint16_t* X;  // fragment layout, round32(M) rows, K columns
+    const uint16_t* Wp;
+    int M, N, K, S, KW;
+    float* part;  // EPI_PARTIAL: [S][M][N]
+};
+
+template <int EPI>
+__device__ __forceinline__ void epilogue_elem(float val, float partner, int m, int p, const GemmArgs& ga,
+                                              const EpiArgs& ea) {
+    if (EPI == EPI_STORE) {
+        ea.out[(size_t)m * ea.ld_out + p] = val;
+    } else if (EPI == EPI_PARTIAL) {
+        ga.part[((size_t)blockIdx.y * ga.M + m) * ga.N + p] = val;
+    } else if (EPI == EPI_SWIGLU) {
+        if (p & 16) return;
+        const int f = (p >> 5) * 16 + (p & 15);
+        const float s = val / (1.0f + __expf(-val));
+        ea.act[frag_index(m, f, ea.ld_act)] = f2bf(s * partner);
+    } else {  // EPI_QKV
+        const int g = p >> 5, w = p & 31, half = w >> 4, jj = w & 15;
+        const int gph = ea.hd >> 5;  // groups per head
+        const int hg = ea.H * gph;
+        const int part = g / hg, rem = g - part * hg;
+        const int head = rem / gph, gi = rem - head * gph;
+        const int j = gi * 16 + jj;
+        const int dim = j + half * (ea.hd >> 1);
+        float outv = val;
+        if (part < 2) {
+            const double ang = (double)ea.pos[m] * pow((double)ea.rope_base, -2.0 * j / ea.hd);
+            double sn, cs;
+            sincos(ang, &sn, &cs);
+            const float c = (float)cs, s = (float)sn;
+            const float xf = half ? partner : val, xs = half ? val : partner;
+            outv = half ? (xs * c + xf * s) : (xf * c - xs * s);
         }
+        if (part == 0) {
+            ea.q[(size_t)m * (ea.H * ea.hd) + head * ea.hd + dim] = outv;
+            return;
+        }
+        const KvTarget& kv = ea.kv;
+        const int sq = ea.seq[m], ps = ea.pos[m];
+        const int plane = kv.c_row ? kv.c_row[m] + 1 : kv.plane_fixed;
+        const int pg = ps / kPage;
+        int pid = -1;
+        if (sq >= 0 && sq < kv.max_seqs && pg >= 0 && pg < kv.max_pages && plane >= 0 && plane < kv.n_planes)
+            pid = kv.page_table[((size_t)sq * kv.n_planes + plane) * kv.max_pages + pg];
+        if (pid < 0 || pid >= kv.n_pages) {
+            set_err(ea.err, CDB_DEV_UNMAPPED_PAGE);
+            return;
+        }
+        const size_t page_elems = (size_t)kv.n_layers * 2 * ea.H * kPage * ea.hd;
+        const size_t off = (size_t)pid * page_elems +
+                           ((((size_t)kv.layer * 2 + (part - 1)) * ea.H + head) * kPage + (ps % kPage)) * ea.hd + dim;
+        kv.pool[off] = f2bf(outv);
     }
 }
 
-template <int EPI>
-__global__ __launch_bounds__(256) void k_gemm(const uint16_t* __restrict__ X, int ldx, const uint16_t* __restrict__ Wp,
-                                              int M, int N, int K, int S, float* __restrict__ part,
-                                              int* __restrict__ counters, EpiArgs ea) {
-    extern __shared__ __align__(16) unsigned char smem[];
-    __shared__ int s_last;
+// MT = 32-row tiles of M covered by one pass (M <= 32 * MT).
+template <int EPI, int MT>
+__global__ __launch_bounds__(512) void k_gemm(GemmArgs ga, EpiArgs ea) {
+    extern __shared__ __align__(16) float smem[];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int KT = K >> 5;
+    const int KW = ga.KW;
+    const int KS = ga.K >> 4;  // 16-wide k steps
     const int s = blockIdx.y;
-    const int kt0 = (int)(((long)s * KT) / S), kt1 = (int)(((long)(s + 1) * KT) / S);
-    const int nk = kt1 - kt0;
-    const int n_base = blockIdx.x * kTileN;
-    const int nt = blockIdx.x * kWaves + wave;  // 16-column stripe of this wave
-    const bool wave_ok = nt * 16 < N;
+    const int a0 = (int)(((long)s * KS) / ga.S), a1 = (int)(((long)(s + 1) * KS) / ga.S);
+    const int ks0 = a0 + (int)(((long)wave * (a1 - a0)) / KW);
+    const int ks1 = a0 + (int)(((long)(wave + 1) * (a1 - a0)) / KW);
+    const int nt = blockIdx.x;  // 32-column stripe
+    const int M = ga.M;
 
-    // all W operand tiles of this split, straight into registers
-    u32x4 wf[kMaxKt];
-    if (wave_ok) {
-        const u32x4* src = reinterpret_cast<const u32x4*>(Wp) + ((size_t)nt * KT + kt0) * 64 + lane;
+    floatx16 acc[MT];
 #pragma unroll
-        for (int i = 0; i < kMaxKt; ++i)
-            if (i < nk) wf[i] = __builtin_nontemporal_load(src + (size_t)i * 64);
-    }
+    for (int t = 0; t < MT; ++t)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) acc[t][j] = 0.f;
 
-    uint16_t* xs = reinterpret_cast<uint16_t*>(smem);
-    float* ft = reinterpret_cast<float*>(smem);
-    const int xld = nk * 32 + 8;  // LDS row stride (elements), padded against bank conflicts
+    const u32x4* wsrc = reinterpret_cast<const u32x4*>(ga.Wp) + (size_t)nt * KS * 64 + lane;
+    // X is in fragment layout: the operand of m-tile t at k step k is the 1 KiB tile (t, k)
+    const u32x4* xsrc = reinterpret_cast<const u32x4*>(ga.X) + lane;
+    constexpr int CH = MT <= 2 ? 8 : (MT == 4 ? 4 : 2);  // k steps whose loads are all in flight together
 
-    for (int m0 = 0; m0 < M; m0 += kChunkM) {
-        __syncthreads();
-        // stage X[m0 .. m0+64)[kt0*32 .. kt1*32) in LDS, 16 bytes per thread-step
-        const int vec_per_row = nk * 4;
-        for (int v = tid; v < kChunkM * vec_per_row; v += 256) {
-            const int r = v / vec_per_row, cv = v - r * vec_per_row;
-            uint4 val = make_uint4(0, 0, 0, 0);
-            if (m0 + r < M) val = *reinterpret_cast<const uint4*>(X + (size_t)(m0 + r) * ldx + kt0 * 32 + cv * 8);
-            *reinterpret_cast<uint4*>(xs + r * xld + cv * 8) = val;
-        }
-        __syncthreads();
-        floatx4 acc[4];
+    for (int c0 = ks0; c0 < ks1; c0 += CH) {
+        const int n = min(CH, ks1 - c0);
+        u32x4 wf[CH];
+        u32x4 xf[CH][MT];
 #pragma unroll
-        for (int mt = 0; mt < 4; ++mt) acc[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
-        if (wave_ok) {
+        for (int i = 0; i < CH; ++i) {
+            if (i < n) {
+                wf[i] = __builtin_nontemporal_load(wsrc + (size_t)(c0 + i) * 64);
 #pragma unroll
-            for (int i = 0; i < kMaxKt; ++i) {
-                if (i < nk) {
-                    const bf16x8 a = __builtin_bit_cast(bf16x8, wf[i]);
-#pragma unroll
-                    for (int mt = 0; mt < 4; ++mt) {
-                        const uint4 bv = *reinterpret_cast<const uint4*>(xs + (mt * 16 + (lane & 15)) * xld + i * 32 +
-                                                                         (lane >> 4) * 8);
-                        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, __builtin_bit_cast(bf16x8, bv), acc[mt],
-                                                                          0, 0, 0);
-                    }
+                for (int t = 0; t < MT; ++t) {
+                    u32x4 v = {0u, 0u, 0u, 0u};
+                    if (t * 32 < M) v = xsrc[((size_t)t * KS + c0 + i) * 64];  // buffers hold round32(M) rows
+                    xf[i][t] = v;
                 }
             }
         }
-        // lane holds D[n = 4*(lane/16) + j][m = lane%16] of each 16x16 tile
-        const int ncol = nt * 16 + 4 * (lane >> 4);
-        if (S == 1) {
-            __syncthreads();  // xs is about to be overwritten by the output tile
-            if (wave_ok) {
 #pragma unroll
-                for (int mt = 0; mt < 4; ++mt)
+        for (int i = 0; i < CH; ++i) {
+            if (i < n) {
+                const bf16x8 a = __builtin_bit_cast(bf16x8, wf[i]);
 #pragma unroll
-                    for (int j = 0; j < 4; ++j)
-                        ft[(mt * 16 + (lane & 15)) * kFtileLd + wave * 16 + 4 * (lane >> 4) + j] = acc[mt][j];
-            }
-            __syncthreads();
-            epilogue(EPI, ft, m0, M, n_base, N, ea);
-        } else if (wave_ok) {
-#pragma unroll
-            for (int mt = 0; mt < 4; ++mt) {
-                const int m = m0 + mt * 16 + (lane & 15);
-                if (m < M)
-                    *reinterpret_cast<float4*>(part + ((size_t)s * M + m) * N + ncol) =
-                        make_float4(acc[mt][0], acc[mt][1], acc[mt][2], acc[mt][3]);
+                for (int t = 0; t < MT; ++t)
+                    acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, __builtin_bit_cast(bf16x8, xf[i][t]), acc[t], 0,
+                                                                     0, 0);
             }
         }
     }
-    if (S == 1) return;
 
-    // split-K: the last workgroup of this column tile sums the partials in order
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) {
-        const int old = atomicAdd(&counters[blockIdx.x], 1);
-        s_last = (old == S - 1);
-    }
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-    for (int m0 = 0; m0 < M; m0 += kChunkM) {
-        __syncthreads();
-        for (int v = tid; v < kChunkM * (kTileN / 4); v += 256) {
-            const int r = v / (kTileN / 4), c4 = (v - r * (kTileN / 4)) * 4;
-            const int m = m0 + r, n = n_base + c4;
-            float4 sum = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (m < M && n < N) {
-                for (int ss = 0; ss < S; ++ss) {
-                    const floatx4 pv = __builtin_nontemporal_load(
-                        reinterpret_cast<const floatx4*>(part + ((size_t)ss * M + m) * N + n));
-                    sum.x += pv[0];
-                    sum.y += pv[1];
-                    sum.z += pv[2];
-                    sum.w += pv[3];
-                }
-            }
-            *reinterpret_cast<float4*>(ft + r * kFtileLd + c4) = sum;
+    // Sum the KW wave tiles in wave order, one 32x32 m-tile at a time.
+    // acc[t][j] holds D[n = (j/4)*8 + (lane/32)*4 + j%4][m = t*32 + lane%32].
+    float* red = smem;                    // [KW][32 n][32 m]
+    float* fin = smem + KW * 1024;        // [32 n][MT*32 m + 1]
+    const int fld = MT * 32 + 1;
+#pragma unroll
+    for (int t = 0; t < MT; ++t) {
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const int nn = (j >> 2) * 8 + (lane >> 5) * 4 + (j & 3);
+            red[wave * 1024 + nn * 32 + (lane & 31)] = acc[t][j];
         }
         __syncthreads();
-        epilogue(EPI, ft, m0, M, n_base, N, ea);
+        for (int e = tid; e < 1024; e += KW * 64) {
+            float sum = 0.f;
+            for (int w = 0; w < KW; ++w) sum += red[w * 1024 + e];
+            fin[(e >> 5) * fld + t * 32 + (e & 31)] = sum;
+        }
+        __syncthreads();
     }
-    if (tid == 0) atomicExch(&counters[blockIdx.x], 0);
+
+    // epilogue: element (n, m) of the stripe; consecutive threads take consecutive n
+    const int mcap = min(M, MT * 32);
+    for (int e = tid; e < 32 * mcap; e += KW * 64) {
+        const int m = e >> 5, nn = e & 31;
+        const int p = nt * 32 + nn;
+        const float val = fin[nn * fld + m];
+        const float partner = fin[(nn ^ 16) * fld + m];
+        epilogue_elem<EPI>(val, partner, m, p, ga, ea);
+    }
 }
 
-GemmShape gemm_shape(int N, int K) {
-    const int tiles = (N + kTileN - 1) / kTileN;
-    const int KT = K / 32;
-    int S = (512 + tiles - 1) / tiles;
-    if (S > KT / 4) S = KT / 4;
-    const int smin = (KT + kMaxKt - 1) / kMaxKt;
-    if (S < smin) S = smin;
-    if (S < 1) S = 1;
-    return GemmShape{N, K, S};
+GemmShape gemm_shape(int N, int K, int epi) {
+    const int stripes = N / 32;
+    const int KS = K / 16;
+    int S = 1;
+    if (epi == EPI_PARTIAL) {
+        while (stripes * S < 256 && KS / (S * 2) >= 32) S *= 2;
+    }
+    // enough waves that each streams about one chunk of k steps
+    const int ch = 8;
+    int KW = 4;
+    while (KW < kMaxKw && (KS / S + KW - 1) / KW > ch) KW *= 2;
+    return GemmShape{N, K, S, KW};
 }
 
-template <int EPI>
-static hipError_t launch_one(const uint16_t* X, int ldx, const uint16_t* Wp, int M, GemmShape g, float* part,
-                             int* counters, const EpiArgs& ea, hipStream_t st) {
+template <int EPI, int MT>
+static hipError_t launch_mt(const GemmArgs& ga, const EpiArgs& ea, hipStream_t st) {
     static bool attr_set = false;
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm<EPI>),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, 96 * 1024);
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm<EPI, MT>),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
-    const int KT = g.K / 32;
-    const int nk_max = (KT + g.S - 1) / g.S;
-    size_t lds = (size_t)kChunkM * (nk_max * 32 + 8) * 2;
-    const size_t lds_ft = (size_t)kChunkM * kFtileLd * 4;
-    if (lds < lds_ft) lds = lds_ft;
-    dim3 grid((g.N + kTileN - 1) / kTileN, g.S);
-    k_gemm<EPI><<<grid, 256, lds, st>>>(X, ldx, Wp, M, g.N, g.K, g.S, part, counters, ea);
+    const size_t lds = ((size_t)ga.KW * 1024 + 32 * (MT * 32 + 1)) * 4;
+    dim3 grid(ga.N / 32, ga.S);
+    k_gemm<EPI, MT><<<grid, ga.KW * 64, lds, st>>>(ga, ea);
     return hipGetLastError();
 }
 
-hipError_t launch_gemm(int epi, const uint16_t* X, int ldx, const uint16_t* Wp, int M, GemmShape g, float* part,
-                       int* counters, const EpiArgs& ea, hipStream_t st) {
+template <int EPI>
+static hipError_t launch_epi(const GemmArgs& ga, const EpiArgs& ea, hipStream_t st) {
+    if (ga.M <= 32) return launch_mt<EPI, 1>(ga, ea, st);
+    if (ga.M <= 64) return launch_mt<EPI, 2>(ga, ea, st);
+    if (ga.M <= 128) return launch_mt<EPI, 4>(ga, ea, st);
+    return launch_mt<EPI, 8>(ga, ea, st);
+}
+
+hipError_t launch_gemm(int epi, const uint16_t* X, const uint16_t* Wp, int M, GemmShape g, float* part,
+                       const EpiArgs& ea, hipStream_t st) {
     if (M <= 0) return hipSuccess;
+    if (M > kMaxRows || g.N % 32 || g.K % 16 || g.KW < 1 || g.KW > kMaxKw) return hipErrorInvalidValue;
+    GemmArgs ga{X, Wp, M, g.N, g.K, g.S, g.KW, part};
     switch (epi) {
-        case EPI_QKV: return launch_one<EPI_QKV>(X, ldx, Wp, M, g, part, counters, ea, st);
-        case EPI_RESID: return launch_one<EPI_RESID>(X, ldx, Wp, M, g, part, counters, ea, st);
-        case EPI_SWIGLU: return launch_one<EPI_SWIGLU>(X, ldx, Wp, M, g, part, counters, ea, st);
-        default: return launch_one<EPI_STORE>(X, ldx, Wp, M, g, part, counters, ea, st);
+        case EPI_QKV: return launch_epi<EPI_QKV>(ga, ea, st);
+        case EPI_SWIGLU: return launch_epi<EPI_SWIGLU>(ga, ea, st);
+        case EPI_PARTIAL: return launch_epi<EPI_PARTIAL>(ga, ea, st);
+        default: return launch_epi<EPI_STORE>(ga, ea, st);
     }
 }
 

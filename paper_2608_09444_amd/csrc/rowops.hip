@@ -38,11 +38,15 @@ __global__ __launch_bounds__(256) void k_gather(int d, int r_max, int n_slots, i
         float4 v = ok ? *reinterpret_cast<const float4*>(sh + (size_t)sl * d + k) : make_float4(0.f, 0.f, 0.f, 0.f);
         *reinterpret_cast<float4*>(h + (size_t)i * d + k) = v;
         *reinterpret_cast<float4*>(h_in + (size_t)i * d + k) = v;
-        if (xcat) {
+        if (xcat) {  // adapter input [h; e], fragment layout with K = 2d
             float4 e = ok ? *reinterpret_cast<const float4*>(se + (size_t)sl * d + k) : make_float4(0.f, 0.f, 0.f, 0.f);
-            uint16_t* x = xcat + (size_t)i * 2 * d;
-            x[k] = f2bf(v.x); x[k + 1] = f2bf(v.y); x[k + 2] = f2bf(v.z); x[k + 3] = f2bf(v.w);
-            x[d + k] = f2bf(e.x); x[d + k + 1] = f2bf(e.y); x[d + k + 2] = f2bf(e.z); x[d + k + 3] = f2bf(e.w);
+            uint2 ph, pe;
+            ph.x = (uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16);
+            ph.y = (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16);
+            pe.x = (uint32_t)f2bf(e.x) | ((uint32_t)f2bf(e.y) << 16);
+            pe.y = (uint32_t)f2bf(e.z) | ((uint32_t)f2bf(e.w) << 16);
+            *reinterpret_cast<uint2*>(xcat + frag_index(i, k, 2 * d)) = ph;
+            *reinterpret_cast<uint2*>(xcat + frag_index(i, d + k, 2 * d)) = pe;
         }
     }
 }
@@ -59,27 +63,36 @@ __global__ __launch_bounds__(256) void k_load_state(int d, int n_slots, const in
             ok ? *reinterpret_cast<const float4*>(sh + (size_t)sl * d + k) : make_float4(0.f, 0.f, 0.f, 0.f);
 }
 
-// ------------------------------------------------------------------ RMSNorm
-// out[i] = bf16(h[i] / sqrt(mean(h[i]^2) + eps)), unit gains
-__global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ h, int d, float eps,
-                                                 uint16_t* __restrict__ out, int ldo) {
+// ------------------------------------------------------------------ residual + RMSNorm
+// h[i] += sum_s part[s][i] (split order 0..S-1); out[i] = bf16(h[i] / sqrt(mean(h[i]^2) + eps)),
+// unit gains.  Row i is one workgroup.
+__global__ __launch_bounds__(256) void k_resid_norm(float* __restrict__ h, const float* __restrict__ part, int S, int M,
+                                                    int d, float eps, uint16_t* __restrict__ out) {
     __shared__ float red[4];
     const int i = blockIdx.x;
-    const float* x = h + (size_t)i * d;
+    float* x = h + (size_t)i * d;
     float ss = 0.f;
     for (int k = threadIdx.x * 4; k < d; k += 1024) {
-        const float4 v = *reinterpret_cast<const float4*>(x + k);
+        float4 v = *reinterpret_cast<const float4*>(x + k);
+        for (int s = 0; s < S; ++s) {
+            const float4 p = *reinterpret_cast<const float4*>(part + ((size_t)s * M + i) * d + k);
+            v.x += p.x;
+            v.y += p.y;
+            v.z += p.z;
+            v.w += p.w;
+        }
+        if (S > 0) *reinterpret_cast<float4*>(x + k) = v;
         ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
     }
+    if (!out) return;
     ss = block_sum(ss, red);
     const float inv = 1.0f / sqrtf(ss / d + eps);
-    uint16_t* o = out + (size_t)i * ldo;
     for (int k = threadIdx.x * 4; k < d; k += 1024) {
         const float4 v = *reinterpret_cast<const float4*>(x + k);
         uint2 pk;
         pk.x = (uint32_t)f2bf(v.x * inv) | ((uint32_t)f2bf(v.y * inv) << 16);
         pk.y = (uint32_t)f2bf(v.z * inv) | ((uint32_t)f2bf(v.w * inv) << 16);
-        *reinterpret_cast<uint2*>(o + k) = pk;
+        *reinterpret_cast<uint2*>(out + frag_index(i, k, d)) = pk;  // 4 consecutive k share one 8-slot run
     }
 }
 
@@ -277,18 +290,19 @@ __global__ __launch_bounds__(256) void k_argmax(int V, const float* __restrict__
 }
 
 // ------------------------------------------------------------------ packing
-// dst tile (nt, kt), lane l, element e  <-  row r(nt*16 + l%16), column kt*32 + 8*(l/16) + e
+// dst tile (nt, ks), lane l, element e  <-  row r(nt*32 + l%32), column ks*16 + 8*(l/32) + e
+// (A operand of v_mfma_f32_32x32x16_bf16, tiles of a 32-column stripe contiguous along K)
 __global__ __launch_bounds__(256) void k_pack(int kind, const uint16_t* __restrict__ A, const uint16_t* __restrict__ B,
                                               const uint16_t* __restrict__ Cm, int N, int K, int hd, int H,
                                               uint16_t* __restrict__ dst) {
-    const size_t KT = K / 32;
-    const size_t total = (size_t)(N / 16) * KT * 64;
+    const size_t KS = K / 16;
+    const size_t total = (size_t)(N / 32) * KS * 64;
     for (size_t t = (size_t)blockIdx.x * 256 + threadIdx.x; t < total; t += (size_t)gridDim.x * 256) {
         const int lane = (int)(t & 63);
         const size_t tile = t >> 6;
-        const int nt = (int)(tile / KT), kt = (int)(tile % KT);
-        const int p = nt * 16 + (lane & 15);
-        const int k = kt * 32 + 8 * (lane >> 4);
+        const int nt = (int)(tile / KS), ks = (int)(tile % KS);
+        const int p = nt * 32 + (lane & 31);
+        const int k = ks * 16 + 8 * (lane >> 5);
         const uint16_t* src;
         int row;
         if (kind == PACK_QKV) {
@@ -314,9 +328,8 @@ __global__ void k_copy16(const uint16_t* __restrict__ s, size_t n, uint16_t* __r
     for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256) d[i] = s[i];
 }
 
-__global__ void k_ws_init(int* err, int* counters, int n) {
-    for (int i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) counters[i] = 0;
-    if (blockIdx.x == 0 && threadIdx.x == 0) *err = 0;
+__global__ void k_ws_init(int* err) {
+    if (threadIdx.x == 0) *err = 0;
 }
 
 // ------------------------------------------------------------------ launchers
@@ -337,9 +350,10 @@ hipError_t launch_load_state(int M, int d, const int32_t* slot, const float* sta
     return hipGetLastError();
 }
 
-hipError_t launch_rmsnorm(const float* h, int M, int d, float eps, uint16_t* out, int ldo, hipStream_t st) {
+hipError_t launch_resid_norm(float* h, const float* part, int S, int M, int d, float eps, uint16_t* out,
+                             hipStream_t st) {
     if (M <= 0) return hipSuccess;
-    k_rmsnorm<<<M, 256, 0, st>>>(h, d, eps, out, ldo);
+    k_resid_norm<<<M, 256, 0, st>>>(h, part, S, M, d, eps, out);
     return hipGetLastError();
 }
 
@@ -407,8 +421,8 @@ hipError_t launch_copy_bf16(const uint16_t* src, size_t n, uint16_t* dst, hipStr
     return hipGetLastError();
 }
 
-hipError_t launch_ws_init(int* err, int* counters, int n, hipStream_t st) {
-    k_ws_init<<<64, 256, 0, st>>>(err, counters, n);
+hipError_t launch_ws_init(int* err, hipStream_t st) {
+    k_ws_init<<<1, 64, 0, st>>>(err);
     return hipGetLastError();
 }
 

@@ -20,7 +20,7 @@ def declared_functions():
 
 def test_library_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 9
+    assert len(names) == 10
     assert set(names) == set(cdb.EXPORTED)
     L = cdb.lib()
     for n in names:
