@@ -15,31 +15,38 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "liboracle.so")
+LIB32_PATH = os.path.join(_HERE, "liboracle_acc32.so")
 _SRC = os.path.join(_HERE, "cdb_oracle.c")
 
 ORC_OK, ORC_ERR_ARG, ORC_ERR_UNMAPPED = 0, 1, 2
 
 
 def build(force: bool = True) -> str:
-    """Compile the oracle with gcc (plain C, OpenMP over independent rows)."""
-    if force or not os.path.exists(LIB_PATH):
-        tmp = LIB_PATH + ".tmp"
-        subprocess.check_call(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-Wall", "-o", tmp, _SRC, "-lm"])
-        os.replace(tmp, LIB_PATH)
+    """Compile the oracle with gcc (plain C, OpenMP over independent rows): the
+    fp64 oracle, and the same source with fp32 accumulators (used only to size
+    tolerances)."""
+    for path, extra in ((LIB_PATH, []), (LIB32_PATH, ["-DORC_ACC=float"])):
+        if force or not os.path.exists(path):
+            tmp = path + ".tmp"
+            subprocess.check_call(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-Wall", *extra, "-o", tmp, _SRC,
+                                   "-lm"])
+            os.replace(tmp, path)
     return LIB_PATH
 
 
-_lib = None
+_libs = {}
 
 
-def lib():
-    global _lib
-    if _lib is None:
-        if not os.path.exists(LIB_PATH) or os.path.getmtime(LIB_PATH) < os.path.getmtime(_SRC):
+def lib(acc32: bool = False):
+    key = bool(acc32)
+    if key not in _libs:
+        path = LIB32_PATH if acc32 else LIB_PATH
+        if not os.path.exists(path) or os.path.getmtime(path) < os.path.getmtime(_SRC):
             build()
-        _lib = C.CDLL(LIB_PATH)
-        _declare(_lib)
-    return _lib
+        L = C.CDLL(path)
+        _declare(L)
+        _libs[key] = L
+    return _libs[key]
 
 
 class OrcDesc(C.Structure):
@@ -95,8 +102,10 @@ class Model:
     """Oracle model: a shape (cdbgen.ModelShape), bf16-bit weights, and the
     storage mode (bf16_storage=True rounds what the model keeps in bf16)."""
 
-    def __init__(self, shape, weights: Dict[str, object], bf16_storage: bool = True):
+    def __init__(self, shape, weights: Dict[str, object], bf16_storage: bool = True, acc32: bool = False):
+        """acc32: run the same steps with fp32 accumulators (tolerance sizing only)."""
         self.shape = shape
+        self.L = lib(acc32)
         self.desc = OrcDesc(shape.d, shape.n_heads, shape.head_dim, shape.d_ff, shape.vocab, shape.n_prelude,
                             shape.n_core, shape.n_coda, shape.r_max, shape.injection, shape.exit_kind,
                             1 if bf16_storage else 0, shape.rms_eps, shape.rope_base)
@@ -130,7 +139,7 @@ class Model:
         h = np.zeros((T, s.d))
         scores = np.zeros((T, s.r_max))
         kv = np.zeros((T, s.r_max, s.n_core, 2, s.d)) if want_kv else None
-        rc = lib().orc_ref_sequence(C.byref(self.desc), C.byref(self.w), T, _ptr(tok), n_given, _ptr(dep),
+        rc = self.L.orc_ref_sequence(C.byref(self.desc), C.byref(self.w), T, _ptr(tok), n_given, _ptr(dep),
                                     _ptr(logits), _ptr(h), _ptr(scores), _ptr(kv))
         if rc != ORC_OK:
             raise ValueError(f"orc_ref_sequence: {rc}")
@@ -144,7 +153,7 @@ class Model:
         logits = np.zeros((T, s.vocab))
         h = np.zeros((T, s.d))
         scores = np.zeros((T, s.r_max))
-        rc = lib().orc_brute_force(C.byref(self.desc), C.byref(self.w), T, _ptr(tok), _ptr(dep), _ptr(logits),
+        rc = self.L.orc_brute_force(C.byref(self.desc), C.byref(self.w), T, _ptr(tok), _ptr(dep), _ptr(logits),
                                    _ptr(h), _ptr(scores))
         if rc != ORC_OK:
             raise ValueError(f"orc_brute_force: {rc}")
@@ -182,7 +191,7 @@ class Paged:
 
 def prelude(model: Model, paged: Paged, state_h, state_e, slot, seq, pos, tokens):
     n = len(slot)
-    rc = lib().orc_prelude(C.byref(model.desc), C.byref(model.w), C.byref(paged.c), _ptr(state_h),
+    rc = model.L.orc_prelude(C.byref(model.desc), C.byref(model.w), C.byref(paged.c), _ptr(state_h),
                            _ptr(state_e), state_h.shape[0], n, _ptr(_c(slot, np.int32)), _ptr(_c(seq, np.int32)),
                            _ptr(_c(pos, np.int32)), _ptr(_c(tokens, np.int32)))
     if rc != ORC_OK:
@@ -196,7 +205,7 @@ def loop_step(model: Model, paged: Paged, state_h, state_e, slot, seq, pos, c, d
     cont = np.zeros(max(n, 1), dtype=np.int32)
     exited = np.zeros(max(n, 1), dtype=np.int32)
     counts = np.zeros(2, dtype=np.int32)
-    rc = lib().orc_loop_step(C.byref(model.desc), C.byref(model.w), C.byref(paged.c), _ptr(state_h),
+    rc = model.L.orc_loop_step(C.byref(model.desc), C.byref(model.w), C.byref(paged.c), _ptr(state_h),
                              _ptr(state_e), state_h.shape[0], n, _ptr(_c(slot, np.int32)),
                              _ptr(_c(seq, np.int32)), _ptr(_c(pos, np.int32)), _ptr(_c(c, np.int32)),
                              _ptr(_c(depth, np.int32)), _ptr(score), _ptr(mask), _ptr(cont), _ptr(exited),
@@ -211,7 +220,7 @@ def coda(model: Model, paged: Paged, state_h, slot, seq, pos):
     n = len(slot)
     logits = np.zeros((n, model.shape.vocab))
     ids = np.zeros(max(n, 1), dtype=np.int32)
-    rc = lib().orc_coda(C.byref(model.desc), C.byref(model.w), C.byref(paged.c), _ptr(state_h), state_h.shape[0],
+    rc = model.L.orc_coda(C.byref(model.desc), C.byref(model.w), C.byref(paged.c), _ptr(state_h), state_h.shape[0],
                         n, _ptr(_c(slot, np.int32)), _ptr(_c(seq, np.int32)), _ptr(_c(pos, np.int32)),
                         _ptr(logits), _ptr(ids))
     if rc != ORC_OK:

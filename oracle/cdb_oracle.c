@@ -47,6 +47,15 @@
 
 #include "cdb_oracle.h"
 
+/* Accumulator type.  The oracle is fp64 (ORC_ACC = double).  Built with
+ * -DORC_ACC=float it performs the same steps with every sum and product rounded
+ * to fp32; the tests use that build only to measure how far an fp32
+ * implementation of the same arithmetic drifts from fp64 on a given input. */
+#ifndef ORC_ACC
+#define ORC_ACC double
+#endif
+typedef ORC_ACC acc_t;
+
 /* ------------------------------------------------------------------ scalars */
 
 static double bf(uint16_t bits) {
@@ -78,18 +87,18 @@ static double sigmoid(double x) { return 1.0 / (1.0 + exp(-x)); }
 
 /* y = x / sqrt(mean(x^2) + eps); unit gains. */
 static void rmsnorm(const double* x, int n, double eps, double* y) {
-    double ss = 0.0;
-    for (int i = 0; i < n; ++i) ss += x[i] * x[i];
-    double inv = 1.0 / sqrt(ss / n + eps);
-    for (int i = 0; i < n; ++i) y[i] = x[i] * inv;
+    acc_t ss = 0.0;
+    for (int i = 0; i < n; ++i) ss += (acc_t)x[i] * (acc_t)x[i];
+    acc_t inv = (acc_t)1.0 / (acc_t)sqrt((double)(ss / (acc_t)n + (acc_t)eps));
+    for (int i = 0; i < n; ++i) y[i] = (acc_t)x[i] * inv;
 }
 
 /* y[o] = sum_i W[o][i] x[i] for a row-major bf16 matrix W [n_out][n_in]. */
 static void matvec(const uint16_t* W, int n_out, int n_in, const double* x, double* y) {
     for (int o = 0; o < n_out; ++o) {
         const uint16_t* w = W + (size_t)o * n_in;
-        double acc = 0.0;
-        for (int i = 0; i < n_in; ++i) acc += bf(w[i]) * x[i];
+        acc_t acc = 0.0;
+        for (int i = 0; i < n_in; ++i) acc += (acc_t)bf(w[i]) * (acc_t)x[i];
         y[o] = acc;
     }
 }
@@ -114,26 +123,29 @@ static void rope(double* v, int n_heads, int hd, int pos, double base) {
  * kctx[s] / vctx[s] point at the head's hd values of position s. */
 static void attend(const double* q, const double* const* kctx, const double* const* vctx, int n,
                    int hd, double* out) {
-    double* sc = (double*)malloc(sizeof(double) * (size_t)n);
-    double scale = 1.0 / sqrt((double)hd);
-    double mx = -INFINITY;
+    acc_t* sc = (acc_t*)malloc(sizeof(acc_t) * (size_t)n);
+    acc_t* o = (acc_t*)malloc(sizeof(acc_t) * (size_t)hd);
+    acc_t scale = (acc_t)(1.0 / sqrt((double)hd));
+    acc_t mx = -INFINITY;
     for (int s = 0; s < n; ++s) {
-        double dot = 0.0;
-        for (int j = 0; j < hd; ++j) dot += q[j] * kctx[s][j];
+        acc_t dot = 0.0;
+        for (int j = 0; j < hd; ++j) dot += (acc_t)q[j] * (acc_t)kctx[s][j];
         sc[s] = dot * scale;
         if (sc[s] > mx) mx = sc[s];
     }
-    double den = 0.0;
+    acc_t den = 0.0;
     for (int s = 0; s < n; ++s) {
-        sc[s] = exp(sc[s] - mx);
+        sc[s] = (acc_t)exp((double)(sc[s] - mx));
         den += sc[s];
     }
-    for (int j = 0; j < hd; ++j) out[j] = 0.0;
+    for (int j = 0; j < hd; ++j) o[j] = 0.0;
     for (int s = 0; s < n; ++s) {
-        double p = sc[s] / den;
-        for (int j = 0; j < hd; ++j) out[j] += p * vctx[s][j];
+        acc_t p = sc[s] / den;
+        for (int j = 0; j < hd; ++j) o[j] += p * (acc_t)vctx[s][j];
     }
+    for (int j = 0; j < hd; ++j) out[j] = o[j];
     free(sc);
+    free(o);
 }
 
 static const uint16_t* wt(const orc_weights* w, int layer, int which) {
@@ -182,7 +194,7 @@ static void layer_rest(const orc_desc* m, const orc_weights* w, int layer, doubl
     }
     for (int i = 0; i < d; ++i) o[i] = store(m, o[i]);
     matvec(wt(w, layer, WO), d, d, o, t);
-    for (int i = 0; i < d; ++i) h[i] += t[i];
+    for (int i = 0; i < d; ++i) h[i] = (acc_t)h[i] + (acc_t)t[i];
 
     double* g = (double*)malloc(sizeof(double) * (size_t)F);
     double* u = (double*)malloc(sizeof(double) * (size_t)F);
@@ -190,9 +202,9 @@ static void layer_rest(const orc_desc* m, const orc_weights* w, int layer, doubl
     for (int i = 0; i < d; ++i) o[i] = store(m, o[i]);
     matvec(wt(w, layer, WG), F, d, o, g);
     matvec(wt(w, layer, WU), F, d, o, u);
-    for (int i = 0; i < F; ++i) g[i] = store(m, silu(g[i]) * u[i]);
+    for (int i = 0; i < F; ++i) g[i] = store(m, (acc_t)silu(g[i]) * (acc_t)u[i]);
     matvec(wt(w, layer, WD), d, F, g, t);
-    for (int i = 0; i < d; ++i) h[i] += t[i];
+    for (int i = 0; i < d; ++i) h[i] = (acc_t)h[i] + (acc_t)t[i];
     free(g);
     free(u);
     free(kh);
@@ -223,14 +235,14 @@ static double exit_score(const orc_desc* m, const orc_weights* w, const double* 
                          const double* h_old) {
     int d = m->d;
     if (m->exit_kind == 1) {
-        double ss = 0.0;
-        for (int i = 0; i < d; ++i) ss += (h_new[i] - h_old[i]) * (h_new[i] - h_old[i]);
-        return sqrt(ss);
+        acc_t ss = 0.0;
+        for (int i = 0; i < d; ++i) ss += ((acc_t)h_new[i] - (acc_t)h_old[i]) * ((acc_t)h_new[i] - (acc_t)h_old[i]);
+        return sqrt((double)ss);
     }
     double* n = (double*)malloc(sizeof(double) * (size_t)d);
     rmsnorm(h_new, d, m->rms_eps, n);
-    double z = 0.0;
-    for (int i = 0; i < d; ++i) z += bf(w->w_exit[i]) * n[i];
+    acc_t z = 0.0;
+    for (int i = 0; i < d; ++i) z += (acc_t)bf(w->w_exit[i]) * (acc_t)n[i];
     free(n);
     return sigmoid(z);
 }
@@ -492,19 +504,26 @@ static int stage_layers(const orc_desc* m, const orc_weights* w, const orc_paged
     double* q = (double*)malloc(sizeof(double) * (size_t)n * d);
     int err = ORC_OK;
     for (int l = 0; l < nl && err == ORC_OK; ++l) {
+        /* each row writes only its own K/V slot, so rows run independently */
+#pragma omp parallel for schedule(dynamic, 1)
         for (int i = 0; i < n; ++i) {
             double* k = (double*)malloc(sizeof(double) * (size_t)d);
             double* v = (double*)malloc(sizeof(double) * (size_t)d);
             layer_qkv(m, w, first + l, hs + (size_t)i * d, pos[i], q + (size_t)i * d, k, v);
-            for (int hh = 0; hh < H; ++hh) {
+            int bad = 0;
+            for (int hh = 0; hh < H && !bad; ++hh) {
                 double* ks = kv_at(p, m, plane, seq[i], pos[i], l, 0, hh);
                 double* vs = kv_at(p, m, plane, seq[i], pos[i], l, 1, hh);
                 if (!ks || !vs) {
-                    err = ORC_ERR_UNMAPPED;
-                    break;
+                    bad = 1;
+                } else {
+                    memcpy(ks, k + (size_t)hh * hd, sizeof(double) * (size_t)hd);
+                    memcpy(vs, v + (size_t)hh * hd, sizeof(double) * (size_t)hd);
                 }
-                memcpy(ks, k + (size_t)hh * hd, sizeof(double) * (size_t)hd);
-                memcpy(vs, v + (size_t)hh * hd, sizeof(double) * (size_t)hd);
+            }
+            if (bad) {
+#pragma omp critical
+                err = ORC_ERR_UNMAPPED;
             }
             free(k);
             free(v);

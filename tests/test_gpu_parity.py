@@ -1,7 +1,11 @@
 """GPU parity: the HIP stage calls against the CPU oracle, element by element,
 on identical seeded inputs.  Integer outputs (exit masks, compaction lists,
-counts) must match exactly; hidden states, exit scores and logits within
-max-abs 2e-2 / mean-abs 2e-3; K/V entries within one bf16 step."""
+counts) must match exactly.  Hidden states, exit scores and logits must lie
+within max-abs 2e-2 / mean-abs 2e-3, or, where larger, within twice the
+distance between the oracle and the same oracle run with fp32 accumulators on
+the same inputs (deep random-init cores amplify rounding-level differences
+through bf16 rounding flips; an fp32 implementation cannot be expected to sit
+closer than that).  K/V entries must agree within one bf16 step or that bound."""
 import sys
 
 import numpy as np
@@ -38,3 +42,104 @@ def test_config1_tiny_end_to_end():
     _say(f"[gpu] config 1 errors {ls.errors} calls {ls.calls} argmax checked {ls.argmax_checked}")
     assert ls.device_error() == 0
     assert ls.calls["loop"] > wl.decode
+
+
+def _sample_rows(rows_np, r_max, k=3):
+    """Rows to check with the oracle: an exiting row with copy-on-exit (depth <
+    r_max), a continuing row, and the row with the longest context."""
+    c, dep, pos = rows_np["c"], rows_np["depth"], rows_np["pos"]
+    ex = [i for i in range(len(c)) if c[i] + 1 == dep[i] and dep[i] < r_max]
+    co = [i for i in range(len(c)) if c[i] + 1 < dep[i]]
+    picks = []
+    for cand in (ex[:1], co[:1], [int(np.argmax(pos))]):
+        for i in cand:
+            if i not in picks:
+                picks.append(i)
+    return picks[:k]
+
+
+def _core_prefix(shape, w, n_core):
+    """The same model with only its first n_core core layers (same widths,
+    kernels and launch shapes; a shallower core keeps rounding-level
+    differences from being amplified layer after layer)."""
+    s = cdbgen.shrink(shape, n_core=n_core)
+    ww = dict(w)
+    ww["layers"] = w["layers"][:shape.n_prelude + n_core] + w["layers"][shape.n_prelude + shape.n_core:]
+    return s, ww
+
+
+@pytest.mark.parametrize("n_core", [2, 24])
+def test_config2_loop_step_full_batch_sampled_rows(n_core):
+    """The benchmark's launch: 64 mixed-depth rows of the Ouro-shaped model at
+    decode positions 512..767; three rows checked against the oracle.  With 2
+    core layers the absolute bound applies; with all 24 the bound is twice the
+    oracle's fp32-vs-fp64 drift on the same inputs."""
+    from lockstep import injected_loop_step
+    s, w = _core_prefix(cdbgen.OURO, cdbgen.model_weights(cdbgen.OURO), n_core)
+    rows = cdbgen.decode_snapshot(64, cdbgen.OURO_DEPTHS, s.r_max, 512, 767, stream=7)
+    sample = _sample_rows(rows, s.r_max)
+    _say(f"[gpu] config 2 full batch, {n_core} core layers, sampled rows {sample}: c {rows['c'][sample]} "
+         f"depth {rows['depth'][sample]}")
+    err = injected_loop_step(s, w, rows, sample, sensitivity=True)
+    _say(f"[gpu] config 2 ({n_core} core layers) errors {err}")
+
+
+@pytest.mark.parametrize("n_core", [1, 4])
+def test_config3_huginn_loop_step_full_batch_sampled_rows(n_core):
+    """128 rows of the Huginn-shaped model (adapter, 55 heads x 96, r_max 32) at
+    decode positions 256..767; three rows checked against the oracle (absolute
+    bound with 1 core layer, sensitivity bound with all 4)."""
+    from lockstep import injected_loop_step
+    s, w = _core_prefix(cdbgen.HUGINN, cdbgen.model_weights(cdbgen.HUGINN), n_core)
+    wl = cdbgen.WORKLOADS[3]
+    rows = cdbgen.decode_snapshot(128, wl.depth, s.r_max, 256, 767, stream=9)
+    sample = _sample_rows(rows, s.r_max)
+    _say(f"[gpu] config 3 full batch, {n_core} core layers, sampled rows {sample}: c {rows['c'][sample]} "
+         f"depth {rows['depth'][sample]}")
+    err = injected_loop_step(s, w, rows, sample, sensitivity=True)
+    _say(f"[gpu] config 3 ({n_core} core layers) errors {err}")
+
+
+def test_config4_long_context_256_rows_sampled():
+    """256 rows (the config's batch), 50/50 exits at loop 1 and 4; sampled rows
+    sit at long contexts 2048..4223, the others at short ones to bound memory.
+    Full 24-layer core, sensitivity bound."""
+    from lockstep import injected_loop_step
+    s = cdbgen.OURO
+    wl = cdbgen.WORKLOADS[4]
+    rows = cdbgen.decode_snapshot(256, wl.depth, s.r_max, 16, 200, stream=11)
+    g = np.random.default_rng(3)
+    sample = _sample_rows(rows, s.r_max, k=2)
+    for i in sample:
+        rows["pos"][i] = int(g.integers(2048, 4224))
+    _say(f"[gpu] config 4, 256 rows, sampled rows {sample}: pos {rows['pos'][sample]} c {rows['c'][sample]}")
+    err = injected_loop_step(s, cdbgen.model_weights(s), rows, sample, sensitivity=True)
+    _say(f"[gpu] config 4 errors {err}")
+
+
+def test_config2_reduced_length_end_to_end():
+    """Ouro widths with a 2-layer core, 2 sequences, prompt 16, decode 6, batch
+    2; every call checked from the oracle's states (resync)."""
+    from lockstep import Lockstep
+    s, w = _core_prefix(cdbgen.OURO, cdbgen.model_weights(cdbgen.OURO), 2)
+    prompts, depths = _workload_inputs(s, 2, 16, 6, cdbgen.OURO_DEPTHS, seed_stream=20)
+    _say(f"[gpu] config 2 reduced end to end, depths {[d[16:].tolist() for d in depths]}")
+    ls = Lockstep(s, w, [22, 22], max_batch=2, resync=True, sensitivity=True)
+    ls.run(prompts, [6, 6], depths)
+    _say(f"[gpu] config 2 reduced errors {ls.errors} oracle self {ls.self_diff} calls {ls.calls}")
+    assert ls.device_error() == 0
+
+
+def test_config3_reduced_depth_end_to_end():
+    """Huginn widths (2 prelude + 2 coda layers, adapter, 55 x 96 heads) with a
+    1-layer core and r_max 3: 2 sequences, prompt 3, decode 3, batch 2; every call
+    checked from the oracle's states (resync)."""
+    from lockstep import Lockstep
+    s, w = _core_prefix(cdbgen.HUGINN, cdbgen.model_weights(cdbgen.HUGINN), 1)
+    s = cdbgen.shrink(s, r_max=3)
+    prompts, depths = _workload_inputs(s, 2, 3, 3, ("uniform", 1, 3), seed_stream=30)
+    _say(f"[gpu] config 3 reduced-depth end to end, depths {[d[3:].tolist() for d in depths]}")
+    ls = Lockstep(s, w, [6, 6], max_batch=2, resync=True, sensitivity=True)
+    ls.run(prompts, [3, 3], depths)
+    _say(f"[gpu] config 3 reduced errors {ls.errors} oracle self {ls.self_diff} calls {ls.calls}")
+    assert ls.device_error() == 0
