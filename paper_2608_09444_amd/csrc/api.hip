@@ -62,7 +62,7 @@ static ModelGemms model_gemms(const cdb_model_desc& d) {
 
 WsLayout ws_layout(const cdb_model_desc& d, int rows) {
     WsLayout L;
-    const size_t D = d.d, F = d.d_ff, M = rows, M32 = round32(rows);
+    const size_t D = d.d, F = d.d_ff, M = rows, M32 = gemm_rows(rows);
     const ModelGemms g = model_gemms(d);
     const size_t part = (size_t)(g.o.S > g.down.S ? g.o.S : g.down.S) * D;  // split-K partials of O / down
     size_t off = 0;
@@ -80,6 +80,8 @@ WsLayout ws_layout(const cdb_model_desc& d, int rows) {
     off = align256(off + M32 * F * 2);
     L.part = off;
     off = align256(off + part * M * 4);
+    L.rope = off;
+    off = align256(off + M * (size_t)(d.head_dim / 2) * 8);
     L.total = off;
     return L;
 }
@@ -99,6 +101,7 @@ struct Ctx {
     uint16_t* x;
     uint16_t* act;
     float* part;
+    float2* rope;
 };
 
 static Ctx make_ctx(const cdb_model* model, void* ws, int rows) {
@@ -116,6 +119,7 @@ static Ctx make_ctx(const cdb_model* model, void* ws, int rows) {
     c.x = reinterpret_cast<uint16_t*>(c.ws + c.L.x);
     c.act = reinterpret_cast<uint16_t*>(c.ws + c.L.act);
     c.part = reinterpret_cast<float*>(c.ws + c.L.part);
+    c.rope = reinterpret_cast<float2*>(c.ws + c.L.rope);
     return c;
 }
 
@@ -142,7 +146,7 @@ static cdb_status run_layers(const Ctx& c, int first, int count, KvTarget kv, co
         ea.pos = r.pos;
         ea.H = d.n_heads;
         ea.hd = d.head_dim;
-        ea.rope_base = d.rope_base;
+        ea.rope = c.rope;
         ea.err = c.err;
         ea.kv = kv;
         ea.q = c.q;
@@ -270,7 +274,7 @@ cdb_status cdb_boundary_prelude(const cdb_model* model, const cdb_kv* kv, const 
     if (d.injection && !state->e) return CDB_ERR_INVALID_ARG;
     if (rows->n_rows == 0) return CDB_OK;
     Ctx c = make_ctx(model, ws, rows->n_rows);
-    HIPCHK(launch_embed(d, wptr(c, c.wl.embed), tokens, *rows, *kv, state->n_slots, c.h, c.err, st));
+    HIPCHK(launch_embed(d, wptr(c, c.wl.embed), tokens, *rows, *kv, state->n_slots, c.h, c.rope, c.err, st));
     s = run_layers(c, 0, d.n_prelude, stage_target(d, *kv, 0), *rows, false, st);
     if (s != CDB_OK) return s;
     HIPCHK(launch_store_state(rows->n_rows, d.d, state->n_slots, rows->slot, c.h, state->h,
@@ -290,7 +294,7 @@ cdb_status cdb_loop_step(const cdb_model* model, const cdb_kv* kv, const cdb_sta
     const int M = rows->n_rows;
     Ctx c = make_ctx(model, ws, M);
     if (M > 0) {
-        HIPCHK(launch_gather(d, *state, *rows, *kv, c.h, c.h_in, d.injection ? c.x : nullptr, c.err, st));
+        HIPCHK(launch_gather(d, *state, *rows, *kv, c.h, c.h_in, d.injection ? c.x : nullptr, c.rope, c.err, st));
         if (d.injection) {
             EpiArgs ea{};
             ea.out = c.h;
@@ -318,7 +322,7 @@ cdb_status cdb_boundary_coda(const cdb_model* model, const cdb_kv* kv, const cdb
     const int M = rows->n_rows;
     if (M == 0) return CDB_OK;
     Ctx c = make_ctx(model, ws, M);
-    HIPCHK(launch_load_state(M, d.d, rows->slot, state->h, state->n_slots, c.h, c.err, st));
+    HIPCHK(launch_load_state(d, M, rows->slot, rows->pos, state->h, state->n_slots, c.h, c.rope, c.err, st));
     s = run_layers(c, d.n_prelude + d.n_core, d.n_coda, stage_target(d, *kv, 2), *rows, true, st);
     if (s != CDB_OK) return s;
     EpiArgs ea{};

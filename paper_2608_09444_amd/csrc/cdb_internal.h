@@ -38,6 +38,9 @@ __host__ __device__ __forceinline__ size_t frag_index(int m, int k, int K) {
     return ((((size_t)(m >> 5) * (K >> 4) + (k >> 4)) * 64 + (m & 31) + 32 * ((k & 15) >> 3)) << 3) + (k & 7);
 }
 __host__ __device__ __forceinline__ int round32(int m) { return (m + 31) & ~31; }
+// Rows a GEMM input buffer must hold for M rows: the GEMM covers M with 1, 2, 4
+// or 8 tiles of 32 rows and reads every row of them.
+__host__ __device__ __forceinline__ int gemm_rows(int m) { return m <= 32 ? 32 : m <= 64 ? 64 : m <= 128 ? 128 : 256; }
 
 // First sticky error wins.
 __device__ __forceinline__ void set_err(int* err, int code) { atomicCAS(err, 0, code); }
@@ -66,8 +69,8 @@ struct EpiArgs {
     KvTarget kv;
     const int32_t* seq;
     const int32_t* pos;
+    const float2* rope;  // [M][hd/2] (cos, sin) of pos * base^(-2j/hd), one table per stage call
     int H, hd;
-    float rope_base;
     int* err;
 };
 
@@ -84,7 +87,7 @@ struct WeightLayout {
 bool weight_layout(const cdb_model_desc& d, WeightLayout* out);
 
 struct WsLayout {
-    size_t err, h, h_in, q, x, act, part, total;
+    size_t err, h, h_in, q, x, act, part, rope, total;
 };
 WsLayout ws_layout(const cdb_model_desc& d, int rows);
 
@@ -100,14 +103,16 @@ hipError_t launch_attention(const float* q, const KvTarget& kv, const int32_t* s
 // out = bf16(RMSNorm(h)) in fragment layout.
 hipError_t launch_resid_norm(float* h, const float* part, int S, int M, int d, float eps, uint16_t* out,
                              hipStream_t st);
+// The row-entry kernels of the three stage calls also fill the call's RoPE
+// table rope[M][hd/2] = (cos, sin) of pos * base^(-2j/hd), angles in fp64.
 hipError_t launch_gather(const cdb_model_desc& md, const cdb_state& s, const cdb_rows& r, const cdb_kv& kv,
-                         float* h, float* h_in, uint16_t* xcat, int* err, hipStream_t st);
+                         float* h, float* h_in, uint16_t* xcat, float2* rope, int* err, hipStream_t st);
 hipError_t launch_embed(const cdb_model_desc& md, const uint16_t* embed, const int32_t* tokens, const cdb_rows& r,
-                        const cdb_kv& kv, int n_slots, float* h, int* err, hipStream_t st);
+                        const cdb_kv& kv, int n_slots, float* h, float2* rope, int* err, hipStream_t st);
 hipError_t launch_store_state(int M, int d, int n_slots, const int32_t* slot, const float* h, float* state_h,
                               float* state_e, hipStream_t st);
-hipError_t launch_load_state(int M, int d, const int32_t* slot, const float* state_h, int n_slots, float* h,
-                             int* err, hipStream_t st);
+hipError_t launch_load_state(const cdb_model_desc& md, int M, const int32_t* slot, const int32_t* pos,
+                             const float* state_h, int n_slots, float* h, float2* rope, int* err, hipStream_t st);
 hipError_t launch_exit(const cdb_model_desc& md, const cdb_rows& r, const float* h, const float* h_in,
                        const uint16_t* w_exit, float* state_h, int n_slots, const cdb_step_out& o, hipStream_t st);
 hipError_t launch_compact(int M, const uint8_t* mask, int32_t* cont, int32_t* exited, int32_t* counts,

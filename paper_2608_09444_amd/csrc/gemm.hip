@@ -9,9 +9,10 @@
 //    along K.  A 32-wide stripe halves the activation (B operand) traffic per
 //    weight byte compared with a 16-wide one.
 //  * A workgroup owns one 32-column stripe and one K split; its KW waves split
-//    that K range further.  Each wave issues the loads of (up to 16) weight
-//    tiles up front, and streams the activation fragments (L2-resident) two
-//    steps ahead.  The KW partial tiles are summed in LDS in wave order.
+//    that K range further.  Each wave streams its weight tiles and the matching
+//    activation fragments (L2-resident) in batches, double-buffered in
+//    registers so one batch is in flight while the previous one feeds the
+//    MFMAs.  The KW partial tiles are summed in LDS in wave order.
 //  * No reduction crosses workgroups inside the kernel.  Stripes whose K is
 //    split over S workgroups write fp32 partial tiles; the row kernel that
 //    runs next (residual add + RMSNorm) adds them in split order.  Every
@@ -30,7 +31,7 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 constexpr int kMaxKw = 8;     // waves per workgroup (2 per SIMD, so 256 registers each)
 
 struct GemmArgs {
-    const uint16_t* X;  // fragment layout, round32(M) rows, K columns
+    const uint16_t* X;  // fragment layout, gemm_rows(M) rows (rows >= M are never read back), K columns
     const uint16_t* Wp;
     int M, N, K, S, KW;
     float* part;  // EPI_PARTIAL: [S][M][N]
@@ -58,12 +59,9 @@ __device__ __forceinline__ void epilogue_elem(float val, float partner, int m, i
         const int dim = j + half * (ea.hd >> 1);
         float outv = val;
         if (part < 2) {
-            const double ang = (double)ea.pos[m] * pow((double)ea.rope_base, -2.0 * j / ea.hd);
-            double sn, cs;
-            sincos(ang, &sn, &cs);
-            const float c = (float)cs, s = (float)sn;
+            const float2 cs = ea.rope[(size_t)m * (ea.hd >> 1) + j];
             const float xf = half ? partner : val, xs = half ? val : partner;
-            outv = half ? (xs * c + xf * s) : (xf * c - xs * s);
+            outv = half ? (xs * cs.x + xf * cs.y) : (xf * cs.x - xs * cs.y);
         }
         if (part == 0) {
             ea.q[(size_t)m * (ea.H * ea.hd) + head * ea.hd + dim] = outv;
@@ -110,34 +108,42 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs ga, EpiArgs ea) {
     const u32x4* wsrc = reinterpret_cast<const u32x4*>(ga.Wp) + (size_t)nt * KS * 64 + lane;
     // X is in fragment layout: the operand of m-tile t at k step k is the 1 KiB tile (t, k)
     const u32x4* xsrc = reinterpret_cast<const u32x4*>(ga.X) + lane;
-    constexpr int CH = MT <= 2 ? 8 : (MT == 4 ? 4 : 2);  // k steps whose loads are all in flight together
+    constexpr int CH = MT <= 2 ? 8 : (MT == 4 ? 4 : 1);  // k steps per load batch
 
-    for (int c0 = ks0; c0 < ks1; c0 += CH) {
-        const int n = min(CH, ks1 - c0);
-        u32x4 wf[CH];
-        u32x4 xf[CH][MT];
+    // Two register sets: the next batch's loads are in flight while the
+    // current batch feeds the MFMAs.
+    u32x4 wa[CH], wb[CH];
+    u32x4 xa[CH][MT], xb[CH][MT];
+    // Loads are unconditional (steps past the wave's range re-read its last
+    // step, whose weight tile is then zeroed) so that the compiler keeps each
+    // batch's loads in flight across the other batch's MFMAs.
+    auto load = [&](u32x4 (&w)[CH], u32x4 (&x)[CH][MT], int c0) {
 #pragma unroll
         for (int i = 0; i < CH; ++i) {
-            if (i < n) {
-                wf[i] = __builtin_nontemporal_load(wsrc + (size_t)(c0 + i) * 64);
+            const int ks = min(c0 + i, ks1 - 1);
+            w[i] = wsrc[(size_t)ks * 64];
 #pragma unroll
-                for (int t = 0; t < MT; ++t) {
-                    u32x4 v = {0u, 0u, 0u, 0u};
-                    if (t * 32 < M) v = xsrc[((size_t)t * KS + c0 + i) * 64];  // buffers hold round32(M) rows
-                    xf[i][t] = v;
-                }
-            }
+            for (int t = 0; t < MT; ++t) x[i][t] = xsrc[((size_t)t * KS + ks) * 64];
         }
+    };
+    auto compute = [&](const u32x4 (&w)[CH], const u32x4 (&x)[CH][MT], int c0) {
 #pragma unroll
         for (int i = 0; i < CH; ++i) {
-            if (i < n) {
-                const bf16x8 a = __builtin_bit_cast(bf16x8, wf[i]);
+            const uint32_t keep = c0 + i < ks1 ? 0xffffffffu : 0u;
+            const u32x4 wm = w[i] & keep;
+            const bf16x8 a = __builtin_bit_cast(bf16x8, wm);
 #pragma unroll
-                for (int t = 0; t < MT; ++t)
-                    acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, __builtin_bit_cast(bf16x8, xf[i][t]), acc[t], 0,
-                                                                     0, 0);
-            }
+            for (int t = 0; t < MT; ++t)
+                acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, __builtin_bit_cast(bf16x8, x[i][t]), acc[t], 0, 0,
+                                                                 0);
         }
+    };
+    if (ks0 < ks1) load(wa, xa, ks0);
+    for (int c0 = ks0; c0 < ks1; c0 += 2 * CH) {
+        if (c0 + CH < ks1) load(wb, xb, c0 + CH);
+        compute(wa, xa, c0);
+        if (c0 + 2 * CH < ks1) load(wa, xa, c0 + 2 * CH);
+        if (c0 + CH < ks1) compute(wb, xb, c0 + CH);
     }
 
     // Sum the KW wave tiles in wave order, one 32x32 m-tile at a time.
@@ -179,10 +185,10 @@ GemmShape gemm_shape(int N, int K, int epi) {
     if (epi == EPI_PARTIAL) {
         while (stripes * S < 256 && KS / (S * 2) >= 32) S *= 2;
     }
-    // enough waves that each streams about one chunk of k steps
-    const int ch = 8;
+    // waves per workgroup: 4, or 8 when there are too few workgroups to cover
+    // the chip (every wave then streams twice as many k steps in flight)
     int KW = 4;
-    while (KW < kMaxKw && (KS / S + KW - 1) / KW > ch) KW *= 2;
+    if (stripes * S < 256 && KS / S >= 64) KW = 8;
     return GemmShape{N, K, S, KW};
 }
 

@@ -6,28 +6,43 @@
 
 namespace cdb {
 
-// Block-wide fp32 sum for 256 threads (4 waves); result broadcast to all.
+// Block-wide fp32 sum (blockDim.x a multiple of 64, at most 1024); result
+// broadcast to all threads, summed in wave order.
 __device__ __forceinline__ float block_sum(float v, float* red) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-    const int w = threadIdx.x >> 6;
+    const int w = threadIdx.x >> 6, nw = blockDim.x >> 6;
     __syncthreads();
     if ((threadIdx.x & 63) == 0) red[w] = v;
     __syncthreads();
-    return red[0] + red[1] + red[2] + red[3];
+    float t = 0.f;
+    for (int i = 0; i < nw; ++i) t += red[i];
+    return t;
+}
+
+// RoPE table of one row: (cos, sin) of pos * base^(-2j/hd) for j < hd/2, fp64 angles.
+__device__ __forceinline__ void rope_row(int pos, int hd, float base, float2* out) {
+    for (int j = threadIdx.x; j < hd / 2; j += blockDim.x) {
+        const double ang = (double)pos * pow((double)base, -2.0 * j / hd);
+        double sn, cs;
+        sincos(ang, &sn, &cs);
+        out[j] = make_float2((float)cs, (float)sn);
+    }
 }
 
 // ------------------------------------------------------------------ gather
 // h[i] = state.h[slot[i]]; h_in[i] = h[i] (exit score of the L2 criterion);
 // xcat[i] = bf16([h; e]) for the input-injection adapter.  Validates the row.
-__global__ __launch_bounds__(256) void k_gather(int d, int r_max, int n_slots, int max_seqs, int max_pos,
-                                                const int32_t* __restrict__ slot, const int32_t* __restrict__ seq,
-                                                const int32_t* __restrict__ pos, const int32_t* __restrict__ c,
-                                                const int32_t* __restrict__ depth, const float* __restrict__ sh,
-                                                const float* __restrict__ se, float* __restrict__ h,
-                                                float* __restrict__ h_in, uint16_t* __restrict__ xcat, int* err) {
+__global__ __launch_bounds__(256) void k_gather(int d, int r_max, int n_slots, int max_seqs, int max_pos, int hd,
+                                                float base, const int32_t* __restrict__ slot,
+                                                const int32_t* __restrict__ seq, const int32_t* __restrict__ pos,
+                                                const int32_t* __restrict__ c, const int32_t* __restrict__ depth,
+                                                const float* __restrict__ sh, const float* __restrict__ se,
+                                                float* __restrict__ h, float* __restrict__ h_in,
+                                                uint16_t* __restrict__ xcat, float2* __restrict__ rope, int* err) {
     const int i = blockIdx.x;
     const int sl = slot[i];
+    rope_row(pos[i], hd, base, rope + (size_t)i * (hd / 2));
     if (threadIdx.x == 0) {
         if (depth[i] < 1 || depth[i] > r_max || c[i] < 0 || c[i] >= depth[i]) set_err(err, CDB_DEV_BAD_DEPTH);
         if (sl < 0 || sl >= n_slots || seq[i] < 0 || seq[i] >= max_seqs || pos[i] < 0 || pos[i] >= max_pos)
@@ -52,10 +67,13 @@ __global__ __launch_bounds__(256) void k_gather(int d, int r_max, int n_slots, i
 }
 
 // h[i] = state.h[slot[i]] (coda input)
-__global__ __launch_bounds__(256) void k_load_state(int d, int n_slots, const int32_t* __restrict__ slot,
-                                                    const float* __restrict__ sh, float* __restrict__ h, int* err) {
+__global__ __launch_bounds__(256) void k_load_state(int d, int n_slots, int hd, float base,
+                                                    const int32_t* __restrict__ slot, const int32_t* __restrict__ pos,
+                                                    const float* __restrict__ sh, float* __restrict__ h,
+                                                    float2* __restrict__ rope, int* err) {
     const int i = blockIdx.x;
     const int sl = slot[i];
+    rope_row(pos[i], hd, base, rope + (size_t)i * (hd / 2));
     const bool ok = sl >= 0 && sl < n_slots;
     if (!ok && threadIdx.x == 0) set_err(err, CDB_DEV_BAD_INDEX);
     for (int k = threadIdx.x * 4; k < d; k += 1024)
@@ -66,13 +84,14 @@ __global__ __launch_bounds__(256) void k_load_state(int d, int n_slots, const in
 // ------------------------------------------------------------------ residual + RMSNorm
 // h[i] += sum_s part[s][i] (split order 0..S-1); out[i] = bf16(h[i] / sqrt(mean(h[i]^2) + eps)),
 // unit gains.  Row i is one workgroup.
-__global__ __launch_bounds__(256) void k_resid_norm(float* __restrict__ h, const float* __restrict__ part, int S, int M,
-                                                    int d, float eps, uint16_t* __restrict__ out) {
-    __shared__ float red[4];
+__global__ __launch_bounds__(1024) void k_resid_norm(float* __restrict__ h, const float* __restrict__ part, int S, int M,
+                                                     int d, float eps, uint16_t* __restrict__ out) {
+    __shared__ float red[16];
     const int i = blockIdx.x;
+    const int step = blockDim.x * 4;
     float* x = h + (size_t)i * d;
     float ss = 0.f;
-    for (int k = threadIdx.x * 4; k < d; k += 1024) {
+    for (int k = threadIdx.x * 4; k < d; k += step) {
         float4 v = *reinterpret_cast<const float4*>(x + k);
         for (int s = 0; s < S; ++s) {
             const float4 p = *reinterpret_cast<const float4*>(part + ((size_t)s * M + i) * d + k);
@@ -87,7 +106,7 @@ __global__ __launch_bounds__(256) void k_resid_norm(float* __restrict__ h, const
     if (!out) return;
     ss = block_sum(ss, red);
     const float inv = 1.0f / sqrtf(ss / d + eps);
-    for (int k = threadIdx.x * 4; k < d; k += 1024) {
+    for (int k = threadIdx.x * 4; k < d; k += step) {
         const float4 v = *reinterpret_cast<const float4*>(x + k);
         uint2 pk;
         pk.x = (uint32_t)f2bf(v.x * inv) | ((uint32_t)f2bf(v.y * inv) << 16);
@@ -97,11 +116,13 @@ __global__ __launch_bounds__(256) void k_resid_norm(float* __restrict__ h, const
 }
 
 // ------------------------------------------------------------------ embedding
-__global__ __launch_bounds__(256) void k_embed(int d, int vocab, int n_slots, int max_seqs, int max_pos,
-                                               const uint16_t* __restrict__ E, const int32_t* __restrict__ tok,
-                                               const int32_t* __restrict__ slot, const int32_t* __restrict__ seq,
-                                               const int32_t* __restrict__ pos, float* __restrict__ h, int* err) {
+__global__ __launch_bounds__(256) void k_embed(int d, int vocab, int n_slots, int max_seqs, int max_pos, int hd,
+                                               float base, const uint16_t* __restrict__ E,
+                                               const int32_t* __restrict__ tok, const int32_t* __restrict__ slot,
+                                               const int32_t* __restrict__ seq, const int32_t* __restrict__ pos,
+                                               float* __restrict__ h, float2* __restrict__ rope, int* err) {
     const int i = blockIdx.x;
+    rope_row(pos[i], hd, base, rope + (size_t)i * (hd / 2));
     const int t = tok[i];
     const bool ok = t >= 0 && t < vocab;
     if (threadIdx.x == 0 && (!ok || slot[i] < 0 || slot[i] >= n_slots || seq[i] < 0 || seq[i] >= max_seqs ||
@@ -336,32 +357,35 @@ __global__ void k_ws_init(int* err) {
 static int page_cap(const cdb_kv& kv) { return kv.max_pages * kPage; }
 
 hipError_t launch_gather(const cdb_model_desc& md, const cdb_state& s, const cdb_rows& r, const cdb_kv& kv, float* h,
-                         float* h_in, uint16_t* xcat, int* err, hipStream_t st) {
+                         float* h_in, uint16_t* xcat, float2* rope, int* err, hipStream_t st) {
     if (r.n_rows <= 0) return hipSuccess;
-    k_gather<<<r.n_rows, 256, 0, st>>>(md.d, md.r_max, s.n_slots, kv.max_seqs, page_cap(kv), r.slot, r.seq, r.pos, r.c,
-                                        r.depth, s.h, s.e, h, h_in, xcat, err);
+    k_gather<<<r.n_rows, 256, 0, st>>>(md.d, md.r_max, s.n_slots, kv.max_seqs, page_cap(kv), md.head_dim, md.rope_base,
+                                        r.slot, r.seq, r.pos, r.c, r.depth, s.h, s.e, h, h_in, xcat, rope, err);
     return hipGetLastError();
 }
 
-hipError_t launch_load_state(int M, int d, const int32_t* slot, const float* state_h, int n_slots, float* h, int* err,
-                             hipStream_t st) {
+hipError_t launch_load_state(const cdb_model_desc& md, int M, const int32_t* slot, const int32_t* pos,
+                             const float* state_h, int n_slots, float* h, float2* rope, int* err, hipStream_t st) {
     if (M <= 0) return hipSuccess;
-    k_load_state<<<M, 256, 0, st>>>(d, n_slots, slot, state_h, h, err);
+    k_load_state<<<M, 256, 0, st>>>(md.d, n_slots, md.head_dim, md.rope_base, slot, pos, state_h, h, rope, err);
     return hipGetLastError();
 }
 
 hipError_t launch_resid_norm(float* h, const float* part, int S, int M, int d, float eps, uint16_t* out,
                              hipStream_t st) {
     if (M <= 0) return hipSuccess;
-    k_resid_norm<<<M, 256, 0, st>>>(h, part, S, M, d, eps, out);
+    // one workgroup per row, about 4 elements per thread
+    int threads = 64;
+    while (threads < 1024 && threads * 4 < d) threads *= 2;
+    k_resid_norm<<<M, threads, 0, st>>>(h, part, S, M, d, eps, out);
     return hipGetLastError();
 }
 
 hipError_t launch_embed(const cdb_model_desc& md, const uint16_t* embed, const int32_t* tokens, const cdb_rows& r,
-                        const cdb_kv& kv, int n_slots, float* h, int* err, hipStream_t st) {
+                        const cdb_kv& kv, int n_slots, float* h, float2* rope, int* err, hipStream_t st) {
     if (r.n_rows <= 0) return hipSuccess;
-    k_embed<<<r.n_rows, 256, 0, st>>>(md.d, md.vocab, n_slots, kv.max_seqs, page_cap(kv), embed, tokens, r.slot, r.seq,
-                                       r.pos, h, err);
+    k_embed<<<r.n_rows, 256, 0, st>>>(md.d, md.vocab, n_slots, kv.max_seqs, page_cap(kv), md.head_dim, md.rope_base,
+                                       embed, tokens, r.slot, r.seq, r.pos, h, rope, err);
     return hipGetLastError();
 }
 
