@@ -106,10 +106,11 @@ typedef struct {
     cdb_model_desc desc;
 } cdb_model;
 
-/* Paged, depth-indexed KV cache (Sections 4.2).  Three pools of 16-token
- * pages, one per stage; a page of a stage with L layers holds
- *     bf16 [L][2 (K, V)][n_heads][16 tokens][head_dim]
- * (K and V after RoPE on K).  page_table (device, int32) is
+/* Paged, depth-indexed KV cache (Section 4.2).  Three pools of 16-token
+ * pages, one per stage.  A page id addresses the same slot in every layer of
+ * its stage; a pool of a stage with L layers and P pages is layer-major:
+ *     bf16 [L][P][2 (K, V)][n_heads][16 tokens][head_dim]
+ * (K after RoPE).  page_table (device, int32) is
  *     [max_seqs][r_max + 2][max_pages]
  * plane 0 -> prelude pool, planes 1..r_max -> core pool (loop index c, 0-based,
  * uses plane c + 1), plane r_max + 1 -> coda pool; entry = page id within that
@@ -202,11 +203,16 @@ cdb_status cdb_boundary_coda(const cdb_model* model, const cdb_kv* kv, const cdb
  *   out[i][h*hd + :] = softmax_s(q[i][h*hd + :] . K_s / sqrt(hd)) V_s
  * over positions s = 0..pos[i] of sequence seq[i] in the row's plane of stage
  * `stage` (0 prelude, 1 core -> plane c[i] + 1, 2 coda), layer `layer` of that
- * stage.  q: device fp32 [n_rows][d] (after RoPE); out: device bf16
- * [n_rows][d].  Reads the cache only. */
+ * stage.  q: device fp32 [n_rows][d] (after RoPE); out: device bf16 in the
+ * fragment order of the output projection's input: element (m, k) at
+ * ((m/32 * d/16 + k/16) * 64 + m%32 + 32*((k%16)/8)) * 8 + k%8, rows rounded up
+ * to 32/64/128/256.  order: optional device int32 [n_rows], the rows ranked by
+ * descending pos (ties by index); NULL makes the call compute it into the
+ * workspace at byte offset 256, from where later calls on the same rows may
+ * pass it.  ws: at least 256 + 4 * 256 bytes.  Reads the cache only. */
 cdb_status cdb_paged_attention(const cdb_model_desc* desc, const cdb_kv* kv, const cdb_rows* rows, int32_t stage,
-                               int32_t layer, const float* q, void* out, void* ws, size_t ws_bytes,
-                               hipStream_t stream);
+                               int32_t layer, const float* q, const int32_t* order, void* out, void* ws,
+                               size_t ws_bytes, hipStream_t stream);
 
 /* Reads (and clears) the workspace's sticky device error code.  Synchronises
  * `stream`; not for the hot path. */

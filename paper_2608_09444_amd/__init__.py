@@ -85,7 +85,7 @@ def lib() -> C.CDLL:
         L.cdb_boundary_prelude.argtypes = [P, P, P, P, P, P, S, P]
         L.cdb_loop_step.argtypes = [P, P, P, P, P, P, S, P]
         L.cdb_boundary_coda.argtypes = [P, P, P, P, P, P, P, S, P]
-        L.cdb_paged_attention.argtypes = [P, P, P, I, I, P, P, P, S, P]
+        L.cdb_paged_attention.argtypes = [P, P, P, I, I, P, P, P, P, S, P]
         L.cdb_read_device_error.argtypes = [P, P, P]
         L.cdb_status_str.argtypes = [C.c_int]
         L.cdb_status_str.restype = C.c_char_p
@@ -161,9 +161,12 @@ def cdb_boundary_coda(model: cdb_model, kv: cdb_kv, state: cdb_state, rows: cdb_
 
 
 def cdb_paged_attention(desc: cdb_model_desc, kv: cdb_kv, rows: cdb_rows, stage: int, layer: int, q, out, ws,
-                        stream=None):
+                        stream=None, order=None):
+    """order: None (computed into ws[256:]) or an int32 device tensor / address of a
+    previous call's order."""
+    optr = order if isinstance(order, int) else _ptr(order)
     _check("cdb_paged_attention", lib().cdb_paged_attention(C.byref(desc), C.byref(kv), C.byref(rows), stage, layer,
-                                                            _ptr(q), _ptr(out), _ptr(ws), ws.numel(),
+                                                            _ptr(q), optr, _ptr(out), _ptr(ws), ws.numel(),
                                                             _stream(stream)))
 
 
@@ -220,8 +223,8 @@ class DeviceModel:
 
 
 class PagedKV:
-    """Device KV pools (bf16 pages of [layers][2][H][16][hd] per stage) and the
-    int32 page table [max_seqs][r_max + 2][max_pages] (-1 = unmapped)."""
+    """Device KV pools (bf16, layer-major [layers][pages][2][H][16][hd] per stage)
+    and the int32 page table [max_seqs][r_max + 2][max_pages] (-1 = unmapped)."""
 
     def __init__(self, shape, max_seqs, max_pages, pre_pages, core_pages, coda_pages, device="cuda", fill=None):
         import torch
@@ -231,7 +234,7 @@ class PagedKV:
         def pool(nl, n):
             if nl == 0 or n == 0:
                 return torch.zeros(1, dtype=torch.bfloat16, device=device)
-            t = torch.empty((n, nl, 2, H, PAGE_TOKENS, hd), dtype=torch.bfloat16, device=device)
+            t = torch.empty((nl, n, 2, H, PAGE_TOKENS, hd), dtype=torch.bfloat16, device=device)
             if fill is None:
                 t.zero_()
             return t

@@ -82,6 +82,8 @@ WsLayout ws_layout(const cdb_model_desc& d, int rows) {
     off = align256(off + part * M * 4);
     L.rope = off;
     off = align256(off + M * (size_t)(d.head_dim / 2) * 8);
+    L.order = off;
+    off = align256(off + M * 4);
     L.total = off;
     return L;
 }
@@ -102,6 +104,7 @@ struct Ctx {
     uint16_t* act;
     float* part;
     float2* rope;
+    int32_t* order;
 };
 
 static Ctx make_ctx(const cdb_model* model, void* ws, int rows) {
@@ -120,6 +123,7 @@ static Ctx make_ctx(const cdb_model* model, void* ws, int rows) {
     c.act = reinterpret_cast<uint16_t*>(c.ws + c.L.act);
     c.part = reinterpret_cast<float*>(c.ws + c.L.part);
     c.rope = reinterpret_cast<float2*>(c.ws + c.L.rope);
+    c.order = reinterpret_cast<int32_t*>(c.ws + c.L.order);
     return c;
 }
 
@@ -138,6 +142,7 @@ static cdb_status run_layers(const Ctx& c, int first, int count, KvTarget kv, co
     const cdb_model_desc& d = *c.md;
     const int M = r.n_rows;
     int pending = 0;  // split-K partials of the previous down projection not yet added to h
+    if (count > 0) HIPCHK(launch_row_order(r.pos, M, c.order, st));
     for (int l = 0; l < count; ++l) {
         const size_t lb = (size_t)(first + l) * c.wl.layer_stride;
         kv.layer = l;
@@ -155,7 +160,7 @@ static cdb_status run_layers(const Ctx& c, int first, int count, KvTarget kv, co
         // attention half: h += down partials; x = RMSNorm(h); q/k/v + RoPE + K/V write
         HIPCHK(launch_resid_norm(c.h, c.part, pending, M, d.d, d.rms_eps, c.x, st));
         HIPCHK(launch_gemm(EPI_QKV, c.x, wptr(c, lb + c.wl.qkv), M, c.gm.qkv, c.part, ea, st));
-        HIPCHK(launch_attention(c.q, kv, r.seq, r.pos, M, d.n_heads, d.head_dim, c.x, c.err, st));
+        HIPCHK(launch_attention(c.q, kv, r.seq, r.pos, c.order, M, d.n_heads, d.head_dim, c.x, c.err, st));
         HIPCHK(launch_gemm(EPI_PARTIAL, c.x, wptr(c, lb + c.wl.o), M, c.gm.o, c.part, ea, st));
         // MLP half: h += O partials; x = RMSNorm(h); act = SwiGLU; down partials
         HIPCHK(launch_resid_norm(c.h, c.part, c.gm.o.S, M, d.d, d.rms_eps, c.x, st));
@@ -335,7 +340,8 @@ cdb_status cdb_boundary_coda(const cdb_model* model, const cdb_kv* kv, const cdb
 }
 
 cdb_status cdb_paged_attention(const cdb_model_desc* desc, const cdb_kv* kv, const cdb_rows* rows, int32_t stage,
-                               int32_t layer, const float* q, void* out, void* ws, size_t ws_bytes, hipStream_t st) {
+                               int32_t layer, const float* q, const int32_t* order, void* out, void* ws,
+                               size_t ws_bytes, hipStream_t st) {
     if (!desc || !kv || !rows || !q || !out || !ws) return CDB_ERR_INVALID_ARG;
     const cdb_model_desc& d = *desc;
     if (!desc_supported(d)) return CDB_ERR_UNSUPPORTED;
@@ -343,14 +349,19 @@ cdb_status cdb_paged_attention(const cdb_model_desc* desc, const cdb_kv* kv, con
     const int layers = stage == 0 ? d.n_prelude : (stage == 1 ? d.n_core : d.n_coda);
     if (layer < 0 || layer >= layers) return CDB_ERR_INVALID_ARG;
     if (rows->n_rows > kMaxRows) return CDB_ERR_CAPACITY;
-    if (ws_bytes < 256) return CDB_ERR_CAPACITY;
+    if (ws_bytes < 256 + (size_t)kMaxRows * 4) return CDB_ERR_CAPACITY;
     if (rows->n_rows == 0) return CDB_OK;
     if (!rows->seq || !rows->pos || (stage == 1 && !rows->c) || !kv->page_table) return CDB_ERR_INVALID_ARG;
     KvTarget t = stage_target(d, *kv, stage);
     if (!t.pool) return CDB_ERR_INVALID_ARG;
     t.layer = layer;
     if (stage == 1) t.c_row = rows->c;
-    HIPCHK(launch_attention(q, t, rows->seq, rows->pos, rows->n_rows, d.n_heads, d.head_dim,
+    if (!order) {
+        int32_t* own = reinterpret_cast<int32_t*>(static_cast<unsigned char*>(ws) + 256);
+        HIPCHK(launch_row_order(rows->pos, rows->n_rows, own, st));
+        order = own;
+    }
+    HIPCHK(launch_attention(q, t, rows->seq, rows->pos, order, rows->n_rows, d.n_heads, d.head_dim,
                             static_cast<uint16_t*>(out), static_cast<int*>(ws), st));
     return CDB_OK;
 }

@@ -42,6 +42,14 @@ __host__ __device__ __forceinline__ int round32(int m) { return (m + 31) & ~31; 
 // or 8 tiles of 32 rows and reads every row of them.
 __host__ __device__ __forceinline__ int gemm_rows(int m) { return m <= 32 ? 32 : m <= 64 ? 64 : m <= 128 ? 128 : 256; }
 
+// Element offset of (layer, page, K/V, head, token) in a stage pool laid out
+// [layers][pages][K, V][heads][16 tokens][hd]: one layer's pages are
+// contiguous, so one layer's working set spans few translation fragments.
+__host__ __device__ __forceinline__ size_t kv_offset(int layer, int pid, int n_pages, int kv, int head, int H, int tok,
+                                                     int hd) {
+    return (((((size_t)layer * n_pages + pid) * 2 + kv) * H + head) * 16 + tok) * (size_t)hd;
+}
+
 // First sticky error wins.
 __device__ __forceinline__ void set_err(int* err, int code) { atomicCAS(err, 0, code); }
 
@@ -87,7 +95,7 @@ struct WeightLayout {
 bool weight_layout(const cdb_model_desc& d, WeightLayout* out);
 
 struct WsLayout {
-    size_t err, h, h_in, q, x, act, part, rope, total;
+    size_t err, h, h_in, q, x, act, part, rope, order, total;
 };
 WsLayout ws_layout(const cdb_model_desc& d, int rows);
 
@@ -97,8 +105,10 @@ bool desc_supported(const cdb_model_desc& d);
 // ---------------------------------------------------------------- launchers
 hipError_t launch_gemm(int epi, const uint16_t* X, const uint16_t* Wp, int M, GemmShape g, float* part,
                        const EpiArgs& ea, hipStream_t st);
-hipError_t launch_attention(const float* q, const KvTarget& kv, const int32_t* seq, const int32_t* pos, int M,
-                            int H, int hd, uint16_t* out, int* err, hipStream_t st);
+// order: the call's rows ranked by descending position (launch_row_order)
+hipError_t launch_attention(const float* q, const KvTarget& kv, const int32_t* seq, const int32_t* pos,
+                            const int32_t* order, int M, int H, int hd, uint16_t* out, int* err, hipStream_t st);
+hipError_t launch_row_order(const int32_t* pos, int M, int32_t* order, hipStream_t st);
 // h[i] += sum over s < S of part[s][i] (split order), then, when out is set,
 // out = bf16(RMSNorm(h)) in fragment layout.
 hipError_t launch_resid_norm(float* h, const float* part, int S, int M, int d, float eps, uint16_t* out,

@@ -78,10 +78,7 @@ __device__ __forceinline__ void epilogue_elem(float val, float partner, int m, i
             set_err(ea.err, CDB_DEV_UNMAPPED_PAGE);
             return;
         }
-        const size_t page_elems = (size_t)kv.n_layers * 2 * ea.H * kPage * ea.hd;
-        const size_t off = (size_t)pid * page_elems +
-                           ((((size_t)kv.layer * 2 + (part - 1)) * ea.H + head) * kPage + (ps % kPage)) * ea.hd + dim;
-        kv.pool[off] = f2bf(outv);
+        kv.pool[kv_offset(kv.layer, pid, kv.n_pages, part - 1, head, ea.H, ps % kPage, ea.hd) + dim] = f2bf(outv);
     }
 }
 

@@ -259,7 +259,6 @@ __global__ __launch_bounds__(256) void k_copy_on_exit(int H, int hd, int r_max, 
         if (threadIdx.x == 0) set_err(err, CDB_DEV_UNMAPPED_PAGE);
         return;
     }
-    const size_t page_elems = (size_t)kv.n_layers * 2 * H * kPage * hd;
     const int vec_per_head = hd / 8;  // 16-byte vectors per (kv, head) entry
     const int nvec = 2 * H * vec_per_head;
     for (int pl = dep + 1; pl <= r_max; ++pl) {
@@ -271,9 +270,10 @@ __global__ __launch_bounds__(256) void k_copy_on_exit(int H, int hd, int r_max, 
         if (dst == src) continue;
         for (int v = threadIdx.x; v < nvec; v += 256) {
             const int kvh = v / vec_per_head, e = v - kvh * vec_per_head;  // kvh = kv*H + head
-            const size_t off = (((size_t)l * 2 * H + kvh) * kPage + (ps % kPage)) * hd + e * 8;
-            *reinterpret_cast<uint4*>(kv.pool + (size_t)dst * page_elems + off) =
-                *reinterpret_cast<const uint4*>(kv.pool + (size_t)src * page_elems + off);
+            const int kvi = kvh / H, hh = kvh - kvi * H;
+            const size_t so = kv_offset(l, src, kv.n_pages, kvi, hh, H, ps % kPage, hd) + e * 8;
+            const size_t dof = kv_offset(l, dst, kv.n_pages, kvi, hh, H, ps % kPage, hd) + e * 8;
+            *reinterpret_cast<uint4*>(kv.pool + dof) = *reinterpret_cast<const uint4*>(kv.pool + so);
         }
     }
 }

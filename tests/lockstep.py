@@ -127,7 +127,7 @@ class Lockstep:
                     gp, opool = self.gkv.coda, self.op.coda
                 else:
                     gp, opool = self.gkv.core, self.op.core
-                g = gp[pid, :, :, :, t % PAGE, :].float().cpu().numpy()
+                g = gp[:, pid, :, :, t % PAGE, :].float().cpu().numpy()  # device pools are layer-major
                 o = opool[pid, :, :, :, t % PAGE, :]
                 d = np.abs(g - o)
                 self.errors["kv_max"] = max(self.errors["kv_max"], float(d.max()))
@@ -136,7 +136,7 @@ class Lockstep:
                 assert not bad.any() and float(d.mean()) <= self.tol[1], \
                     f"{what}: kv plane {plane} seq {q} pos {t}: max {d.max():.3e} mean {d.mean():.3e}"
                 if self.resync:  # oracle entries are bf16 values in bf16-storage mode
-                    gp[pid, :, :, :, t % PAGE, :] = torch.from_numpy(o.astype(np.float32)).to("cuda").to(torch.bfloat16)
+                    gp[:, pid, :, :, t % PAGE, :] = torch.from_numpy(o.astype(np.float32)).to("cuda").to(torch.bfloat16)
 
     # -------------------------------------------------------------- stages
     def prelude(self, seqs, poss, toks):
@@ -325,7 +325,7 @@ def injected_loop_step(shape, weights, rows_np, sample, seed=11, gpu_model=None,
                 op.page_table[j, pl, pg] = nxt_o
                 bits = cdbgen.random_kv_bf16(op.core.shape[1:], seed, stream=int(i) * 1000 + pl * 100 + pg)
                 op.core[nxt_o] = cdbgen.bf16_to_f32(bits)
-                gkv.core[int(pt[i, pl, pg])].copy_(
+                gkv.core[:, int(pt[i, pl, pg])].copy_(
                     torch.from_numpy(bits.view(np.int16)).to("cuda").view(torch.bfloat16))
                 nxt_o += 1
     # states
@@ -376,7 +376,7 @@ def injected_loop_step(shape, weights, rows_np, sample, seed=11, gpu_model=None,
             planes += list(range(int(deps[i]) + 1, R + 1))
         t = int(pos[i])
         for pl in planes:
-            gpage = gkv.core[int(pt[i, pl, t // PAGE])][:, :, :, t % PAGE, :].float().cpu().numpy()
+            gpage = gkv.core[:, int(pt[i, pl, t // PAGE])][:, :, :, t % PAGE, :].float().cpu().numpy()
             opage = op.core[int(op.page_table[j, pl, t // PAGE])][:, :, :, t % PAGE, :]
             dd = np.abs(gpage - opage)
             kv_max = max(kv_max, float(dd.max()))
