@@ -125,6 +125,11 @@ typedef struct {
     int32_t max_seqs, max_pages;
 } cdb_kv;
 
+/* Bytes of one page of a stage's pool (stage 0 prelude, 1 core, 2 coda): the
+ * stage's layers x 2 x n_heads x 16 x head_dim bf16; 0 if the stage has no
+ * layers or the shape is unsupported. */
+size_t cdb_kv_page_bytes(const cdb_model_desc* desc, int32_t stage);
+
 /* Per-token latent state (device, fp32): h [n_slots][d]; e [n_slots][d] holds
  * the prelude output for injection models (may be NULL otherwise). */
 typedef struct {

@@ -1,0 +1,118 @@
+/*
+ * libcdb driver -- host-side continuous-depth-batching scheduler (paper
+ * Section 4.1) over the libcdb stage calls.  Not part of the optimised path:
+ * it decides which rows each stage call gets, maps KV pages, and enqueues the
+ * calls; it never reads device results back (exit decisions are replayed from
+ * each sequence's depth table, App. B.2).
+ *
+ * Two queues: the boundary queue (tokens that left the core -> coda, then the
+ * prelude of their next input; newly admitted sequences -> prelude) and the
+ * loop queue (tokens in the core).  Boundary work runs first once
+ * min_coda_batch exits are waiting, or when no loop work is left.
+ *   refill       running loop rows stay in the batch; freed rows are filled
+ *                from the loop queue at the next step (Section 4.1, Fig. 1)
+ *   no-refill    a batch is formed once per round and shrinks until all its
+ *                tokens exited; coda and prelude then run for the round
+ *   fixed_depth  every token runs r_max loops (continuous batching baseline)
+ * Pages: every plane of a sequence is mapped at admission (lowest free id
+ * first, (sequence, page, plane) order) and released when it finishes.
+ */
+#ifndef LIBCDB_DRIVER_H
+#define LIBCDB_DRIVER_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "libcdb.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct cdb_driver cdb_driver;
+
+typedef struct {
+    int32_t max_batch;       /* rows per loop step (<= 256) */
+    int32_t max_active;      /* sequences in flight at once */
+    int32_t refill;          /* 1 refill, 0 no-refill */
+    int32_t fixed_depth;     /* 1: every token loops r_max times */
+    int32_t min_coda_batch;  /* exits to accumulate before the coda runs (>= 1) */
+    int32_t r_max;
+    int32_t has_prelude, has_coda;  /* whether the model has prelude / coda layers (their pools are used) */
+    int32_t max_seqs, max_pages;    /* page-table shape [max_seqs][r_max + 2][max_pages] */
+    int32_t pre_pages, core_pages, coda_pages;  /* pool sizes */
+    int32_t kv_layout;              /* CDB_KV_FULL, CDB_KV_SHARED or CDB_KV_FIRST_THEN_SHARED */
+} cdb_driver_config;
+
+/* Core KV layouts (Section 4.2, App. C.1, Table 1), all by page-table aliasing:
+ *   FULL              one page per core plane (depth-indexed, last-exited copies)
+ *   SHARED            every core plane maps the same page: one slot per layer,
+ *                     overwritten at every loop
+ *   FIRST_THEN_SHARED plane 1 private, planes 2..r_max share a second page */
+enum { CDB_KV_FULL = 0, CDB_KV_SHARED = 1, CDB_KV_FIRST_THEN_SHARED = 2 };
+
+enum { CDB_TICK_NONE = 0, CDB_TICK_PRELUDE_FIRST = 1, CDB_TICK_LOOP = 2, CDB_TICK_CODA = 3 };
+
+/* One planned stage call (host arrays of up to 256 rows).  For CDB_TICK_CODA
+ * the first n_continue rows continue (the prelude of their next input follows
+ * in the same tick, at pos + 1); the rest finish their sequence. */
+typedef struct {
+    int32_t stage;
+    int32_t n_rows, n_continue;
+    int32_t slot[256], seq[256], pos[256], c[256], depth[256], decode_index[256];
+    double wait_until;
+} cdb_driver_tick;
+
+typedef struct {
+    int64_t loop_steps, loop_rows, idle_rows;  /* idle_rows: max_batch - rows, summed over loop steps */
+    int64_t coda_calls, coda_rows, prelude_calls, prelude_rows;
+    int64_t tokens;                            /* decode tokens finished (coda rows) */
+} cdb_driver_stats;
+
+cdb_driver* cdb_driver_create(const cdb_driver_config* cfg);
+void cdb_driver_destroy(cdb_driver* d);
+
+/* Adds a request in arrival order: its prompt (already prefilled: its KV must
+ * be present when the sequence is admitted) and the exit depth of each of its
+ * n_decode decode inputs.  Returns the sequence id (= its row of the page
+ * table and its state slot) or -1. */
+int32_t cdb_driver_add_sequence(cdb_driver* d, int32_t prompt_len, int32_t n_decode, const int32_t* depths,
+                                double arrival);
+
+/* Host page table [max_seqs][r_max + 2][max_pages] as the driver maintains it. */
+const int32_t* cdb_driver_page_table(cdb_driver* d);
+
+/* Scheduler stepping without a device (tests, simulations): next() plans a
+ * call (1), reports completion of all work (0) or that nothing can run before
+ * t->wait_until (-1); complete() applies a planned call's effect. */
+int32_t cdb_driver_next(cdb_driver* d, cdb_driver_tick* t);
+int32_t cdb_driver_complete(cdb_driver* d, const cdb_driver_tick* t);
+void cdb_driver_set_time(cdb_driver* d, double now_seconds);
+
+int32_t cdb_driver_get_stats(const cdb_driver* d, cdb_driver_stats* out);
+
+/* Pages currently mapped in each pool (aliased pages count once). */
+int32_t cdb_driver_pages_in_use(const cdb_driver* d, int32_t* pre, int32_t* core, int32_t* coda);
+
+/* Normalised latency per sequence (finish - arrival) / n_decode, in seconds;
+ * -1 for unfinished ones.  Returns the number written. */
+int32_t cdb_driver_latencies(const cdb_driver* d, double* normalized, int32_t n);
+
+/* Device scratch cdb_driver_run needs for a model with `vocab` logits. */
+size_t cdb_driver_scratch_bytes(int32_t vocab);
+
+/* Runs every added request to completion on the device: plans each call,
+ * stages its rows through pinned host memory, enqueues the stage call on
+ * `stream`.  first_tokens (host, per sequence) is each sequence's first decode
+ * input; later inputs are the coda's greedy ids, passed on device.  The page
+ * table in kv->page_table (device) is overwritten from the driver's.
+ * scratch: device, cdb_driver_scratch_bytes(vocab).  Returns a cdb_status;
+ * *seconds = wall time including the final synchronisation. */
+int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, const cdb_state* state, void* scratch,
+                       size_t scratch_bytes, const int32_t* first_tokens, void* ws, size_t ws_bytes,
+                       hipStream_t stream, double* seconds);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -52,7 +52,9 @@ def lib(acc32: bool = False):
 class OrcDesc(C.Structure):
     _fields_ = [(n, C.c_int32) for n in ("d", "n_heads", "head_dim", "d_ff", "vocab", "n_prelude", "n_core",
                                           "n_coda", "r_max", "injection", "exit_kind", "bf16_storage")] + \
-               [("rms_eps", C.c_double), ("rope_base", C.c_double)]
+               [("rms_eps", C.c_double), ("rope_base", C.c_double), ("kv_layout", C.c_int32)]
+
+KV_FULL, KV_SHARED, KV_FIRST_THEN_SHARED = 0, 1, 2
 
 
 class OrcWeights(C.Structure):
@@ -72,8 +74,8 @@ _I = C.c_int32
 
 
 def _declare(L):
-    L.orc_ref_sequence.argtypes = [_P, _P, _I, _P, _I, _P, _P, _P, _P, _P]
-    L.orc_brute_force.argtypes = [_P, _P, _I, _P, _P, _P, _P, _P]
+    L.orc_ref_sequence.argtypes = [_P, _P, _I, _P, _I, _I, _P, _P, _P, _P, _P]
+    L.orc_brute_force.argtypes = [_P, _P, _I, _P, _I, _P, _P, _P, _P]
     L.orc_prelude.argtypes = [_P, _P, _P, _P, _P, _I, _I, _P, _P, _P, _P]
     L.orc_loop_step.argtypes = [_P, _P, _P, _P, _P, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]
     L.orc_coda.argtypes = [_P, _P, _P, _P, _I, _I, _P, _P, _P, _P, _P]
@@ -102,13 +104,16 @@ class Model:
     """Oracle model: a shape (cdbgen.ModelShape), bf16-bit weights, and the
     storage mode (bf16_storage=True rounds what the model keeps in bf16)."""
 
-    def __init__(self, shape, weights: Dict[str, object], bf16_storage: bool = True, acc32: bool = False):
-        """acc32: run the same steps with fp32 accumulators (tolerance sizing only)."""
+    def __init__(self, shape, weights: Dict[str, object], bf16_storage: bool = True, acc32: bool = False,
+                 kv_layout: int = KV_FULL):
+        """acc32: run the same steps with fp32 accumulators (tolerance sizing only).
+        kv_layout: the core KV layout the dense references follow (the paged
+        operators follow whatever the page table maps)."""
         self.shape = shape
         self.L = lib(acc32)
         self.desc = OrcDesc(shape.d, shape.n_heads, shape.head_dim, shape.d_ff, shape.vocab, shape.n_prelude,
                             shape.n_core, shape.n_coda, shape.r_max, shape.injection, shape.exit_kind,
-                            1 if bf16_storage else 0, shape.rms_eps, shape.rope_base)
+                            1 if bf16_storage else 0, shape.rms_eps, shape.rope_base, kv_layout)
         self._keep = []
         names = ("q", "k", "v", "o", "gate", "up", "down")
         ptrs = []
@@ -129,32 +134,38 @@ class Model:
                             C.cast(self._layer_ptrs, C.POINTER(C.c_void_p)))
 
     # -- dense references -------------------------------------------------
-    def ref_sequence(self, tokens, depth, n_given: Optional[int] = None, want_kv: bool = False):
+    def ref_sequence(self, tokens, depth, n_given: Optional[int] = None, want_kv: bool = False,
+                     n_prefill: Optional[int] = None):
+        """n_given: leading tokens taken as given (the rest are greedy);
+        n_prefill: leading tokens run as one prefill block (default n_given)."""
         s = self.shape
         tok = _c(tokens, np.int32).copy()
         dep = _c(depth, np.int32)
         T = len(tok)
         n_given = T if n_given is None else n_given
+        n_prefill = n_given if n_prefill is None else n_prefill
         logits = np.zeros((T, s.vocab))
         h = np.zeros((T, s.d))
         scores = np.zeros((T, s.r_max))
         kv = np.zeros((T, s.r_max, s.n_core, 2, s.d)) if want_kv else None
-        rc = self.L.orc_ref_sequence(C.byref(self.desc), C.byref(self.w), T, _ptr(tok), n_given, _ptr(dep),
-                                    _ptr(logits), _ptr(h), _ptr(scores), _ptr(kv))
+        rc = self.L.orc_ref_sequence(C.byref(self.desc), C.byref(self.w), T, _ptr(tok), n_given, n_prefill,
+                                    _ptr(dep), _ptr(logits), _ptr(h), _ptr(scores), _ptr(kv))
         if rc != ORC_OK:
             raise ValueError(f"orc_ref_sequence: {rc}")
         return {"tokens": tok, "logits": logits, "h": h, "scores": scores, "core_kv": kv}
 
-    def brute_force(self, tokens, depth):
+    def brute_force(self, tokens, depth, n_prefill: Optional[int] = None):
+        """n_prefill: leading tokens run as one prefill block (default all)."""
         s = self.shape
         tok = _c(tokens, np.int32)
         dep = _c(depth, np.int32)
         T = len(tok)
+        n_prefill = T if n_prefill is None else n_prefill
         logits = np.zeros((T, s.vocab))
         h = np.zeros((T, s.d))
         scores = np.zeros((T, s.r_max))
-        rc = self.L.orc_brute_force(C.byref(self.desc), C.byref(self.w), T, _ptr(tok), _ptr(dep), _ptr(logits),
-                                   _ptr(h), _ptr(scores))
+        rc = self.L.orc_brute_force(C.byref(self.desc), C.byref(self.w), T, _ptr(tok), n_prefill, _ptr(dep),
+                                   _ptr(logits), _ptr(h), _ptr(scores))
         if rc != ORC_OK:
             raise ValueError(f"orc_brute_force: {rc}")
         return {"logits": logits, "h": h, "scores": scores}

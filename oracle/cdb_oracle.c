@@ -30,6 +30,14 @@
  * or, for the convergence criterion (App. C.2), the L2 distance between the
  * states before and after the loop.
  *
+ * Other core KV layouts (Section 4.2; App. C.1, Table 1): with a single shared
+ * slot per layer, every loop overwrites the token's one K/V entry, so a later
+ * token reads each earlier token's most recent state -- that of its final loop
+ * d_s -- at every loop; with first-then-shared, loop 1 keeps a private slot and
+ * loops 2..r_max share a second one, so loop 1 reads loop 1 and later loops
+ * read loop d_s (a token that exits after loop 1 has its loop-1 state copied
+ * into the shared slot by the same last-exited rule).
+ *
  * Three independent executors are provided:
  *   orc_brute_force   -- no cache at all: every position is recomputed from the
  *                        token sequence, reading earlier tokens' K/V of loop
@@ -55,6 +63,23 @@
 #define ORC_ACC double
 #endif
 typedef ORC_ACC acc_t;
+
+/* ------------------------------------------------------------------ layouts */
+
+/* The loop of an earlier token s (exit depth ds) whose K/V a token at loop r
+ * attends to, by definition of the layout. */
+static int read_loop(int layout, int r, int ds) {
+    if (layout == ORC_KV_SHARED) return ds;
+    if (layout == ORC_KV_FIRST_THEN_SHARED) return r == 1 ? 1 : ds;
+    return r < ds ? r : ds;
+}
+
+/* The physical slot (0-based) that loop r writes in a dense per-token cache. */
+static int write_slot(int layout, int r) {
+    if (layout == ORC_KV_SHARED) return 0;
+    if (layout == ORC_KV_FIRST_THEN_SHARED) return r == 1 ? 0 : 1;
+    return r - 1;
+}
 
 /* ------------------------------------------------------------------ scalars */
 
@@ -313,71 +338,100 @@ static void run_layer(const orc_desc* m, const orc_weights* w, int layer, double
     free(q);
 }
 
+/* Tokens are processed in blocks: the first n_prefill tokens form one prefill
+ * block, run loop by loop over the whole block (every block token finishes
+ * loop r before any starts loop r + 1); each later token is a block of its
+ * own.  Under the full layout the blocking changes nothing; under the shared
+ * layouts it decides which state of an earlier token is the most recent one
+ * when it is read (within a block: the loop being run). */
 int orc_ref_sequence(const orc_desc* m, const orc_weights* w, int32_t T, int32_t* tokens, int32_t n_given,
-                     const int32_t* depth, double* logits_out, double* h_out, double* scores_out,
+                     int32_t n_prefill, const int32_t* depth, double* logits_out, double* h_out, double* scores_out,
                      double* core_kv_out) {
     int d = m->d, R = m->r_max;
+    if (n_prefill < 0 || n_prefill > n_given || n_prefill > T) return ORC_ERR_ARG;
     for (int t = 0; t < T; ++t)
         if (depth[t] < 1 || depth[t] > R) return ORC_ERR_ARG;
     dense_kv kv;
     dense_alloc(&kv, m, T);
-    double* h = (double*)malloc(sizeof(double) * (size_t)d);
-    double* e = (double*)malloc(sizeof(double) * (size_t)d);
+    const int maxb = n_prefill > 1 ? n_prefill : 1;
+    double* hb = (double*)malloc(sizeof(double) * (size_t)maxb * d); /* per block token: h */
+    double* eb = (double*)malloc(sizeof(double) * (size_t)maxb * d); /* per block token: e */
     double* hp = (double*)malloc(sizeof(double) * (size_t)d);
     double* logits = (double*)malloc(sizeof(double) * (size_t)m->vocab);
     const double** kr = (const double**)malloc(sizeof(double*) * (size_t)T);
     const double** vr = (const double**)malloc(sizeof(double*) * (size_t)T);
 
-    for (int t = 0; t < T; ++t) {
-        embed(m, w, tokens[t], h);
-        for (int l = 0; l < m->n_prelude; ++l) {
-            for (int s = 0; s < t; ++s) {
-                kr[s] = dk_pre(&kv, s, l, 0);
-                vr[s] = dk_pre(&kv, s, l, 1);
-            }
-            run_layer(m, w, l, h, t, dk_pre(&kv, t, l, 0), dk_pre(&kv, t, l, 1), kr, vr);
-        }
-        memcpy(e, h, sizeof(double) * (size_t)d);
-        for (int r = 1; r <= depth[t]; ++r) {
-            memcpy(hp, h, sizeof(double) * (size_t)d);
-            core_input(m, w, hp, e, h);
-            for (int l = 0; l < m->n_core; ++l) {
+    for (int b0 = 0; b0 < T;) {
+        const int b1 = b0 < n_prefill ? n_prefill : b0 + 1; /* block [b0, b1) */
+        for (int t = b0; t < b1; ++t) {
+            double* h = hb + (size_t)(t - b0) * d;
+            embed(m, w, tokens[t], h);
+            for (int l = 0; l < m->n_prelude; ++l) {
                 for (int s = 0; s < t; ++s) {
-                    kr[s] = dk_core(&kv, s, r - 1, l, 0);
-                    vr[s] = dk_core(&kv, s, r - 1, l, 1);
+                    kr[s] = dk_pre(&kv, s, l, 0);
+                    vr[s] = dk_pre(&kv, s, l, 1);
                 }
-                run_layer(m, w, m->n_prelude + l, h, t, dk_core(&kv, t, r - 1, l, 0),
-                          dk_core(&kv, t, r - 1, l, 1), kr, vr);
+                run_layer(m, w, l, h, t, dk_pre(&kv, t, l, 0), dk_pre(&kv, t, l, 1), kr, vr);
             }
-            if (scores_out) scores_out[(size_t)t * R + (r - 1)] = exit_score(m, w, h, hp);
+            memcpy(eb + (size_t)(t - b0) * d, h, sizeof(double) * (size_t)d);
         }
-        if (scores_out)
-            for (int r = depth[t] + 1; r <= R; ++r) scores_out[(size_t)t * R + (r - 1)] = NAN;
-        /* last-exited cache: planes depth..R-1 receive a copy of plane depth-1 */
-        for (int p = depth[t]; p < R; ++p)
-            for (int l = 0; l < m->n_core; ++l)
-                for (int kvi = 0; kvi < 2; ++kvi)
-                    memcpy(dk_core(&kv, t, p, l, kvi), dk_core(&kv, t, depth[t] - 1, l, kvi),
-                           sizeof(double) * (size_t)d);
-        if (h_out) memcpy(h_out + (size_t)t * d, h, sizeof(double) * (size_t)d);
-        for (int l = 0; l < m->n_coda; ++l) {
-            for (int s = 0; s < t; ++s) {
-                kr[s] = dk_coda(&kv, s, l, 0);
-                vr[s] = dk_coda(&kv, s, l, 1);
+        for (int r = 1; r <= R; ++r) {
+            const int slot = write_slot(m->kv_layout, r);
+            for (int t = b0; t < b1; ++t) {
+                if (depth[t] < r) continue;
+                double* h = hb + (size_t)(t - b0) * d;
+                memcpy(hp, h, sizeof(double) * (size_t)d);
+                core_input(m, w, hp, eb + (size_t)(t - b0) * d, h);
+                for (int l = 0; l < m->n_core; ++l) {
+                    for (int s = 0; s < t; ++s) {
+                        kr[s] = dk_core(&kv, s, slot, l, 0);
+                        vr[s] = dk_core(&kv, s, slot, l, 1);
+                    }
+                    run_layer(m, w, m->n_prelude + l, h, t, dk_core(&kv, t, slot, l, 0),
+                              dk_core(&kv, t, slot, l, 1), kr, vr);
+                }
+                if (scores_out) scores_out[(size_t)t * R + (r - 1)] = exit_score(m, w, h, hp);
             }
-            run_layer(m, w, m->n_prelude + m->n_core + l, h, t, dk_coda(&kv, t, l, 0), dk_coda(&kv, t, l, 1),
-                      kr, vr);
+            /* last-exited cache: a token that exits after loop r gets the slots
+             * of loops r+1..R filled with a copy of the slot of loop r (nothing
+             * to do where they are the same slot) */
+            for (int t = b0; t < b1; ++t) {
+                if (depth[t] != r) continue;
+                for (int r2 = r + 1; r2 <= R; ++r2) {
+                    const int dst = write_slot(m->kv_layout, r2);
+                    if (dst == slot) continue;
+                    for (int l = 0; l < m->n_core; ++l)
+                        for (int kvi = 0; kvi < 2; ++kvi)
+                            memcpy(dk_core(&kv, t, dst, l, kvi), dk_core(&kv, t, slot, l, kvi),
+                                   sizeof(double) * (size_t)d);
+                }
+            }
         }
-        int32_t nxt = lm_head(m, w, h, logits);
-        if (logits_out) memcpy(logits_out + (size_t)t * m->vocab, logits, sizeof(double) * (size_t)m->vocab);
-        if (t + 1 < T && t + 1 >= n_given) tokens[t + 1] = nxt;
+        for (int t = b0; t < b1; ++t) {
+            double* h = hb + (size_t)(t - b0) * d;
+            if (scores_out)
+                for (int r = depth[t] + 1; r <= R; ++r) scores_out[(size_t)t * R + (r - 1)] = NAN;
+            if (h_out) memcpy(h_out + (size_t)t * d, h, sizeof(double) * (size_t)d);
+            for (int l = 0; l < m->n_coda; ++l) {
+                for (int s = 0; s < t; ++s) {
+                    kr[s] = dk_coda(&kv, s, l, 0);
+                    vr[s] = dk_coda(&kv, s, l, 1);
+                }
+                run_layer(m, w, m->n_prelude + m->n_core + l, h, t, dk_coda(&kv, t, l, 0), dk_coda(&kv, t, l, 1),
+                          kr, vr);
+            }
+            int32_t nxt = lm_head(m, w, h, logits);
+            if (logits_out) memcpy(logits_out + (size_t)t * m->vocab, logits, sizeof(double) * (size_t)m->vocab);
+            if (t + 1 < T && t + 1 >= n_given) tokens[t + 1] = nxt;
+        }
+        b0 = b1;
     }
     if (core_kv_out)
         memcpy(core_kv_out, kv.core, sizeof(double) * (size_t)T * R * m->n_core * 2 * d);
     free(kr);
     free(vr);
-    free(h);
-    free(e);
+    free(hb);
+    free(eb);
     free(hp);
     free(logits);
     dense_free(&kv);
@@ -385,11 +439,15 @@ int orc_ref_sequence(const orc_desc* m, const orc_weights* w, int32_t T, int32_t
 }
 
 /* No cache: for every position t the whole prefix 0..t is recomputed from the
- * tokens; a token at loop r reads earlier token s's K/V of loop min(r, d_s),
- * indexed directly (no copy-on-exit). */
-int orc_brute_force(const orc_desc* m, const orc_weights* w, int32_t T, const int32_t* tokens,
+ * tokens; a token at loop r reads earlier token s's K/V of loop
+ * read_loop(layout, r, d_s) -- min(r, d_s) for the full layout -- indexed
+ * directly by loop (no copy-on-exit, no slot sharing).  Within the prefill
+ * block (both tokens below n_prefill) s's most recent state at loop r is that
+ * of loop min(r, d_s) under every layout. */
+int orc_brute_force(const orc_desc* m, const orc_weights* w, int32_t T, const int32_t* tokens, int32_t n_prefill,
                     const int32_t* depth, double* logits_out, double* h_out, double* scores_out) {
     int d = m->d, R = m->r_max;
+    if (n_prefill < 0 || n_prefill > T) return ORC_ERR_ARG;
     for (int t = 0; t < T; ++t)
         if (depth[t] < 1 || depth[t] > R) return ORC_ERR_ARG;
     double* h = (double*)malloc(sizeof(double) * (size_t)d);
@@ -417,7 +475,8 @@ int orc_brute_force(const orc_desc* m, const orc_weights* w, int32_t T, const in
                 core_input(m, w, hp, e, h);
                 for (int l = 0; l < m->n_core; ++l) {
                     for (int s = 0; s < t; ++s) {
-                        int rs = r < depth[s] ? r : depth[s];
+                        const int rs = t < n_prefill ? (r < depth[s] ? r : depth[s])
+                                                     : read_loop(m->kv_layout, r, depth[s]);
                         kr[s] = dk_core(&kv, s, rs - 1, l, 0);
                         vr[s] = dk_core(&kv, s, rs - 1, l, 1);
                     }

@@ -20,7 +20,11 @@ typedef struct {
     int32_t exit_kind;    /* 0: sigmoid(w_exit . RMSNorm(h)); 1: ||h_new - h_old||_2 */
     int32_t bf16_storage; /* 1: round the values the model stores in bf16 */
     double rms_eps, rope_base;
+    int32_t kv_layout;    /* core KV layout: ORC_KV_FULL, ORC_KV_SHARED, ORC_KV_FIRST_THEN_SHARED */
 } orc_desc;
+
+/* Core KV layouts (Section 4.2; App. C.1, Table 1). */
+enum { ORC_KV_FULL = 0, ORC_KV_SHARED = 1, ORC_KV_FIRST_THEN_SHARED = 2 };
 
 typedef struct {
     const uint16_t* embed;        /* [vocab][d] */
@@ -41,9 +45,9 @@ typedef struct {
 } orc_paged;
 
 int orc_ref_sequence(const orc_desc* m, const orc_weights* w, int32_t T, int32_t* tokens, int32_t n_given,
-                     const int32_t* depth, double* logits_out, double* h_out, double* scores_out,
+                     int32_t n_prefill, const int32_t* depth, double* logits_out, double* h_out, double* scores_out,
                      double* core_kv_out);
-int orc_brute_force(const orc_desc* m, const orc_weights* w, int32_t T, const int32_t* tokens,
+int orc_brute_force(const orc_desc* m, const orc_weights* w, int32_t T, const int32_t* tokens, int32_t n_prefill,
                     const int32_t* depth, double* logits_out, double* h_out, double* scores_out);
 int orc_prelude(const orc_desc* m, const orc_weights* w, const orc_paged* p, double* state_h, double* state_e,
                 int32_t n_slots, int32_t n, const int32_t* slot, const int32_t* seq, const int32_t* pos,

@@ -9,7 +9,10 @@ changing the model's predictions, Section 3).
 
 Prompt tokens run at depth r_max; decode tokens use their depth-table entry.
 Pages: lowest free id first, every page of a sequence and every plane mapped
-at admission, in (sequence, page index, plane) order.
+at admission, in (sequence, page index, plane) order.  The shared core
+layouts (Section 4.2; App. C.1) are page-table aliasing: under the single
+shared slot every core plane of a token page maps one page; under
+first-then-shared plane 1 has its own page and planes 2..r_max share another.
 """
 from __future__ import annotations
 
@@ -18,7 +21,7 @@ from typing import Dict, List, Optional
 
 import numpy as np
 
-from . import Model, Paged, coda, loop_step, prelude
+from . import KV_FIRST_THEN_SHARED, KV_FULL, KV_SHARED, Model, Paged, coda, loop_step, prelude
 
 PAGE = 16
 
@@ -34,8 +37,18 @@ class Allocator:
         return self.free.pop(0)
 
 
+def core_pages_per_page(r_max: int, kv_layout: int) -> int:
+    """Distinct core pages behind one 16-token page of a sequence."""
+    if kv_layout == KV_SHARED:
+        return 1
+    if kv_layout == KV_FIRST_THEN_SHARED:
+        return min(2, r_max)
+    return r_max
+
+
 def run(model: Model, prompts: List[np.ndarray], n_decode: List[int], depths: List[np.ndarray],
-        forced: Optional[List[np.ndarray]] = None, max_batch: int = 4) -> List[Dict[str, np.ndarray]]:
+        forced: Optional[List[np.ndarray]] = None, max_batch: int = 4,
+        kv_layout: int = KV_FULL) -> List[Dict[str, np.ndarray]]:
     """Decode every sequence with the refill policy.
 
     prompts[i]: prompt ids; n_decode[i]: decode inputs; depths[i]: exit depth per
@@ -49,11 +62,13 @@ def run(model: Model, prompts: List[np.ndarray], n_decode: List[int], depths: Li
     T = [len(p) + n for p, n in zip(prompts, n_decode)]
     max_pages = max((t + PAGE - 1) // PAGE for t in T)
     tot_pages = sum((t + PAGE - 1) // PAGE for t in T)
-    paged = Paged(s, n_seq, max_pages, tot_pages if s.n_prelude else 0, tot_pages * R,
+    n_core_pages = tot_pages * core_pages_per_page(R, kv_layout)
+    paged = Paged(s, n_seq, max_pages, tot_pages if s.n_prelude else 0, n_core_pages,
                   tot_pages if s.n_coda else 0)
-    a_pre, a_core, a_coda = Allocator(tot_pages), Allocator(tot_pages * R), Allocator(tot_pages)
+    a_pre, a_core, a_coda = Allocator(tot_pages), Allocator(n_core_pages), Allocator(tot_pages)
     for q in range(n_seq):
         for pg in range((T[q] + PAGE - 1) // PAGE):
+            shared = -1
             for plane in range(R + 2):
                 if plane == 0:
                     if s.n_prelude:
@@ -61,6 +76,10 @@ def run(model: Model, prompts: List[np.ndarray], n_decode: List[int], depths: Li
                 elif plane == R + 1:
                     if s.n_coda:
                         paged.page_table[q, plane, pg] = a_coda.take()
+                elif kv_layout == KV_SHARED or (kv_layout == KV_FIRST_THEN_SHARED and plane >= 2):
+                    if shared < 0:
+                        shared = a_core.take()
+                    paged.page_table[q, plane, pg] = shared
                 else:
                     paged.page_table[q, plane, pg] = a_core.take()
 

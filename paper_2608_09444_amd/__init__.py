@@ -19,9 +19,9 @@ CDB_DEV_OK, CDB_DEV_UNMAPPED_PAGE, CDB_DEV_BAD_DEPTH, CDB_DEV_BAD_INDEX = range(
 PAGE_TOKENS = 16
 MAX_ROWS = 256
 
-EXPORTED = ("cdb_packed_weight_bytes", "cdb_pack_weights", "cdb_workspace_bytes", "cdb_workspace_init",
-            "cdb_boundary_prelude", "cdb_loop_step", "cdb_boundary_coda", "cdb_paged_attention",
-            "cdb_read_device_error", "cdb_status_str")
+EXPORTED = ("cdb_packed_weight_bytes", "cdb_pack_weights", "cdb_kv_page_bytes", "cdb_workspace_bytes",
+            "cdb_workspace_init", "cdb_boundary_prelude", "cdb_loop_step", "cdb_boundary_coda",
+            "cdb_paged_attention", "cdb_read_device_error", "cdb_status_str")
 
 
 class CdbError(RuntimeError):
@@ -79,6 +79,8 @@ def lib() -> C.CDLL:
         L.cdb_packed_weight_bytes.argtypes = [P]
         L.cdb_packed_weight_bytes.restype = S
         L.cdb_pack_weights.argtypes = [P, P, P, S, P]
+        L.cdb_kv_page_bytes.argtypes = [P, I]
+        L.cdb_kv_page_bytes.restype = S
         L.cdb_workspace_bytes.argtypes = [P, I]
         L.cdb_workspace_bytes.restype = S
         L.cdb_workspace_init.argtypes = [P, S, P]
@@ -131,6 +133,10 @@ def cdb_packed_weight_bytes(desc: cdb_model_desc) -> int:
 def cdb_pack_weights(desc: cdb_model_desc, w: cdb_plain_weights, packed, stream=None):
     _check("cdb_pack_weights", lib().cdb_pack_weights(C.byref(desc), C.byref(w), _ptr(packed),
                                                       packed.numel() * packed.element_size(), _stream(stream)))
+
+
+def cdb_kv_page_bytes(desc: cdb_model_desc, stage: int) -> int:
+    return lib().cdb_kv_page_bytes(C.byref(desc), stage)
 
 
 def cdb_workspace_bytes(desc: cdb_model_desc, max_rows: int) -> int:

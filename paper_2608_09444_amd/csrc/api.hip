@@ -258,6 +258,12 @@ cdb_status cdb_pack_weights(const cdb_model_desc* desc, const cdb_plain_weights*
     return CDB_OK;
 }
 
+size_t cdb_kv_page_bytes(const cdb_model_desc* desc, int32_t stage) {
+    if (!desc || !desc_supported(*desc) || stage < 0 || stage > 2) return 0;
+    const int layers = stage == 0 ? desc->n_prelude : (stage == 1 ? desc->n_core : desc->n_coda);
+    return (size_t)layers * 2 * desc->n_heads * kPage * desc->head_dim * 2;
+}
+
 size_t cdb_workspace_bytes(const cdb_model_desc* desc, int32_t max_rows) {
     if (!desc || !desc_supported(*desc) || max_rows < 0 || max_rows > kMaxRows) return 0;
     return ws_layout(*desc, max_rows).total;

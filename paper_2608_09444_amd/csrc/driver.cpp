@@ -1,0 +1,516 @@
+// Host driver for continuous depth batching (paper Section 4.1): a two-queue
+// scheduler (boundary stages, loop steps) that builds every stage call's
+// batch, a page allocator, and a runner that enqueues the libcdb stage calls.
+//
+// Scheduling (host only, no device access):
+//  * Sequences are admitted in arrival order while fewer than `max_active` are
+//    in flight and their pages fit; pages of every plane are mapped at
+//    admission, lowest free id first.
+//  * Boundary queue: tokens that just exited the core (coda, then the prelude
+//    of the next token) and newly admitted sequences (prelude of the first
+//    decode input).  It runs first when it holds at least `min_coda_batch`
+//    exits, or when no loop work is left (Section 4.1: coda has priority, the
+//    prelude follows it directly; a minimum coda batch lets exits accumulate).
+//  * Loop queue: tokens in the core.  Refill mode keeps the rows of the
+//    running batch at the front and fills freed rows from the queue; no-refill
+//    mode forms a batch once per round and lets it shrink until every token has
+//    exited (Section 4.1, Fig. 1 right).  Fixed-depth mode runs every token for
+//    r_max loops (continuous batching, the baseline the paper compares with).
+//  * Exit decisions are replayed from each sequence's depth table
+//    (App. B.2), so the host knows every exit without reading the device.
+//
+// Running (cdb_driver_run): each tick's rows go through pinned host buffers and
+// one asynchronous copy to the device, then the stage call; the coda batch
+// lists continuing sequences first, so its device-side next-token ids are the
+// prelude's tokens for the next tick without any host round trip.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <algorithm>
+#include <chrono>
+#include <deque>
+#include <vector>
+
+#include "../../include/libcdb.h"
+#include "../../include/libcdb_driver.h"
+
+namespace {
+
+enum SeqState { WAITING = 0, PRELUDE = 1, LOOP = 2, EXITED = 3, DONE = 4 };
+
+struct Seq {
+    int32_t prompt_len = 0, n_decode = 0;
+    std::vector<int32_t> depth;  // per decode input
+    double arrival = 0.0;
+    int state = WAITING;
+    int32_t t = 0;  // decode input index of the token in flight (position prompt_len + t)
+    int32_t c = 0;  // loops completed by that token
+    int32_t pages = 0;
+    double admit_time = -1.0, done_time = -1.0;
+};
+
+struct Allocator {
+    std::vector<int32_t> free_ids;  // kept sorted descending: back() is the lowest
+    explicit Allocator(int32_t n = 0) {
+        for (int32_t i = n - 1; i >= 0; --i) free_ids.push_back(i);
+    }
+    int32_t available() const { return (int32_t)free_ids.size(); }
+    int32_t take() {
+        const int32_t id = free_ids.back();
+        free_ids.pop_back();
+        return id;
+    }
+    void give(int32_t id) {
+        free_ids.insert(std::upper_bound(free_ids.begin(), free_ids.end(), id, std::greater<int32_t>()), id);
+    }
+};
+
+}  // namespace
+
+struct cdb_driver {
+    cdb_driver_config cfg;
+    std::vector<Seq> seqs;
+    std::vector<int32_t> page_table;  // [max_seqs][r_max + 2][max_pages]
+    Allocator pre, core, coda;
+    size_t next_arrival = 0;  // index into seqs in arrival order (sequences are added in arrival order)
+    int32_t active = 0;
+    std::deque<int32_t> exited;   // sequences whose token left the core, awaiting the coda
+    std::deque<int32_t> fresh;    // admitted sequences awaiting the prelude of their first input
+    std::deque<int32_t> loopq;    // sequences whose token waits for its next loop
+    std::vector<int32_t> batch;   // rows of the running loop batch (refill keeps it)
+    bool round_open = false;      // no-refill: a round is running
+    cdb_driver_stats stats;
+    double now = 0.0;  // seconds, advanced by the runner (or by tests)
+    bool table_dirty = true;
+};
+
+static int32_t planes(const cdb_driver* d) { return d->cfg.r_max + 2; }
+
+static int32_t depth_of(const cdb_driver* d, const Seq& s) {
+    if (d->cfg.fixed_depth) return d->cfg.r_max;
+    return s.depth[s.t];
+}
+
+// Distinct core pages per token page under the layout.
+static int32_t core_slots(const cdb_driver* d) {
+    if (d->cfg.kv_layout == CDB_KV_SHARED) return 1;
+    if (d->cfg.kv_layout == CDB_KV_FIRST_THEN_SHARED) return d->cfg.r_max > 1 ? 2 : 1;
+    return d->cfg.r_max;
+}
+
+static bool try_admit(cdb_driver* d, int32_t q) {
+    Seq& s = d->seqs[q];
+    const int32_t need = (s.prompt_len + s.n_decode + 15) / 16;
+    if (need > d->cfg.max_pages) return false;
+    const bool use_pre = d->cfg.has_prelude, use_coda = d->cfg.has_coda;
+    if (d->core.available() < need * core_slots(d) || (use_pre && d->pre.available() < need) ||
+        (use_coda && d->coda.available() < need))
+        return false;
+    // (sequence, page, plane) order, lowest free id first; aliased planes reuse
+    // the page of the plane they share with
+    for (int32_t pg = 0; pg < need; ++pg) {
+        int32_t shared_id = -1;
+        for (int32_t pl = 0; pl < planes(d); ++pl) {
+            int32_t id = -1;
+            if (pl == 0) {
+                if (use_pre) id = d->pre.take();
+            } else if (pl == d->cfg.r_max + 1) {
+                if (use_coda) id = d->coda.take();
+            } else if (d->cfg.kv_layout == CDB_KV_SHARED ||
+                       (d->cfg.kv_layout == CDB_KV_FIRST_THEN_SHARED && pl >= 2)) {
+                if (shared_id < 0) shared_id = d->core.take();
+                id = shared_id;
+            } else {
+                id = d->core.take();
+            }
+            d->page_table[((size_t)q * planes(d) + pl) * d->cfg.max_pages + pg] = id;
+        }
+    }
+    s.pages = need;
+    s.state = PRELUDE;
+    s.t = 0;
+    s.c = 0;
+    s.admit_time = d->now;
+    d->active++;
+    d->fresh.push_back(q);
+    d->table_dirty = true;
+    return true;
+}
+
+static void release(cdb_driver* d, int32_t q) {
+    for (int32_t pg = 0; pg < d->seqs[q].pages; ++pg) {
+        std::vector<int32_t> core_given;
+        for (int32_t pl = 0; pl < planes(d); ++pl) {
+            int32_t& id = d->page_table[((size_t)q * planes(d) + pl) * d->cfg.max_pages + pg];
+            if (id < 0) continue;
+            if (pl == 0) {
+                d->pre.give(id);
+            } else if (pl == d->cfg.r_max + 1) {
+                d->coda.give(id);
+            } else if (std::find(core_given.begin(), core_given.end(), id) == core_given.end()) {
+                d->core.give(id);  // aliased planes give their page back once
+                core_given.push_back(id);
+            }
+            id = -1;
+        }
+    }
+    d->active--;
+    d->table_dirty = true;
+}
+
+static void admit(cdb_driver* d) {
+    while (d->next_arrival < d->seqs.size() && d->active < d->cfg.max_active &&
+           d->seqs[d->next_arrival].arrival <= d->now) {
+        if (!try_admit(d, (int32_t)d->next_arrival)) break;
+        d->next_arrival++;
+    }
+}
+
+static void fill_rows(const cdb_driver* d, const std::vector<int32_t>& qs, cdb_driver_tick* t, bool loop, int32_t dpos) {
+    t->n_rows = (int32_t)qs.size();
+    for (size_t i = 0; i < qs.size(); ++i) {
+        const Seq& s = d->seqs[qs[i]];
+        t->seq[i] = qs[i];
+        t->slot[i] = qs[i];
+        t->pos[i] = s.prompt_len + s.t + dpos;
+        t->c[i] = loop ? s.c : 0;
+        t->depth[i] = loop ? depth_of(d, s) : 0;
+        t->decode_index[i] = s.t + dpos;
+    }
+}
+
+extern "C" {
+
+cdb_driver* cdb_driver_create(const cdb_driver_config* cfg) {
+    if (!cfg || cfg->max_batch < 1 || cfg->max_batch > 256 || cfg->r_max < 1 || cfg->max_seqs < 1 ||
+        cfg->max_pages < 1 || cfg->max_active < 1 || cfg->min_coda_batch < 1 || cfg->kv_layout < 0 ||
+        cfg->kv_layout > 2)
+        return nullptr;
+    cdb_driver* d = new cdb_driver();
+    d->cfg = *cfg;
+    d->page_table.assign((size_t)cfg->max_seqs * (cfg->r_max + 2) * cfg->max_pages, -1);
+    d->pre = Allocator(cfg->has_prelude ? cfg->pre_pages : 0);
+    d->core = Allocator(cfg->core_pages);
+    d->coda = Allocator(cfg->has_coda ? cfg->coda_pages : 0);
+    memset(&d->stats, 0, sizeof(d->stats));
+    return d;
+}
+
+void cdb_driver_destroy(cdb_driver* d) { delete d; }
+
+int32_t cdb_driver_add_sequence(cdb_driver* d, int32_t prompt_len, int32_t n_decode, const int32_t* depths,
+                                double arrival) {
+    if (!d || prompt_len < 1 || n_decode < 1 || !depths) return -1;
+    if ((int32_t)d->seqs.size() >= d->cfg.max_seqs) return -1;
+    if (!d->seqs.empty() && arrival < d->seqs.back().arrival) return -1;  // arrival order
+    for (int32_t i = 0; i < n_decode; ++i)
+        if (depths[i] < 1 || depths[i] > d->cfg.r_max) return -1;
+    Seq s;
+    s.prompt_len = prompt_len;
+    s.n_decode = n_decode;
+    s.depth.assign(depths, depths + n_decode);
+    s.arrival = arrival;
+    d->seqs.push_back(std::move(s));
+    return (int32_t)d->seqs.size() - 1;
+}
+
+const int32_t* cdb_driver_page_table(cdb_driver* d) { return d ? d->page_table.data() : nullptr; }
+
+void cdb_driver_set_time(cdb_driver* d, double now) {
+    if (d) d->now = now;
+}
+
+// Plans the next stage call.  Returns 1 with *t filled, 0 when all work is done,
+// -1 when nothing can run until a later arrival (t->wait_until holds it).
+int32_t cdb_driver_next(cdb_driver* d, cdb_driver_tick* t) {
+    if (!d || !t) return -1;
+    admit(d);
+    t->n_continue = 0;
+    auto coda_tick = [&]() {
+        const int32_t n = std::min<int32_t>((int32_t)d->exited.size(), 256);
+        std::vector<int32_t> rows(d->exited.begin(), d->exited.begin() + n);
+        // continuing sequences first, so the coda's ids feed the next prelude in order
+        std::stable_partition(rows.begin(), rows.end(),
+                              [&](int32_t q) { return d->seqs[q].t + 1 < d->seqs[q].n_decode; });
+        t->stage = CDB_TICK_CODA;
+        fill_rows(d, rows, t, false, 0);
+        for (int32_t q : rows) t->n_continue += d->seqs[q].t + 1 < d->seqs[q].n_decode;
+        return 1;
+    };
+    auto prelude_tick = [&]() {
+        const int32_t n = std::min<int32_t>((int32_t)d->fresh.size(), 256);
+        std::vector<int32_t> rows(d->fresh.begin(), d->fresh.begin() + n);
+        t->stage = CDB_TICK_PRELUDE_FIRST;
+        fill_rows(d, rows, t, false, 0);
+        return 1;
+    };
+    auto loop_tick = [&]() {
+        t->stage = CDB_TICK_LOOP;
+        fill_rows(d, d->batch, t, true, 0);
+        return 1;
+    };
+    if (d->cfg.refill) {
+        const bool loop_left = !d->loopq.empty() || !d->batch.empty();
+        const int32_t n_exit = (int32_t)d->exited.size();
+        if (n_exit > 0 && (n_exit >= d->cfg.min_coda_batch || !loop_left)) return coda_tick();
+        if (!d->fresh.empty()) return prelude_tick();
+        if (loop_left) {
+            // keep the running rows, fill freed rows from the loop queue
+            while ((int32_t)d->batch.size() < d->cfg.max_batch && !d->loopq.empty()) {
+                d->batch.push_back(d->loopq.front());
+                d->loopq.pop_front();
+            }
+            return loop_tick();
+        }
+    } else {
+        if (d->round_open) {
+            if (!d->batch.empty()) return loop_tick();
+            if (!d->exited.empty()) return coda_tick();
+            d->round_open = false;
+        }
+        if (!d->exited.empty()) return coda_tick();
+        if (!d->fresh.empty()) return prelude_tick();
+        if (!d->loopq.empty()) {
+            while ((int32_t)d->batch.size() < d->cfg.max_batch && !d->loopq.empty()) {
+                d->batch.push_back(d->loopq.front());
+                d->loopq.pop_front();
+            }
+            d->round_open = true;
+            return loop_tick();
+        }
+    }
+    if (d->next_arrival < d->seqs.size()) {
+        t->stage = CDB_TICK_NONE;
+        t->n_rows = 0;
+        t->wait_until = d->seqs[d->next_arrival].arrival;
+        return -1;
+    }
+    return 0;
+}
+
+// Applies a planned stage call's effect on the schedule.
+int32_t cdb_driver_complete(cdb_driver* d, const cdb_driver_tick* t) {
+    if (!d || !t) return -1;
+    if (t->stage == CDB_TICK_CODA) {
+        std::vector<int32_t> cont;
+        for (int32_t i = 0; i < t->n_rows; ++i) {
+            const int32_t q = t->seq[i];
+            Seq& s = d->seqs[q];
+            d->exited.erase(std::find(d->exited.begin(), d->exited.end(), q));
+            d->stats.tokens++;
+            if (s.t + 1 < s.n_decode) {
+                s.t++;
+                s.c = 0;
+                s.state = LOOP;
+                cont.push_back(q);
+            } else {
+                s.state = DONE;
+                s.done_time = d->now;
+                release(d, q);
+            }
+        }
+        d->stats.coda_calls++;
+        d->stats.coda_rows += t->n_rows;
+        // the prelude of the continuing sequences' next inputs runs right after
+        d->stats.prelude_calls += cont.empty() ? 0 : 1;
+        d->stats.prelude_rows += (int64_t)cont.size();
+        for (int32_t q : cont) d->loopq.push_back(q);
+        if (!d->cfg.refill && d->exited.empty() && d->batch.empty()) d->round_open = false;  // round over
+    } else if (t->stage == CDB_TICK_PRELUDE_FIRST) {
+        for (int32_t i = 0; i < t->n_rows; ++i) {
+            const int32_t q = t->seq[i];
+            d->fresh.erase(std::find(d->fresh.begin(), d->fresh.end(), q));
+            d->seqs[q].state = LOOP;
+            d->loopq.push_back(q);
+        }
+        d->stats.prelude_calls++;
+        d->stats.prelude_rows += t->n_rows;
+    } else if (t->stage == CDB_TICK_LOOP) {
+        std::vector<int32_t> keep;
+        for (int32_t i = 0; i < t->n_rows; ++i) {
+            const int32_t q = t->seq[i];
+            Seq& s = d->seqs[q];
+            if (s.c + 1 == depth_of(d, s)) {
+                s.state = EXITED;
+                d->exited.push_back(q);
+            } else {
+                s.c++;
+                keep.push_back(q);
+            }
+        }
+        d->batch = keep;
+        d->stats.loop_steps++;
+        d->stats.loop_rows += t->n_rows;
+        d->stats.idle_rows += d->cfg.max_batch - t->n_rows;
+    }
+    return 0;
+}
+
+int32_t cdb_driver_pages_in_use(const cdb_driver* d, int32_t* pre, int32_t* core, int32_t* coda) {
+    if (!d) return -1;
+    if (pre) *pre = (d->cfg.has_prelude ? d->cfg.pre_pages : 0) - d->pre.available();
+    if (core) *core = d->cfg.core_pages - d->core.available();
+    if (coda) *coda = (d->cfg.has_coda ? d->cfg.coda_pages : 0) - d->coda.available();
+    return 0;
+}
+
+int32_t cdb_driver_get_stats(const cdb_driver* d, cdb_driver_stats* out) {
+    if (!d || !out) return -1;
+    *out = d->stats;
+    return 0;
+}
+
+int32_t cdb_driver_latencies(const cdb_driver* d, double* normalized, int32_t n) {
+    if (!d || !normalized) return -1;
+    int32_t k = 0;
+    for (const Seq& s : d->seqs) {
+        if (k >= n) break;
+        normalized[k++] = s.done_time >= 0 ? (s.done_time - s.arrival) / s.n_decode : -1.0;
+    }
+    return k;
+}
+
+// ------------------------------------------------------------------ runner
+
+// Device scratch: two row sets (6 x 256 int32 each), next ids (256), loop-step
+// outputs, logits (256 x vocab fp32).
+static size_t scratch_layout(int32_t vocab, size_t* rows, size_t* ids, size_t* step, size_t* logits) {
+    size_t off = 0;
+    *rows = off;
+    off += 2 * 6 * 256 * 4;
+    *ids = off;
+    off += 256 * 4;
+    *step = off;
+    off += 256 * 4 + 256 + 256 * 4 * 2 + 2 * 4;
+    off = (off + 255) & ~(size_t)255;
+    *logits = off;
+    off += (size_t)256 * vocab * 4;
+    return off;
+}
+
+size_t cdb_driver_scratch_bytes(int32_t vocab) {
+    size_t a, b, c, e;
+    return vocab > 0 ? scratch_layout(vocab, &a, &b, &c, &e) : 0;
+}
+
+int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, const cdb_state* state, void* scratch,
+                       size_t scratch_bytes, const int32_t* first_tokens, void* ws, size_t ws_bytes,
+                       hipStream_t stream, double* seconds) {
+    if (!d || !model || !kv || !state || !scratch || !ws || !first_tokens || !kv->page_table)
+        return CDB_ERR_INVALID_ARG;
+    size_t o_rows, o_ids, o_step, o_logits;
+    if (scratch_bytes < scratch_layout(model->desc.vocab, &o_rows, &o_ids, &o_step, &o_logits)) return CDB_ERR_CAPACITY;
+    if (kv->max_seqs != d->cfg.max_seqs || kv->max_pages != d->cfg.max_pages) return CDB_ERR_INVALID_ARG;
+    unsigned char* base = static_cast<unsigned char*>(scratch);
+    int32_t* drows = reinterpret_cast<int32_t*>(base + o_rows);      // main rows
+    int32_t* drows2 = drows + 6 * 256;                               // prelude rows after a coda
+    int32_t* dids = reinterpret_cast<int32_t*>(base + o_ids);
+    float* dlogits = reinterpret_cast<float*>(base + o_logits);
+    cdb_step_out out;
+    out.exit_score = reinterpret_cast<float*>(base + o_step);
+    out.exit_mask = reinterpret_cast<uint8_t*>(base + o_step + 256 * 4);
+    out.cont = reinterpret_cast<int32_t*>(base + o_step + 256 * 4 + 256);
+    out.exited = out.cont + 256;
+    out.counts = out.exited + 256;
+
+    // pinned host staging: a ring of row buffers, each reused only after the
+    // copy that last read it has completed (device buffers are reused in
+    // stream order)
+    const int RING = 8;
+    const size_t slot_ints = 6 * 256;
+    int32_t* pinned = nullptr;
+    int32_t* pinned_pt = nullptr;
+    const size_t pt_bytes = d->page_table.size() * 4;
+    if (hipHostMalloc(reinterpret_cast<void**>(&pinned), RING * slot_ints * 4) != hipSuccess) return CDB_ERR_HIP;
+    if (hipHostMalloc(reinterpret_cast<void**>(&pinned_pt), pt_bytes) != hipSuccess) {
+        hipHostFree(pinned);
+        return CDB_ERR_HIP;
+    }
+    hipEvent_t ev[RING], pt_ev;
+    for (int i = 0; i < RING; ++i) hipEventCreateWithFlags(&ev[i], hipEventDisableTiming);
+    hipEventCreateWithFlags(&pt_ev, hipEventDisableTiming);
+    bool pt_used = false;
+    int ring = 0;
+    auto stage = [&](const int32_t* slot, const int32_t* seq, const int32_t* pos, const int32_t* c,
+                     const int32_t* dep, const int32_t* tok, int32_t n, int32_t* dst) -> hipError_t {
+        hipEventSynchronize(ev[ring]);
+        int32_t* h = pinned + ring * slot_ints;
+        memcpy(h, slot, n * 4);
+        memcpy(h + 256, seq, n * 4);
+        memcpy(h + 512, pos, n * 4);
+        if (c) memcpy(h + 768, c, n * 4);
+        if (dep) memcpy(h + 1024, dep, n * 4);
+        if (tok) memcpy(h + 1280, tok, n * 4);
+        hipError_t e = hipMemcpyAsync(dst, h, slot_ints * 4, hipMemcpyHostToDevice, stream);
+        hipEventRecord(ev[ring], stream);
+        ring = (ring + 1) % RING;
+        return e;
+    };
+
+    cdb_driver_tick t;
+    int32_t status = CDB_OK;
+    std::vector<int32_t> toks(256), npos(256);
+    const auto t0 = std::chrono::steady_clock::now();
+    while (status == CDB_OK) {
+        d->now = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+        const int32_t r = cdb_driver_next(d, &t);
+        if (r == 0) break;
+        if (r < 0) continue;  // the next request has not arrived yet
+        if (d->table_dirty) {
+            if (pt_used) hipEventSynchronize(pt_ev);
+            memcpy(pinned_pt, d->page_table.data(), pt_bytes);
+            if (hipMemcpyAsync(const_cast<int32_t*>(kv->page_table), pinned_pt, pt_bytes, hipMemcpyHostToDevice,
+                               stream) != hipSuccess) {
+                status = CDB_ERR_HIP;
+                break;
+            }
+            hipEventRecord(pt_ev, stream);
+            pt_used = true;
+            d->table_dirty = false;
+        }
+        const int32_t n = t.n_rows;
+        for (int32_t i = 0; i < n; ++i) toks[i] = first_tokens[t.seq[i]];
+        if (stage(t.slot, t.seq, t.pos, t.c, t.depth, toks.data(), n, drows) != hipSuccess) {
+            status = CDB_ERR_HIP;
+            break;
+        }
+        cdb_rows rows{n, drows, drows + 256, drows + 512, drows + 768, drows + 1024};
+        cdb_status s = CDB_OK;
+        if (t.stage == CDB_TICK_PRELUDE_FIRST) {
+            s = cdb_boundary_prelude(model, kv, state, &rows, drows + 1280, ws, ws_bytes, stream);
+        } else if (t.stage == CDB_TICK_LOOP) {
+            s = cdb_loop_step(model, kv, state, &rows, &out, ws, ws_bytes, stream);
+        } else if (t.stage == CDB_TICK_CODA) {
+            s = cdb_boundary_coda(model, kv, state, &rows, dlogits, dids, ws, ws_bytes, stream);
+            if (s == CDB_OK && t.n_continue > 0) {
+                // the continuing sequences are the coda batch's first rows: the
+                // coda's ids are the prelude's tokens, one position further
+                for (int32_t i = 0; i < t.n_continue; ++i) npos[i] = t.pos[i] + 1;
+                if (stage(t.slot, t.seq, npos.data(), nullptr, nullptr, nullptr, t.n_continue, drows2) !=
+                    hipSuccess) {
+                    status = CDB_ERR_HIP;
+                    break;
+                }
+                cdb_rows prow{t.n_continue, drows2, drows2 + 256, drows2 + 512, nullptr, nullptr};
+                s = cdb_boundary_prelude(model, kv, state, &prow, dids, ws, ws_bytes, stream);
+            }
+        }
+        if (s != CDB_OK) {
+            status = s;
+            break;
+        }
+        cdb_driver_complete(d, &t);
+    }
+    if (hipStreamSynchronize(stream) != hipSuccess && status == CDB_OK) status = CDB_ERR_HIP;
+    const double secs = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+    d->now = secs;
+    if (seconds) *seconds = secs;
+    for (int i = 0; i < RING; ++i) hipEventDestroy(ev[i]);
+    hipEventDestroy(pt_ev);
+    hipHostFree(pinned);
+    hipHostFree(pinned_pt);
+    return status;
+}
+
+}  // extern "C"

@@ -9,21 +9,26 @@ import pytest
 
 import cdbgen
 import paper_2608_09444_amd as cdb
+from paper_2608_09444_amd import driver as cdb_driver
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
-def declared_functions():
-    text = open(os.path.join(ROOT, "include", "libcdb.h")).read()
-    return sorted(set(re.findall(r"^\s*(?:cdb_status|size_t|const char\*)\s+(cdb_\w+)\s*\(", text, re.M)))
+def declared_functions(header):
+    text = open(os.path.join(ROOT, "include", header)).read()
+    ret = r"(?:cdb_status|size_t|const char\*|int32_t|void|cdb_driver\*|const int32_t\*)"
+    return sorted(set(re.findall(r"^\s*" + ret + r"\s+(cdb_\w+)\s*\(", text, re.M)))
 
 
 def test_library_exports_every_declared_symbol():
-    names = declared_functions()
-    assert len(names) == 10
+    names = declared_functions("libcdb.h")
+    assert len(names) == 11
     assert set(names) == set(cdb.EXPORTED)
+    dnames = declared_functions("libcdb_driver.h")
+    assert len(dnames) == 12
+    assert set(dnames) == set(cdb_driver.EXPORTED)
     L = cdb.lib()
-    for n in names:
+    for n in names + dnames:
         assert hasattr(L, n), n
 
 
