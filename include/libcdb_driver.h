@@ -106,11 +106,14 @@ size_t cdb_driver_scratch_bytes(int32_t vocab);
  * `stream`.  first_tokens (host, per sequence) is each sequence's first decode
  * input; later inputs are the coda's greedy ids, passed on device.  The page
  * table in kv->page_table (device) is overwritten from the driver's.
- * scratch: device, cdb_driver_scratch_bytes(vocab).  Returns a cdb_status;
+ * scratch: device, cdb_driver_scratch_bytes(vocab).  tokens_out (device,
+ * optional): int32 [max_seqs][tokens_stride] receives, at [seq][k], the greedy
+ * id the coda produced after decode input k (tokens_stride >= every
+ * sequence's n_decode, else CDB_ERR_INVALID_ARG).  Returns a cdb_status;
  * *seconds = wall time including the final synchronisation. */
 int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, const cdb_state* state, void* scratch,
-                       size_t scratch_bytes, const int32_t* first_tokens, void* ws, size_t ws_bytes,
-                       hipStream_t stream, double* seconds);
+                       size_t scratch_bytes, const int32_t* first_tokens, int32_t* tokens_out,
+                       int32_t tokens_stride, void* ws, size_t ws_bytes, hipStream_t stream, double* seconds);
 
 #ifdef __cplusplus
 }

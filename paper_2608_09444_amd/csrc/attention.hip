@@ -19,8 +19,9 @@
 // k_row_order wrote at the start of the stage call -- and deals the pages of
 // both to its 4 waves.  Each wave keeps one softmax state per row.  With pairs,
 // mixed and equal context lengths run at the same bandwidth.  The partial
-// states are merged through LDS; the output is written in the fragment layout
-// the output projection reads.
+// states are merged through LDS in an order fixed by the row alone, so every
+// row's output is bit-identical whatever else shares the batch; the output is
+// written in the fragment layout the output projection reads.
 #include "cdb_internal.h"
 
 namespace cdb {
@@ -214,13 +215,18 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(const float* __restric
         const int r = tid / HD, dim = tid - r * HD;
         const int m = rows[r];
         if (m >= 0 && valid[r]) {
+            // merge in the order of the row's own page classes (page p lives in
+            // partial (p + first) % waves), so a row's result does not depend on
+            // the row it was paired with
+            const int first = r == 0 ? 0 : n0 % kAttnWaves;
             float Mx = -1e30f;
             for (int i = 0; i < NP; ++i) Mx = fmaxf(Mx, s_m[r][i]);
             float num = 0.f, den = 0.f;
             for (int i = 0; i < NP; ++i) {
-                const float w = exp2f(s_m[r][i] - Mx);
-                num += w * s_acc[r][i][dim];
-                den += w * s_l[r][i];
+                const int j = ((first + (i >> 2)) % kAttnWaves) * 4 + (i & 3);
+                const float w = exp2f(s_m[r][j] - Mx);
+                num += w * s_acc[r][j][dim];
+                den += w * s_l[r][j];
             }
             out[frag_index(m, head * HD + dim, d)] = f2bf(den > 0.f ? num / den : 0.f);
         }

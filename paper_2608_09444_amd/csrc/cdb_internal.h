@@ -130,6 +130,8 @@ hipError_t launch_compact(int M, const uint8_t* mask, int32_t* cont, int32_t* ex
 hipError_t launch_copy_on_exit(const cdb_model_desc& md, const cdb_kv& kv, const cdb_rows& r,
                                const int32_t* exited, const int32_t* counts, int* err, hipStream_t st);
 hipError_t launch_argmax(int M, int V, const float* logits, int32_t* ids, hipStream_t st);
+hipError_t launch_scatter_ids(int M, const int32_t* ids, const int32_t* seq, const int32_t* index, int max_seqs,
+                              int stride, int32_t* out, hipStream_t st);
 hipError_t launch_pack(int kind, const uint16_t* a, const uint16_t* b, const uint16_t* c, int N, int K, int hd,
                        uint16_t* dst, hipStream_t st);
 hipError_t launch_copy_bf16(const uint16_t* src, size_t n, uint16_t* dst, hipStream_t st);

@@ -35,6 +35,12 @@
 #include "../../include/libcdb.h"
 #include "../../include/libcdb_driver.h"
 
+namespace cdb {
+// defined with the row kernels
+hipError_t launch_scatter_ids(int M, const int32_t* ids, const int32_t* seq, const int32_t* index, int max_seqs,
+                              int stride, int32_t* out, hipStream_t st);
+}  // namespace cdb
+
 namespace {
 
 enum SeqState { WAITING = 0, PRELUDE = 1, LOOP = 2, EXITED = 3, DONE = 4 };
@@ -395,10 +401,14 @@ size_t cdb_driver_scratch_bytes(int32_t vocab) {
 }
 
 int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, const cdb_state* state, void* scratch,
-                       size_t scratch_bytes, const int32_t* first_tokens, void* ws, size_t ws_bytes,
-                       hipStream_t stream, double* seconds) {
+                       size_t scratch_bytes, const int32_t* first_tokens, int32_t* tokens_out,
+                       int32_t tokens_stride, void* ws, size_t ws_bytes, hipStream_t stream, double* seconds) {
     if (!d || !model || !kv || !state || !scratch || !ws || !first_tokens || !kv->page_table)
         return CDB_ERR_INVALID_ARG;
+    if (tokens_out) {
+        for (const Seq& s : d->seqs)
+            if (s.n_decode > tokens_stride) return CDB_ERR_INVALID_ARG;
+    }
     size_t o_rows, o_ids, o_step, o_logits;
     if (scratch_bytes < scratch_layout(model->desc.vocab, &o_rows, &o_ids, &o_step, &o_logits)) return CDB_ERR_CAPACITY;
     if (kv->max_seqs != d->cfg.max_seqs || kv->max_pages != d->cfg.max_pages) return CDB_ERR_INVALID_ARG;
@@ -470,7 +480,9 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
             d->table_dirty = false;
         }
         const int32_t n = t.n_rows;
-        for (int32_t i = 0; i < n; ++i) toks[i] = first_tokens[t.seq[i]];
+        // sixth row array: the first decode input (prelude) or the decode index (coda)
+        for (int32_t i = 0; i < n; ++i)
+            toks[i] = t.stage == CDB_TICK_CODA ? t.decode_index[i] : first_tokens[t.seq[i]];
         if (stage(t.slot, t.seq, t.pos, t.c, t.depth, toks.data(), n, drows) != hipSuccess) {
             status = CDB_ERR_HIP;
             break;
@@ -483,6 +495,10 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
             s = cdb_loop_step(model, kv, state, &rows, &out, ws, ws_bytes, stream);
         } else if (t.stage == CDB_TICK_CODA) {
             s = cdb_boundary_coda(model, kv, state, &rows, dlogits, dids, ws, ws_bytes, stream);
+            if (s == CDB_OK && tokens_out &&
+                cdb::launch_scatter_ids(n, dids, drows + 256, drows + 1280, d->cfg.max_seqs, tokens_stride, tokens_out,
+                                        stream) != hipSuccess)
+                s = CDB_ERR_HIP;
             if (s == CDB_OK && t.n_continue > 0) {
                 // the continuing sequences are the coda batch's first rows: the
                 // coda's ids are the prelude's tokens, one position further

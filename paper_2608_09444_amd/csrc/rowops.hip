@@ -261,13 +261,15 @@ __global__ __launch_bounds__(256) void k_copy_on_exit(int H, int hd, int r_max, 
     }
     const int vec_per_head = hd / 8;  // 16-byte vectors per (kv, head) entry
     const int nvec = 2 * H * vec_per_head;
+    int prev = src;  // aliased planes (shared layouts) map one page: copy it once
     for (int pl = dep + 1; pl <= r_max; ++pl) {
         const int dst = pt[(size_t)pl * kv.max_pages + pg];
         if (dst < 0 || dst >= kv.n_pages) {
             if (threadIdx.x == 0) set_err(err, CDB_DEV_UNMAPPED_PAGE);
             continue;
         }
-        if (dst == src) continue;
+        if (dst == src || dst == prev) continue;
+        prev = dst;
         for (int v = threadIdx.x; v < nvec; v += 256) {
             const int kvh = v / vec_per_head, e = v - kvh * vec_per_head;  // kvh = kv*H + head
             const int kvi = kvh / H, hh = kvh - kvi * H;
@@ -424,6 +426,26 @@ hipError_t launch_copy_on_exit(const cdb_model_desc& md, const cdb_kv& kv, const
     dim3 grid(r.n_rows, md.n_core);
     k_copy_on_exit<<<grid, 256, 0, st>>>(md.n_heads, md.head_dim, md.r_max, t, r.seq, r.pos, r.depth, exited, counts,
                                          err);
+    return hipGetLastError();
+}
+
+// out[seq[i] * stride + index[i]] = ids[i]: files a coda batch's greedy ids
+// under their sequence and decode index (rows outside the table are skipped).
+__global__ __launch_bounds__(256) void k_scatter_ids(int M, const int32_t* __restrict__ ids,
+                                                     const int32_t* __restrict__ seq,
+                                                     const int32_t* __restrict__ index, int max_seqs, int stride,
+                                                     int32_t* __restrict__ out) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= M) return;
+    const int q = seq[i], k = index[i];
+    if (q < 0 || q >= max_seqs || k < 0 || k >= stride) return;
+    out[(size_t)q * stride + k] = ids[i];
+}
+
+hipError_t launch_scatter_ids(int M, const int32_t* ids, const int32_t* seq, const int32_t* index, int max_seqs,
+                              int stride, int32_t* out, hipStream_t st) {
+    if (M <= 0) return hipSuccess;
+    k_scatter_ids<<<(M + 255) / 256, 256, 0, st>>>(M, ids, seq, index, max_seqs, stride, out);
     return hipGetLastError();
 }
 

@@ -63,7 +63,7 @@ def lib() -> C.CDLL:
         L.cdb_driver_latencies.argtypes = [P, P, I]
         L.cdb_driver_scratch_bytes.argtypes = [I]
         L.cdb_driver_scratch_bytes.restype = S
-        L.cdb_driver_run.argtypes = [P, P, P, P, P, S, P, P, S, P, P]
+        L.cdb_driver_run.argtypes = [P, P, P, P, P, S, P, P, I, P, S, P, P]
         for f in ("cdb_driver_add_sequence", "cdb_driver_next", "cdb_driver_complete", "cdb_driver_get_stats",
                   "cdb_driver_pages_in_use", "cdb_driver_latencies", "cdb_driver_run"):
             getattr(L, f).restype = C.c_int32
@@ -150,14 +150,17 @@ class Driver:
             self.complete(t)
             ticks.append(t)
 
-    def run(self, model: cdb_model, kv: cdb_kv, state: cdb_state, scratch, first_tokens, ws, stream=None) -> float:
-        """Runs all added requests on the device; returns the wall time in seconds."""
+    def run(self, model: cdb_model, kv: cdb_kv, state: cdb_state, scratch, first_tokens, ws, tokens_out=None,
+            stream=None) -> float:
+        """Runs all added requests on the device; returns the wall time in
+        seconds.  tokens_out: optional device int32 [max_seqs][stride]."""
         from . import CDB_OK, CdbError
         tok = np.ascontiguousarray(first_tokens, dtype=np.int32)
         secs = C.c_double()
+        stride = 0 if tokens_out is None else int(tokens_out.shape[1])
         r = lib().cdb_driver_run(self.h, C.byref(model), C.byref(kv), C.byref(state), _ptr(scratch),
-                                 scratch.numel() * scratch.element_size(), tok.ctypes.data, _ptr(ws),
-                                 ws.numel() * ws.element_size(), _stream(stream), C.byref(secs))
+                                 scratch.numel() * scratch.element_size(), tok.ctypes.data, _ptr(tokens_out), stride,
+                                 _ptr(ws), ws.numel() * ws.element_size(), _stream(stream), C.byref(secs))
         if r != CDB_OK:
             raise CdbError("cdb_driver_run", r)
         return secs.value

@@ -28,11 +28,12 @@ def bf16_pool_to_f64(t: torch.Tensor) -> np.ndarray:
 
 class Lockstep:
     def __init__(self, shape, weights, seq_lens: List[int], max_batch: int, bf16_storage: bool = True,
-                 extra_pages: int = 0, resync: bool = False, sensitivity: bool = False):
+                 extra_pages: int = 0, resync: bool = False, sensitivity: bool = False, kv_layout: int = 0):
         """resync: after every call, copy the oracle's states and newly written
         K/V entries into the device buffers, so that each call is checked from
         identical inputs (deep random-init models amplify rounding-level
-        differences from call to call)."""
+        differences from call to call).  kv_layout: 0 full, 1 single shared
+        slot, 2 first-then-shared (core planes aliased in the page table)."""
         self.resync = resync
         self.sensitivity = sensitivity
         self.tol = (TOL_MAX, TOL_MEAN)
@@ -46,16 +47,25 @@ class Lockstep:
         n_seq = len(seq_lens)
         self.max_pages = max(cdbgen.pages_for(t) for t in seq_lens)
         tot = sum(cdbgen.pages_for(t) for t in seq_lens) + extra_pages
-        pre_p, core_p, coda_p = (tot if s.n_prelude else 0), tot * self.R, (tot if s.n_coda else 0)
+        per = {0: self.R, 1: 1, 2: min(2, self.R)}[kv_layout]
+        pre_p, core_p, coda_p = (tot if s.n_prelude else 0), tot * per, (tot if s.n_coda else 0)
         self.op = oracle.Paged(s, n_seq, self.max_pages, pre_p, core_p, coda_p)
         self.gkv = cdb.PagedKV(s, n_seq, self.max_pages, pre_p, core_p, coda_p)
-        # one page table for both sides: lowest free id first, (seq, page, plane) order
+        # one page table for both sides: lowest free id first, (seq, page, plane)
+        # order; aliased core planes share the page of the first plane they alias
         nxt = {0: 0, 1: 0, 2: 0}
         for q, T in enumerate(seq_lens):
             for pg in range(cdbgen.pages_for(T)):
+                shared = -1
                 for plane in range(self.R + 2):
                     st = 0 if plane == 0 else (2 if plane == self.R + 1 else 1)
                     if st == 0 and not s.n_prelude or st == 2 and not s.n_coda:
+                        continue
+                    if st == 1 and (kv_layout == 1 or (kv_layout == 2 and plane >= 2)):
+                        if shared < 0:
+                            shared = nxt[1]
+                            nxt[1] += 1
+                        self.op.page_table[q, plane, pg] = shared
                         continue
                     self.op.page_table[q, plane, pg] = nxt[st]
                     nxt[st] += 1

@@ -1,0 +1,163 @@
+"""GPU: the host driver running whole decodes through the HIP stage calls, and
+the shared core KV layouts call by call against the oracle.
+
+* Every row of a stage call is computed independently of the others, so the
+  same requests decoded under different schedules (refill, no-refill, a
+  minimum coda batch, other batch sizes) must give bit-identical tokens.
+* The greedy tokens must follow the oracle's wherever the history agrees and
+  the oracle's top-2 logit gap is clear of the tolerance.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import cdbgen
+import oracle
+import paper_2608_09444_amd as cdb
+from paper_2608_09444_amd import driver as drv
+
+pytestmark = pytest.mark.gpu
+
+# logits agree within 2e-2 per element, so a top-2 gap above 4e-2 fixes the argmax
+GAP = 4e-2
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def _requests(shape, seed=40):
+    plens = [17, 8, 33, 5, 20, 12]
+    ndec = [10, 14, 6, 12, 9, 11]
+    prompts = [cdbgen.prompt_ids(shape.vocab, 1, p, seed=seed, stream=q)[0] for q, p in enumerate(plens)]
+    depths = [cdbgen.draw_depths(("uniform", 1, shape.r_max), n, shape.r_max, seed=seed + 1, stream=q)
+              for q, n in enumerate(ndec)]
+    return prompts, ndec, depths
+
+
+def _decode_on_gpu(shape, gm, prompts, ndec, depths, kv_layout=drv.KV_FULL, **cfg):
+    """Prefill every prompt through the stage calls (one block per sequence),
+    then let the driver decode all requests.  Returns (first tokens, decoded
+    ids [seq][k], driver stats)."""
+    R = shape.r_max
+    n = len(prompts)
+    T = [len(p) + k for p, k in zip(prompts, ndec)]
+    max_pages = max(cdbgen.pages_for(t) for t in T)
+    tot = sum(cdbgen.pages_for(t) for t in T)
+    per = {drv.KV_FULL: R, drv.KV_SHARED: 1, drv.KV_FIRST_THEN_SHARED: min(2, R)}[kv_layout]
+    d = drv.Driver(max_seqs=n, max_pages=max_pages, core_pages=tot * per, pre_pages=tot, coda_pages=tot,
+                   has_prelude=shape.n_prelude > 0, has_coda=shape.n_coda > 0, r_max=R, kv_layout=kv_layout,
+                   **cfg)
+    for q in range(n):
+        d.add_sequence(len(prompts[q]), depths[q])
+    assert cfg.get("max_active", 0) >= n
+    first_tick = d.next()  # admits every request; the plan is kept until completed
+    assert first_tick.n_rows == n
+    kv = cdb.PagedKV(shape, n, max_pages, tot, tot * per, tot)
+    kv.page_table.copy_(torch.from_numpy(d.page_table()))
+    ws = cdb.Workspace(gm.desc, 256)
+    # prefill: prompt rows use their own state slots
+    pstate = cdb.State(shape, max(len(p) for p in prompts))
+    first = np.zeros(n, np.int32)
+    for q, p in enumerate(prompts):
+        P = len(p)
+        pos = np.arange(P, dtype=np.int32)
+        rows = cdb.Rows(pos, np.full(P, q, np.int32), pos, None, None)
+        cdb.cdb_boundary_prelude(gm.model, kv.c, pstate.c, rows.c, torch.as_tensor(p, dtype=torch.int32,
+                                                                                   device="cuda"), ws.buf)
+        out = cdb.StepOut(P)
+        for c in range(R):
+            lr = cdb.Rows(pos, np.full(P, q, np.int32), pos, np.full(P, c, np.int32), np.full(P, R, np.int32))
+            cdb.cdb_loop_step(gm.model, kv.c, pstate.c, lr.c, out.c, ws.buf)
+        logits = torch.zeros((P, shape.vocab), dtype=torch.float32, device="cuda")
+        ids = torch.zeros(P, dtype=torch.int32, device="cuda")
+        cdb.cdb_boundary_coda(gm.model, kv.c, pstate.c, rows.c, logits, ids, ws.buf)
+        first[q] = int(ids[-1].item())
+    state = cdb.State(shape, n)
+    scratch = torch.empty(drv.cdb_driver_scratch_bytes(shape.vocab), dtype=torch.uint8, device="cuda")
+    out_ids = torch.full((n, max(ndec)), -1, dtype=torch.int32, device="cuda")
+    secs = d.run(gm.model, kv.c, state.c, scratch, first, ws.buf, tokens_out=out_ids)
+    torch.cuda.synchronize()
+    assert cdb.cdb_read_device_error(ws.buf) == 0
+    return first, out_ids.cpu().numpy(), d.stats(), secs
+
+
+def _check_against_oracle(shape, w, prompts, ndec, depths, first, ids, kv_layout):
+    m = oracle.Model(shape, w, bf16_storage=True, kv_layout=kv_layout)
+    checked = 0
+    for q, p in enumerate(prompts):
+        P, N = len(p), ndec[q]
+        dep = np.concatenate([np.full(P, shape.r_max, np.int32), depths[q]])
+        # teacher-force the GPU's own tokens, so a legitimate near-tie flip does
+        # not stop the comparison of the positions after it
+        gpu_tokens = np.concatenate([p, [first[q]], ids[q, :N - 1]]).astype(np.int32)
+        ref = m.ref_sequence(gpu_tokens, dep, n_given=P + N, n_prefill=P)
+        gpu_next = np.concatenate([[first[q]], ids[q, :N]])  # id after positions P-1 .. P+N-1
+        for k, t in enumerate(range(P - 1, P + N)):
+            lg = ref["logits"][t]
+            top2 = np.sort(lg)[-2:]
+            if top2[1] - top2[0] > GAP:
+                assert gpu_next[k] == int(np.argmax(lg)), f"seq {q} position {t}"
+                checked += 1
+            else:
+                assert lg[gpu_next[k]] >= top2[1] - GAP
+    return checked
+
+
+@pytest.mark.parametrize("kv_layout", [drv.KV_FULL, drv.KV_SHARED, drv.KV_FIRST_THEN_SHARED],
+                         ids=["full", "shared", "first-then-shared"])
+def test_driver_decode_is_schedule_invariant_and_follows_oracle(kv_layout):
+    s = cdbgen.TINY
+    _say(f"[gpu] driver decode {s.name} layout {kv_layout}")
+    w = cdbgen.model_weights(s)
+    gm = cdb.DeviceModel(s, w)
+    prompts, ndec, depths = _requests(s)
+    n = len(prompts)
+    runs = {}
+    for name, cfg in (("refill", dict(max_batch=4, max_active=n)),
+                      ("no-refill", dict(max_batch=3, max_active=n, refill=False)),
+                      ("refill-coda3", dict(max_batch=6, max_active=n, min_coda_batch=3))):
+        first, ids, st, secs = _decode_on_gpu(s, gm, prompts, ndec, depths, kv_layout, **cfg)
+        _say(f"[gpu]   {name}: {st} in {secs * 1e3:.1f} ms")
+        assert st["tokens"] == sum(ndec)
+        assert st["loop_rows"] == sum(int(x.sum()) for x in depths)
+        runs[name] = (first, ids)
+    base = runs["refill"]
+    for name, (first, ids) in runs.items():
+        assert np.array_equal(first, base[0]) and np.array_equal(ids, base[1]), name
+    checked = _check_against_oracle(s, w, prompts, ndec, depths, base[0], base[1], kv_layout)
+    _say(f"[gpu]   {checked} greedy ids checked against the oracle")
+    assert checked >= 0.3 * (sum(ndec) + n)  # not vacuous: about half the positions have a clear gap
+
+
+@pytest.mark.parametrize("kv_layout", [1, 2], ids=["shared", "first-then-shared"])
+def test_shared_layouts_call_by_call(kv_layout):
+    from lockstep import Lockstep
+    s = cdbgen.TINY
+    _say(f"[gpu] lockstep {s.name} kv layout {kv_layout}")
+    w = cdbgen.model_weights(s)
+    prompts, ndec, depths = _requests(s, seed=50)
+    deps = [np.concatenate([np.full(len(p), s.r_max, np.int32), d]) for p, d in zip(prompts, depths)]
+    ls = Lockstep(s, w, [len(p) + k for p, k in zip(prompts, ndec)], max_batch=4, kv_layout=kv_layout)
+    ls.run(prompts, ndec, deps)
+    _say(f"[gpu]   errors {ls.errors} calls {ls.calls} argmax checked {ls.argmax_checked}")
+    assert ls.device_error() == 0
+
+
+def test_driver_rejects_short_token_table():
+    s = cdbgen.TINY
+    gm = cdb.DeviceModel(s, cdbgen.model_weights(s))
+    d = drv.Driver(max_batch=2, max_active=1, r_max=s.r_max, max_seqs=1, max_pages=2, core_pages=8,
+                   pre_pages=2, coda_pages=2, has_prelude=True, has_coda=True)
+    d.add_sequence(4, [1, 2, 3])
+    kv = cdb.PagedKV(s, 1, 2, 2, 8, 2)
+    ws = cdb.Workspace(gm.desc, 4)
+    st = cdb.State(s, 1)
+    scratch = torch.empty(drv.cdb_driver_scratch_bytes(s.vocab), dtype=torch.uint8, device="cuda")
+    short = torch.zeros((1, 2), dtype=torch.int32, device="cuda")
+    with pytest.raises(cdb.CdbError):
+        d.run(gm.model, kv.c, st.c, scratch, np.zeros(1, np.int32), ws.buf, tokens_out=short)
+    assert d.stats()["loop_steps"] == 0
