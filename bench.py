@@ -12,7 +12,11 @@ resident in HBM before timing starts.
 
 Prints one JSON line: loop-step rows (tokens) per second, ms per step, the
 roofline of the dominant kernel (paged attention, HBM-bound) and the CPU
-oracle's rate on a bounded sample of the same workload.
+oracle's rate on a bounded sample of the same workload.  The "e2e" object
+times whole decodes of the same workload through the host driver -- 64
+requests, 256 decode tokens each after a 512-token prompt whose KV is
+synthesized -- under CDB with refill, CDB without refill, and fixed-depth
+continuous batching, next to the FLOP bound on the speed-up (Section 5, Eq. 2).
 """
 from __future__ import annotations
 
@@ -175,12 +179,60 @@ def cpu_baseline(shape, w, rows_np, n_sample, threads, min_s=10.0):
                       f"indices and depths; seeded random KV/state), {steps} loop steps in {dt:.1f}s"}
 
 
+def e2e_decode(shape, dm, kv, n_seqs, prompt, n_decode, seed=3):
+    """Whole decodes through the host driver in three modes; the KV pool's
+    random contents stand in for the prompts' prefilled KV."""
+    import numpy as np
+    import torch
+
+    import cdbgen
+    import paper_2608_09444_amd as cdb
+    from paper_2608_09444_amd import cost
+    from paper_2608_09444_amd import driver as drv
+    R = shape.r_max
+    depths = [cdbgen.draw_depths(cdbgen.OURO_DEPTHS, n_decode, R, seed=seed, stream=q) for q in range(n_seqs)]
+    mean_depth = float(np.mean(np.concatenate(depths)))
+    first = cdbgen.prompt_ids(shape.vocab, 1, n_seqs, seed=seed + 1)[0]
+    max_pages = kv.c.max_pages
+    state = cdb.State(shape, n_seqs)
+    ws = cdb.Workspace(dm.desc, 256)
+    scratch = torch.empty(drv.cdb_driver_scratch_bytes(shape.vocab), dtype=torch.uint8, device="cuda")
+    out_ids = torch.empty((n_seqs, n_decode), dtype=torch.int32, device="cuda")
+
+    def run(n, nd, **mode):
+        d = drv.Driver(max_batch=64, max_active=n, r_max=R, max_seqs=n_seqs, max_pages=max_pages,
+                       core_pages=kv.c.core_pages, **mode)
+        for q in range(n):
+            d.add_sequence(prompt, depths[q][:nd])
+        secs = d.run(dm.model, kv.c, state.c, scratch, first, ws.buf, tokens_out=out_ids)
+        if cdb.cdb_read_device_error(ws.buf) != 0:
+            raise RuntimeError("device error in the driver run")
+        return secs, d.stats()
+
+    run(4, 8)  # first use of the boundary kernels
+    res = {"workload": f"{n_seqs} requests, prompt {prompt} (KV synthesized), {n_decode} decode tokens each, "
+                       f"depths categorical {{1:.3,2:.3,3:.2,4:.2}}, max batch 64, full depth-indexed KV",
+           "mean_depth": round(mean_depth, 4), "flop_bound": round(cost.flop_bound(shape, mean_depth), 4)}
+    for name, mode in (("cdb_refill", {}), ("cdb_no_refill", {"refill": False}), ("cb_fixed_depth",
+                                                                               {"fixed_depth": True})):
+        secs, st = run(n_seqs, n_decode, **mode)
+        res[name] = {"tokens_per_s": round(st["tokens"] / secs, 1), "seconds": round(secs, 4),
+                     "loop_steps": st["loop_steps"], "idle_rows": st["idle_rows"],
+                     "coda_calls": st["coda_calls"]}
+        log(f"e2e {name}: {st['tokens']} tokens in {secs:.3f}s, {st['loop_steps']} loop steps")
+    cb = res["cb_fixed_depth"]["tokens_per_s"]
+    res["speedup_refill_vs_cb"] = round(res["cdb_refill"]["tokens_per_s"] / cb, 4)
+    res["speedup_no_refill_vs_cb"] = round(res["cdb_no_refill"]["tokens_per_s"] / cb, 4)
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--cpu-sample", type=int, default=16, help="rows in the CPU-oracle sample (0 = skip)")
+    ap.add_argument("--no-e2e", action="store_true", help="skip the whole-decode driver runs")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="run one plain device copy of this many MiB first (a known-size reference for HBM counters)")
     args = ap.parse_args()
@@ -238,6 +290,10 @@ def main():
     attn_gbs = ab / (attn_ms * 1e-3) / 1e9
     log(f"attention {attn_ms * 1e3:.1f} us/launch, {ab / 1e6:.1f} MB -> {attn_gbs:.0f} GB/s")
 
+    e2e = None
+    if not args.no_e2e:
+        e2e = e2e_decode(shape, dm, kv, n_rows, pos_lo, pos_hi + 1 - pos_lo)
+
     cpu = None
     if args.cpu_sample > 0:
         threads = min(16, os.cpu_count() or 1)
@@ -272,6 +328,7 @@ def main():
                           "frac": round(sb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                           "flops": step_flops(shape, rows_np)},
         "cpu_baseline": cpu,
+        "e2e": e2e,
     }
     print(json.dumps(res), flush=True)
 
