@@ -84,6 +84,8 @@ WsLayout ws_layout(const cdb_model_desc& d, int rows) {
     off = align256(off + M * (size_t)(d.head_dim / 2) * 8);
     L.order = off;
     off = align256(off + M * 4);
+    L.kvpid = off;
+    off = align256(off + M * 4);
     L.total = off;
     return L;
 }
@@ -105,6 +107,7 @@ struct Ctx {
     float* part;
     float2* rope;
     int32_t* order;
+    int32_t* kvpid;
 };
 
 static Ctx make_ctx(const cdb_model* model, void* ws, int rows) {
@@ -124,6 +127,7 @@ static Ctx make_ctx(const cdb_model* model, void* ws, int rows) {
     c.part = reinterpret_cast<float*>(c.ws + c.L.part);
     c.rope = reinterpret_cast<float2*>(c.ws + c.L.rope);
     c.order = reinterpret_cast<int32_t*>(c.ws + c.L.order);
+    c.kvpid = reinterpret_cast<int32_t*>(c.ws + c.L.kvpid);
     return c;
 }
 
@@ -147,7 +151,7 @@ static cdb_status run_layers(const Ctx& c, int first, int count, KvTarget kv, co
         const size_t lb = (size_t)(first + l) * c.wl.layer_stride;
         kv.layer = l;
         EpiArgs ea{};
-        ea.seq = r.seq;
+        ea.kvpid = c.kvpid;
         ea.pos = r.pos;
         ea.H = d.n_heads;
         ea.hd = d.head_dim;
@@ -285,8 +289,10 @@ cdb_status cdb_boundary_prelude(const cdb_model* model, const cdb_kv* kv, const 
     if (d.injection && !state->e) return CDB_ERR_INVALID_ARG;
     if (rows->n_rows == 0) return CDB_OK;
     Ctx c = make_ctx(model, ws, rows->n_rows);
-    HIPCHK(launch_embed(d, wptr(c, c.wl.embed), tokens, *rows, *kv, state->n_slots, c.h, c.rope, c.err, st));
-    s = run_layers(c, 0, d.n_prelude, stage_target(d, *kv, 0), *rows, false, st);
+    const KvTarget t = stage_target(d, *kv, 0);
+    HIPCHK(launch_embed(d, wptr(c, c.wl.embed), tokens, *rows, *kv, t, state->n_slots, c.h, c.rope, c.kvpid, c.err,
+                        st));
+    s = run_layers(c, 0, d.n_prelude, t, *rows, false, st);
     if (s != CDB_OK) return s;
     HIPCHK(launch_store_state(rows->n_rows, d.d, state->n_slots, rows->slot, c.h, state->h,
                               d.injection ? state->e : nullptr, st));
@@ -305,7 +311,10 @@ cdb_status cdb_loop_step(const cdb_model* model, const cdb_kv* kv, const cdb_sta
     const int M = rows->n_rows;
     Ctx c = make_ctx(model, ws, M);
     if (M > 0) {
-        HIPCHK(launch_gather(d, *state, *rows, *kv, c.h, c.h_in, d.injection ? c.x : nullptr, c.rope, c.err, st));
+        KvTarget t = stage_target(d, *kv, 1);
+        t.c_row = rows->c;
+        HIPCHK(launch_gather(d, *state, *rows, *kv, t, c.h, c.h_in, d.injection ? c.x : nullptr, c.rope, c.kvpid,
+                             c.err, st));
         if (d.injection) {
             EpiArgs ea{};
             ea.out = c.h;
@@ -313,8 +322,6 @@ cdb_status cdb_loop_step(const cdb_model* model, const cdb_kv* kv, const cdb_sta
             ea.err = c.err;
             HIPCHK(launch_gemm(EPI_STORE, c.x, wptr(c, c.wl.adapter), M, c.gm.adapter, c.part, ea, st));
         }
-        KvTarget t = stage_target(d, *kv, 1);
-        t.c_row = rows->c;
         s = run_layers(c, d.n_prelude, d.n_core, t, *rows, false, st);
         if (s != CDB_OK) return s;
         HIPCHK(launch_exit(d, *rows, c.h, c.h_in, wptr(c, c.wl.w_exit), state->h, state->n_slots, *out, st));
@@ -333,8 +340,10 @@ cdb_status cdb_boundary_coda(const cdb_model* model, const cdb_kv* kv, const cdb
     const int M = rows->n_rows;
     if (M == 0) return CDB_OK;
     Ctx c = make_ctx(model, ws, M);
-    HIPCHK(launch_load_state(d, M, rows->slot, rows->pos, state->h, state->n_slots, c.h, c.rope, c.err, st));
-    s = run_layers(c, d.n_prelude + d.n_core, d.n_coda, stage_target(d, *kv, 2), *rows, true, st);
+    const KvTarget t = stage_target(d, *kv, 2);
+    HIPCHK(launch_load_state(d, M, rows->slot, rows->seq, rows->pos, t, state->h, state->n_slots, c.h, c.rope, c.kvpid,
+                             c.err, st));
+    s = run_layers(c, d.n_prelude + d.n_core, d.n_coda, t, *rows, true, st);
     if (s != CDB_OK) return s;
     EpiArgs ea{};
     ea.out = logits;

@@ -75,7 +75,7 @@ struct EpiArgs {
     int ld_act;     // F
     float* q;       // QKV: q after RoPE [M][d]
     KvTarget kv;
-    const int32_t* seq;
+    const int32_t* kvpid;  // QKV: page id of each row's K/V write in this stage's pool, -1 = none
     const int32_t* pos;
     const float2* rope;  // [M][hd/2] (cos, sin) of pos * base^(-2j/hd), one table per stage call
     int H, hd;
@@ -95,7 +95,7 @@ struct WeightLayout {
 bool weight_layout(const cdb_model_desc& d, WeightLayout* out);
 
 struct WsLayout {
-    size_t err, h, h_in, q, x, act, part, rope, order, total;
+    size_t err, h, h_in, q, x, act, part, rope, order, kvpid, total;
 };
 WsLayout ws_layout(const cdb_model_desc& d, int rows);
 
@@ -114,15 +114,20 @@ hipError_t launch_row_order(const int32_t* pos, int M, int32_t* order, hipStream
 hipError_t launch_resid_norm(float* h, const float* part, int S, int M, int d, float eps, uint16_t* out,
                              hipStream_t st);
 // The row-entry kernels of the three stage calls also fill the call's RoPE
-// table rope[M][hd/2] = (cos, sin) of pos * base^(-2j/hd), angles in fp64.
+// table rope[M][hd/2] = (cos, sin) of pos * base^(-2j/hd), angles in fp64,
+// and kvpid[M], the page of the stage's pool that receives each row's K/V
+// (the page table looked up once per call; -1 and a device error if unmapped).
 hipError_t launch_gather(const cdb_model_desc& md, const cdb_state& s, const cdb_rows& r, const cdb_kv& kv,
-                         float* h, float* h_in, uint16_t* xcat, float2* rope, int* err, hipStream_t st);
+                         const KvTarget& kt, float* h, float* h_in, uint16_t* xcat, float2* rope, int32_t* kvpid,
+                         int* err, hipStream_t st);
 hipError_t launch_embed(const cdb_model_desc& md, const uint16_t* embed, const int32_t* tokens, const cdb_rows& r,
-                        const cdb_kv& kv, int n_slots, float* h, float2* rope, int* err, hipStream_t st);
+                        const cdb_kv& kv, const KvTarget& kt, int n_slots, float* h, float2* rope, int32_t* kvpid,
+                        int* err, hipStream_t st);
 hipError_t launch_store_state(int M, int d, int n_slots, const int32_t* slot, const float* h, float* state_h,
                               float* state_e, hipStream_t st);
-hipError_t launch_load_state(const cdb_model_desc& md, int M, const int32_t* slot, const int32_t* pos,
-                             const float* state_h, int n_slots, float* h, float2* rope, int* err, hipStream_t st);
+hipError_t launch_load_state(const cdb_model_desc& md, int M, const int32_t* slot, const int32_t* seq,
+                             const int32_t* pos, const KvTarget& kt, const float* state_h, int n_slots, float* h,
+                             float2* rope, int32_t* kvpid, int* err, hipStream_t st);
 hipError_t launch_exit(const cdb_model_desc& md, const cdb_rows& r, const float* h, const float* h_in,
                        const uint16_t* w_exit, float* state_h, int n_slots, const cdb_step_out& o, hipStream_t st);
 hipError_t launch_compact(int M, const uint8_t* mask, int32_t* cont, int32_t* exited, int32_t* counts,

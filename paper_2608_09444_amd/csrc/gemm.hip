@@ -37,9 +37,18 @@ struct GemmArgs {
     float* part;  // EPI_PARTIAL: [S][M][N]
 };
 
+// Inputs of the q/k/v epilogue, staged in LDS: the RoPE factors of the
+// stripe's 16 rotary pairs for every row, and each row's K/V write page and
+// slot within it.
+struct QkvStage {
+    const float2* rope;  // [rows][16]
+    const int* pid;      // [rows]
+    const int* tok;      // [rows]
+};
+
 template <int EPI>
 __device__ __forceinline__ void epilogue_elem(float val, float partner, int m, int p, const GemmArgs& ga,
-                                              const EpiArgs& ea) {
+                                              const EpiArgs& ea, const QkvStage& qs) {
     if (EPI == EPI_STORE) {
         ea.out[(size_t)m * ea.ld_out + p] = val;
     } else if (EPI == EPI_PARTIAL) {
@@ -55,11 +64,10 @@ __device__ __forceinline__ void epilogue_elem(float val, float partner, int m, i
         const int hg = ea.H * gph;
         const int part = g / hg, rem = g - part * hg;
         const int head = rem / gph, gi = rem - head * gph;
-        const int j = gi * 16 + jj;
-        const int dim = j + half * (ea.hd >> 1);
+        const int dim = gi * 16 + jj + half * (ea.hd >> 1);
         float outv = val;
         if (part < 2) {
-            const float2 cs = ea.rope[(size_t)m * (ea.hd >> 1) + j];
+            const float2 cs = qs.rope[m * 16 + jj];
             const float xf = half ? partner : val, xs = half ? val : partner;
             outv = half ? (xs * cs.x + xf * cs.y) : (xf * cs.x - xs * cs.y);
         }
@@ -67,18 +75,10 @@ __device__ __forceinline__ void epilogue_elem(float val, float partner, int m, i
             ea.q[(size_t)m * (ea.H * ea.hd) + head * ea.hd + dim] = outv;
             return;
         }
+        const int pid = qs.pid[m];  // -1: unmapped (reported by the row-entry kernel)
+        if (pid < 0) return;
         const KvTarget& kv = ea.kv;
-        const int sq = ea.seq[m], ps = ea.pos[m];
-        const int plane = kv.c_row ? kv.c_row[m] + 1 : kv.plane_fixed;
-        const int pg = ps / kPage;
-        int pid = -1;
-        if (sq >= 0 && sq < kv.max_seqs && pg >= 0 && pg < kv.max_pages && plane >= 0 && plane < kv.n_planes)
-            pid = kv.page_table[((size_t)sq * kv.n_planes + plane) * kv.max_pages + pg];
-        if (pid < 0 || pid >= kv.n_pages) {
-            set_err(ea.err, CDB_DEV_UNMAPPED_PAGE);
-            return;
-        }
-        kv.pool[kv_offset(kv.layer, pid, kv.n_pages, part - 1, head, ea.H, ps % kPage, ea.hd) + dim] = f2bf(outv);
+        kv.pool[kv_offset(kv.layer, pid, kv.n_pages, part - 1, head, ea.H, qs.tok[m], ea.hd) + dim] = f2bf(outv);
     }
 }
 
@@ -136,6 +136,32 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs ga, EpiArgs ea) {
         }
     };
     if (ks0 < ks1) load(wa, xa, ks0);
+
+    // q/k/v epilogue inputs, loaded while the weight stream is in flight (no
+    // wait on them before the main loop ends)
+    const int mcap = min(M, MT * 32);
+    const int nthr = KW * 64;
+    constexpr int RP = MT * 2;  // >= mcap * 16 / nthr, as nthr >= 256
+    float2 pf_rope[EPI == EPI_QKV ? RP : 1];
+    int pf_pid = -1, pf_tok = 0;
+    int q_part = 0;
+    if constexpr (EPI == EPI_QKV) {
+        const int gph = ea.hd >> 5, hg = ea.H * gph;
+        q_part = nt / hg;
+        const int gi = (nt - q_part * hg) % gph;
+        if (q_part < 2) {
+#pragma unroll
+            for (int r = 0; r < RP; ++r) {
+                const int idx = tid + r * nthr;
+                if (idx < mcap * 16) pf_rope[r] = ea.rope[(size_t)(idx >> 4) * (ea.hd >> 1) + gi * 16 + (idx & 15)];
+            }
+        }
+        if (q_part > 0 && tid < mcap) {
+            pf_pid = ea.kvpid[tid];
+            pf_tok = ea.pos[tid] % kPage;
+        }
+    }
+
     for (int c0 = ks0; c0 < ks1; c0 += 2 * CH) {
         if (c0 + CH < ks1) load(wb, xb, c0 + CH);
         compute(wa, xa, c0);
@@ -148,6 +174,24 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs ga, EpiArgs ea) {
     float* red = smem;                    // [KW][32 n][32 m]
     float* fin = smem + KW * 1024;        // [32 n][MT*32 m + 1]
     const int fld = MT * 32 + 1;
+    QkvStage qs{};
+    if constexpr (EPI == EPI_QKV) {
+        float2* s_rope = reinterpret_cast<float2*>(fin + 32 * fld);  // [MT*32][16]; 32 * fld is even
+        int* s_pid = reinterpret_cast<int*>(s_rope + MT * 32 * 16);
+        int* s_tok = s_pid + MT * 32;
+        if (q_part < 2) {
+#pragma unroll
+            for (int r = 0; r < RP; ++r) {
+                const int idx = tid + r * nthr;
+                if (idx < mcap * 16) s_rope[idx] = pf_rope[r];
+            }
+        }
+        if (tid < mcap) {
+            s_pid[tid] = pf_pid;
+            s_tok[tid] = pf_tok;
+        }
+        qs = QkvStage{s_rope, s_pid, s_tok};  // visible after the reduction's barriers
+    }
 #pragma unroll
     for (int t = 0; t < MT; ++t) {
 #pragma unroll
@@ -165,13 +209,12 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs ga, EpiArgs ea) {
     }
 
     // epilogue: element (n, m) of the stripe; consecutive threads take consecutive n
-    const int mcap = min(M, MT * 32);
     for (int e = tid; e < 32 * mcap; e += KW * 64) {
         const int m = e >> 5, nn = e & 31;
         const int p = nt * 32 + nn;
         const float val = fin[nn * fld + m];
         const float partner = fin[(nn ^ 16) * fld + m];
-        epilogue_elem<EPI>(val, partner, m, p, ga, ea);
+        epilogue_elem<EPI>(val, partner, m, p, ga, ea, qs);
     }
 }
 
@@ -182,10 +225,10 @@ GemmShape gemm_shape(int N, int K, int epi) {
     if (epi == EPI_PARTIAL) {
         while (stripes * S < 256 && KS / (S * 2) >= 32) S *= 2;
     }
-    // waves per workgroup: 4, or 8 when there are too few workgroups to cover
-    // the chip (every wave then streams twice as many k steps in flight)
+    // waves per workgroup: 8 (more weight bytes in flight per CU) while the
+    // grid fits the chip in one round, else 4
     int KW = 4;
-    if (stripes * S < 256 && KS / S >= 64) KW = 8;
+    if (stripes * S <= 256 && KS / S >= 32) KW = 8;
     return GemmShape{N, K, S, KW};
 }
 
@@ -198,7 +241,8 @@ static hipError_t launch_mt(const GemmArgs& ga, const EpiArgs& ea, hipStream_t s
         if (e != hipSuccess) return e;
         attr_set = true;
     }
-    const size_t lds = ((size_t)ga.KW * 1024 + 32 * (MT * 32 + 1)) * 4;
+    size_t lds = ((size_t)ga.KW * 1024 + 32 * (MT * 32 + 1)) * 4;
+    if (EPI == EPI_QKV) lds += (size_t)MT * 32 * 16 * 8 + (size_t)MT * 32 * 2 * 4;
     dim3 grid(ga.N / 32, ga.S);
     k_gemm<EPI, MT><<<grid, ga.KW * 64, lds, st>>>(ga, ea);
     return hipGetLastError();
@@ -216,6 +260,7 @@ hipError_t launch_gemm(int epi, const uint16_t* X, const uint16_t* Wp, int M, Ge
                        const EpiArgs& ea, hipStream_t st) {
     if (M <= 0) return hipSuccess;
     if (M > kMaxRows || g.N % 32 || g.K % 16 || g.KW < 1 || g.KW > kMaxKw) return hipErrorInvalidValue;
+    if (epi == EPI_QKV && g.KW < 4) return hipErrorInvalidValue;  // the epilogue staging assumes >= 256 threads
     GemmArgs ga{X, Wp, M, g.N, g.K, g.S, g.KW, part};
     switch (epi) {
         case EPI_QKV: return launch_epi<EPI_QKV>(ga, ea, st);

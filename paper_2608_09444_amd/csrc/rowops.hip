@@ -33,13 +33,32 @@ __device__ __forceinline__ void rope_row(int pos, int hd, float base, float2* ou
 // ------------------------------------------------------------------ gather
 // h[i] = state.h[slot[i]]; h_in[i] = h[i] (exit score of the L2 criterion);
 // xcat[i] = bf16([h; e]) for the input-injection adapter.  Validates the row.
+// kvpid[i]: the page of the stage pool that receives row i's K/V (plane c+1 of
+// the core, or the stage's fixed plane); -1 when the stage has no layers.
+__device__ __forceinline__ void write_page(const KvTarget& kt, int i, int sq, int ps, const int32_t* c_row,
+                                           int32_t* kvpid, int* err) {
+    int pid = -1;
+    if (kt.n_layers > 0) {
+        const int plane = c_row ? c_row[i] + 1 : kt.plane_fixed;
+        const int pg = ps >= 0 ? ps / kPage : -1;
+        if (sq >= 0 && sq < kt.max_seqs && pg >= 0 && pg < kt.max_pages && plane >= 0 && plane < kt.n_planes)
+            pid = kt.page_table[((size_t)sq * kt.n_planes + plane) * kt.max_pages + pg];
+        if (pid < 0 || pid >= kt.n_pages) {
+            set_err(err, CDB_DEV_UNMAPPED_PAGE);
+            pid = -1;
+        }
+    }
+    kvpid[i] = pid;
+}
+
 __global__ __launch_bounds__(256) void k_gather(int d, int r_max, int n_slots, int max_seqs, int max_pos, int hd,
                                                 float base, const int32_t* __restrict__ slot,
                                                 const int32_t* __restrict__ seq, const int32_t* __restrict__ pos,
                                                 const int32_t* __restrict__ c, const int32_t* __restrict__ depth,
                                                 const float* __restrict__ sh, const float* __restrict__ se,
                                                 float* __restrict__ h, float* __restrict__ h_in,
-                                                uint16_t* __restrict__ xcat, float2* __restrict__ rope, int* err) {
+                                                uint16_t* __restrict__ xcat, float2* __restrict__ rope, KvTarget kt,
+                                                int32_t* __restrict__ kvpid, int* err) {
     const int i = blockIdx.x;
     const int sl = slot[i];
     rope_row(pos[i], hd, base, rope + (size_t)i * (hd / 2));
@@ -47,6 +66,7 @@ __global__ __launch_bounds__(256) void k_gather(int d, int r_max, int n_slots, i
         if (depth[i] < 1 || depth[i] > r_max || c[i] < 0 || c[i] >= depth[i]) set_err(err, CDB_DEV_BAD_DEPTH);
         if (sl < 0 || sl >= n_slots || seq[i] < 0 || seq[i] >= max_seqs || pos[i] < 0 || pos[i] >= max_pos)
             set_err(err, CDB_DEV_BAD_INDEX);
+        write_page(kt, i, seq[i], pos[i], c, kvpid, err);
     }
     const bool ok = sl >= 0 && sl < n_slots;
     for (int k = threadIdx.x * 4; k < d; k += 256 * 4) {
@@ -68,14 +88,18 @@ __global__ __launch_bounds__(256) void k_gather(int d, int r_max, int n_slots, i
 
 // h[i] = state.h[slot[i]] (coda input)
 __global__ __launch_bounds__(256) void k_load_state(int d, int n_slots, int hd, float base,
-                                                    const int32_t* __restrict__ slot, const int32_t* __restrict__ pos,
+                                                    const int32_t* __restrict__ slot, const int32_t* __restrict__ seq,
+                                                    const int32_t* __restrict__ pos, KvTarget kt,
                                                     const float* __restrict__ sh, float* __restrict__ h,
-                                                    float2* __restrict__ rope, int* err) {
+                                                    float2* __restrict__ rope, int32_t* __restrict__ kvpid, int* err) {
     const int i = blockIdx.x;
     const int sl = slot[i];
     rope_row(pos[i], hd, base, rope + (size_t)i * (hd / 2));
     const bool ok = sl >= 0 && sl < n_slots;
-    if (!ok && threadIdx.x == 0) set_err(err, CDB_DEV_BAD_INDEX);
+    if (threadIdx.x == 0) {
+        if (!ok) set_err(err, CDB_DEV_BAD_INDEX);
+        write_page(kt, i, seq[i], pos[i], nullptr, kvpid, err);
+    }
     for (int k = threadIdx.x * 4; k < d; k += 1024)
         *reinterpret_cast<float4*>(h + (size_t)i * d + k) =
             ok ? *reinterpret_cast<const float4*>(sh + (size_t)sl * d + k) : make_float4(0.f, 0.f, 0.f, 0.f);
@@ -120,14 +144,18 @@ __global__ __launch_bounds__(256) void k_embed(int d, int vocab, int n_slots, in
                                                float base, const uint16_t* __restrict__ E,
                                                const int32_t* __restrict__ tok, const int32_t* __restrict__ slot,
                                                const int32_t* __restrict__ seq, const int32_t* __restrict__ pos,
-                                               float* __restrict__ h, float2* __restrict__ rope, int* err) {
+                                               float* __restrict__ h, float2* __restrict__ rope, KvTarget kt,
+                                               int32_t* __restrict__ kvpid, int* err) {
     const int i = blockIdx.x;
     rope_row(pos[i], hd, base, rope + (size_t)i * (hd / 2));
     const int t = tok[i];
     const bool ok = t >= 0 && t < vocab;
-    if (threadIdx.x == 0 && (!ok || slot[i] < 0 || slot[i] >= n_slots || seq[i] < 0 || seq[i] >= max_seqs ||
-                             pos[i] < 0 || pos[i] >= max_pos))
-        set_err(err, CDB_DEV_BAD_INDEX);
+    if (threadIdx.x == 0) {
+        if (!ok || slot[i] < 0 || slot[i] >= n_slots || seq[i] < 0 || seq[i] >= max_seqs || pos[i] < 0 ||
+            pos[i] >= max_pos)
+            set_err(err, CDB_DEV_BAD_INDEX);
+        write_page(kt, i, seq[i], pos[i], nullptr, kvpid, err);
+    }
     for (int k = threadIdx.x * 4; k < d; k += 1024) {
         float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
         if (ok) {
@@ -358,18 +386,22 @@ __global__ void k_ws_init(int* err) {
 // ------------------------------------------------------------------ launchers
 static int page_cap(const cdb_kv& kv) { return kv.max_pages * kPage; }
 
-hipError_t launch_gather(const cdb_model_desc& md, const cdb_state& s, const cdb_rows& r, const cdb_kv& kv, float* h,
-                         float* h_in, uint16_t* xcat, float2* rope, int* err, hipStream_t st) {
+hipError_t launch_gather(const cdb_model_desc& md, const cdb_state& s, const cdb_rows& r, const cdb_kv& kv,
+                         const KvTarget& kt, float* h, float* h_in, uint16_t* xcat, float2* rope, int32_t* kvpid,
+                         int* err, hipStream_t st) {
     if (r.n_rows <= 0) return hipSuccess;
     k_gather<<<r.n_rows, 256, 0, st>>>(md.d, md.r_max, s.n_slots, kv.max_seqs, page_cap(kv), md.head_dim, md.rope_base,
-                                        r.slot, r.seq, r.pos, r.c, r.depth, s.h, s.e, h, h_in, xcat, rope, err);
+                                        r.slot, r.seq, r.pos, r.c, r.depth, s.h, s.e, h, h_in, xcat, rope, kt, kvpid,
+                                        err);
     return hipGetLastError();
 }
 
-hipError_t launch_load_state(const cdb_model_desc& md, int M, const int32_t* slot, const int32_t* pos,
-                             const float* state_h, int n_slots, float* h, float2* rope, int* err, hipStream_t st) {
+hipError_t launch_load_state(const cdb_model_desc& md, int M, const int32_t* slot, const int32_t* seq,
+                             const int32_t* pos, const KvTarget& kt, const float* state_h, int n_slots, float* h,
+                             float2* rope, int32_t* kvpid, int* err, hipStream_t st) {
     if (M <= 0) return hipSuccess;
-    k_load_state<<<M, 256, 0, st>>>(md.d, n_slots, md.head_dim, md.rope_base, slot, pos, state_h, h, rope, err);
+    k_load_state<<<M, 256, 0, st>>>(md.d, n_slots, md.head_dim, md.rope_base, slot, seq, pos, kt, state_h, h, rope,
+                                    kvpid, err);
     return hipGetLastError();
 }
 
@@ -384,10 +416,11 @@ hipError_t launch_resid_norm(float* h, const float* part, int S, int M, int d, f
 }
 
 hipError_t launch_embed(const cdb_model_desc& md, const uint16_t* embed, const int32_t* tokens, const cdb_rows& r,
-                        const cdb_kv& kv, int n_slots, float* h, float2* rope, int* err, hipStream_t st) {
+                        const cdb_kv& kv, const KvTarget& kt, int n_slots, float* h, float2* rope, int32_t* kvpid,
+                        int* err, hipStream_t st) {
     if (r.n_rows <= 0) return hipSuccess;
     k_embed<<<r.n_rows, 256, 0, st>>>(md.d, md.vocab, n_slots, kv.max_seqs, page_cap(kv), md.head_dim, md.rope_base,
-                                       embed, tokens, r.slot, r.seq, r.pos, h, rope, err);
+                                       embed, tokens, r.slot, r.seq, r.pos, h, rope, kt, kvpid, err);
     return hipGetLastError();
 }
 

@@ -80,39 +80,72 @@ class Lockstep:
                                          "kv_max": 0.0, "score_max": 0.0}
         self.calls = {"prelude": 0, "loop": 0, "coda": 0}
         self.argmax_checked = 0
+        # mean-abs bookkeeping per output kind over the whole run: sum of |error|,
+        # element count, and the per-call mean bound weighted by elements
+        self.run_sums: Dict[str, List[float]] = {}
 
     # -------------------------------------------------------------- compare helpers
     def _cmp(self, key_max, key_mean, got, want, what):
+        """max-abs is checked per call; mean-abs is a statistic of the whole
+        result, checked over the run by check_means() (a call of two rows is
+        dominated by single bf16 rounding flips)."""
         d = np.abs(np.asarray(got, np.float64) - want)
         mx, mn = float(d.max()) if d.size else 0.0, float(d.mean()) if d.size else 0.0
         self.errors[key_max] = max(self.errors[key_max], mx)
         if key_mean:
             self.errors[key_mean] = max(self.errors[key_mean], mn)
-        tmax, tmean = self.tol
-        assert mx <= tmax and mn <= tmean, f"{what}: max abs {mx:.3e}, mean abs {mn:.3e} (bound {tmax:.3e}, {tmean:.3e})"
+            acc = self.run_sums.setdefault(key_mean, [0.0, 0, 0.0])
+            acc[0] += float(d.sum())
+            acc[1] += d.size
+            acc[2] += self.tol[1] * d.size
+        tmax = self.tol[0]
+        assert mx <= tmax, f"{what}: max abs {mx:.3e}, mean abs {mn:.3e} (max bound {tmax:.3e})"
+
+    def check_means(self):
+        """Mean-abs error of each output kind over the run against the
+        element-weighted mean of the per-call bounds."""
+        for key, (tot, n, bound) in self.run_sums.items():
+            if n:
+                assert tot / n <= bound / n, f"{key}: run mean abs {tot / n:.3e} > bound {bound / n:.3e}"
 
     def _oracle_bound(self, run32, out_of):
-        """Run the call once through the fp32-accumulator oracle on copies of the
-        oracle's buffers, then restore them; this call's bound is the larger of
-        the absolute tolerance and twice the fp32-vs-fp64 drift of the oracle's
-        own outputs.  `out_of(result)` picks the compared output."""
+        """Run the call through several fp32-level realizations of the oracle's
+        arithmetic on copies of the oracle's buffers, restoring them after each:
+        the same steps with fp32 accumulators; the fp64 steps from the residual
+        state rounded to fp32 (as the device keeps it); and the fp64 steps from
+        the state under two draws of fp32-sized relative noise.  This call's
+        bound is the larger of the absolute tolerance and twice the largest
+        distance of any of them from the oracle's own outputs: in a call of a
+        few rows the error is set by a handful of bf16 rounding flips, which one
+        realization undersamples.  `out_of(result)` picks the compared output."""
         self.tol = (TOL_MAX, TOL_MEAN)
         if not self.sensitivity:
             return None
-        saved = [a.copy() for a in (self.oh, self.op.pre, self.op.core, self.op.coda)]
-        saved_e = None if self.oe is None else self.oe.copy()
-        got32 = out_of(run32(self.om32))
-        for a, b in zip((self.oh, self.op.pre, self.op.core, self.op.coda), saved):
-            a[...] = b
-        if saved_e is not None:
-            self.oe[...] = saved_e
-        return got32
+        bufs = [self.oh, self.op.pre, self.op.core, self.op.coda] + ([self.oe] if self.oe is not None else [])
+        saved = [a.copy() for a in bufs]
 
-    def _set_bound(self, got32, got64):
-        if got32 is None:
+        def restore():
+            for a, b in zip(bufs, saved):
+                a[...] = b
+
+        got = [out_of(run32(self.om32))]
+        restore()
+        rng = np.random.default_rng(1000 + sum(self.calls.values()))
+        for k in range(3):
+            for a in ([self.oh] + ([self.oe] if self.oe is not None else [])):
+                if k == 0:
+                    a[...] = a.astype(np.float32)
+                else:
+                    a *= 1.0 + 2.0 ** -24 * rng.standard_normal(a.shape)
+            got.append(out_of(run32(self.om)))
+            restore()
+        return got
+
+    def _set_bound(self, variants, got64):
+        if variants is None:
             return
-        d = np.abs(got32 - got64)
-        mx, mn = float(d.max()), float(d.mean())
+        mx = max(float(np.abs(v - got64).max()) for v in variants)
+        mn = max(float(np.abs(v - got64).mean()) for v in variants)
         self.self_diff["max"] = max(self.self_diff["max"], mx)
         self.self_diff["mean"] = max(self.self_diff["mean"], mn)
         self.tol = (max(TOL_MAX, 2 * mx), max(TOL_MEAN, 2 * mn))
@@ -272,6 +305,7 @@ class Lockstep:
                     if t + 1 < len(toks[q]):
                         toks[q][t + 1] = oid[j]
                         boundary.append((q, t + 1))
+        self.check_means()
         return toks
 
 
