@@ -84,6 +84,7 @@ struct EpiArgs {
 
 struct GemmShape {
     int N, K, S, KW;  // packed output columns, reduction length, K splits over workgroups, waves per workgroup
+    int NS;           // 32-column stripes per workgroup (1 or 2)
 };
 
 // ---------------------------------------------------------------- layouts

@@ -82,9 +82,11 @@ __device__ __forceinline__ void epilogue_elem(float val, float partner, int m, i
     }
 }
 
-// MT = 32-row tiles of M covered by one pass (M <= 32 * MT).
-template <int EPI, int MT>
+// MT = 32-row tiles of M covered by one pass (M <= 32 * MT); NS = adjacent
+// 32-column stripes per workgroup (they share every activation load).
+template <int EPI, int MT, int NS>
 __global__ __launch_bounds__(512) void k_gemm(GemmArgs ga, EpiArgs ea) {
+    static_assert(EPI != EPI_QKV || NS == 1, "the q/k/v epilogue stages one stripe");
     extern __shared__ __align__(16) float smem[];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int KW = ga.KW;
@@ -93,67 +95,76 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs ga, EpiArgs ea) {
     const int a0 = (int)(((long)s * KS) / ga.S), a1 = (int)(((long)(s + 1) * KS) / ga.S);
     const int ks0 = a0 + (int)(((long)wave * (a1 - a0)) / KW);
     const int ks1 = a0 + (int)(((long)(wave + 1) * (a1 - a0)) / KW);
-    const int nt = blockIdx.x;  // 32-column stripe
+    const int nt = blockIdx.x * NS;  // first 32-column stripe
     const int M = ga.M;
 
-    floatx16 acc[MT];
+    floatx16 acc[NS][MT];
 #pragma unroll
-    for (int t = 0; t < MT; ++t)
+    for (int ns = 0; ns < NS; ++ns)
 #pragma unroll
-        for (int j = 0; j < 16; ++j) acc[t][j] = 0.f;
+        for (int t = 0; t < MT; ++t)
+#pragma unroll
+            for (int j = 0; j < 16; ++j) acc[ns][t][j] = 0.f;
 
     const u32x4* wsrc = reinterpret_cast<const u32x4*>(ga.Wp) + (size_t)nt * KS * 64 + lane;
     // X is in fragment layout: the operand of m-tile t at k step k is the 1 KiB tile (t, k)
     const u32x4* xsrc = reinterpret_cast<const u32x4*>(ga.X) + lane;
-    constexpr int CH = MT <= 2 ? 8 : (MT == 4 ? 4 : 1);  // k steps per load batch
+    // k steps per load batch (register budget: two batches of NS + MT operands)
+    constexpr int CH = NS == 1 ? (MT <= 2 ? 8 : (MT == 4 ? 4 : 1)) : (MT <= 2 ? 4 : (MT == 4 ? 2 : 1));
 
     // Two register sets: the next batch's loads are in flight while the
     // current batch feeds the MFMAs.
-    u32x4 wa[CH], wb[CH];
+    u32x4 wa[CH][NS], wb[CH][NS];
     u32x4 xa[CH][MT], xb[CH][MT];
     // Loads are unconditional (steps past the wave's range re-read its last
     // step, whose weight tile is then zeroed) so that the compiler keeps each
     // batch's loads in flight across the other batch's MFMAs.
-    auto load = [&](u32x4 (&w)[CH], u32x4 (&x)[CH][MT], int c0) {
+    auto load = [&](u32x4 (&w)[CH][NS], u32x4 (&x)[CH][MT], int c0) {
 #pragma unroll
         for (int i = 0; i < CH; ++i) {
             const int ks = min(c0 + i, ks1 - 1);
-            w[i] = wsrc[(size_t)ks * 64];
+#pragma unroll
+            for (int ns = 0; ns < NS; ++ns) w[i][ns] = wsrc[((size_t)ns * KS + ks) * 64];
 #pragma unroll
             for (int t = 0; t < MT; ++t) x[i][t] = xsrc[((size_t)t * KS + ks) * 64];
         }
     };
-    auto compute = [&](const u32x4 (&w)[CH], const u32x4 (&x)[CH][MT], int c0) {
+    auto compute = [&](const u32x4 (&w)[CH][NS], const u32x4 (&x)[CH][MT], int c0) {
 #pragma unroll
         for (int i = 0; i < CH; ++i) {
             const uint32_t keep = c0 + i < ks1 ? 0xffffffffu : 0u;
-            const u32x4 wm = w[i] & keep;
-            const bf16x8 a = __builtin_bit_cast(bf16x8, wm);
 #pragma unroll
-            for (int t = 0; t < MT; ++t)
-                acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, __builtin_bit_cast(bf16x8, x[i][t]), acc[t], 0, 0,
-                                                                 0);
+            for (int ns = 0; ns < NS; ++ns) {
+                const u32x4 wm = w[i][ns] & keep;
+                const bf16x8 a = __builtin_bit_cast(bf16x8, wm);
+#pragma unroll
+                for (int t = 0; t < MT; ++t)
+                    acc[ns][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, __builtin_bit_cast(bf16x8, x[i][t]),
+                                                                         acc[ns][t], 0, 0, 0);
+            }
         }
     };
     if (ks0 < ks1) load(wa, xa, ks0);
 
     // q/k/v epilogue inputs, loaded while the weight stream is in flight (no
-    // wait on them before the main loop ends)
+    // wait on them before the main loop ends); above 64 rows the RoPE factors
+    // would cost more registers than the loop can spare and are loaded after it
     const int mcap = min(M, MT * 32);
     const int nthr = KW * 64;
-    constexpr int RP = MT * 2;  // >= mcap * 16 / nthr, as nthr >= 256
-    float2 pf_rope[EPI == EPI_QKV ? RP : 1];
+    constexpr int RP = MT <= 2 ? MT * 2 : 1;  // MT <= 2: >= mcap * 16 / nthr, as nthr >= 256
+    float2 pf_rope[RP];
     int pf_pid = -1, pf_tok = 0;
-    int q_part = 0;
+    int q_part = 0, q_gi = 0;
     if constexpr (EPI == EPI_QKV) {
         const int gph = ea.hd >> 5, hg = ea.H * gph;
         q_part = nt / hg;
-        const int gi = (nt - q_part * hg) % gph;
-        if (q_part < 2) {
+        q_gi = (nt - q_part * hg) % gph;
+        if (MT <= 2 && q_part < 2) {
 #pragma unroll
             for (int r = 0; r < RP; ++r) {
                 const int idx = tid + r * nthr;
-                if (idx < mcap * 16) pf_rope[r] = ea.rope[(size_t)(idx >> 4) * (ea.hd >> 1) + gi * 16 + (idx & 15)];
+                if (idx < mcap * 16)
+                    pf_rope[r] = ea.rope[(size_t)(idx >> 4) * (ea.hd >> 1) + q_gi * 16 + (idx & 15)];
             }
         }
         if (q_part > 0 && tid < mcap) {
@@ -170,20 +181,26 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs ga, EpiArgs ea) {
     }
 
     // Sum the KW wave tiles in wave order, one 32x32 m-tile at a time.
-    // acc[t][j] holds D[n = (j/4)*8 + (lane/32)*4 + j%4][m = t*32 + lane%32].
+    // acc[ns][t][j] holds D[n = (j/4)*8 + (lane/32)*4 + j%4][m = t*32 + lane%32]
+    // of stripe nt + ns.
     float* red = smem;                    // [KW][32 n][32 m]
-    float* fin = smem + KW * 1024;        // [32 n][MT*32 m + 1]
+    float* fin = smem + KW * 1024;        // [NS][32 n][MT*32 m + 1]
     const int fld = MT * 32 + 1;
     QkvStage qs{};
     if constexpr (EPI == EPI_QKV) {
-        float2* s_rope = reinterpret_cast<float2*>(fin + 32 * fld);  // [MT*32][16]; 32 * fld is even
+        float2* s_rope = reinterpret_cast<float2*>(fin + NS * 32 * fld);  // [MT*32][16]; 32 * fld is even
         int* s_pid = reinterpret_cast<int*>(s_rope + MT * 32 * 16);
         int* s_tok = s_pid + MT * 32;
         if (q_part < 2) {
+            if (MT <= 2) {
 #pragma unroll
-            for (int r = 0; r < RP; ++r) {
-                const int idx = tid + r * nthr;
-                if (idx < mcap * 16) s_rope[idx] = pf_rope[r];
+                for (int r = 0; r < RP; ++r) {
+                    const int idx = tid + r * nthr;
+                    if (idx < mcap * 16) s_rope[idx] = pf_rope[r];
+                }
+            } else {
+                for (int idx = tid; idx < mcap * 16; idx += nthr)
+                    s_rope[idx] = ea.rope[(size_t)(idx >> 4) * (ea.hd >> 1) + q_gi * 16 + (idx & 15)];
             }
         }
         if (tid < mcap) {
@@ -193,28 +210,32 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs ga, EpiArgs ea) {
         qs = QkvStage{s_rope, s_pid, s_tok};  // visible after the reduction's barriers
     }
 #pragma unroll
-    for (int t = 0; t < MT; ++t) {
+    for (int ns = 0; ns < NS; ++ns) {
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-            const int nn = (j >> 2) * 8 + (lane >> 5) * 4 + (j & 3);
-            red[wave * 1024 + nn * 32 + (lane & 31)] = acc[t][j];
+        for (int t = 0; t < MT; ++t) {
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+                const int nn = (j >> 2) * 8 + (lane >> 5) * 4 + (j & 3);
+                red[wave * 1024 + nn * 32 + (lane & 31)] = acc[ns][t][j];
+            }
+            __syncthreads();
+            for (int e = tid; e < 1024; e += nthr) {
+                float sum = 0.f;
+                for (int w = 0; w < KW; ++w) sum += red[w * 1024 + e];
+                fin[ns * 32 * fld + (e >> 5) * fld + t * 32 + (e & 31)] = sum;
+            }
+            __syncthreads();
         }
-        __syncthreads();
-        for (int e = tid; e < 1024; e += KW * 64) {
-            float sum = 0.f;
-            for (int w = 0; w < KW; ++w) sum += red[w * 1024 + e];
-            fin[(e >> 5) * fld + t * 32 + (e & 31)] = sum;
-        }
-        __syncthreads();
     }
 
-    // epilogue: element (n, m) of the stripe; consecutive threads take consecutive n
-    for (int e = tid; e < 32 * mcap; e += KW * 64) {
-        const int m = e >> 5, nn = e & 31;
-        const int p = nt * 32 + nn;
-        const float val = fin[nn * fld + m];
-        const float partner = fin[(nn ^ 16) * fld + m];
-        epilogue_elem<EPI>(val, partner, m, p, ga, ea, qs);
+    // epilogue: element (n, m) of stripe nt + ns; consecutive threads take consecutive n
+    const int E = 32 * mcap;
+    for (int e = tid; e < NS * E; e += nthr) {
+        const int ns = e / E, r = e - ns * E;
+        const int m = r >> 5, nn = r & 31;
+        const int p = (nt + ns) * 32 + nn;
+        const float* f = fin + ns * 32 * fld;
+        epilogue_elem<EPI>(f[nn * fld + m], f[(nn ^ 16) * fld + m], m, p, ga, ea, qs);
     }
 }
 
@@ -229,44 +250,61 @@ GemmShape gemm_shape(int N, int K, int epi) {
     // grid fits the chip in one round, else 4
     int KW = 4;
     if (stripes * S <= 256 && KS / S >= 32) KW = 8;
-    return GemmShape{N, K, S, KW};
+    // wide projections without a K split (gate/up, LM head): two stripes per
+    // workgroup share the activation loads, with 8 waves
+    int NS = 1;
+    if (epi != EPI_QKV && S == 1 && stripes > 256 && stripes % 2 == 0 && KS >= 64) {
+        NS = 2;
+        KW = 8;
+    }
+    return GemmShape{N, K, S, KW, NS};
 }
 
-template <int EPI, int MT>
+template <int EPI, int MT, int NS>
 static hipError_t launch_mt(const GemmArgs& ga, const EpiArgs& ea, hipStream_t st) {
     static bool attr_set = false;
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm<EPI, MT>),
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm<EPI, MT, NS>),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
-    size_t lds = ((size_t)ga.KW * 1024 + 32 * (MT * 32 + 1)) * 4;
+    size_t lds = ((size_t)ga.KW * 1024 + (size_t)NS * 32 * (MT * 32 + 1)) * 4;
     if (EPI == EPI_QKV) lds += (size_t)MT * 32 * 16 * 8 + (size_t)MT * 32 * 2 * 4;
-    dim3 grid(ga.N / 32, ga.S);
-    k_gemm<EPI, MT><<<grid, ga.KW * 64, lds, st>>>(ga, ea);
+    dim3 grid(ga.N / (32 * NS), ga.S);
+    k_gemm<EPI, MT, NS><<<grid, ga.KW * 64, lds, st>>>(ga, ea);
     return hipGetLastError();
 }
 
+template <int EPI, int NS>
+static hipError_t launch_ns(const GemmArgs& ga, const EpiArgs& ea, hipStream_t st) {
+    if (ga.M <= 32) return launch_mt<EPI, 1, NS>(ga, ea, st);
+    if (ga.M <= 64) return launch_mt<EPI, 2, NS>(ga, ea, st);
+    if (ga.M <= 128) return launch_mt<EPI, 4, NS>(ga, ea, st);
+    return launch_mt<EPI, 8, 1>(ga, ea, st);  // two stripes of 256 rows exceed the register file
+}
+
 template <int EPI>
-static hipError_t launch_epi(const GemmArgs& ga, const EpiArgs& ea, hipStream_t st) {
-    if (ga.M <= 32) return launch_mt<EPI, 1>(ga, ea, st);
-    if (ga.M <= 64) return launch_mt<EPI, 2>(ga, ea, st);
-    if (ga.M <= 128) return launch_mt<EPI, 4>(ga, ea, st);
-    return launch_mt<EPI, 8>(ga, ea, st);
+static hipError_t launch_epi(const GemmArgs& ga, const EpiArgs& ea, int ns, hipStream_t st) {
+    if constexpr (EPI == EPI_QKV) {
+        return launch_ns<EPI, 1>(ga, ea, st);
+    } else {
+        return ns == 2 ? launch_ns<EPI, 2>(ga, ea, st) : launch_ns<EPI, 1>(ga, ea, st);
+    }
 }
 
 hipError_t launch_gemm(int epi, const uint16_t* X, const uint16_t* Wp, int M, GemmShape g, float* part,
                        const EpiArgs& ea, hipStream_t st) {
     if (M <= 0) return hipSuccess;
-    if (M > kMaxRows || g.N % 32 || g.K % 16 || g.KW < 1 || g.KW > kMaxKw) return hipErrorInvalidValue;
-    if (epi == EPI_QKV && g.KW < 4) return hipErrorInvalidValue;  // the epilogue staging assumes >= 256 threads
+    if (M > kMaxRows || g.K % 16 || g.KW < 1 || g.KW > kMaxKw || (g.NS != 1 && g.NS != 2) || g.N % (32 * g.NS))
+        return hipErrorInvalidValue;
+    if (epi == EPI_QKV && (g.KW < 4 || g.NS != 1)) return hipErrorInvalidValue;  // epilogue staging: >= 256 threads
     GemmArgs ga{X, Wp, M, g.N, g.K, g.S, g.KW, part};
     switch (epi) {
-        case EPI_QKV: return launch_epi<EPI_QKV>(ga, ea, st);
-        case EPI_SWIGLU: return launch_epi<EPI_SWIGLU>(ga, ea, st);
-        case EPI_PARTIAL: return launch_epi<EPI_PARTIAL>(ga, ea, st);
-        default: return launch_epi<EPI_STORE>(ga, ea, st);
+        case EPI_QKV: return launch_epi<EPI_QKV>(ga, ea, g.NS, st);
+        case EPI_SWIGLU: return launch_epi<EPI_SWIGLU>(ga, ea, g.NS, st);
+        case EPI_PARTIAL: return launch_epi<EPI_PARTIAL>(ga, ea, g.NS, st);
+        default: return launch_epi<EPI_STORE>(ga, ea, g.NS, st);
     }
 }
 
