@@ -196,7 +196,6 @@ def e2e_decode(shape, dm, kv, n_seqs, prompt, n_decode, seed=3):
     max_pages = kv.c.max_pages
     state = cdb.State(shape, n_seqs)
     ws = cdb.Workspace(dm.desc, 256)
-    scratch = torch.empty(drv.cdb_driver_scratch_bytes(shape.vocab), dtype=torch.uint8, device="cuda")
     out_ids = torch.empty((n_seqs, n_decode), dtype=torch.int32, device="cuda")
 
     def run(n, nd, **mode):
@@ -204,6 +203,7 @@ def e2e_decode(shape, dm, kv, n_seqs, prompt, n_decode, seed=3):
                        core_pages=kv.c.core_pages, **mode)
         for q in range(n):
             d.add_sequence(prompt, depths[q][:nd])
+        scratch = torch.empty(d.scratch_bytes(shape.vocab), dtype=torch.uint8, device="cuda")
         secs = d.run(dm.model, kv.c, state.c, scratch, first, ws.buf, tokens_out=out_ids)
         if cdb.cdb_read_device_error(ws.buf) != 0:
             raise RuntimeError("device error in the driver run")

@@ -157,14 +157,35 @@ typedef struct {
 
 /* Loop-step outputs (device): exit_score fp32 [n_rows]; exit_mask uint8
  * [n_rows]; cont / exited int32 [n_rows] = batch indices of continuing / exiting
- * rows in batch order (stable compaction); counts int32 [2] = {n_cont, n_exit}. */
+ * rows in batch order (stable compaction); counts int32 [2] = {n_cont, n_exit};
+ * exit_next uint8 [n_rows] (optional, may be NULL) = 1 for a continuing row
+ * whose token will exit after its next loop. */
 typedef struct {
     float* exit_score;
     uint8_t* exit_mask;
     int32_t* cont;
     int32_t* exited;
     int32_t* counts;
+    uint8_t* exit_next;
 } cdb_step_out;
+
+/* Threshold exits decided on the device (Section 4.3, lookahead gate; App. C.2).
+ * The criterion is the model's: exit_kind 0 exits when the gate score after a
+ * loop is >= threshold; exit_kind 1 (convergence) when the distance between the
+ * states before and after a loop is < threshold, from loop 2 on (after loop 1
+ * it compares the recurrent state with the prelude output).  Without lookahead
+ * a decision taken after loop r makes r the token's last loop; with lookahead
+ * it makes r + 1 the last, so the exit is known one loop step before it
+ * happens (minimum depth 2 for the gate, 3 for convergence).  Every token
+ * exits after loop r_max at the latest.
+ *   pending: device uint8 [n_slots], the lookahead decision carried from one
+ *   loop step to the next per state slot; read and written by the library;
+ *   the caller zeroes it once when allocating. */
+typedef struct {
+    float threshold;
+    int32_t lookahead;
+    uint8_t* pending;
+} cdb_gate;
 
 /* Workspace (device scratch) needed for calls with up to max_rows rows. */
 size_t cdb_workspace_bytes(const cdb_model_desc* desc, int32_t max_rows);
@@ -186,7 +207,8 @@ cdb_status cdb_boundary_prelude(const cdb_model* model, const cdb_kv* kv, const 
  *   every core layer: RMSNorm, q/k/v, RoPE, K/V written to plane c + 1 at pos,
  *   paged attention over positions 0..pos of plane c + 1, output projection and
  *   residual, RMSNorm, SwiGLU MLP and residual;
- *   exit score; exit = (c + 1 == depth); state.h[slot] = h;
+ *   exit score; exit = (c + 1 == depth), exit_next = (c + 2 == depth);
+ *   state.h[slot] = h;
  *   stable compaction into cont / exited;
  *   copy-on-exit (last-exited cache, Section 4.2, Fig. 2): for an exiting row
  *   with depth < r_max, its K/V at pos in plane depth is copied to planes
@@ -194,6 +216,13 @@ cdb_status cdb_boundary_prelude(const cdb_model* model, const cdb_kv* kv, const 
  * The caller advances c of continuing rows. */
 cdb_status cdb_loop_step(const cdb_model* model, const cdb_kv* kv, const cdb_state* state, const cdb_rows* rows,
                          const cdb_step_out* out, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* cdb_loop_step with exits decided on the device by `gate` instead of replayed
+ * depths (rows->depth is not read and may be NULL): everything else as
+ * cdb_loop_step, with copy-on-exit from plane c + 1 of each exiting row. */
+cdb_status cdb_loop_step_gated(const cdb_model* model, const cdb_kv* kv, const cdb_state* state,
+                               const cdb_rows* rows, const cdb_gate* gate, const cdb_step_out* out, void* ws,
+                               size_t ws_bytes, hipStream_t stream);
 
 /* Coda stage (Section 4.1; Eq. 1 p(x_{t+1}) = softmax(C(h))): coda layers with
  * KV plane r_max + 1 on h = state.h[slot], final RMSNorm, LM head.  logits:

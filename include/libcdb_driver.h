@@ -14,6 +14,11 @@
  *   no-refill    a batch is formed once per round and shrinks until all its
  *                tokens exited; coda and prelude then run for the round
  *   fixed_depth  every token runs r_max loops (continuous batching baseline)
+ *   gated        exits decided on the device by a threshold (Section 4.3;
+ *                App. C.2).  With lookahead the device's decision after one
+ *                loop step governs the step after next, so the host plans
+ *                each step from results one step old and never stalls the
+ *                device; without it every loop step waits for its own result.
  * Pages: every plane of a sequence is mapped at admission (lowest free id
  * first, (sequence, page, plane) order) and released when it finishes.
  */
@@ -42,6 +47,9 @@ typedef struct {
     int32_t max_seqs, max_pages;    /* page-table shape [max_seqs][r_max + 2][max_pages] */
     int32_t pre_pages, core_pages, coda_pages;  /* pool sizes */
     int32_t kv_layout;              /* CDB_KV_FULL, CDB_KV_SHARED or CDB_KV_FIRST_THEN_SHARED */
+    int32_t gated;                  /* 1: exits decided on the device by a threshold (cdb_gate) */
+    int32_t lookahead;              /* gated: the decision after loop r ends the token after loop r + 1 */
+    float threshold;                /* gated: the criterion's threshold */
 } cdb_driver_config;
 
 /* Core KV layouts (Section 4.2, App. C.1, Table 1), all by page-table aliasing:
@@ -74,8 +82,8 @@ void cdb_driver_destroy(cdb_driver* d);
 
 /* Adds a request in arrival order: its prompt (already prefilled: its KV must
  * be present when the sequence is admitted) and the exit depth of each of its
- * n_decode decode inputs.  Returns the sequence id (= its row of the page
- * table and its state slot) or -1. */
+ * n_decode decode inputs (NULL in gated mode).  Returns the sequence id (= its
+ * row of the page table and its state slot) or -1. */
 int32_t cdb_driver_add_sequence(cdb_driver* d, int32_t prompt_len, int32_t n_decode, const int32_t* depths,
                                 double arrival);
 
@@ -87,6 +95,14 @@ const int32_t* cdb_driver_page_table(cdb_driver* d);
  * t->wait_until (-1); complete() applies a planned call's effect. */
 int32_t cdb_driver_next(cdb_driver* d, cdb_driver_tick* t);
 int32_t cdb_driver_complete(cdb_driver* d, const cdb_driver_tick* t);
+
+/* Gated mode: the device's exit_mask and exit_next (uint8 per row, in the
+ * tick's row order) of a completed loop tick.  Without lookahead it must be
+ * given before that tick is completed; with lookahead before the next loop
+ * tick is completed.  Returns -1 if the mask disagrees with the exits the
+ * scheduler applied. */
+int32_t cdb_driver_loop_result(cdb_driver* d, const cdb_driver_tick* t, const uint8_t* exit_mask,
+                               const uint8_t* exit_next);
 void cdb_driver_set_time(cdb_driver* d, double now_seconds);
 
 int32_t cdb_driver_get_stats(const cdb_driver* d, cdb_driver_stats* out);
@@ -98,19 +114,24 @@ int32_t cdb_driver_pages_in_use(const cdb_driver* d, int32_t* pre, int32_t* core
  * -1 for unfinished ones.  Returns the number written. */
 int32_t cdb_driver_latencies(const cdb_driver* d, double* normalized, int32_t n);
 
-/* Device scratch cdb_driver_run needs for a model with `vocab` logits. */
-size_t cdb_driver_scratch_bytes(int32_t vocab);
+/* Device scratch cdb_driver_run needs for this driver and a model with
+ * `vocab` logits. */
+size_t cdb_driver_scratch_bytes(const cdb_driver* d, int32_t vocab);
 
 /* Runs every added request to completion on the device: plans each call,
  * stages its rows through pinned host memory, enqueues the stage call on
  * `stream`.  first_tokens (host, per sequence) is each sequence's first decode
  * input; later inputs are the coda's greedy ids, passed on device.  The page
  * table in kv->page_table (device) is overwritten from the driver's.
- * scratch: device, cdb_driver_scratch_bytes(vocab).  tokens_out (device,
+ * state needs a slot per sequence (n_slots >= max_seqs).  scratch: device,
+ * cdb_driver_scratch_bytes(d, vocab).  tokens_out (device,
  * optional): int32 [max_seqs][tokens_stride] receives, at [seq][k], the greedy
  * id the coda produced after decode input k (tokens_stride >= every
- * sequence's n_decode, else CDB_ERR_INVALID_ARG).  Returns a cdb_status;
- * *seconds = wall time including the final synchronisation. */
+ * sequence's n_decode, else CDB_ERR_INVALID_ARG).  Gated mode: the device's
+ * exit decisions are copied back after every loop step and fed to the
+ * scheduler (one step late with lookahead); CDB_ERR_INVALID_ARG if they ever
+ * disagree with the exits applied.  Returns a cdb_status; *seconds = wall
+ * time including the final synchronisation. */
 int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, const cdb_state* state, void* scratch,
                        size_t scratch_bytes, const int32_t* first_tokens, int32_t* tokens_out,
                        int32_t tokens_stride, void* ws, size_t ws_bytes, hipStream_t stream, double* seconds);

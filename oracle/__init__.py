@@ -76,6 +76,8 @@ _I = C.c_int32
 def _declare(L):
     L.orc_ref_sequence.argtypes = [_P, _P, _I, _P, _I, _I, _P, _P, _P, _P, _P]
     L.orc_brute_force.argtypes = [_P, _P, _I, _P, _I, _P, _P, _P, _P]
+    L.orc_ref_sequence_gated.argtypes = [_P, _P, _I, _P, _I, _I, C.c_double, _I, _P, _P, _P, _P]
+    L.orc_gate_decide.argtypes = [_P, _I, _P, _P, C.c_double, _I, _P, _P, _P]
     L.orc_prelude.argtypes = [_P, _P, _P, _P, _P, _I, _I, _P, _P, _P, _P]
     L.orc_loop_step.argtypes = [_P, _P, _P, _P, _P, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]
     L.orc_coda.argtypes = [_P, _P, _P, _P, _I, _I, _P, _P, _P, _P, _P]
@@ -87,7 +89,8 @@ def _declare(L):
     L.orc_silu.restype = C.c_double
     L.orc_to_bf16.argtypes = [C.c_double]
     L.orc_to_bf16.restype = C.c_double
-    for f in ("orc_ref_sequence", "orc_brute_force", "orc_prelude", "orc_loop_step", "orc_coda",
+    for f in ("orc_ref_sequence", "orc_ref_sequence_gated", "orc_gate_decide", "orc_brute_force", "orc_prelude",
+              "orc_loop_step", "orc_coda",
               "orc_exit_compact"):
         getattr(L, f).restype = C.c_int
 
@@ -153,6 +156,41 @@ class Model:
         if rc != ORC_OK:
             raise ValueError(f"orc_ref_sequence: {rc}")
         return {"tokens": tok, "logits": logits, "h": h, "scores": scores, "core_kv": kv}
+
+    def ref_sequence_gated(self, tokens, n_given: int, threshold: float, lookahead: bool,
+                           n_prefill: Optional[int] = None):
+        """Decode tokens take the depth the threshold rule gives on their own
+        scores; the first n_prefill (default n_given) tokens are one prefill
+        block at r_max."""
+        s = self.shape
+        tok = _c(tokens, np.int32).copy()
+        T = len(tok)
+        n_prefill = n_given if n_prefill is None else n_prefill
+        logits = np.zeros((T, s.vocab))
+        h = np.zeros((T, s.d))
+        scores = np.zeros((T, s.r_max))
+        depth = np.zeros(T, np.int32)
+        rc = self.L.orc_ref_sequence_gated(C.byref(self.desc), C.byref(self.w), T, _ptr(tok), n_given, n_prefill,
+                                          float(threshold), 1 if lookahead else 0, _ptr(depth), _ptr(logits),
+                                          _ptr(h), _ptr(scores))
+        if rc != ORC_OK:
+            raise ValueError(f"orc_ref_sequence_gated: {rc}")
+        return {"tokens": tok, "logits": logits, "h": h, "scores": scores, "depth": depth}
+
+    def gate_decide(self, c, score, threshold: float, lookahead: bool, pending):
+        """One loop step's threshold decisions (exit_mask, exit_next); pending
+        (uint8 per row) is updated in place."""
+        c = _c(c, np.int32)
+        sc = _c(score, np.float64)
+        assert pending.dtype == np.uint8 and pending.flags.c_contiguous
+        n = len(c)
+        mask = np.zeros(n, np.uint8)
+        nxt = np.zeros(n, np.uint8)
+        rc = self.L.orc_gate_decide(C.byref(self.desc), n, _ptr(c), _ptr(sc), float(threshold),
+                                    1 if lookahead else 0, _ptr(pending), _ptr(mask), _ptr(nxt))
+        if rc != ORC_OK:
+            raise ValueError(f"orc_gate_decide: {rc}")
+        return mask, nxt
 
     def brute_force(self, tokens, depth, n_prefill: Optional[int] = None):
         """n_prefill: leading tokens run as one prefill block (default all)."""

@@ -344,13 +344,31 @@ static void run_layer(const orc_desc* m, const orc_weights* w, int layer, double
  * own.  Under the full layout the blocking changes nothing; under the shared
  * layouts it decides which state of an earlier token is the most recent one
  * when it is read (within a block: the loop being run). */
-int orc_ref_sequence(const orc_desc* m, const orc_weights* w, int32_t T, int32_t* tokens, int32_t n_given,
-                     int32_t n_prefill, const int32_t* depth, double* logits_out, double* h_out, double* scores_out,
-                     double* core_kv_out) {
+/* Threshold exit rule (Section 4.3; App. C.2): whether the score after loop r
+ * meets the model's criterion -- gate score >= threshold, or for the
+ * convergence criterion a distance below threshold from loop 2 on (the distance
+ * after loop 1 compares the recurrent state with the prelude output). */
+static int gate_meets(const orc_desc* m, int r, double score, double threshold) {
+    if (m->exit_kind == 1) return r >= 2 && score < threshold;
+    return score >= threshold;
+}
+
+/* depth: the exit depth of every token, or NULL for threshold exits (gate) of
+ * the decode tokens t >= n_prefill; prefill tokens then run r_max loops. */
+typedef struct {
+    double threshold;
+    int lookahead;
+    int32_t* depth_out;
+} gate_args;
+
+static int ref_sequence(const orc_desc* m, const orc_weights* w, int32_t T, int32_t* tokens, int32_t n_given,
+                        int32_t n_prefill, const int32_t* depth, const gate_args* gate, double* logits_out,
+                        double* h_out, double* scores_out, double* core_kv_out) {
     int d = m->d, R = m->r_max;
     if (n_prefill < 0 || n_prefill > n_given || n_prefill > T) return ORC_ERR_ARG;
-    for (int t = 0; t < T; ++t)
-        if (depth[t] < 1 || depth[t] > R) return ORC_ERR_ARG;
+    if (depth)
+        for (int t = 0; t < T; ++t)
+            if (depth[t] < 1 || depth[t] > R) return ORC_ERR_ARG;
     dense_kv kv;
     dense_alloc(&kv, m, T);
     const int maxb = n_prefill > 1 ? n_prefill : 1;
@@ -360,6 +378,8 @@ int orc_ref_sequence(const orc_desc* m, const orc_weights* w, int32_t T, int32_t
     double* logits = (double*)malloc(sizeof(double) * (size_t)m->vocab);
     const double** kr = (const double**)malloc(sizeof(double*) * (size_t)T);
     const double** vr = (const double**)malloc(sizeof(double*) * (size_t)T);
+    int32_t* dep = (int32_t*)malloc(sizeof(int32_t) * (size_t)(T > 0 ? T : 1)); /* exit depth, 0 while running */
+    int* pending = (int*)calloc((size_t)(T > 0 ? T : 1), sizeof(int));       /* lookahead: exits after next loop */
 
     for (int b0 = 0; b0 < T;) {
         const int b1 = b0 < n_prefill ? n_prefill : b0 + 1; /* block [b0, b1) */
@@ -375,10 +395,11 @@ int orc_ref_sequence(const orc_desc* m, const orc_weights* w, int32_t T, int32_t
             }
             memcpy(eb + (size_t)(t - b0) * d, h, sizeof(double) * (size_t)d);
         }
+        for (int t = b0; t < b1; ++t) dep[t] = 0;
         for (int r = 1; r <= R; ++r) {
             const int slot = write_slot(m->kv_layout, r);
             for (int t = b0; t < b1; ++t) {
-                if (depth[t] < r) continue;
+                if (dep[t]) continue; /* exited */
                 double* h = hb + (size_t)(t - b0) * d;
                 memcpy(hp, h, sizeof(double) * (size_t)d);
                 core_input(m, w, hp, eb + (size_t)(t - b0) * d, h);
@@ -390,13 +411,27 @@ int orc_ref_sequence(const orc_desc* m, const orc_weights* w, int32_t T, int32_t
                     run_layer(m, w, m->n_prelude + l, h, t, dk_core(&kv, t, slot, l, 0),
                               dk_core(&kv, t, slot, l, 1), kr, vr);
                 }
-                if (scores_out) scores_out[(size_t)t * R + (r - 1)] = exit_score(m, w, h, hp);
+                const double sc = exit_score(m, w, h, hp);
+                if (scores_out) scores_out[(size_t)t * R + (r - 1)] = sc;
+                /* is loop r the token's last? */
+                int last;
+                if (depth) {
+                    last = r == depth[t];
+                } else if (t < n_prefill) {
+                    last = r == R;
+                } else if (gate->lookahead) {
+                    last = r == R || pending[t];
+                    pending[t] = !last && gate_meets(m, r, sc, gate->threshold);
+                } else {
+                    last = r == R || gate_meets(m, r, sc, gate->threshold);
+                }
+                if (last) dep[t] = r;
             }
             /* last-exited cache: a token that exits after loop r gets the slots
              * of loops r+1..R filled with a copy of the slot of loop r (nothing
              * to do where they are the same slot) */
             for (int t = b0; t < b1; ++t) {
-                if (depth[t] != r) continue;
+                if (dep[t] != r) continue;
                 for (int r2 = r + 1; r2 <= R; ++r2) {
                     const int dst = write_slot(m->kv_layout, r2);
                     if (dst == slot) continue;
@@ -410,7 +445,8 @@ int orc_ref_sequence(const orc_desc* m, const orc_weights* w, int32_t T, int32_t
         for (int t = b0; t < b1; ++t) {
             double* h = hb + (size_t)(t - b0) * d;
             if (scores_out)
-                for (int r = depth[t] + 1; r <= R; ++r) scores_out[(size_t)t * R + (r - 1)] = NAN;
+                for (int r = dep[t] + 1; r <= R; ++r) scores_out[(size_t)t * R + (r - 1)] = NAN;
+            if (gate && gate->depth_out) gate->depth_out[t] = dep[t];
             if (h_out) memcpy(h_out + (size_t)t * d, h, sizeof(double) * (size_t)d);
             for (int l = 0; l < m->n_coda; ++l) {
                 for (int s = 0; s < t; ++s) {
@@ -434,8 +470,52 @@ int orc_ref_sequence(const orc_desc* m, const orc_weights* w, int32_t T, int32_t
     free(eb);
     free(hp);
     free(logits);
+    free(dep);
+    free(pending);
     dense_free(&kv);
     return ORC_OK;
+}
+
+int orc_ref_sequence(const orc_desc* m, const orc_weights* w, int32_t T, int32_t* tokens, int32_t n_given,
+                     int32_t n_prefill, const int32_t* depth, double* logits_out, double* h_out, double* scores_out,
+                     double* core_kv_out) {
+    if (!depth) return ORC_ERR_ARG;
+    return ref_sequence(m, w, T, tokens, n_given, n_prefill, depth, NULL, logits_out, h_out, scores_out,
+                        core_kv_out);
+}
+
+/* One loop step's threshold decisions for n rows at loop index c[i] with exit
+ * score score[i] (the state after loop c[i] + 1): exit_mask[i] = this loop is
+ * the token's last; exit_next[i] = a continuing token's next loop will be its
+ * last.  pending[i] (in/out) carries the lookahead decision of the row's token
+ * between steps. */
+int orc_gate_decide(const orc_desc* m, int32_t n, const int32_t* c, const double* score, double threshold,
+                    int32_t lookahead, uint8_t* pending, uint8_t* exit_mask, uint8_t* exit_next) {
+    const int R = m->r_max;
+    for (int i = 0; i < n; ++i) {
+        if (c[i] < 0 || c[i] >= R) return ORC_ERR_ARG;
+        const int r = c[i] + 1;
+        const int meets = gate_meets(m, r, score[i], threshold);
+        int last, next;
+        if (lookahead) {
+            last = r == R || pending[i];
+            next = !last && (meets || r + 1 == R);
+            pending[i] = (uint8_t)next;
+        } else {
+            last = r == R || meets;
+            next = !last && r + 1 == R;
+        }
+        exit_mask[i] = (uint8_t)last;
+        exit_next[i] = (uint8_t)next;
+    }
+    return ORC_OK;
+}
+
+int orc_ref_sequence_gated(const orc_desc* m, const orc_weights* w, int32_t T, int32_t* tokens, int32_t n_given,
+                           int32_t n_prefill, double threshold, int32_t lookahead, int32_t* depth_out,
+                           double* logits_out, double* h_out, double* scores_out) {
+    gate_args g = {threshold, lookahead != 0, depth_out};
+    return ref_sequence(m, w, T, tokens, n_given, n_prefill, NULL, &g, logits_out, h_out, scores_out, NULL);
 }
 
 /* No cache: for every position t the whole prefix 0..t is recomputed from the

@@ -47,6 +47,15 @@ typedef struct {
 int orc_ref_sequence(const orc_desc* m, const orc_weights* w, int32_t T, int32_t* tokens, int32_t n_given,
                      int32_t n_prefill, const int32_t* depth, double* logits_out, double* h_out, double* scores_out,
                      double* core_kv_out);
+/* As orc_ref_sequence, with each decode token's depth decided by the
+ * threshold rule on its own exit scores (lookahead: the decision after loop r
+ * ends the token after loop r + 1); prefill tokens run r_max loops.
+ * depth_out [T] receives every token's depth. */
+int orc_ref_sequence_gated(const orc_desc* m, const orc_weights* w, int32_t T, int32_t* tokens, int32_t n_given,
+                           int32_t n_prefill, double threshold, int32_t lookahead, int32_t* depth_out,
+                           double* logits_out, double* h_out, double* scores_out);
+int orc_gate_decide(const orc_desc* m, int32_t n, const int32_t* c, const double* score, double threshold,
+                    int32_t lookahead, uint8_t* pending, uint8_t* exit_mask, uint8_t* exit_next);
 int orc_brute_force(const orc_desc* m, const orc_weights* w, int32_t T, const int32_t* tokens, int32_t n_prefill,
                     const int32_t* depth, double* logits_out, double* h_out, double* scores_out);
 int orc_prelude(const orc_desc* m, const orc_weights* w, const orc_paged* p, double* state_h, double* state_e,

@@ -20,7 +20,7 @@ PAGE_TOKENS = 16
 MAX_ROWS = 256
 
 EXPORTED = ("cdb_packed_weight_bytes", "cdb_pack_weights", "cdb_kv_page_bytes", "cdb_workspace_bytes",
-            "cdb_workspace_init", "cdb_boundary_prelude", "cdb_loop_step", "cdb_boundary_coda",
+            "cdb_workspace_init", "cdb_boundary_prelude", "cdb_loop_step", "cdb_loop_step_gated", "cdb_boundary_coda",
             "cdb_paged_attention", "cdb_read_device_error", "cdb_status_str")
 
 
@@ -62,7 +62,11 @@ class cdb_rows(C.Structure):
 
 class cdb_step_out(C.Structure):
     _fields_ = [("exit_score", C.c_void_p), ("exit_mask", C.c_void_p), ("cont", C.c_void_p),
-                ("exited", C.c_void_p), ("counts", C.c_void_p)]
+                ("exited", C.c_void_p), ("counts", C.c_void_p), ("exit_next", C.c_void_p)]
+
+
+class cdb_gate(C.Structure):
+    _fields_ = [("threshold", C.c_float), ("lookahead", C.c_int32), ("pending", C.c_void_p)]
 
 
 _lib = None
@@ -86,12 +90,13 @@ def lib() -> C.CDLL:
         L.cdb_workspace_init.argtypes = [P, S, P]
         L.cdb_boundary_prelude.argtypes = [P, P, P, P, P, P, S, P]
         L.cdb_loop_step.argtypes = [P, P, P, P, P, P, S, P]
+        L.cdb_loop_step_gated.argtypes = [P, P, P, P, P, P, P, S, P]
         L.cdb_boundary_coda.argtypes = [P, P, P, P, P, P, P, S, P]
         L.cdb_paged_attention.argtypes = [P, P, P, I, I, P, P, P, P, S, P]
         L.cdb_read_device_error.argtypes = [P, P, P]
         L.cdb_status_str.argtypes = [C.c_int]
         L.cdb_status_str.restype = C.c_char_p
-        for f in ("cdb_pack_weights", "cdb_workspace_init", "cdb_boundary_prelude", "cdb_loop_step",
+        for f in ("cdb_pack_weights", "cdb_workspace_init", "cdb_boundary_prelude", "cdb_loop_step", "cdb_loop_step_gated",
                   "cdb_boundary_coda", "cdb_paged_attention", "cdb_read_device_error"):
             getattr(L, f).restype = C.c_int
         _lib = L
@@ -157,6 +162,13 @@ def cdb_loop_step(model: cdb_model, kv: cdb_kv, state: cdb_state, rows: cdb_rows
                   stream=None):
     _check("cdb_loop_step", lib().cdb_loop_step(C.byref(model), C.byref(kv), C.byref(state), C.byref(rows),
                                                 C.byref(out), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def cdb_loop_step_gated(model: cdb_model, kv: cdb_kv, state: cdb_state, rows: cdb_rows, gate: cdb_gate,
+                        out: cdb_step_out, ws, stream=None):
+    _check("cdb_loop_step_gated", lib().cdb_loop_step_gated(C.byref(model), C.byref(kv), C.byref(state),
+                                                            C.byref(rows), C.byref(gate), C.byref(out), _ptr(ws),
+                                                            ws.numel(), _stream(stream)))
 
 
 def cdb_boundary_coda(model: cdb_model, kv: cdb_kv, state: cdb_state, rows: cdb_rows, logits, next_ids, ws,
@@ -297,5 +309,15 @@ class StepOut:
         self.cont = torch.zeros(m, dtype=torch.int32, device=device)
         self.exited = torch.zeros(m, dtype=torch.int32, device=device)
         self.counts = torch.zeros(2, dtype=torch.int32, device=device)
+        self.exit_next = torch.zeros(m, dtype=torch.uint8, device=device)
         self.c = cdb_step_out(self.score.data_ptr(), self.mask.data_ptr(), self.cont.data_ptr(),
-                              self.exited.data_ptr(), self.counts.data_ptr())
+                              self.exited.data_ptr(), self.counts.data_ptr(), self.exit_next.data_ptr())
+
+
+class Gate:
+    """Threshold exits (cdb_gate) with the per-slot lookahead flags on the device."""
+
+    def __init__(self, threshold: float, lookahead: bool, n_slots: int, device="cuda"):
+        import torch
+        self.pending = torch.zeros(max(n_slots, 1), dtype=torch.uint8, device=device)
+        self.c = cdb_gate(threshold, 1 if lookahead else 0, self.pending.data_ptr())

@@ -86,6 +86,8 @@ WsLayout ws_layout(const cdb_model_desc& d, int rows) {
     off = align256(off + M * 4);
     L.kvpid = off;
     off = align256(off + M * 4);
+    L.deff = off;
+    off = align256(off + M * 4);
     L.total = off;
     return L;
 }
@@ -108,6 +110,7 @@ struct Ctx {
     float2* rope;
     int32_t* order;
     int32_t* kvpid;
+    int32_t* deff;
 };
 
 static Ctx make_ctx(const cdb_model* model, void* ws, int rows) {
@@ -128,6 +131,7 @@ static Ctx make_ctx(const cdb_model* model, void* ws, int rows) {
     c.rope = reinterpret_cast<float2*>(c.ws + c.L.rope);
     c.order = reinterpret_cast<int32_t*>(c.ws + c.L.order);
     c.kvpid = reinterpret_cast<int32_t*>(c.ws + c.L.kvpid);
+    c.deff = reinterpret_cast<int32_t*>(c.ws + c.L.deff);
     return c;
 }
 
@@ -299,22 +303,25 @@ cdb_status cdb_boundary_prelude(const cdb_model* model, const cdb_kv* kv, const 
     return CDB_OK;
 }
 
-cdb_status cdb_loop_step(const cdb_model* model, const cdb_kv* kv, const cdb_state* state, const cdb_rows* rows,
-                         const cdb_step_out* out, void* ws, size_t ws_bytes, hipStream_t st) {
+static cdb_status loop_step(const cdb_model* model, const cdb_kv* kv, const cdb_state* state, const cdb_rows* rows,
+                            const cdb_gate* gate, const cdb_step_out* out, void* ws, size_t ws_bytes, hipStream_t st) {
     cdb_status s = check_common(model, kv, state, rows, ws, ws_bytes, 1);
     if (s != CDB_OK) return s;
     const cdb_model_desc& d = model->desc;
     if (!out || !out->exit_score || !out->exit_mask || !out->cont || !out->exited || !out->counts)
         return CDB_ERR_INVALID_ARG;
-    if (rows->n_rows > 0 && (!rows->c || !rows->depth)) return CDB_ERR_INVALID_ARG;
+    if (rows->n_rows > 0 && (!rows->c || (!gate && !rows->depth))) return CDB_ERR_INVALID_ARG;
+    if (gate && gate->lookahead && !gate->pending) return CDB_ERR_INVALID_ARG;
     if (d.injection && !state->e) return CDB_ERR_INVALID_ARG;
     const int M = rows->n_rows;
     Ctx c = make_ctx(model, ws, M);
+    cdb_rows r = *rows;
+    if (gate) r.depth = nullptr;
     if (M > 0) {
         KvTarget t = stage_target(d, *kv, 1);
-        t.c_row = rows->c;
-        HIPCHK(launch_gather(d, *state, *rows, *kv, t, c.h, c.h_in, d.injection ? c.x : nullptr, c.rope, c.kvpid,
-                             c.err, st));
+        t.c_row = r.c;
+        HIPCHK(launch_gather(d, *state, r, *kv, t, c.h, c.h_in, d.injection ? c.x : nullptr, c.rope, c.kvpid, c.err,
+                             st));
         if (d.injection) {
             EpiArgs ea{};
             ea.out = c.h;
@@ -322,13 +329,25 @@ cdb_status cdb_loop_step(const cdb_model* model, const cdb_kv* kv, const cdb_sta
             ea.err = c.err;
             HIPCHK(launch_gemm(EPI_STORE, c.x, wptr(c, c.wl.adapter), M, c.gm.adapter, c.part, ea, st));
         }
-        s = run_layers(c, d.n_prelude, d.n_core, t, *rows, false, st);
+        s = run_layers(c, d.n_prelude, d.n_core, t, r, false, st);
         if (s != CDB_OK) return s;
-        HIPCHK(launch_exit(d, *rows, c.h, c.h_in, wptr(c, c.wl.w_exit), state->h, state->n_slots, *out, st));
+        HIPCHK(launch_exit(d, r, c.h, c.h_in, wptr(c, c.wl.w_exit), state->h, state->n_slots, *out, gate, c.deff, st));
     }
     HIPCHK(launch_compact(M, out->exit_mask, out->cont, out->exited, out->counts, st));
-    if (M > 0) HIPCHK(launch_copy_on_exit(d, *kv, *rows, out->exited, out->counts, c.err, st));
+    if (M > 0) HIPCHK(launch_copy_on_exit(d, *kv, r, c.deff, out->exited, out->counts, c.err, st));
     return CDB_OK;
+}
+
+cdb_status cdb_loop_step(const cdb_model* model, const cdb_kv* kv, const cdb_state* state, const cdb_rows* rows,
+                         const cdb_step_out* out, void* ws, size_t ws_bytes, hipStream_t st) {
+    return loop_step(model, kv, state, rows, nullptr, out, ws, ws_bytes, st);
+}
+
+cdb_status cdb_loop_step_gated(const cdb_model* model, const cdb_kv* kv, const cdb_state* state,
+                               const cdb_rows* rows, const cdb_gate* gate, const cdb_step_out* out, void* ws,
+                               size_t ws_bytes, hipStream_t st) {
+    if (!gate) return CDB_ERR_INVALID_ARG;
+    return loop_step(model, kv, state, rows, gate, out, ws, ws_bytes, st);
 }
 
 cdb_status cdb_boundary_coda(const cdb_model* model, const cdb_kv* kv, const cdb_state* state, const cdb_rows* rows,

@@ -96,7 +96,7 @@ struct WeightLayout {
 bool weight_layout(const cdb_model_desc& d, WeightLayout* out);
 
 struct WsLayout {
-    size_t err, h, h_in, q, x, act, part, rope, order, kvpid, total;
+    size_t err, h, h_in, q, x, act, part, rope, order, kvpid, deff, total;
 };
 WsLayout ws_layout(const cdb_model_desc& d, int rows);
 
@@ -129,11 +129,13 @@ hipError_t launch_store_state(int M, int d, int n_slots, const int32_t* slot, co
 hipError_t launch_load_state(const cdb_model_desc& md, int M, const int32_t* slot, const int32_t* seq,
                              const int32_t* pos, const KvTarget& kt, const float* state_h, int n_slots, float* h,
                              float2* rope, int32_t* kvpid, int* err, hipStream_t st);
+// gate: NULL replays rows.depth; deff[M] receives each exiting row's depth.
 hipError_t launch_exit(const cdb_model_desc& md, const cdb_rows& r, const float* h, const float* h_in,
-                       const uint16_t* w_exit, float* state_h, int n_slots, const cdb_step_out& o, hipStream_t st);
+                       const uint16_t* w_exit, float* state_h, int n_slots, const cdb_step_out& o,
+                       const cdb_gate* gate, int32_t* deff, hipStream_t st);
 hipError_t launch_compact(int M, const uint8_t* mask, int32_t* cont, int32_t* exited, int32_t* counts,
                           hipStream_t st);
-hipError_t launch_copy_on_exit(const cdb_model_desc& md, const cdb_kv& kv, const cdb_rows& r,
+hipError_t launch_copy_on_exit(const cdb_model_desc& md, const cdb_kv& kv, const cdb_rows& r, const int32_t* deff,
                                const int32_t* exited, const int32_t* counts, int* err, hipStream_t st);
 hipError_t launch_argmax(int M, int V, const float* logits, int32_t* ids, hipStream_t st);
 hipError_t launch_scatter_ids(int M, const int32_t* ids, const int32_t* seq, const int32_t* index, int max_seqs,

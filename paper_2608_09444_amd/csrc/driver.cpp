@@ -17,7 +17,9 @@
 //    exited (Section 4.1, Fig. 1 right).  Fixed-depth mode runs every token for
 //    r_max loops (continuous batching, the baseline the paper compares with).
 //  * Exit decisions are replayed from each sequence's depth table
-//    (App. B.2), so the host knows every exit without reading the device.
+//    (App. B.2), so the host knows every exit without reading the device; in
+//    gated mode they come from the device (cdb_driver_loop_result), one loop
+//    step late with the lookahead gate (Section 4.3).
 //
 // Running (cdb_driver_run): each tick's rows go through pinned host buffers and
 // one asynchronous copy to the device, then the stage call; the coda batch
@@ -54,6 +56,7 @@ struct Seq {
     int32_t c = 0;  // loops completed by that token
     int32_t pages = 0;
     double admit_time = -1.0, done_time = -1.0;
+    bool exit_now = false;  // gated: the current loop is the token's last (known before the step completes)
 };
 
 struct Allocator {
@@ -89,13 +92,23 @@ struct cdb_driver {
     cdb_driver_stats stats;
     double now = 0.0;  // seconds, advanced by the runner (or by tests)
     bool table_dirty = true;
+    std::vector<uint8_t> last_plan;  // gated: exits applied to the last completed loop tick, in row order
+    bool result_pending = false;     // gated lookahead: the last completed loop tick's result is still due
 };
 
 static int32_t planes(const cdb_driver* d) { return d->cfg.r_max + 2; }
 
 static int32_t depth_of(const cdb_driver* d, const Seq& s) {
     if (d->cfg.fixed_depth) return d->cfg.r_max;
+    if (d->cfg.gated) return 0;  // decided on the device
     return s.depth[s.t];
+}
+
+// Whether the token's current loop (index s.c) is its last.
+static bool exits_now(const cdb_driver* d, const Seq& s) {
+    if (s.c + 1 >= d->cfg.r_max) return true;
+    if (d->cfg.gated) return s.exit_now;
+    return s.c + 1 == depth_of(d, s);
 }
 
 // Distinct core pages per token page under the layout.
@@ -191,7 +204,7 @@ extern "C" {
 cdb_driver* cdb_driver_create(const cdb_driver_config* cfg) {
     if (!cfg || cfg->max_batch < 1 || cfg->max_batch > 256 || cfg->r_max < 1 || cfg->max_seqs < 1 ||
         cfg->max_pages < 1 || cfg->max_active < 1 || cfg->min_coda_batch < 1 || cfg->kv_layout < 0 ||
-        cfg->kv_layout > 2)
+        cfg->kv_layout > 2 || (cfg->gated && cfg->fixed_depth))
         return nullptr;
     cdb_driver* d = new cdb_driver();
     d->cfg = *cfg;
@@ -207,15 +220,16 @@ void cdb_driver_destroy(cdb_driver* d) { delete d; }
 
 int32_t cdb_driver_add_sequence(cdb_driver* d, int32_t prompt_len, int32_t n_decode, const int32_t* depths,
                                 double arrival) {
-    if (!d || prompt_len < 1 || n_decode < 1 || !depths) return -1;
+    if (!d || prompt_len < 1 || n_decode < 1 || (!depths && !d->cfg.gated)) return -1;
     if ((int32_t)d->seqs.size() >= d->cfg.max_seqs) return -1;
     if (!d->seqs.empty() && arrival < d->seqs.back().arrival) return -1;  // arrival order
-    for (int32_t i = 0; i < n_decode; ++i)
-        if (depths[i] < 1 || depths[i] > d->cfg.r_max) return -1;
+    if (depths)
+        for (int32_t i = 0; i < n_decode; ++i)
+            if (depths[i] < 1 || depths[i] > d->cfg.r_max) return -1;
     Seq s;
     s.prompt_len = prompt_len;
     s.n_decode = n_decode;
-    s.depth.assign(depths, depths + n_decode);
+    if (depths) s.depth.assign(depths, depths + n_decode);
     s.arrival = arrival;
     d->seqs.push_back(std::move(s));
     return (int32_t)d->seqs.size() - 1;
@@ -308,6 +322,7 @@ int32_t cdb_driver_complete(cdb_driver* d, const cdb_driver_tick* t) {
             if (s.t + 1 < s.n_decode) {
                 s.t++;
                 s.c = 0;
+                s.exit_now = false;
                 s.state = LOOP;
                 cont.push_back(q);
             } else {
@@ -333,24 +348,49 @@ int32_t cdb_driver_complete(cdb_driver* d, const cdb_driver_tick* t) {
         d->stats.prelude_calls++;
         d->stats.prelude_rows += t->n_rows;
     } else if (t->stage == CDB_TICK_LOOP) {
+        if (d->cfg.gated && d->cfg.lookahead && d->result_pending) return -1;  // previous loop's result not given
         std::vector<int32_t> keep;
+        d->last_plan.assign(t->n_rows, 0);
         for (int32_t i = 0; i < t->n_rows; ++i) {
             const int32_t q = t->seq[i];
             Seq& s = d->seqs[q];
-            if (s.c + 1 == depth_of(d, s)) {
+            if (exits_now(d, s)) {
                 s.state = EXITED;
                 d->exited.push_back(q);
+                d->last_plan[i] = 1;
             } else {
                 s.c++;
+                s.exit_now = false;
                 keep.push_back(q);
             }
         }
+        d->result_pending = d->cfg.gated && d->cfg.lookahead;
         d->batch = keep;
         d->stats.loop_steps++;
         d->stats.loop_rows += t->n_rows;
         d->stats.idle_rows += d->cfg.max_batch - t->n_rows;
     }
     return 0;
+}
+
+int32_t cdb_driver_loop_result(cdb_driver* d, const cdb_driver_tick* t, const uint8_t* exit_mask,
+                               const uint8_t* exit_next) {
+    if (!d || !t || !exit_mask || t->stage != CDB_TICK_LOOP || !d->cfg.gated) return -1;
+    if (!d->cfg.lookahead) {
+        // before completion: the step's own decisions end the tokens
+        for (int32_t i = 0; i < t->n_rows; ++i) d->seqs[t->seq[i]].exit_now = exit_mask[i] != 0;
+        return 0;
+    }
+    // after completion: check the exits applied, carry the next decisions
+    if (!d->result_pending || (int32_t)d->last_plan.size() != t->n_rows) return -1;
+    d->result_pending = false;
+    int32_t status = 0;
+    for (int32_t i = 0; i < t->n_rows; ++i) {
+        if ((exit_mask[i] != 0) != (d->last_plan[i] != 0)) status = -1;
+        Seq& s = d->seqs[t->seq[i]];
+        if (!d->last_plan[i] && exit_next) s.exit_now = exit_next[i] != 0;
+    }
+    return status;
 }
 
 int32_t cdb_driver_pages_in_use(const cdb_driver* d, int32_t* pre, int32_t* core, int32_t* coda) {
@@ -380,24 +420,32 @@ int32_t cdb_driver_latencies(const cdb_driver* d, double* normalized, int32_t n)
 // ------------------------------------------------------------------ runner
 
 // Device scratch: two row sets (6 x 256 int32 each), next ids (256), loop-step
-// outputs, logits (256 x vocab fp32).
-static size_t scratch_layout(int32_t vocab, size_t* rows, size_t* ids, size_t* step, size_t* logits) {
+// outputs (scores, mask, cont, exited, counts, exit_next), the gate's pending
+// flags (max_seqs), logits (256 x vocab fp32).
+struct ScratchLayout {
+    size_t rows, ids, step, pending, logits, total;
+};
+
+static ScratchLayout scratch_layout(int32_t max_seqs, int32_t vocab) {
+    ScratchLayout L;
     size_t off = 0;
-    *rows = off;
+    L.rows = off;
     off += 2 * 6 * 256 * 4;
-    *ids = off;
+    L.ids = off;
     off += 256 * 4;
-    *step = off;
-    off += 256 * 4 + 256 + 256 * 4 * 2 + 2 * 4;
+    L.step = off;
+    off += 256 * 4 + 256 + 256 * 4 * 2 + 2 * 4 + 256;
     off = (off + 255) & ~(size_t)255;
-    *logits = off;
+    L.pending = off;
+    off += ((size_t)max_seqs + 255) & ~(size_t)255;
+    L.logits = off;
     off += (size_t)256 * vocab * 4;
-    return off;
+    L.total = off;
+    return L;
 }
 
-size_t cdb_driver_scratch_bytes(int32_t vocab) {
-    size_t a, b, c, e;
-    return vocab > 0 ? scratch_layout(vocab, &a, &b, &c, &e) : 0;
+size_t cdb_driver_scratch_bytes(const cdb_driver* d, int32_t vocab) {
+    return d && vocab > 0 ? scratch_layout(d->cfg.max_seqs, vocab).total : 0;
 }
 
 int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, const cdb_state* state, void* scratch,
@@ -409,39 +457,56 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
         for (const Seq& s : d->seqs)
             if (s.n_decode > tokens_stride) return CDB_ERR_INVALID_ARG;
     }
-    size_t o_rows, o_ids, o_step, o_logits;
-    if (scratch_bytes < scratch_layout(model->desc.vocab, &o_rows, &o_ids, &o_step, &o_logits)) return CDB_ERR_CAPACITY;
+    const ScratchLayout SL = scratch_layout(d->cfg.max_seqs, model->desc.vocab);
+    if (scratch_bytes < SL.total) return CDB_ERR_CAPACITY;
     if (kv->max_seqs != d->cfg.max_seqs || kv->max_pages != d->cfg.max_pages) return CDB_ERR_INVALID_ARG;
+    if (state->n_slots < d->cfg.max_seqs) return CDB_ERR_INVALID_ARG;
     unsigned char* base = static_cast<unsigned char*>(scratch);
-    int32_t* drows = reinterpret_cast<int32_t*>(base + o_rows);      // main rows
-    int32_t* drows2 = drows + 6 * 256;                               // prelude rows after a coda
-    int32_t* dids = reinterpret_cast<int32_t*>(base + o_ids);
-    float* dlogits = reinterpret_cast<float*>(base + o_logits);
+    int32_t* drows = reinterpret_cast<int32_t*>(base + SL.rows);  // main rows
+    int32_t* drows2 = drows + 6 * 256;                            // prelude rows after a coda
+    int32_t* dids = reinterpret_cast<int32_t*>(base + SL.ids);
+    float* dlogits = reinterpret_cast<float*>(base + SL.logits);
     cdb_step_out out;
-    out.exit_score = reinterpret_cast<float*>(base + o_step);
-    out.exit_mask = reinterpret_cast<uint8_t*>(base + o_step + 256 * 4);
-    out.cont = reinterpret_cast<int32_t*>(base + o_step + 256 * 4 + 256);
+    out.exit_score = reinterpret_cast<float*>(base + SL.step);
+    out.exit_mask = reinterpret_cast<uint8_t*>(base + SL.step + 256 * 4);
+    out.cont = reinterpret_cast<int32_t*>(base + SL.step + 256 * 4 + 256);
     out.exited = out.cont + 256;
     out.counts = out.exited + 256;
+    out.exit_next = reinterpret_cast<uint8_t*>(out.counts + 2);
+    cdb_gate gate;
+    gate.threshold = d->cfg.threshold;
+    gate.lookahead = d->cfg.lookahead;
+    gate.pending = base + SL.pending;
+    const bool gated = d->cfg.gated != 0;
+    if (gated && hipMemsetAsync(gate.pending, 0, d->cfg.max_seqs, stream) != hipSuccess) return CDB_ERR_HIP;
 
     // pinned host staging: a ring of row buffers, each reused only after the
     // copy that last read it has completed (device buffers are reused in
-    // stream order)
+    // stream order); a second ring receives the gated steps' decisions
     const int RING = 8;
     const size_t slot_ints = 6 * 256;
     int32_t* pinned = nullptr;
     int32_t* pinned_pt = nullptr;
+    uint8_t* pinned_rb = nullptr;
     const size_t pt_bytes = d->page_table.size() * 4;
     if (hipHostMalloc(reinterpret_cast<void**>(&pinned), RING * slot_ints * 4) != hipSuccess) return CDB_ERR_HIP;
     if (hipHostMalloc(reinterpret_cast<void**>(&pinned_pt), pt_bytes) != hipSuccess) {
         hipHostFree(pinned);
         return CDB_ERR_HIP;
     }
-    hipEvent_t ev[RING], pt_ev;
-    for (int i = 0; i < RING; ++i) hipEventCreateWithFlags(&ev[i], hipEventDisableTiming);
+    if (hipHostMalloc(reinterpret_cast<void**>(&pinned_rb), RING * 512) != hipSuccess) {
+        hipHostFree(pinned);
+        hipHostFree(pinned_pt);
+        return CDB_ERR_HIP;
+    }
+    hipEvent_t ev[RING], rb_ev[RING], pt_ev;
+    for (int i = 0; i < RING; ++i) {
+        hipEventCreateWithFlags(&ev[i], hipEventDisableTiming);
+        hipEventCreateWithFlags(&rb_ev[i], hipEventDisableTiming);
+    }
     hipEventCreateWithFlags(&pt_ev, hipEventDisableTiming);
     bool pt_used = false;
-    int ring = 0;
+    int ring = 0, rb_ring = 0;
     auto stage = [&](const int32_t* slot, const int32_t* seq, const int32_t* pos, const int32_t* c,
                      const int32_t* dep, const int32_t* tok, int32_t n, int32_t* dst) -> hipError_t {
         hipEventSynchronize(ev[ring]);
@@ -457,6 +522,9 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
         ring = (ring + 1) % RING;
         return e;
     };
+    // gated: the previous loop tick and the ring slot of its decisions
+    cdb_driver_tick prev;
+    int prev_rb = -1;
 
     cdb_driver_tick t;
     int32_t status = CDB_OK;
@@ -492,7 +560,39 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
         if (t.stage == CDB_TICK_PRELUDE_FIRST) {
             s = cdb_boundary_prelude(model, kv, state, &rows, drows + 1280, ws, ws_bytes, stream);
         } else if (t.stage == CDB_TICK_LOOP) {
-            s = cdb_loop_step(model, kv, state, &rows, &out, ws, ws_bytes, stream);
+            if (!gated) {
+                s = cdb_loop_step(model, kv, state, &rows, &out, ws, ws_bytes, stream);
+            } else {
+                rows.depth = nullptr;
+                s = cdb_loop_step_gated(model, kv, state, &rows, &gate, &out, ws, ws_bytes, stream);
+                if (s == CDB_OK) {
+                    // this step's decisions to the host
+                    const int rs = rb_ring;
+                    rb_ring = (rb_ring + 1) % RING;
+                    hipEventSynchronize(rb_ev[rs]);
+                    uint8_t* hb = pinned_rb + rs * 512;
+                    if (hipMemcpyAsync(hb, out.exit_mask, n, hipMemcpyDeviceToHost, stream) != hipSuccess ||
+                        hipMemcpyAsync(hb + 256, out.exit_next, n, hipMemcpyDeviceToHost, stream) != hipSuccess) {
+                        status = CDB_ERR_HIP;
+                        break;
+                    }
+                    hipEventRecord(rb_ev[rs], stream);
+                    if (!d->cfg.lookahead) {
+                        // the step's own exits are needed before it completes
+                        hipEventSynchronize(rb_ev[rs]);
+                        cdb_driver_loop_result(d, &t, hb, hb + 256);
+                    } else {
+                        // lookahead: the previous step's decisions complete this one
+                        if (prev_rb >= 0) {
+                            hipEventSynchronize(rb_ev[prev_rb]);
+                            const uint8_t* pb = pinned_rb + prev_rb * 512;
+                            if (cdb_driver_loop_result(d, &prev, pb, pb + 256) != 0) s = CDB_ERR_INVALID_ARG;
+                        }
+                        prev = t;
+                        prev_rb = rs;
+                    }
+                }
+            }
         } else if (t.stage == CDB_TICK_CODA) {
             s = cdb_boundary_coda(model, kv, state, &rows, dlogits, dids, ws, ws_bytes, stream);
             if (s == CDB_OK && tokens_out &&
@@ -516,16 +616,23 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
             status = s;
             break;
         }
-        cdb_driver_complete(d, &t);
+        if (cdb_driver_complete(d, &t) != 0) {
+            status = CDB_ERR_INVALID_ARG;
+            break;
+        }
     }
     if (hipStreamSynchronize(stream) != hipSuccess && status == CDB_OK) status = CDB_ERR_HIP;
     const double secs = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
     d->now = secs;
     if (seconds) *seconds = secs;
-    for (int i = 0; i < RING; ++i) hipEventDestroy(ev[i]);
+    for (int i = 0; i < RING; ++i) {
+        hipEventDestroy(ev[i]);
+        hipEventDestroy(rb_ev[i]);
+    }
     hipEventDestroy(pt_ev);
     hipHostFree(pinned);
     hipHostFree(pinned_pt);
+    hipHostFree(pinned_rb);
     return status;
 }
 

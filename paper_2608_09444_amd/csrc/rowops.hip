@@ -63,7 +63,8 @@ __global__ __launch_bounds__(256) void k_gather(int d, int r_max, int n_slots, i
     const int sl = slot[i];
     rope_row(pos[i], hd, base, rope + (size_t)i * (hd / 2));
     if (threadIdx.x == 0) {
-        if (depth[i] < 1 || depth[i] > r_max || c[i] < 0 || c[i] >= depth[i]) set_err(err, CDB_DEV_BAD_DEPTH);
+        if (depth ? (depth[i] < 1 || depth[i] > r_max || c[i] < 0 || c[i] >= depth[i]) : (c[i] < 0 || c[i] >= r_max))
+            set_err(err, CDB_DEV_BAD_DEPTH);
         if (sl < 0 || sl >= n_slots || seq[i] < 0 || seq[i] >= max_seqs || pos[i] < 0 || pos[i] >= max_pos)
             set_err(err, CDB_DEV_BAD_INDEX);
         write_page(kt, i, seq[i], pos[i], c, kvpid, err);
@@ -182,12 +183,20 @@ __global__ __launch_bounds__(256) void k_store_state(int d, int n_slots, const i
 // ------------------------------------------------------------------ exit
 // score: sigmoid(w_exit . RMSNorm(h)) or ||h - h_in||_2; exit = (c + 1 == depth);
 // state.h[slot] = h.
+// Exit score and decision of every row.  Replayed depths (gated == 0):
+// exit = (c + 1 == depth).  Threshold gate (gated == 1, Section 4.3; App. C.2):
+// the criterion (score >= threshold, or for convergence distance < threshold
+// from loop 2 on) ends the token after this loop, or with lookahead after the
+// next one, carried in pending[slot]; loop r_max always ends it.  deff[i] is
+// the exiting row's depth (c + 1), 0 for continuing rows.
 __global__ __launch_bounds__(256) void k_exit(int d, float eps, int exit_kind, int r_max, int n_slots,
                                               const int32_t* __restrict__ slot, const int32_t* __restrict__ c,
                                               const int32_t* __restrict__ depth, const float* __restrict__ h,
                                               const float* __restrict__ h_in, const uint16_t* __restrict__ w_exit,
                                               float* __restrict__ sh, float* __restrict__ score,
-                                              uint8_t* __restrict__ mask) {
+                                              uint8_t* __restrict__ mask, uint8_t* __restrict__ exit_next,
+                                              int32_t* __restrict__ deff, int gated, float threshold, int lookahead,
+                                              uint8_t* __restrict__ pending) {
     __shared__ float red[4];
     const int i = blockIdx.x;
     const float* x = h + (size_t)i * d;
@@ -208,6 +217,7 @@ __global__ __launch_bounds__(256) void k_exit(int d, float eps, int exit_kind, i
     a = block_sum(a, red);
     b = block_sum(b, red);
     const int sl = slot[i];
+    const bool slot_ok = sl >= 0 && sl < n_slots;
     if (threadIdx.x == 0) {
         float sc;
         if (exit_kind == 1) {
@@ -217,16 +227,32 @@ __global__ __launch_bounds__(256) void k_exit(int d, float eps, int exit_kind, i
             sc = 1.0f / (1.0f + __expf(-z));
         }
         score[i] = sc;
-        const bool valid = depth[i] >= 1 && depth[i] <= r_max && c[i] >= 0 && c[i] < depth[i];
-        mask[i] = (uint8_t)(valid && c[i] + 1 == depth[i]);
+        const int r = c[i] + 1;  // loops done after this step
+        bool ex, nxt;
+        if (!gated) {
+            const bool valid = depth[i] >= 1 && depth[i] <= r_max && c[i] >= 0 && c[i] < depth[i];
+            ex = valid && r == depth[i];
+            nxt = valid && r + 1 == depth[i];
+        } else {
+            const bool valid = c[i] >= 0 && c[i] < r_max && slot_ok;
+            const bool meets = r >= (exit_kind == 1 ? 2 : 1) && (exit_kind == 1 ? sc < threshold : sc >= threshold);
+            if (lookahead) {
+                ex = valid && (r == r_max || pending[sl] != 0);
+                nxt = valid && !ex && (meets || r + 1 == r_max);
+                if (valid) pending[sl] = nxt ? 1 : 0;
+            } else {
+                ex = valid && (r == r_max || meets);
+                nxt = valid && !ex && r + 1 == r_max;
+            }
+        }
+        mask[i] = (uint8_t)ex;
+        if (exit_next) exit_next[i] = (uint8_t)nxt;
+        deff[i] = ex ? r : 0;
     }
-    if (sl >= 0 && sl < n_slots)
+    if (slot_ok)
         for (int k = threadIdx.x * 4; k < d; k += 1024)
             *reinterpret_cast<float4*>(sh + (size_t)sl * d + k) = *reinterpret_cast<const float4*>(x + k);
 }
-
-// Stable partition of the batch into continuing and exiting rows (one
-// workgroup; blocked scan over chunks of 256 rows).
 __global__ __launch_bounds__(256) void k_compact(int M, const uint8_t* __restrict__ mask, int32_t* __restrict__ cont,
                                                  int32_t* __restrict__ exited, int32_t* __restrict__ counts) {
     __shared__ int s_scan[256];
@@ -433,10 +459,13 @@ hipError_t launch_store_state(int M, int d, int n_slots, const int32_t* slot, co
 }
 
 hipError_t launch_exit(const cdb_model_desc& md, const cdb_rows& r, const float* h, const float* h_in,
-                       const uint16_t* w_exit, float* state_h, int n_slots, const cdb_step_out& o, hipStream_t st) {
+                       const uint16_t* w_exit, float* state_h, int n_slots, const cdb_step_out& o,
+                       const cdb_gate* gate, int32_t* deff, hipStream_t st) {
     if (r.n_rows <= 0) return hipSuccess;
     k_exit<<<r.n_rows, 256, 0, st>>>(md.d, md.rms_eps, md.exit_kind, md.r_max, n_slots, r.slot, r.c, r.depth, h,
-                                      h_in, w_exit, state_h, o.exit_score, o.exit_mask);
+                                      h_in, w_exit, state_h, o.exit_score, o.exit_mask, o.exit_next, deff,
+                                      gate ? 1 : 0, gate ? gate->threshold : 0.f, gate ? gate->lookahead : 0,
+                                      gate ? gate->pending : nullptr);
     return hipGetLastError();
 }
 
@@ -445,8 +474,8 @@ hipError_t launch_compact(int M, const uint8_t* mask, int32_t* cont, int32_t* ex
     return hipGetLastError();
 }
 
-hipError_t launch_copy_on_exit(const cdb_model_desc& md, const cdb_kv& kv, const cdb_rows& r, const int32_t* exited,
-                               const int32_t* counts, int* err, hipStream_t st) {
+hipError_t launch_copy_on_exit(const cdb_model_desc& md, const cdb_kv& kv, const cdb_rows& r, const int32_t* deff,
+                               const int32_t* exited, const int32_t* counts, int* err, hipStream_t st) {
     if (r.n_rows <= 0 || md.n_core <= 0) return hipSuccess;
     KvTarget t{};
     t.pool = static_cast<uint16_t*>(kv.core_pool);
@@ -457,7 +486,7 @@ hipError_t launch_copy_on_exit(const cdb_model_desc& md, const cdb_kv& kv, const
     t.max_pages = kv.max_pages;
     t.n_planes = md.r_max + 2;
     dim3 grid(r.n_rows, md.n_core);
-    k_copy_on_exit<<<grid, 256, 0, st>>>(md.n_heads, md.head_dim, md.r_max, t, r.seq, r.pos, r.depth, exited, counts,
+    k_copy_on_exit<<<grid, 256, 0, st>>>(md.n_heads, md.head_dim, md.r_max, t, r.seq, r.pos, deff, exited, counts,
                                          err);
     return hipGetLastError();
 }

@@ -14,7 +14,8 @@ import numpy as np
 from . import _ptr, _stream, cdb_kv, cdb_model, cdb_state, lib as _lib
 
 EXPORTED = ("cdb_driver_create", "cdb_driver_destroy", "cdb_driver_add_sequence", "cdb_driver_page_table",
-            "cdb_driver_next", "cdb_driver_complete", "cdb_driver_set_time", "cdb_driver_get_stats",
+            "cdb_driver_next", "cdb_driver_complete", "cdb_driver_loop_result", "cdb_driver_set_time",
+            "cdb_driver_get_stats",
             "cdb_driver_pages_in_use", "cdb_driver_latencies", "cdb_driver_scratch_bytes", "cdb_driver_run")
 
 KV_FULL, KV_SHARED, KV_FIRST_THEN_SHARED = 0, 1, 2
@@ -25,7 +26,8 @@ MAX_ROWS = 256
 class cdb_driver_config(C.Structure):
     _fields_ = [(n, C.c_int32) for n in ("max_batch", "max_active", "refill", "fixed_depth", "min_coda_batch",
                                           "r_max", "has_prelude", "has_coda", "max_seqs", "max_pages",
-                                          "pre_pages", "core_pages", "coda_pages", "kv_layout")]
+                                          "pre_pages", "core_pages", "coda_pages", "kv_layout", "gated",
+                                          "lookahead")] + [("threshold", C.c_float)]
 
 
 class cdb_driver_tick(C.Structure):
@@ -56,23 +58,23 @@ def lib() -> C.CDLL:
         L.cdb_driver_page_table.restype = C.POINTER(C.c_int32)
         L.cdb_driver_next.argtypes = [P, P]
         L.cdb_driver_complete.argtypes = [P, P]
+        L.cdb_driver_loop_result.argtypes = [P, P, P, P]
         L.cdb_driver_set_time.argtypes = [P, D]
         L.cdb_driver_set_time.restype = None
         L.cdb_driver_get_stats.argtypes = [P, P]
         L.cdb_driver_pages_in_use.argtypes = [P, P, P, P]
         L.cdb_driver_latencies.argtypes = [P, P, I]
-        L.cdb_driver_scratch_bytes.argtypes = [I]
+        L.cdb_driver_scratch_bytes.argtypes = [P, I]
         L.cdb_driver_scratch_bytes.restype = S
         L.cdb_driver_run.argtypes = [P, P, P, P, P, S, P, P, I, P, S, P, P]
-        for f in ("cdb_driver_add_sequence", "cdb_driver_next", "cdb_driver_complete", "cdb_driver_get_stats",
+        for f in ("cdb_driver_add_sequence", "cdb_driver_next", "cdb_driver_complete", "cdb_driver_loop_result",
+                  "cdb_driver_get_stats",
                   "cdb_driver_pages_in_use", "cdb_driver_latencies", "cdb_driver_run"):
             getattr(L, f).restype = C.c_int32
         _bound = True
     return L
 
 
-def cdb_driver_scratch_bytes(vocab: int) -> int:
-    return lib().cdb_driver_scratch_bytes(vocab)
 
 
 class Driver:
@@ -82,10 +84,10 @@ class Driver:
     def __init__(self, max_batch: int, max_active: int, r_max: int, max_seqs: int, max_pages: int,
                  core_pages: int, pre_pages: int = 0, coda_pages: int = 0, has_prelude: bool = False,
                  has_coda: bool = False, refill: bool = True, fixed_depth: bool = False, min_coda_batch: int = 1,
-                 kv_layout: int = KV_FULL):
+                 kv_layout: int = KV_FULL, gated: bool = False, lookahead: bool = False, threshold: float = 0.0):
         self.cfg = cdb_driver_config(max_batch, max_active, int(refill), int(fixed_depth), min_coda_batch, r_max,
                                      int(has_prelude), int(has_coda), max_seqs, max_pages, pre_pages, core_pages,
-                                     coda_pages, kv_layout)
+                                     coda_pages, kv_layout, int(gated), int(lookahead), threshold)
         self.h = lib().cdb_driver_create(C.byref(self.cfg))
         if not self.h:
             raise ValueError("cdb_driver_create: invalid configuration")
@@ -96,9 +98,14 @@ class Driver:
             lib().cdb_driver_destroy(h)
             self.h = None
 
-    def add_sequence(self, prompt_len: int, depths: Sequence[int], arrival: float = 0.0) -> int:
-        dep = np.ascontiguousarray(depths, dtype=np.int32)
-        q = lib().cdb_driver_add_sequence(self.h, prompt_len, len(dep), dep.ctypes.data, arrival)
+    def add_sequence(self, prompt_len: int, depths: Optional[Sequence[int]], arrival: float = 0.0,
+                     n_decode: Optional[int] = None) -> int:
+        """depths: exit depth per decode input (None in gated mode, with n_decode)."""
+        if depths is None:
+            q = lib().cdb_driver_add_sequence(self.h, prompt_len, int(n_decode), None, arrival)
+        else:
+            dep = np.ascontiguousarray(depths, dtype=np.int32)
+            q = lib().cdb_driver_add_sequence(self.h, prompt_len, len(dep), dep.ctypes.data, arrival)
         if q < 0:
             raise ValueError("cdb_driver_add_sequence: rejected")
         return q
@@ -116,8 +123,16 @@ class Driver:
         r = lib().cdb_driver_next(self.h, C.byref(t))
         return None if r == 0 else t
 
-    def complete(self, t: cdb_driver_tick):
-        lib().cdb_driver_complete(self.h, C.byref(t))
+    def complete(self, t: cdb_driver_tick) -> int:
+        return lib().cdb_driver_complete(self.h, C.byref(t))
+
+    def loop_result(self, t: cdb_driver_tick, exit_mask, exit_next) -> int:
+        m = np.ascontiguousarray(exit_mask, dtype=np.uint8)
+        n = np.ascontiguousarray(exit_next, dtype=np.uint8)
+        return lib().cdb_driver_loop_result(self.h, C.byref(t), m.ctypes.data, n.ctypes.data)
+
+    def scratch_bytes(self, vocab: int) -> int:
+        return lib().cdb_driver_scratch_bytes(self.h, vocab)
 
     def set_time(self, now: float):
         lib().cdb_driver_set_time(self.h, now)

@@ -28,12 +28,16 @@ def bf16_pool_to_f64(t: torch.Tensor) -> np.ndarray:
 
 class Lockstep:
     def __init__(self, shape, weights, seq_lens: List[int], max_batch: int, bf16_storage: bool = True,
-                 extra_pages: int = 0, resync: bool = False, sensitivity: bool = False, kv_layout: int = 0):
+                 extra_pages: int = 0, resync: bool = False, sensitivity: bool = False, kv_layout: int = 0,
+                 gate=None):
         """resync: after every call, copy the oracle's states and newly written
         K/V entries into the device buffers, so that each call is checked from
         identical inputs (deep random-init models amplify rounding-level
         differences from call to call).  kv_layout: 0 full, 1 single shared
-        slot, 2 first-then-shared (core planes aliased in the page table)."""
+        slot, 2 first-then-shared (core planes aliased in the page table).
+        gate: (threshold, lookahead) for threshold exits decided on the device
+        (lookahead only: each step's exits are fixed by the previous step, so
+        both sides run the same rows); the loop-step depths are then ignored."""
         self.resync = resync
         self.sensitivity = sensitivity
         self.tol = (TOL_MAX, TOL_MEAN)
@@ -80,6 +84,12 @@ class Lockstep:
                                          "kv_max": 0.0, "score_max": 0.0}
         self.calls = {"prelude": 0, "loop": 0, "coda": 0}
         self.argmax_checked = 0
+        self.gate = gate
+        if gate is not None:
+            assert gate[1], "the lockstep gate runs with lookahead"
+            self.ggate = cdb.Gate(gate[0], True, n_slots)
+            self.opending = np.zeros(n_slots, np.uint8)
+            self.gate_stats = {"decisions": 0, "near_threshold": 0, "overridden": 0, "exits_before_r_max": 0}
         # mean-abs bookkeeping per output kind over the whole run: sum of |error|,
         # element count, and the per-call mean bound weighted by elements
         self.run_sums: Dict[str, List[float]] = {}
@@ -197,15 +207,26 @@ class Lockstep:
         if self.s.n_prelude:
             self._cmp_kv(seqs, poss, [0], "prelude kv")
 
-    def loop(self, seqs, poss, cs, deps):
+    def loop(self, seqs, poss, cs, deps, replay=False):
+        """replay: run the given depths even in gated mode (prompt tokens run r_max loops)."""
         slots = (self.base[seqs] + poss).astype(np.int32)
+        gated = self.gate is not None and not replay
+        if gated:
+            # this step's exits were decided by the previous one (or loop r_max)
+            pend = self.opending[slots].copy()
+            exit_now = (pend != 0) | (cs + 1 == self.R)
+            deps = np.where(exit_now, cs + 1, self.R).astype(np.int32)
         g32 = self._oracle_bound(lambda m: oracle.loop_step(m, self.op, self.oh, self.oe, slots, seqs, poss, cs, deps),
                                  lambda _: self.oh[slots].copy())
         o = oracle.loop_step(self.om, self.op, self.oh, self.oe, slots, seqs, poss, cs, deps)
         self._set_bound(g32, self.oh[slots])
-        rows = cdb.Rows(slots, seqs, poss, cs, deps)
+        rows = cdb.Rows(slots, seqs, poss, cs, None if gated else deps)
         out = cdb.StepOut(len(seqs))
-        cdb.cdb_loop_step(self.gm.model, self.gkv.c, self.gstate.c, rows.c, out.c, self.ws.buf)
+        if gated:
+            cdb.cdb_loop_step_gated(self.gm.model, self.gkv.c, self.gstate.c, rows.c, self.ggate.c, out.c,
+                                    self.ws.buf)
+        else:
+            cdb.cdb_loop_step(self.gm.model, self.gkv.c, self.gstate.c, rows.c, out.c, self.ws.buf)
         torch.cuda.synchronize()
         self.calls["loop"] += 1
         n = len(seqs)
@@ -219,12 +240,35 @@ class Lockstep:
         d = np.abs(sc - o["score"])
         self.errors["score_max"] = max(self.errors["score_max"], float(d.max()))
         assert float(d.max()) <= self.tol[0], f"exit score max abs {d.max():.3e}"
+        dev_next = out.exit_next[:n].cpu().numpy()
+        if not gated:
+            # replayed depths: the next loop is the last one exactly when c + 2 == depth
+            assert dev_next.tolist() == ((o["exit_mask"] == 0) & (cs + 2 == deps)).astype(np.uint8).tolist()
+        else:
+            self._gate_next(cs, slots, o, dev_next, pend)
         for i in range(n):
             planes = [int(cs[i]) + 1]
             if o["exit_mask"][i]:
                 planes += list(range(int(deps[i]) + 1, self.R + 1))
             self._cmp_kv([seqs[i]], [poss[i]], planes, "core kv")
         return o
+
+    def _gate_next(self, cs, slots, o, dev_next, pend):
+        """The oracle's decisions for the next loop from its own scores; a
+        device decision may differ only where the oracle's score lies within
+        the score tolerance of the threshold, and is then adopted by both."""
+        thr = self.gate[0]
+        _, o_next = self.om.gate_decide(cs, o["score"], thr, True, pend)
+        exited = o["exit_mask"] != 0
+        self.gate_stats["decisions"] += int((~exited).sum())
+        self.gate_stats["exits_before_r_max"] += int((exited & (cs + 1 < self.R)).sum())
+        near = np.abs(o["score"] - thr) <= self.tol[0]
+        self.gate_stats["near_threshold"] += int((near & ~exited).sum())
+        diff = (dev_next != o_next) & ~exited
+        assert not (diff & ~near).any(), f"exit decisions differ away from the threshold: {o['score'][diff]}"
+        self.gate_stats["overridden"] += int(diff.sum())
+        final = np.where(diff, dev_next, o_next).astype(np.uint8)
+        self.opending[slots] = np.where(exited, 0, final)
 
     def coda(self, seqs, poss):
         slots = (self.base[seqs] + poss).astype(np.int32)
@@ -269,7 +313,8 @@ class Lockstep:
             for c in range(R):
                 for a in range(0, P, cdb.MAX_ROWS):
                     b = slice(a, a + cdb.MAX_ROWS)
-                    self.loop(seq[b], pos[b], np.full(len(pos[b]), c, np.int32), np.full(len(pos[b]), R, np.int32))
+                    self.loop(seq[b], pos[b], np.full(len(pos[b]), c, np.int32), np.full(len(pos[b]), R, np.int32),
+                              replay=True)
             for a in range(0, P, cdb.MAX_ROWS):
                 _, oid = self.coda(seq[a:a + cdb.MAX_ROWS], pos[a:a + cdb.MAX_ROWS])
             if n_decode[q]:

@@ -39,6 +39,7 @@ def _requests(shape, seed=40):
 
 
 def _decode_on_gpu(shape, gm, prompts, ndec, depths, kv_layout=drv.KV_FULL, **cfg):
+    """depths[q] is None in gated mode."""
     """Prefill every prompt through the stage calls (one block per sequence),
     then let the driver decode all requests.  Returns (first tokens, decoded
     ids [seq][k], driver stats)."""
@@ -52,7 +53,7 @@ def _decode_on_gpu(shape, gm, prompts, ndec, depths, kv_layout=drv.KV_FULL, **cf
                    has_prelude=shape.n_prelude > 0, has_coda=shape.n_coda > 0, r_max=R, kv_layout=kv_layout,
                    **cfg)
     for q in range(n):
-        d.add_sequence(len(prompts[q]), depths[q])
+        d.add_sequence(len(prompts[q]), depths[q], n_decode=ndec[q])
     assert cfg.get("max_active", 0) >= n
     first_tick = d.next()  # admits every request; the plan is kept until completed
     assert first_tick.n_rows == n
@@ -77,7 +78,7 @@ def _decode_on_gpu(shape, gm, prompts, ndec, depths, kv_layout=drv.KV_FULL, **cf
         cdb.cdb_boundary_coda(gm.model, kv.c, pstate.c, rows.c, logits, ids, ws.buf)
         first[q] = int(ids[-1].item())
     state = cdb.State(shape, n)
-    scratch = torch.empty(drv.cdb_driver_scratch_bytes(shape.vocab), dtype=torch.uint8, device="cuda")
+    scratch = torch.empty(d.scratch_bytes(shape.vocab), dtype=torch.uint8, device="cuda")
     out_ids = torch.full((n, max(ndec)), -1, dtype=torch.int32, device="cuda")
     secs = d.run(gm.model, kv.c, state.c, scratch, first, ws.buf, tokens_out=out_ids)
     torch.cuda.synchronize()
@@ -156,8 +157,56 @@ def test_driver_rejects_short_token_table():
     kv = cdb.PagedKV(s, 1, 2, 2, 8, 2)
     ws = cdb.Workspace(gm.desc, 4)
     st = cdb.State(s, 1)
-    scratch = torch.empty(drv.cdb_driver_scratch_bytes(s.vocab), dtype=torch.uint8, device="cuda")
+    scratch = torch.empty(d.scratch_bytes(s.vocab), dtype=torch.uint8, device="cuda")
     short = torch.zeros((1, 2), dtype=torch.int32, device="cuda")
     with pytest.raises(cdb.CdbError):
         d.run(gm.model, kv.c, st.c, scratch, np.zeros(1, np.int32), ws.buf, tokens_out=short)
     assert d.stats()["loop_steps"] == 0
+
+
+def _gate_threshold(shape, w, prompts):
+    """A threshold the tiny model's gate scores straddle: the median of the
+    loop-1 scores of the first prompt under the oracle."""
+    m = oracle.Model(shape, w, bf16_storage=True)
+    p = prompts[0]
+    ref = m.ref_sequence(p, np.full(len(p), shape.r_max, np.int32))
+    return float(np.median(ref["scores"][:, 0]))
+
+
+def test_lookahead_gate_call_by_call():
+    from lockstep import Lockstep
+    s = cdbgen.TINY
+    w = cdbgen.model_weights(s)
+    prompts, ndec, depths = _requests(s, seed=70)
+    thr = _gate_threshold(s, w, prompts)
+    _say(f"[gpu] lockstep {s.name} lookahead gate, threshold {thr:.4f}")
+    deps = [np.concatenate([np.full(len(p), s.r_max, np.int32), np.full(k, s.r_max, np.int32)])
+            for p, k in zip(prompts, ndec)]
+    ls = Lockstep(s, w, [len(p) + k for p, k in zip(prompts, ndec)], max_batch=4, gate=(thr, True))
+    ls.run(prompts, ndec, deps)
+    _say(f"[gpu]   errors {ls.errors} calls {ls.calls} gate {ls.gate_stats}")
+    assert ls.device_error() == 0
+    assert ls.gate_stats["exits_before_r_max"] > 0 and ls.gate_stats["decisions"] > 0
+
+
+@pytest.mark.parametrize("lookahead", [True, False], ids=["lookahead", "same-step"])
+def test_gated_driver_decode_is_schedule_invariant(lookahead):
+    s = cdbgen.TINY
+    w = cdbgen.model_weights(s)
+    gm = cdb.DeviceModel(s, w)
+    prompts, ndec, _ = _requests(s, seed=71)
+    n = len(prompts)
+    thr = _gate_threshold(s, w, prompts)
+    _say(f"[gpu] gated driver decode {s.name}, lookahead {lookahead}, threshold {thr:.4f}")
+    runs = {}
+    for name, cfg in (("refill", dict(max_batch=4, max_active=n)),
+                      ("no-refill", dict(max_batch=3, max_active=n, refill=False))):
+        first, ids, st, secs = _decode_on_gpu(s, gm, prompts, ndec, [None] * n, gated=True, lookahead=lookahead,
+                                              threshold=thr, **cfg)
+        _say(f"[gpu]   {name}: {st} in {secs * 1e3:.1f} ms")
+        assert st["tokens"] == sum(ndec)
+        runs[name] = (first, ids, st["loop_rows"])
+    a, b = runs["refill"], runs["no-refill"]
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1]) and a[2] == b[2]
+    lo = sum(ndec) * (2 if lookahead else 1)
+    assert lo <= a[2] < sum(ndec) * s.r_max  # some tokens exit early, none before the minimum depth
