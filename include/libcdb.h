@@ -187,7 +187,8 @@ typedef struct {
     uint8_t* pending;
 } cdb_gate;
 
-/* Workspace (device scratch) needed for calls with up to max_rows rows. */
+/* Workspace (device scratch) needed for calls with up to max_rows rows
+ * (stage calls take up to 256 rows, cdb_prefill up to 512); 0 if unsupported. */
 size_t cdb_workspace_bytes(const cdb_model_desc* desc, int32_t max_rows);
 
 /* Clears the workspace's error code (a kernel, not a memset).  Call once after
@@ -231,6 +232,21 @@ cdb_status cdb_loop_step_gated(const cdb_model* model, const cdb_kv* kv, const c
 cdb_status cdb_boundary_coda(const cdb_model* model, const cdb_kv* kv, const cdb_state* state,
                              const cdb_rows* rows, float* logits, int32_t* next_ids, void* ws, size_t ws_bytes,
                              hipStream_t stream);
+
+/* Chunked prefill of one sequence (the prompt KV every decode reads; Section
+ * 6.1 runs prompts before decoding): rows i = 0..n_rows-1 are positions
+ * pos0 + i with input ids tokens[i] (device int32).  Runs the prelude layers
+ * (plane 0), r_max core loops over the whole chunk (loop r writes plane r;
+ * prompt tokens take every loop), the coda layers (plane r_max + 1), the final
+ * RMSNorm and the LM head: logits device fp32 [n_rows][vocab], next_ids device
+ * int32 [n_rows] (argmax, lowest index on ties).  Positions < pos0 of the
+ * sequence must already be in the cache (earlier chunks); every plane's pages
+ * of positions < pos0 + n_rows must be mapped.  Attention is query-tiled on
+ * MFMA; above 256 rows the projections use compute-bound tiles.
+ * n_rows <= 512; the workspace must be sized for n_rows. */
+cdb_status cdb_prefill(const cdb_model* model, const cdb_kv* kv, int32_t seq, int32_t pos0, int32_t n_rows,
+                       const int32_t* tokens, float* logits, int32_t* next_ids, void* ws, size_t ws_bytes,
+                       hipStream_t stream);
 
 /* Paged decode attention of one layer, alone (the operation every layer of the
  * stage calls runs after writing its K/V; Section 4.2): for row i and head h,

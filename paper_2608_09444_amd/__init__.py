@@ -18,10 +18,11 @@ CDB_OK, CDB_ERR_INVALID_ARG, CDB_ERR_CAPACITY, CDB_ERR_HIP, CDB_ERR_UNSUPPORTED 
 CDB_DEV_OK, CDB_DEV_UNMAPPED_PAGE, CDB_DEV_BAD_DEPTH, CDB_DEV_BAD_INDEX = range(4)
 PAGE_TOKENS = 16
 MAX_ROWS = 256
+MAX_PREFILL_ROWS = 512
 
 EXPORTED = ("cdb_packed_weight_bytes", "cdb_pack_weights", "cdb_kv_page_bytes", "cdb_workspace_bytes",
             "cdb_workspace_init", "cdb_boundary_prelude", "cdb_loop_step", "cdb_loop_step_gated", "cdb_boundary_coda",
-            "cdb_paged_attention", "cdb_read_device_error", "cdb_status_str")
+            "cdb_prefill", "cdb_paged_attention", "cdb_read_device_error", "cdb_status_str")
 
 
 class CdbError(RuntimeError):
@@ -93,11 +94,12 @@ def lib() -> C.CDLL:
         L.cdb_loop_step_gated.argtypes = [P, P, P, P, P, P, P, S, P]
         L.cdb_boundary_coda.argtypes = [P, P, P, P, P, P, P, S, P]
         L.cdb_paged_attention.argtypes = [P, P, P, I, I, P, P, P, P, S, P]
+        L.cdb_prefill.argtypes = [P, P, I, I, I, P, P, P, P, S, P]
         L.cdb_read_device_error.argtypes = [P, P, P]
         L.cdb_status_str.argtypes = [C.c_int]
         L.cdb_status_str.restype = C.c_char_p
         for f in ("cdb_pack_weights", "cdb_workspace_init", "cdb_boundary_prelude", "cdb_loop_step", "cdb_loop_step_gated",
-                  "cdb_boundary_coda", "cdb_paged_attention", "cdb_read_device_error"):
+                  "cdb_boundary_coda", "cdb_paged_attention", "cdb_prefill", "cdb_read_device_error"):
             getattr(L, f).restype = C.c_int
         _lib = L
     return _lib
@@ -176,6 +178,13 @@ def cdb_boundary_coda(model: cdb_model, kv: cdb_kv, state: cdb_state, rows: cdb_
     _check("cdb_boundary_coda", lib().cdb_boundary_coda(C.byref(model), C.byref(kv), C.byref(state), C.byref(rows),
                                                         _ptr(logits), _ptr(next_ids), _ptr(ws), ws.numel(),
                                                         _stream(stream)))
+
+
+def cdb_prefill(model: cdb_model, kv: cdb_kv, seq: int, pos0: int, tokens, logits, next_ids, ws, stream=None):
+    """tokens: device int32 [n]; logits: device fp32 [n][vocab]; next_ids: device int32 [n]."""
+    n = int(tokens.numel())
+    _check("cdb_prefill", lib().cdb_prefill(C.byref(model), C.byref(kv), seq, pos0, n, _ptr(tokens), _ptr(logits),
+                                            _ptr(next_ids), _ptr(ws), ws.numel(), _stream(stream)))
 
 
 def cdb_paged_attention(desc: cdb_model_desc, kv: cdb_kv, rows: cdb_rows, stage: int, layer: int, q, out, ws,

@@ -49,8 +49,19 @@ bool weight_layout(const cdb_model_desc& d, WeightLayout* w) {
 struct ModelGemms {
     GemmShape qkv, o, gu, down, adapter, lm;
 };
-static ModelGemms model_gemms(const cdb_model_desc& d) {
+// Launch shapes of the model's projections for calls of M rows: the skinny
+// weight-streaming kernel up to kMaxRows rows, the tile kernel above.
+static ModelGemms model_gemms(const cdb_model_desc& d, int M = 0) {
     ModelGemms g;
+    if (M > kMaxRows) {
+        g.qkv = gemm_shape_mn(3 * d.d, d.d, M, EPI_QKV);
+        g.o = gemm_shape_mn(d.d, d.d, M, EPI_PARTIAL);
+        g.gu = gemm_shape_mn(2 * d.d_ff, d.d, M, EPI_SWIGLU);
+        g.down = gemm_shape_mn(d.d, d.d_ff, M, EPI_PARTIAL);
+        g.adapter = gemm_shape_mn(d.d, 2 * d.d, M, EPI_STORE);
+        g.lm = gemm_shape_mn(d.vocab, d.d, M, EPI_STORE);
+        return g;
+    }
     g.qkv = gemm_shape(3 * d.d, d.d, EPI_QKV);
     g.o = gemm_shape(d.d, d.d, EPI_PARTIAL);
     g.gu = gemm_shape(2 * d.d_ff, d.d, EPI_SWIGLU);
@@ -63,7 +74,7 @@ static ModelGemms model_gemms(const cdb_model_desc& d) {
 WsLayout ws_layout(const cdb_model_desc& d, int rows) {
     WsLayout L;
     const size_t D = d.d, F = d.d_ff, M = rows, M32 = gemm_rows(rows);
-    const ModelGemms g = model_gemms(d);
+    const ModelGemms g = model_gemms(d, rows);
     const size_t part = (size_t)(g.o.S > g.down.S ? g.o.S : g.down.S) * D;  // split-K partials of O / down
     size_t off = 0;
     L.err = off;
@@ -88,6 +99,8 @@ WsLayout ws_layout(const cdb_model_desc& d, int rows) {
     off = align256(off + M * 4);
     L.deff = off;
     off = align256(off + M * 4);
+    L.prow = off;  // prefill row arrays: slot, seq, pos
+    off = align256(off + 3 * M * 4);
     L.total = off;
     return L;
 }
@@ -111,6 +124,7 @@ struct Ctx {
     int32_t* order;
     int32_t* kvpid;
     int32_t* deff;
+    int32_t* prow;
 };
 
 static Ctx make_ctx(const cdb_model* model, void* ws, int rows) {
@@ -118,7 +132,7 @@ static Ctx make_ctx(const cdb_model* model, void* ws, int rows) {
     c.md = &model->desc;
     c.wb = static_cast<const unsigned char*>(model->packed);
     weight_layout(model->desc, &c.wl);
-    c.gm = model_gemms(model->desc);
+    c.gm = model_gemms(model->desc, rows);
     c.ws = static_cast<unsigned char*>(ws);
     c.L = ws_layout(model->desc, rows);
     c.err = reinterpret_cast<int*>(c.ws + c.L.err);
@@ -132,6 +146,7 @@ static Ctx make_ctx(const cdb_model* model, void* ws, int rows) {
     c.order = reinterpret_cast<int32_t*>(c.ws + c.L.order);
     c.kvpid = reinterpret_cast<int32_t*>(c.ws + c.L.kvpid);
     c.deff = reinterpret_cast<int32_t*>(c.ws + c.L.deff);
+    c.prow = reinterpret_cast<int32_t*>(c.ws + c.L.prow);
     return c;
 }
 
@@ -142,15 +157,21 @@ static const uint16_t* wptr(const Ctx& c, size_t off) { return reinterpret_cast<
         if ((x) != hipSuccess) return CDB_ERR_HIP; \
     } while (0)
 
+// A prefill chunk: the rows are positions pos0.. of sequence seq.
+struct Chunk {
+    int seq, pos0;
+};
+
 // Run `count` transformer layers (global index first..) of one stage over the
 // rows in ctx.h, with K/V in `kv`.  On return ctx.h holds the stage output and
-// ctx.x its RMSNorm when `norm_out` is set.
+// ctx.x its RMSNorm when `norm_out` is set.  With `chunk` the rows are a
+// prefill chunk and attention runs query-tiled on MFMA.
 static cdb_status run_layers(const Ctx& c, int first, int count, KvTarget kv, const cdb_rows& r, bool norm_out,
-                             hipStream_t st) {
+                             hipStream_t st, const Chunk* chunk = nullptr) {
     const cdb_model_desc& d = *c.md;
     const int M = r.n_rows;
     int pending = 0;  // split-K partials of the previous down projection not yet added to h
-    if (count > 0) HIPCHK(launch_row_order(r.pos, M, c.order, st));
+    if (count > 0 && !chunk) HIPCHK(launch_row_order(r.pos, M, c.order, st));
     for (int l = 0; l < count; ++l) {
         const size_t lb = (size_t)(first + l) * c.wl.layer_stride;
         kv.layer = l;
@@ -168,7 +189,11 @@ static cdb_status run_layers(const Ctx& c, int first, int count, KvTarget kv, co
         // attention half: h += down partials; x = RMSNorm(h); q/k/v + RoPE + K/V write
         HIPCHK(launch_resid_norm(c.h, c.part, pending, M, d.d, d.rms_eps, c.x, st));
         HIPCHK(launch_gemm(EPI_QKV, c.x, wptr(c, lb + c.wl.qkv), M, c.gm.qkv, c.part, ea, st));
-        HIPCHK(launch_attention(c.q, kv, r.seq, r.pos, c.order, M, d.n_heads, d.head_dim, c.x, c.err, st));
+        if (chunk)
+            HIPCHK(launch_prefill_attention(c.q, kv, chunk->seq, chunk->pos0, M, d.n_heads, d.head_dim, c.x, c.err,
+                                            st));
+        else
+            HIPCHK(launch_attention(c.q, kv, r.seq, r.pos, c.order, M, d.n_heads, d.head_dim, c.x, c.err, st));
         HIPCHK(launch_gemm(EPI_PARTIAL, c.x, wptr(c, lb + c.wl.o), M, c.gm.o, c.part, ea, st));
         // MLP half: h += O partials; x = RMSNorm(h); act = SwiGLU; down partials
         HIPCHK(launch_resid_norm(c.h, c.part, c.gm.o.S, M, d.d, d.rms_eps, c.x, st));
@@ -273,7 +298,7 @@ size_t cdb_kv_page_bytes(const cdb_model_desc* desc, int32_t stage) {
 }
 
 size_t cdb_workspace_bytes(const cdb_model_desc* desc, int32_t max_rows) {
-    if (!desc || !desc_supported(*desc) || max_rows < 0 || max_rows > kMaxRows) return 0;
+    if (!desc || !desc_supported(*desc) || max_rows < 0 || max_rows > kMaxPrefillRows) return 0;
     return ws_layout(*desc, max_rows).total;
 }
 
@@ -363,6 +388,63 @@ cdb_status cdb_boundary_coda(const cdb_model* model, const cdb_kv* kv, const cdb
     HIPCHK(launch_load_state(d, M, rows->slot, rows->seq, rows->pos, t, state->h, state->n_slots, c.h, c.rope, c.kvpid,
                              c.err, st));
     s = run_layers(c, d.n_prelude + d.n_core, d.n_coda, t, *rows, true, st);
+    if (s != CDB_OK) return s;
+    EpiArgs ea{};
+    ea.out = logits;
+    ea.ld_out = d.vocab;
+    ea.err = c.err;
+    HIPCHK(launch_gemm(EPI_STORE, c.x, wptr(c, c.wl.lm_head), M, c.gm.lm, c.part, ea, st));
+    HIPCHK(launch_argmax(M, d.vocab, logits, next_ids, st));
+    return CDB_OK;
+}
+
+cdb_status cdb_prefill(const cdb_model* model, const cdb_kv* kv, int32_t seq, int32_t pos0, int32_t n_rows,
+                       const int32_t* tokens, float* logits, int32_t* next_ids, void* ws, size_t ws_bytes,
+                       hipStream_t st) {
+    if (!model || !kv || !model->packed || !tokens || !logits || !next_ids || !ws) return CDB_ERR_INVALID_ARG;
+    const cdb_model_desc& d = model->desc;
+    if (!desc_supported(d)) return CDB_ERR_UNSUPPORTED;
+    if (n_rows < 1 || n_rows > kMaxPrefillRows) return CDB_ERR_CAPACITY;
+    if (seq < 0 || seq >= kv->max_seqs || pos0 < 0 || (size_t)pos0 + n_rows > (size_t)kv->max_pages * kPage)
+        return CDB_ERR_INVALID_ARG;
+    if (!kv->page_table) return CDB_ERR_INVALID_ARG;
+    for (int stage = 0; stage < 3; ++stage) {
+        const int layers = stage == 0 ? d.n_prelude : (stage == 1 ? d.n_core : d.n_coda);
+        void* pool = stage == 0 ? kv->pre_pool : (stage == 1 ? kv->core_pool : kv->coda_pool);
+        if (layers > 0 && !pool) return CDB_ERR_INVALID_ARG;
+    }
+    if (ws_bytes < ws_layout(d, n_rows).total) return CDB_ERR_CAPACITY;
+    const int M = n_rows;
+    Ctx c = make_ctx(model, ws, M);
+    const Chunk chunk{seq, pos0};
+    cdb_rows r{M, c.prow, c.prow + M, c.prow + 2 * M, nullptr, nullptr};
+    HIPCHK(launch_prefill_rows(seq, pos0, M, c.prow, st));
+    // prelude (plane 0): embedding, RoPE table, write pages
+    KvTarget t = stage_target(d, *kv, 0);
+    HIPCHK(launch_embed(d, wptr(c, c.wl.embed), tokens, r, *kv, t, M, c.h, c.rope, c.kvpid, c.err, st));
+    cdb_status s = run_layers(c, 0, d.n_prelude, t, r, false, st, &chunk);
+    if (s != CDB_OK) return s;
+    if (d.injection) HIPCHK(hipMemcpyAsync(c.h_in, c.h, (size_t)M * d.d * 4, hipMemcpyDeviceToDevice, st));  // e
+    // r_max core loops over the whole chunk, loop r in plane r (prompt tokens run every loop)
+    for (int loop = 1; loop <= d.r_max; ++loop) {
+        t = stage_target(d, *kv, 1);
+        t.plane_fixed = loop;
+        HIPCHK(launch_kv_pages(t, r, c.kvpid, c.err, st));
+        if (d.injection) {
+            HIPCHK(launch_concat_frag(M, d.d, c.h, c.h_in, c.x, st));
+            EpiArgs ea{};
+            ea.out = c.h;
+            ea.ld_out = d.d;
+            ea.err = c.err;
+            HIPCHK(launch_gemm(EPI_STORE, c.x, wptr(c, c.wl.adapter), M, c.gm.adapter, c.part, ea, st));
+        }
+        s = run_layers(c, d.n_prelude, d.n_core, t, r, false, st, &chunk);
+        if (s != CDB_OK) return s;
+    }
+    // coda (plane r_max + 1), final RMSNorm, LM head, argmax
+    t = stage_target(d, *kv, 2);
+    HIPCHK(launch_kv_pages(t, r, c.kvpid, c.err, st));
+    s = run_layers(c, d.n_prelude + d.n_core, d.n_coda, t, r, true, st, &chunk);
     if (s != CDB_OK) return s;
     EpiArgs ea{};
     ea.out = logits;

@@ -11,8 +11,10 @@
 namespace cdb {
 
 constexpr int kPage = 16;       // tokens per KV page
-constexpr int kMaxRows = 256;   // rows per stage call (workspace and GEMM limit)
+constexpr int kMaxRows = 256;          // rows per stage call
+constexpr int kMaxPrefillRows = 512;   // rows per prefill chunk
 
+typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -40,7 +42,10 @@ __host__ __device__ __forceinline__ size_t frag_index(int m, int k, int K) {
 __host__ __device__ __forceinline__ int round32(int m) { return (m + 31) & ~31; }
 // Rows a GEMM input buffer must hold for M rows: the GEMM covers M with 1, 2, 4
 // or 8 tiles of 32 rows and reads every row of them.
-__host__ __device__ __forceinline__ int gemm_rows(int m) { return m <= 32 ? 32 : m <= 64 ? 64 : m <= 128 ? 128 : 256; }
+// rows a fragment-layout activation buffer holds for m rows (whole tiles of the GEMM that reads it)
+__host__ __device__ __forceinline__ int gemm_rows(int m) {
+    return m <= 32 ? 32 : m <= 64 ? 64 : m <= 128 ? 128 : ((m + 127) / 128) * 128;
+}
 
 // Element offset of (layer, page, K/V, head, token) in a stage pool laid out
 // [layers][pages][K, V][heads][16 tokens][hd]: one layer's pages are
@@ -96,11 +101,12 @@ struct WeightLayout {
 bool weight_layout(const cdb_model_desc& d, WeightLayout* out);
 
 struct WsLayout {
-    size_t err, h, h_in, q, x, act, part, rope, order, kvpid, deff, total;
+    size_t err, h, h_in, q, x, act, part, rope, order, kvpid, deff, prow, total;
 };
 WsLayout ws_layout(const cdb_model_desc& d, int rows);
 
 GemmShape gemm_shape(int N, int K, int epi);
+GemmShape gemm_shape_mn(int N, int K, int M, int epi);  // M > kMaxRows
 bool desc_supported(const cdb_model_desc& d);
 
 // ---------------------------------------------------------------- launchers
@@ -110,6 +116,10 @@ hipError_t launch_gemm(int epi, const uint16_t* X, const uint16_t* Wp, int M, Ge
 hipError_t launch_attention(const float* q, const KvTarget& kv, const int32_t* seq, const int32_t* pos,
                             const int32_t* order, int M, int H, int hd, uint16_t* out, int* err, hipStream_t st);
 hipError_t launch_row_order(const int32_t* pos, int M, int32_t* order, hipStream_t st);
+// causal attention of a prefill chunk: rows are positions pos0..pos0+M-1 of one
+// sequence in the target's fixed plane
+hipError_t launch_prefill_attention(const float* q, const KvTarget& kv, int seq, int pos0, int M, int H, int hd,
+                                    uint16_t* out, int* err, hipStream_t st);
 // h[i] += sum over s < S of part[s][i] (split order), then, when out is set,
 // out = bf16(RMSNorm(h)) in fragment layout.
 hipError_t launch_resid_norm(float* h, const float* part, int S, int M, int d, float eps, uint16_t* out,
@@ -138,6 +148,11 @@ hipError_t launch_compact(int M, const uint8_t* mask, int32_t* cont, int32_t* ex
 hipError_t launch_copy_on_exit(const cdb_model_desc& md, const cdb_kv& kv, const cdb_rows& r, const int32_t* deff,
                                const int32_t* exited, const int32_t* counts, int* err, hipStream_t st);
 hipError_t launch_argmax(int M, int V, const float* logits, int32_t* ids, hipStream_t st);
+// prefill: row arrays slot = i, seq, pos = pos0 + i in rows[0..3M); per-row
+// write pages of a fixed plane; adapter input [h; e] in fragment layout
+hipError_t launch_prefill_rows(int seq, int pos0, int M, int32_t* rows, hipStream_t st);
+hipError_t launch_kv_pages(const KvTarget& kt, const cdb_rows& r, int32_t* kvpid, int* err, hipStream_t st);
+hipError_t launch_concat_frag(int M, int d, const float* h, const float* e, uint16_t* xcat, hipStream_t st);
 hipError_t launch_scatter_ids(int M, const int32_t* ids, const int32_t* seq, const int32_t* index, int max_seqs,
                               int stride, int32_t* out, hipStream_t st);
 hipError_t launch_pack(int kind, const uint16_t* a, const uint16_t* b, const uint16_t* c, int N, int K, int hd,

@@ -26,8 +26,6 @@
 
 namespace cdb {
 
-typedef float floatx16 __attribute__((ext_vector_type(16)));
-
 constexpr int kMaxKw = 8;     // waves per workgroup (2 per SIMD, so 256 registers each)
 
 struct GemmArgs {
@@ -41,18 +39,19 @@ struct GemmArgs {
 // stripe's 16 rotary pairs for every row, and each row's K/V write page and
 // slot within it.
 struct QkvStage {
-    const float2* rope;  // [rows][16]
+    const float2* rope;  // [rows][16]; NULL: read the call's tables in global memory
     const int* pid;      // [rows]
     const int* tok;      // [rows]
 };
 
+// split: the workgroup's K split (EPI_PARTIAL writes partial tile `split`)
 template <int EPI>
-__device__ __forceinline__ void epilogue_elem(float val, float partner, int m, int p, const GemmArgs& ga,
+__device__ __forceinline__ void epilogue_elem(float val, float partner, int m, int p, int split, const GemmArgs& ga,
                                               const EpiArgs& ea, const QkvStage& qs) {
     if (EPI == EPI_STORE) {
         ea.out[(size_t)m * ea.ld_out + p] = val;
     } else if (EPI == EPI_PARTIAL) {
-        ga.part[((size_t)blockIdx.y * ga.M + m) * ga.N + p] = val;
+        ga.part[((size_t)split * ga.M + m) * ga.N + p] = val;
     } else if (EPI == EPI_SWIGLU) {
         if (p & 16) return;
         const int f = (p >> 5) * 16 + (p & 15);
@@ -67,7 +66,7 @@ __device__ __forceinline__ void epilogue_elem(float val, float partner, int m, i
         const int dim = gi * 16 + jj + half * (ea.hd >> 1);
         float outv = val;
         if (part < 2) {
-            const float2 cs = qs.rope[m * 16 + jj];
+            const float2 cs = qs.rope ? qs.rope[m * 16 + jj] : ea.rope[(size_t)m * (ea.hd >> 1) + gi * 16 + jj];
             const float xf = half ? partner : val, xs = half ? val : partner;
             outv = half ? (xs * cs.x + xf * cs.y) : (xf * cs.x - xs * cs.y);
         }
@@ -75,10 +74,11 @@ __device__ __forceinline__ void epilogue_elem(float val, float partner, int m, i
             ea.q[(size_t)m * (ea.H * ea.hd) + head * ea.hd + dim] = outv;
             return;
         }
-        const int pid = qs.pid[m];  // -1: unmapped (reported by the row-entry kernel)
+        const int pid = qs.rope ? qs.pid[m] : ea.kvpid[m];  // -1: unmapped (reported by the row-entry kernel)
         if (pid < 0) return;
         const KvTarget& kv = ea.kv;
-        kv.pool[kv_offset(kv.layer, pid, kv.n_pages, part - 1, head, ea.H, qs.tok[m], ea.hd) + dim] = f2bf(outv);
+        const int tok = qs.rope ? qs.tok[m] : ea.pos[m] % kPage;
+        kv.pool[kv_offset(kv.layer, pid, kv.n_pages, part - 1, head, ea.H, tok, ea.hd) + dim] = f2bf(outv);
     }
 }
 
@@ -235,8 +235,107 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs ga, EpiArgs ea) {
         const int m = r >> 5, nn = r & 31;
         const int p = (nt + ns) * 32 + nn;
         const float* f = fin + ns * 32 * fld;
-        epilogue_elem<EPI>(f[nn * fld + m], f[(nn ^ 16) * fld + m], m, p, ga, ea, qs);
+        epilogue_elem<EPI>(f[nn * fld + m], f[(nn ^ 16) * fld + m], m, p, s, ga, ea, qs);
     }
+}
+
+// Large-M GEMM (prefill chunks of up to 512 rows), where the product is
+// compute-bound (about M FLOP per weight byte).  A workgroup owns a 128-row x
+// 128-column output tile and one K split: 4 waves in 2 x 2, each 64 rows x 64
+// columns (2 m-tiles x 2 stripes, 4 MFMAs per 16-wide k step), operands read
+// straight from the packed weights and the fragment-layout activations (each
+// tile feeds two waves; the second read is served by the caches), double-
+// buffered in registers.  Each wave owns its outputs, so the epilogue runs from
+// the accumulators: column n's RoPE / SwiGLU partner n ^ 16 is element j ^ 8 of
+// the same lane.
+template <int EPI>
+__global__ __launch_bounds__(256) void k_gemm_mn(GemmArgs ga, EpiArgs ea) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int KS = ga.K >> 4;
+    const int stripes = ga.N >> 5;
+    const int mtiles = (gemm_rows(ga.M) + 31) >> 5;  // m-tiles the activation buffer holds
+    const int s = blockIdx.z;
+    const int k0 = (int)(((long)s * KS) / ga.S), k1 = (int)(((long)(s + 1) * KS) / ga.S);
+    const int nt0 = blockIdx.x * 4 + (wave & 1) * 2;   // first stripe of this wave
+    const int mt0 = blockIdx.y * 4 + (wave >> 1) * 2;  // first m-tile of this wave
+
+    floatx16 acc[2][2];
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int j = 0; j < 16; ++j) acc[a][b][j] = 0.f;
+
+    // tiles past the matrix re-read the last one (their results are not stored)
+    const u32x4* wsrc[2];
+    const u32x4* xsrc[2];
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+        wsrc[a] = reinterpret_cast<const u32x4*>(ga.Wp) + (size_t)min(nt0 + a, stripes - 1) * KS * 64 + lane;
+        xsrc[a] = reinterpret_cast<const u32x4*>(ga.X) + (size_t)min(mt0 + a, mtiles - 1) * KS * 64 + lane;
+    }
+    constexpr int CH = 4;
+    u32x4 wa[CH][2], wb[CH][2], xa[CH][2], xb[CH][2];
+    auto load = [&](u32x4 (&w)[CH][2], u32x4 (&x)[CH][2], int c0) {
+#pragma unroll
+        for (int i = 0; i < CH; ++i) {
+            const int ks = min(c0 + i, k1 - 1);
+#pragma unroll
+            for (int a = 0; a < 2; ++a) {
+                w[i][a] = wsrc[a][(size_t)ks * 64];
+                x[i][a] = xsrc[a][(size_t)ks * 64];
+            }
+        }
+    };
+    auto compute = [&](const u32x4 (&w)[CH][2], const u32x4 (&x)[CH][2], int c0) {
+#pragma unroll
+        for (int i = 0; i < CH; ++i) {
+            const uint32_t keep = c0 + i < k1 ? 0xffffffffu : 0u;
+#pragma unroll
+            for (int a = 0; a < 2; ++a) {
+                const bf16x8 wv = __builtin_bit_cast(bf16x8, w[i][a] & keep);
+#pragma unroll
+                for (int b = 0; b < 2; ++b)
+                    acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wv, __builtin_bit_cast(bf16x8, x[i][b]),
+                                                                        acc[a][b], 0, 0, 0);
+            }
+        }
+    };
+    if (k0 < k1) load(wa, xa, k0);
+    for (int c0 = k0; c0 < k1; c0 += 2 * CH) {
+        if (c0 + CH < k1) load(wb, xb, c0 + CH);
+        compute(wa, xa, c0);
+        if (c0 + 2 * CH < k1) load(wa, xa, c0 + 2 * CH);
+        if (c0 + CH < k1) compute(wb, xb, c0 + CH);
+    }
+
+    const QkvStage qs{};  // q/k/v inputs straight from the call's tables
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+        if (nt0 + a >= stripes) continue;
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+            const int m = (mt0 + b) * 32 + (lane & 31);
+            if (m >= ga.M) continue;
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+                const int n = (j >> 2) * 8 + (lane >> 5) * 4 + (j & 3);
+                epilogue_elem<EPI>(acc[a][b][j], acc[a][b][j ^ 8], m, (nt0 + a) * 32 + n, s, ga, ea, qs);
+            }
+        }
+    }
+}
+
+// Launch shape for M > kMaxRows rows (k_gemm_mn): K split only for the
+// split-K partial epilogue, until the grid covers the chip.
+GemmShape gemm_shape_mn(int N, int K, int M, int epi) {
+    const int tiles = ((N / 32 + 3) / 4) * ((M + 127) / 128);
+    const int KS = K / 16;
+    int S = 1;
+    if (epi == EPI_PARTIAL)
+        while (tiles * S < 256 && KS / (S * 2) >= 32) S *= 2;
+    return GemmShape{N, K, S, 4, 4};
 }
 
 GemmShape gemm_shape(int N, int K, int epi) {
@@ -293,13 +392,29 @@ static hipError_t launch_epi(const GemmArgs& ga, const EpiArgs& ea, int ns, hipS
     }
 }
 
+template <int EPI>
+static hipError_t launch_mn(const GemmArgs& ga, const EpiArgs& ea, hipStream_t st) {
+    dim3 grid((ga.N / 32 + 3) / 4, (ga.M + 127) / 128, ga.S);
+    k_gemm_mn<EPI><<<grid, 256, 0, st>>>(ga, ea);
+    return hipGetLastError();
+}
+
 hipError_t launch_gemm(int epi, const uint16_t* X, const uint16_t* Wp, int M, GemmShape g, float* part,
                        const EpiArgs& ea, hipStream_t st) {
     if (M <= 0) return hipSuccess;
-    if (M > kMaxRows || g.K % 16 || g.KW < 1 || g.KW > kMaxKw || (g.NS != 1 && g.NS != 2) || g.N % (32 * g.NS))
-        return hipErrorInvalidValue;
-    if (epi == EPI_QKV && (g.KW < 4 || g.NS != 1)) return hipErrorInvalidValue;  // epilogue staging: >= 256 threads
+    if (g.K % 16 || g.N % 32 || g.S < 1) return hipErrorInvalidValue;
     GemmArgs ga{X, Wp, M, g.N, g.K, g.S, g.KW, part};
+    if (M > kMaxRows) {  // prefill chunks: the compute-bound tile kernel (shape from gemm_shape_mn)
+        if (M > kMaxPrefillRows || g.NS != 4) return hipErrorInvalidValue;
+        switch (epi) {
+            case EPI_QKV: return launch_mn<EPI_QKV>(ga, ea, st);
+            case EPI_SWIGLU: return launch_mn<EPI_SWIGLU>(ga, ea, st);
+            case EPI_PARTIAL: return launch_mn<EPI_PARTIAL>(ga, ea, st);
+            default: return launch_mn<EPI_STORE>(ga, ea, st);
+        }
+    }
+    if (g.KW < 1 || g.KW > kMaxKw || (g.NS != 1 && g.NS != 2) || g.N % (32 * g.NS)) return hipErrorInvalidValue;
+    if (epi == EPI_QKV && (g.KW < 4 || g.NS != 1)) return hipErrorInvalidValue;  // epilogue staging: >= 256 threads
     switch (epi) {
         case EPI_QKV: return launch_epi<EPI_QKV>(ga, ea, g.NS, st);
         case EPI_SWIGLU: return launch_epi<EPI_SWIGLU>(ga, ea, g.NS, st);

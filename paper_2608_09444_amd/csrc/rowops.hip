@@ -511,6 +511,56 @@ hipError_t launch_scatter_ids(int M, const int32_t* ids, const int32_t* seq, con
     return hipGetLastError();
 }
 
+__global__ __launch_bounds__(256) void k_prefill_rows(int seq, int pos0, int M, int32_t* __restrict__ rows) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= M) return;
+    rows[i] = i;
+    rows[M + i] = seq;
+    rows[2 * M + i] = pos0 + i;
+}
+
+hipError_t launch_prefill_rows(int seq, int pos0, int M, int32_t* rows, hipStream_t st) {
+    if (M <= 0) return hipSuccess;
+    k_prefill_rows<<<(M + 255) / 256, 256, 0, st>>>(seq, pos0, M, rows);
+    return hipGetLastError();
+}
+
+__global__ __launch_bounds__(256) void k_kv_pages(KvTarget kt, int M, const int32_t* __restrict__ seq,
+                                                  const int32_t* __restrict__ pos, int32_t* __restrict__ kvpid,
+                                                  int* err) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < M) write_page(kt, i, seq[i], pos[i], nullptr, kvpid, err);
+}
+
+hipError_t launch_kv_pages(const KvTarget& kt, const cdb_rows& r, int32_t* kvpid, int* err, hipStream_t st) {
+    if (r.n_rows <= 0) return hipSuccess;
+    k_kv_pages<<<(r.n_rows + 255) / 256, 256, 0, st>>>(kt, r.n_rows, r.seq, r.pos, kvpid, err);
+    return hipGetLastError();
+}
+
+// xcat[m] = bf16([h[m]; e[m]]) in fragment layout with K = 2d
+__global__ __launch_bounds__(256) void k_concat_frag(int d, const float* __restrict__ h, const float* __restrict__ e,
+                                                     uint16_t* __restrict__ xcat) {
+    const int m = blockIdx.x;
+    for (int k = threadIdx.x * 4; k < d; k += 1024) {
+        const float4 a = *reinterpret_cast<const float4*>(h + (size_t)m * d + k);
+        const float4 b = *reinterpret_cast<const float4*>(e + (size_t)m * d + k);
+        uint2 pa, pb;
+        pa.x = (uint32_t)f2bf(a.x) | ((uint32_t)f2bf(a.y) << 16);
+        pa.y = (uint32_t)f2bf(a.z) | ((uint32_t)f2bf(a.w) << 16);
+        pb.x = (uint32_t)f2bf(b.x) | ((uint32_t)f2bf(b.y) << 16);
+        pb.y = (uint32_t)f2bf(b.z) | ((uint32_t)f2bf(b.w) << 16);
+        *reinterpret_cast<uint2*>(xcat + frag_index(m, k, 2 * d)) = pa;
+        *reinterpret_cast<uint2*>(xcat + frag_index(m, d + k, 2 * d)) = pb;
+    }
+}
+
+hipError_t launch_concat_frag(int M, int d, const float* h, const float* e, uint16_t* xcat, hipStream_t st) {
+    if (M <= 0) return hipSuccess;
+    k_concat_frag<<<M, 256, 0, st>>>(d, h, e, xcat);
+    return hipGetLastError();
+}
+
 hipError_t launch_argmax(int M, int V, const float* logits, int32_t* ids, hipStream_t st) {
     if (M <= 0) return hipSuccess;
     k_argmax<<<M, 256, 0, st>>>(V, logits, ids);

@@ -22,7 +22,7 @@ def declared_functions(header):
 
 def test_library_exports_every_declared_symbol():
     names = declared_functions("libcdb.h")
-    assert len(names) == 12
+    assert len(names) == 13
     assert set(names) == set(cdb.EXPORTED)
     dnames = declared_functions("libcdb_driver.h")
     assert len(dnames) == 13
@@ -42,7 +42,8 @@ def test_layout_sizes(shape):
     assert 2 * params <= nb <= 2 * params + 256 * (4 * shape.n_layers + 8)
     ws = cdb.cdb_workspace_bytes(desc, 64)
     assert ws > 64 * shape.d * 4 * 3
-    assert cdb.cdb_workspace_bytes(desc, cdb.MAX_ROWS + 1) == 0
+    assert cdb.cdb_workspace_bytes(desc, cdb.MAX_PREFILL_ROWS) > cdb.cdb_workspace_bytes(desc, cdb.MAX_ROWS)
+    assert cdb.cdb_workspace_bytes(desc, cdb.MAX_PREFILL_ROWS + 1) == 0
 
 
 def test_unsupported_shapes_are_rejected():
