@@ -226,6 +226,50 @@ def e2e_decode(shape, dm, kv, n_seqs, prompt, n_decode, seed=3):
     return res
 
 
+def prefill_leg(shape, dm, kv, chunk=512, reps=5):
+    """Chunked prefill at full width: one chunk of `chunk` prompt tokens of one
+    sequence (positions 0..chunk-1) through cdb_prefill, timed with events on
+    the stream it runs on.  FLOPs: every projection (2 per weight and row) of
+    r_max core loops plus the LM head, and causal attention (4 * d per
+    query-key pair per core layer and loop)."""
+    import numpy as np
+    import torch
+
+    import cdbgen
+    import paper_2608_09444_amd as cdb
+    R = shape.r_max
+    max_pages = kv.c.max_pages
+    pages = cdbgen.pages_for(chunk)
+    pt = np.full((kv.c.max_seqs, R + 2, max_pages), -1, np.int32)
+    pt[0, 1:R + 1, :pages] = np.arange(pages * R, dtype=np.int32).reshape(R, pages)
+    kv.page_table.copy_(torch.from_numpy(pt))
+    ws = cdb.Workspace(dm.desc, chunk)
+    tok = torch.as_tensor(cdbgen.prompt_ids(shape.vocab, 1, chunk, seed=9)[0], dtype=torch.int32, device="cuda")
+    logits = torch.empty((chunk, shape.vocab), dtype=torch.float32, device="cuda")
+    ids = torch.empty(chunk, dtype=torch.int32, device="cuda")
+    st = torch.cuda.current_stream()
+    cdb.cdb_prefill(dm.model, kv.c, 0, 0, tok, logits, ids, ws.buf)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(st)
+    for _ in range(reps):
+        cdb.cdb_prefill(dm.model, kv.c, 0, 0, tok, logits, ids, ws.buf)
+    e1.record(st)
+    e1.synchronize()
+    if cdb.cdb_read_device_error(ws.buf) != 0:
+        raise RuntimeError("device error in prefill")
+    ms = e0.elapsed_time(e1) / reps
+    pc = cdbgen.param_counts(shape)
+    proj = 2.0 * chunk * (R * pc["core"] + pc["boundary_layers"] + shape.d * shape.vocab)
+    attn = 4.0 * shape.d * shape.n_core * R * chunk * (chunk + 1) / 2
+    tflops = (proj + attn) / (ms * 1e-3) / 1e12
+    log(f"prefill: {chunk} tokens in {ms:.2f} ms, {tflops:.0f} TFLOP/s")
+    return {"workload": f"one {chunk}-token prompt chunk (positions 0..{chunk - 1}), all r_max loops, coda, LM head",
+            "tokens_per_s": round(chunk / (ms * 1e-3), 1), "ms_per_chunk": round(ms, 3),
+            "flops": proj + attn, "achieved_tflops": round(tflops, 1), "peak_tflops": BF16_PEAK_TFLOPS,
+            "mfma_frac": round(tflops / BF16_PEAK_TFLOPS, 4)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -233,6 +277,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--cpu-sample", type=int, default=16, help="rows in the CPU-oracle sample (0 = skip)")
     ap.add_argument("--no-e2e", action="store_true", help="skip the whole-decode driver runs")
+    ap.add_argument("--no-prefill", action="store_true", help="skip the chunked-prefill timing")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="run one plain device copy of this many MiB first (a known-size reference for HBM counters)")
     args = ap.parse_args()
@@ -294,6 +339,10 @@ def main():
     if not args.no_e2e:
         e2e = e2e_decode(shape, dm, kv, n_rows, pos_lo, pos_hi + 1 - pos_lo)
 
+    prefill = None
+    if not args.no_prefill:
+        prefill = prefill_leg(shape, dm, kv)
+
     cpu = None
     if args.cpu_sample > 0:
         threads = min(16, os.cpu_count() or 1)
@@ -329,6 +378,7 @@ def main():
                           "flops": step_flops(shape, rows_np)},
         "cpu_baseline": cpu,
         "e2e": e2e,
+        "prefill": prefill,
     }
     print(json.dumps(res), flush=True)
 
