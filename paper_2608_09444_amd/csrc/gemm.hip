@@ -239,6 +239,70 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs ga, EpiArgs ea) {
     }
 }
 
+// q/k/v epilogue of a wave's 2 x 2 accumulator tiles.  Every input the stores
+// need (each row's write page and slot, the RoPE factors of the lane's 8
+// rotary pairs per stripe and m-tile) is loaded before the first store.
+// Lane l holds column n = (j/4)*8 + (l/32)*4 + j%4 of a stripe in element j:
+// rotary pair jj = n % 16, first half for j < 8, its partner in element j + 8.
+__device__ __forceinline__ void qkv_tile_epilogue(const floatx16 (&acc)[2][2], int nt0, int mt0, int lane,
+                                                  int stripes, int M, const EpiArgs& ea) {
+    const int gph = ea.hd >> 5, hg = ea.H * gph, half_hd = ea.hd >> 1;
+    int m[2], pid[2], tok[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        m[b] = (mt0 + b) * 32 + (lane & 31);
+        const bool ok = m[b] < M;
+        pid[b] = ok ? ea.kvpid[m[b]] : -1;
+        tok[b] = ok ? ea.pos[m[b]] % kPage : 0;
+    }
+    float2 cs[2][2][8];
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+        const int g = min(nt0 + a, stripes - 1);
+        const int part = g / hg, gi = (g - part * hg) % gph;
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int jj = (j >> 2) * 8 + (lane >> 5) * 4 + (j & 3);
+                cs[a][b][j] = (part < 2 && m[b] < M) ? ea.rope[(size_t)m[b] * half_hd + gi * 16 + jj]
+                                                     : make_float2(1.f, 0.f);
+            }
+    }
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+        const int g = nt0 + a;
+        if (g >= stripes) continue;
+        const int part = g / hg, rem = g - part * hg;
+        const int head = rem / gph, gi = rem - head * gph;
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+            if (m[b] >= M) continue;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int jj = (j >> 2) * 8 + (lane >> 5) * 4 + (j & 3);
+                const float x1 = acc[a][b][j], x2 = acc[a][b][j + 8];  // dims jj and jj + hd/2 of the pair
+                float y1 = x1, y2 = x2;
+                if (part < 2) {
+                    y1 = x1 * cs[a][b][j].x - x2 * cs[a][b][j].y;
+                    y2 = x2 * cs[a][b][j].x + x1 * cs[a][b][j].y;
+                }
+                const int d1 = gi * 16 + jj, d2 = d1 + half_hd;
+                if (part == 0) {
+                    float* qrow = ea.q + (size_t)m[b] * (ea.H * ea.hd) + head * ea.hd;
+                    qrow[d1] = y1;
+                    qrow[d2] = y2;
+                } else if (pid[b] >= 0) {
+                    uint16_t* dst = ea.kv.pool + kv_offset(ea.kv.layer, pid[b], ea.kv.n_pages, part - 1, head, ea.H,
+                                                           tok[b], ea.hd);
+                    dst[d1] = f2bf(y1);
+                    dst[d2] = f2bf(y2);
+                }
+            }
+        }
+    }
+}
+
 // Large-M GEMM (prefill chunks of up to 512 rows), where the product is
 // compute-bound (about M FLOP per weight byte).  A workgroup owns a 128-row x
 // 128-column output tile and one K split: 4 waves in 2 x 2, each 64 rows x 64
@@ -310,7 +374,11 @@ __global__ __launch_bounds__(256) void k_gemm_mn(GemmArgs ga, EpiArgs ea) {
         if (c0 + CH < k1) compute(wb, xb, c0 + CH);
     }
 
-    const QkvStage qs{};  // q/k/v inputs straight from the call's tables
+    if constexpr (EPI == EPI_QKV) {
+        qkv_tile_epilogue(acc, nt0, mt0, lane, stripes, ga.M, ea);
+        return;
+    }
+    const QkvStage qs{};
 #pragma unroll
     for (int a = 0; a < 2; ++a) {
         if (nt0 + a >= stripes) continue;
