@@ -82,6 +82,108 @@ __device__ __forceinline__ void epilogue_elem(float val, float partner, int m, i
     }
 }
 
+// Epilogue of the skinny kernel from the reduced tiles fin[ns][n][m] (row
+// pitch fld), with 16-byte stores: each thread takes a run of consecutive
+// output columns of one row (4 fp32 values, or 8 bf16 values in the
+// fragment or K/V layouts).  Same arithmetic per element as epilogue_elem.
+template <int EPI>
+__device__ __forceinline__ void stripe_epilogue(const float* fin, int fld, int nt, int NS, int mcap, int split, int tid,
+                                                int nthr, const GemmArgs& ga, const EpiArgs& ea, const QkvStage& qs) {
+    if (EPI == EPI_PARTIAL || EPI == EPI_STORE) {
+        // (ns, m, 4-column run)
+        const int per = mcap * 8;
+        float* base = EPI == EPI_PARTIAL ? ga.part + (size_t)split * ga.M * ga.N : ea.out;
+        const int ld = EPI == EPI_PARTIAL ? ga.N : ea.ld_out;
+        for (int e = tid; e < NS * per; e += nthr) {
+            const int ns = e / per, r = e - ns * per;
+            const int m = r >> 3, c4 = (r & 7) * 4;
+            const float* f = fin + ns * 32 * fld + c4 * fld + m;
+            const float4 v = make_float4(f[0], f[fld], f[2 * fld], f[3 * fld]);
+            float* dst = base + (size_t)m * ld + (nt + ns) * 32 + c4;
+            if ((ld & 3) == 0) {
+                *reinterpret_cast<float4*>(dst) = v;
+            } else {
+                dst[0] = v.x;
+                dst[1] = v.y;
+                dst[2] = v.z;
+                dst[3] = v.w;
+            }
+        }
+    } else if (EPI == EPI_SWIGLU) {
+        // (ns, m, 8-feature run): gate columns c8 .. c8 + 7, up columns 16 + c8 ..
+        const int per = mcap * 2;
+        for (int e = tid; e < NS * per; e += nthr) {
+            const int ns = e / per, r = e - ns * per;
+            const int m = r >> 1, c8 = (r & 1) * 8;
+            const float* f = fin + ns * 32 * fld + m;
+            uint32_t w[4];
+#pragma unroll
+            for (int i = 0; i < 8; i += 2) {
+                const float g0 = f[(c8 + i) * fld], u0 = f[(16 + c8 + i) * fld];
+                const float g1 = f[(c8 + i + 1) * fld], u1 = f[(16 + c8 + i + 1) * fld];
+                const float s0 = g0 / (1.0f + __expf(-g0)), s1 = g1 / (1.0f + __expf(-g1));
+                w[i / 2] = (uint32_t)f2bf(s0 * u0) | ((uint32_t)f2bf(s1 * u1) << 16);
+            }
+            const int feat = (nt + ns) * 16 + c8;
+            *reinterpret_cast<u32x4*>(ea.act + frag_index(m, feat, ea.ld_act)) = u32x4{w[0], w[1], w[2], w[3]};
+        }
+    } else {  // EPI_QKV, one stripe: 16 rotary pairs (dims gi*16 + jj and + hd/2) of one head
+        const int g = nt, gph = ea.hd >> 5, hg = ea.H * gph;
+        const int part = g / hg, rem = g - part * hg;
+        const int head = rem / gph, gi = rem - head * gph;
+        const int half_hd = ea.hd >> 1;
+        if (part == 0) {
+            // (m, half, 4-pair run) -> 4 consecutive fp32 q values
+            for (int e = tid; e < mcap * 8; e += nthr) {
+                const int m = e >> 3, half = (e >> 2) & 1, j4 = (e & 3) * 4;
+                float o[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int jj = j4 + i;
+                    const float val = fin[(half * 16 + jj) * fld + m], partner = fin[((half ^ 1) * 16 + jj) * fld + m];
+                    const float2 cs = qs.rope ? qs.rope[m * 16 + jj] : ea.rope[(size_t)m * half_hd + gi * 16 + jj];
+                    const float xf = half ? partner : val, xs = half ? val : partner;
+                    o[i] = half ? (xs * cs.x + xf * cs.y) : (xf * cs.x - xs * cs.y);
+                }
+                float* dst = ea.q + (size_t)m * (ea.H * ea.hd) + head * ea.hd + gi * 16 + j4 + half * half_hd;
+                *reinterpret_cast<float4*>(dst) = make_float4(o[0], o[1], o[2], o[3]);
+            }
+        } else {
+            // (m, half, 8-pair run) -> 8 consecutive bf16 K or V values
+            for (int e = tid; e < mcap * 4; e += nthr) {
+                const int m = e >> 2, half = (e >> 1) & 1, j8 = (e & 1) * 8;
+                const int pid = qs.rope ? qs.pid[m] : ea.kvpid[m];  // -1: unmapped (reported by the row-entry kernel)
+                if (pid < 0) continue;
+                const int tok = qs.rope ? qs.tok[m] : ea.pos[m] % kPage;
+                uint32_t w[4];
+#pragma unroll
+                for (int i = 0; i < 8; i += 2) {
+                    float o2[2];
+#pragma unroll
+                    for (int b = 0; b < 2; ++b) {
+                        const int jj = j8 + i + b;
+                        const float val = fin[(half * 16 + jj) * fld + m];
+                        float outv = val;
+                        if (part == 1) {
+                            const float partner = fin[((half ^ 1) * 16 + jj) * fld + m];
+                            const float2 cs =
+                                qs.rope ? qs.rope[m * 16 + jj] : ea.rope[(size_t)m * half_hd + gi * 16 + jj];
+                            const float xf = half ? partner : val, xs = half ? val : partner;
+                            outv = half ? (xs * cs.x + xf * cs.y) : (xf * cs.x - xs * cs.y);
+                        }
+                        o2[b] = outv;
+                    }
+                    w[i / 2] = (uint32_t)f2bf(o2[0]) | ((uint32_t)f2bf(o2[1]) << 16);
+                }
+                const KvTarget& kv = ea.kv;
+                uint16_t* dst = kv.pool + kv_offset(kv.layer, pid, kv.n_pages, part - 1, head, ea.H, tok, ea.hd) +
+                                gi * 16 + j8 + half * half_hd;
+                *reinterpret_cast<u32x4*>(dst) = u32x4{w[0], w[1], w[2], w[3]};
+            }
+        }
+    }
+}
+
 // MT = 32-row tiles of M covered by one pass (M <= 32 * MT); NS = adjacent
 // 32-column stripes per workgroup (they share every activation load).
 template <int EPI, int MT, int NS>
@@ -228,15 +330,7 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs ga, EpiArgs ea) {
         }
     }
 
-    // epilogue: element (n, m) of stripe nt + ns; consecutive threads take consecutive n
-    const int E = 32 * mcap;
-    for (int e = tid; e < NS * E; e += nthr) {
-        const int ns = e / E, r = e - ns * E;
-        const int m = r >> 5, nn = r & 31;
-        const int p = (nt + ns) * 32 + nn;
-        const float* f = fin + ns * 32 * fld;
-        epilogue_elem<EPI>(f[nn * fld + m], f[(nn ^ 16) * fld + m], m, p, s, ga, ea, qs);
-    }
+    stripe_epilogue<EPI>(fin, fld, nt, NS, mcap, s, tid, nthr, ga, ea, qs);
 }
 
 // q/k/v epilogue of a wave's 2 x 2 accumulator tiles.  Every input the stores
