@@ -108,34 +108,49 @@ __global__ __launch_bounds__(256) void k_load_state(int d, int n_slots, int hd, 
 
 // ------------------------------------------------------------------ residual + RMSNorm
 // h[i] += sum_s part[s][i] (split order 0..S-1); out[i] = bf16(h[i] / sqrt(mean(h[i]^2) + eps)),
-// unit gains.  Row i is one workgroup.
+// unit gains.  Row i is one workgroup; each thread keeps its NV runs of 4
+// values in registers between the sum and the normalisation, and issues the
+// partial loads of up to 4 splits at once.
+template <int NV>
 __global__ __launch_bounds__(1024) void k_resid_norm(float* __restrict__ h, const float* __restrict__ part, int S, int M,
                                                      int d, float eps, uint16_t* __restrict__ out) {
     __shared__ float red[16];
     const int i = blockIdx.x;
-    const int step = blockDim.x * 4;
     float* x = h + (size_t)i * d;
+    float4 v[NV];
     float ss = 0.f;
-    for (int k = threadIdx.x * 4; k < d; k += step) {
-        float4 v = *reinterpret_cast<const float4*>(x + k);
-        for (int s = 0; s < S; ++s) {
-            const float4 p = *reinterpret_cast<const float4*>(part + ((size_t)s * M + i) * d + k);
-            v.x += p.x;
-            v.y += p.y;
-            v.z += p.z;
-            v.w += p.w;
+#pragma unroll
+    for (int u = 0; u < NV; ++u) {
+        const int k = (threadIdx.x + u * blockDim.x) * 4;
+        if (k >= d) continue;
+        v[u] = *reinterpret_cast<const float4*>(x + k);
+        for (int s0 = 0; s0 < S; s0 += 4) {
+            float4 p[4];
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+                if (s0 + t < S) p[t] = *reinterpret_cast<const float4*>(part + ((size_t)(s0 + t) * M + i) * d + k);
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+                if (s0 + t < S) {
+                    v[u].x += p[t].x;
+                    v[u].y += p[t].y;
+                    v[u].z += p[t].z;
+                    v[u].w += p[t].w;
+                }
         }
-        if (S > 0) *reinterpret_cast<float4*>(x + k) = v;
-        ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+        if (S > 0) *reinterpret_cast<float4*>(x + k) = v[u];
+        ss += v[u].x * v[u].x + v[u].y * v[u].y + v[u].z * v[u].z + v[u].w * v[u].w;
     }
     if (!out) return;
     ss = block_sum(ss, red);
     const float inv = 1.0f / sqrtf(ss / d + eps);
-    for (int k = threadIdx.x * 4; k < d; k += step) {
-        const float4 v = *reinterpret_cast<const float4*>(x + k);
+#pragma unroll
+    for (int u = 0; u < NV; ++u) {
+        const int k = (threadIdx.x + u * blockDim.x) * 4;
+        if (k >= d) continue;
         uint2 pk;
-        pk.x = (uint32_t)f2bf(v.x * inv) | ((uint32_t)f2bf(v.y * inv) << 16);
-        pk.y = (uint32_t)f2bf(v.z * inv) | ((uint32_t)f2bf(v.w * inv) << 16);
+        pk.x = (uint32_t)f2bf(v[u].x * inv) | ((uint32_t)f2bf(v[u].y * inv) << 16);
+        pk.y = (uint32_t)f2bf(v[u].z * inv) | ((uint32_t)f2bf(v[u].w * inv) << 16);
         *reinterpret_cast<uint2*>(out + frag_index(i, k, d)) = pk;  // 4 consecutive k share one 8-slot run
     }
 }
@@ -434,10 +449,17 @@ hipError_t launch_load_state(const cdb_model_desc& md, int M, const int32_t* slo
 hipError_t launch_resid_norm(float* h, const float* part, int S, int M, int d, float eps, uint16_t* out,
                              hipStream_t st) {
     if (M <= 0) return hipSuccess;
-    // one workgroup per row, about 4 elements per thread
+    // one workgroup per row, runs of 4 elements, at most 4 runs per thread
+    if (d % 4 || d > 16384) return hipErrorInvalidValue;
     int threads = 64;
     while (threads < 1024 && threads * 4 < d) threads *= 2;
-    k_resid_norm<<<M, threads, 0, st>>>(h, part, S, M, d, eps, out);
+    const int nv = (d / 4 + threads - 1) / threads;
+    if (nv == 1)
+        k_resid_norm<1><<<M, threads, 0, st>>>(h, part, S, M, d, eps, out);
+    else if (nv == 2)
+        k_resid_norm<2><<<M, threads, 0, st>>>(h, part, S, M, d, eps, out);
+    else
+        k_resid_norm<4><<<M, threads, 0, st>>>(h, part, S, M, d, eps, out);
     return hipGetLastError();
 }
 
