@@ -299,20 +299,29 @@ __global__ __launch_bounds__(256) void k_prefill_attn(const float* __restrict__ 
         if (s_pid[i] < 0) set_err(err, CDB_DEV_UNMAPPED_PAGE);
     }
 
-    // q as B operands: dims 16t + 8*(lane/32) + e, split into hi + lo
+    // q tile (32 rows x HD, fp32) through LDS: coalesced 16-byte loads, then
+    // each lane takes its B-operand dims 16t + 8*(lane/32) + e of row lane%32,
+    // scaled and split into bf16 hi + lo
+    constexpr int QP = HD + 4;  // row pitch (floats)
+    static_assert(32 * QP * 4 <= 4 * SLOT, "q tile fits the staging area");
+    float* sq = reinterpret_cast<float*>(smem);
+    for (int i = tid; i < 32 * (HD / 4); i += 256) {
+        const int r = i / (HD / 4), c4 = i - r * (HD / 4);
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (row0 + r < M) v = *reinterpret_cast<const float4*>(q + (size_t)(row0 + r) * d + head * HD + c4 * 4);
+        *reinterpret_cast<float4*>(sq + r * QP + c4 * 4) = v;
+    }
+    __syncthreads();  // q tile and page ids
     bf16x8 qh[HD / 16], ql[HD / 16];
 #pragma unroll
     for (int t = 0; t < HD / 16; ++t) {
-        const int d0 = t * 16 + (lane >> 5) * 8;
-        const float* src = q + (size_t)qrow * d + head * HD + d0;
+        const float* src = sq + (lane & 31) * QP + t * 16 + (lane >> 5) * 8;
+        const float4 a = *reinterpret_cast<const float4*>(src), b = *reinterpret_cast<const float4*>(src + 4);
+        const float x[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
         uint32_t hw[4], lw[4];
 #pragma unroll
         for (int e = 0; e < 8; e += 2) {
-            float x0 = 0.f, x1 = 0.f;
-            if (qvalid) {
-                x0 = src[e] * qscale;
-                x1 = src[e + 1] * qscale;
-            }
+            const float x0 = x[e] * qscale, x1 = x[e + 1] * qscale;
             const uint16_t h0 = f2bf(x0), h1 = f2bf(x1);
             const uint16_t l0 = f2bf(x0 - bf2f(h0)), l1 = f2bf(x1 - bf2f(h1));
             hw[e / 2] = (uint32_t)h0 | ((uint32_t)h1 << 16);
@@ -330,32 +339,46 @@ __global__ __launch_bounds__(256) void k_prefill_attn(const float* __restrict__ 
     float m_run = -1e30f, l_run = 0.f;
     uint16_t* sK = reinterpret_cast<uint16_t*>(smem + wave * SLOT);
     uint16_t* sVt = reinterpret_cast<uint16_t*>(smem + wave * SLOT + KBYTES);
-    __syncthreads();  // page ids
+    __syncthreads();  // the q tile is read before the staging area is reused
 
     for (int sb = 0; sb <= last; sb += 4 * KB) {
-        // stage keys sb .. sb + 127: block w in slot w
-        for (int p = tid; p < PIECES; p += 256) {
-            const int blk = p / (2 * KB * (HD / 8));
-            const int r0 = p - blk * 2 * KB * (HD / 8);
-            const int which = r0 / (KB * (HD / 8));
-            const int r = r0 - which * KB * (HD / 8);
-            const int key = r / (HD / 8), c8 = r - key * (HD / 8);
-            const int kp = sb + blk * KB + key;
-            u32x4 v = u32x4{0u, 0u, 0u, 0u};
-            if (kp <= last) {
-                const int pid = s_pid[kp / kPage];
-                if (pid >= 0)
-                    v = *reinterpret_cast<const u32x4*>(
-                        kv.pool + kv_offset(kv.layer, pid, kv.n_pages, which, head, H, kp % kPage, HD) + c8 * 8);
-            }
-            unsigned char* slot = smem + blk * SLOT;
-            if (which == 0) {
-                *reinterpret_cast<u32x4*>(slot + (key * LD + c8 * 8) * 2) = v;
-            } else {
-                uint16_t* vt = reinterpret_cast<uint16_t*>(slot + KBYTES);
-                const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+        // stage keys sb .. sb + 127: block w in slot w; loads in batches of 4
+        // per thread, issued before their LDS writes
+        constexpr int PPT = PIECES / 256, SB = 4;
+        static_assert(PPT % SB == 0, "staging batches");
 #pragma unroll
-                for (int e = 0; e < 8; ++e) vt[(c8 * 8 + e) * LV + key] = (uint16_t)(w[e >> 1] >> ((e & 1) * 16));
+        for (int b0 = 0; b0 < PPT; b0 += SB) {
+            u32x4 v[SB];
+            int slot_off[SB], which_k[SB];
+#pragma unroll
+            for (int i = 0; i < SB; ++i) {
+                const int p = tid + (b0 + i) * 256;
+                const int blk = p / (2 * KB * (HD / 8));
+                const int r0 = p - blk * 2 * KB * (HD / 8);
+                const int which = r0 / (KB * (HD / 8));
+                const int r = r0 - which * KB * (HD / 8);
+                const int key = r / (HD / 8), c8 = r - key * (HD / 8);
+                const int kp = sb + blk * KB + key;
+                v[i] = u32x4{0u, 0u, 0u, 0u};
+                if (kp <= last) {
+                    const int pid = s_pid[kp / kPage];
+                    if (pid >= 0)
+                        v[i] = *reinterpret_cast<const u32x4*>(
+                            kv.pool + kv_offset(kv.layer, pid, kv.n_pages, which, head, H, kp % kPage, HD) + c8 * 8);
+                }
+                slot_off[i] = blk * SLOT + (which == 0 ? (key * LD + c8 * 8) * 2 : KBYTES + (c8 * 8 * LV + key) * 2);
+                which_k[i] = which;
+            }
+#pragma unroll
+            for (int i = 0; i < SB; ++i) {
+                if (which_k[i] == 0) {
+                    *reinterpret_cast<u32x4*>(smem + slot_off[i]) = v[i];
+                } else {
+                    uint16_t* vt = reinterpret_cast<uint16_t*>(smem + slot_off[i]);
+                    const uint32_t w[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) vt[e * LV] = (uint16_t)(w[e >> 1] >> ((e & 1) * 16));
+                }
             }
         }
         __syncthreads();
@@ -460,21 +483,33 @@ __global__ __launch_bounds__(256) void k_prefill_attn(const float* __restrict__ 
         sL[wave * 32 + lane] = l_run;
     }
     __syncthreads();
-    for (int e = tid; e < HD * 32; e += 256) {
-        const int dim = e >> 5, qq = e & 31;
+    // (row, 8-dim run) per item: one 16-byte store in the fragment layout
+    for (int e = tid; e < 32 * (HD / 8); e += 256) {
+        const int qq = e & 31, c8 = e >> 5;
         const int row = row0 + qq;
         if (row >= M) continue;
         float mx = -1e30f;
 #pragma unroll
         for (int w = 0; w < 4; ++w) mx = fmaxf(mx, sM[w * 32 + qq]);
-        float num = 0.f, den = 0.f;
+        float f[4], den = 0.f;
 #pragma unroll
         for (int w = 0; w < 4; ++w) {
-            const float f = exp2f(sM[w * 32 + qq] - mx);
-            num += f * sO[(w * HD + dim) * 32 + qq];
-            den += f * sL[w * 32 + qq];
+            f[w] = exp2f(sM[w * 32 + qq] - mx);
+            den += f[w] * sL[w * 32 + qq];
         }
-        out[frag_index(row, head * HD + dim, d)] = f2bf(den > 0.f ? num / den : 0.f);
+        uint32_t pk[4];
+#pragma unroll
+        for (int i = 0; i < 8; i += 2) {
+            float num[2] = {0.f, 0.f};
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+                num[0] += f[w] * sO[(w * HD + c8 * 8 + i) * 32 + qq];
+                num[1] += f[w] * sO[(w * HD + c8 * 8 + i + 1) * 32 + qq];
+            }
+            pk[i / 2] = (uint32_t)f2bf(den > 0.f ? num[0] / den : 0.f) |
+                        ((uint32_t)f2bf(den > 0.f ? num[1] / den : 0.f) << 16);
+        }
+        *reinterpret_cast<u32x4*>(out + frag_index(row, head * HD + c8 * 8, d)) = u32x4{pk[0], pk[1], pk[2], pk[3]};
     }
 }
 
