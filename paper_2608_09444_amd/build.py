@@ -10,7 +10,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libcdb.so")
 BUILD = os.path.join(HERE, "_build")
-SOURCES = ["gemm.hip", "attention.hip", "rowops.hip", "api.hip", "driver.cpp"]
+SOURCES = ["gemm.hip", "attention.hip", "prefill_attention.hip", "rowops.hip", "api.hip", "driver.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
          # packed fp32 instructions stay off: the compiler may not form them
