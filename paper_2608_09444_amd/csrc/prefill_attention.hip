@@ -5,36 +5,146 @@
 
 namespace cdb {
 
+// LDS reads written as inline assembly: the compiler cannot tell which LDS
+// bytes the direct global->LDS loads in flight will write, and would make
+// every compiler-visible LDS read wait for all of them.  Each helper issues a
+// group of reads and waits for them in the same statement, so its outputs
+// hold the data when the statement ends.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+// N 16-byte reads, v[i] from byte address a[i]
+template <int N>
+__device__ __forceinline__ void lds_read_b128xN(u32x4 (&v)[N], const uint32_t (&a)[N]) {
+    static_assert(N == 2 || N == 4 || N == 6 || N == 8, "read group size");
+    if constexpr (N == 2) {
+        asm volatile("ds_read_b128 %0, %2\n ds_read_b128 %1, %3\n s_waitcnt lgkmcnt(0)"
+                     : "=&v"(v[0]), "=&v"(v[1]) : "v"(a[0]), "v"(a[1]) : "memory");
+    } else if constexpr (N == 4) {
+        asm volatile("ds_read_b128 %0, %4\n ds_read_b128 %1, %5\n ds_read_b128 %2, %6\n ds_read_b128 %3, %7\n"
+                     " s_waitcnt lgkmcnt(0)"
+                     : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3])
+                     : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]) : "memory");
+    } else if constexpr (N == 6) {
+        asm volatile("ds_read_b128 %0, %6\n ds_read_b128 %1, %7\n ds_read_b128 %2, %8\n ds_read_b128 %3, %9\n"
+                     " ds_read_b128 %4, %10\n ds_read_b128 %5, %11\n s_waitcnt lgkmcnt(0)"
+                     : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3]), "=&v"(v[4]), "=&v"(v[5])
+                     : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(a[4]), "v"(a[5]) : "memory");
+    } else {
+        asm volatile("ds_read_b128 %0, %8\n ds_read_b128 %1, %9\n ds_read_b128 %2, %10\n ds_read_b128 %3, %11\n"
+                     " ds_read_b128 %4, %12\n ds_read_b128 %5, %13\n ds_read_b128 %6, %14\n ds_read_b128 %7, %15\n"
+                     " s_waitcnt lgkmcnt(0)"
+                     : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3]), "=&v"(v[4]), "=&v"(v[5]), "=&v"(v[6]), "=&v"(v[7])
+                     : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(a[4]), "v"(a[5]), "v"(a[6]), "v"(a[7])
+                     : "memory");
+    }
+}
+// V^T operands of NB 32-dim blocks: r[8b + e] gets the bf16 value at byte
+// address a[e] + 64b (zero-extended; 16-bit loads into half registers do not
+// keep the other half here), where a[e] is the lane's column in key row e.
+template <int NB>
+__device__ __forceinline__ void lds_read_vcols(uint32_t (&r)[32], const uint32_t (&a)[8]) {
+    static_assert(NB >= 2 && NB <= 4, "32-dim blocks");
+    // outputs are operands 0 .. 8NB-1, the 8 addresses follow
+    if constexpr (NB == 2) {
+        asm volatile("ds_read_u16 %0, %16 offset:0\n" "ds_read_u16 %1, %17 offset:0\n"
+                     "ds_read_u16 %2, %18 offset:0\n" "ds_read_u16 %3, %19 offset:0\n"
+                     "ds_read_u16 %4, %20 offset:0\n" "ds_read_u16 %5, %21 offset:0\n"
+                     "ds_read_u16 %6, %22 offset:0\n" "ds_read_u16 %7, %23 offset:0\n"
+                     "ds_read_u16 %8, %16 offset:64\n" "ds_read_u16 %9, %17 offset:64\n"
+                     "ds_read_u16 %10, %18 offset:64\n" "ds_read_u16 %11, %19 offset:64\n"
+                     "ds_read_u16 %12, %20 offset:64\n" "ds_read_u16 %13, %21 offset:64\n"
+                     "ds_read_u16 %14, %22 offset:64\n" "ds_read_u16 %15, %23 offset:64\n"
+                     " s_waitcnt lgkmcnt(0)"
+                     : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5]), "=&v"(r[6]),
+                       "=&v"(r[7]), "=&v"(r[8]), "=&v"(r[9]), "=&v"(r[10]), "=&v"(r[11]), "=&v"(r[12]),
+                       "=&v"(r[13]), "=&v"(r[14]), "=&v"(r[15])
+                     : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(a[4]), "v"(a[5]), "v"(a[6]), "v"(a[7])
+                     : "memory");
+    } else if constexpr (NB == 3) {
+        asm volatile("ds_read_u16 %0, %24 offset:0\n" "ds_read_u16 %1, %25 offset:0\n"
+                     "ds_read_u16 %2, %26 offset:0\n" "ds_read_u16 %3, %27 offset:0\n"
+                     "ds_read_u16 %4, %28 offset:0\n" "ds_read_u16 %5, %29 offset:0\n"
+                     "ds_read_u16 %6, %30 offset:0\n" "ds_read_u16 %7, %31 offset:0\n"
+                     "ds_read_u16 %8, %24 offset:64\n" "ds_read_u16 %9, %25 offset:64\n"
+                     "ds_read_u16 %10, %26 offset:64\n" "ds_read_u16 %11, %27 offset:64\n"
+                     "ds_read_u16 %12, %28 offset:64\n" "ds_read_u16 %13, %29 offset:64\n"
+                     "ds_read_u16 %14, %30 offset:64\n" "ds_read_u16 %15, %31 offset:64\n"
+                     "ds_read_u16 %16, %24 offset:128\n" "ds_read_u16 %17, %25 offset:128\n"
+                     "ds_read_u16 %18, %26 offset:128\n" "ds_read_u16 %19, %27 offset:128\n"
+                     "ds_read_u16 %20, %28 offset:128\n" "ds_read_u16 %21, %29 offset:128\n"
+                     "ds_read_u16 %22, %30 offset:128\n" "ds_read_u16 %23, %31 offset:128\n"
+                     " s_waitcnt lgkmcnt(0)"
+                     : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5]), "=&v"(r[6]),
+                       "=&v"(r[7]), "=&v"(r[8]), "=&v"(r[9]), "=&v"(r[10]), "=&v"(r[11]), "=&v"(r[12]),
+                       "=&v"(r[13]), "=&v"(r[14]), "=&v"(r[15]), "=&v"(r[16]), "=&v"(r[17]), "=&v"(r[18]),
+                       "=&v"(r[19]), "=&v"(r[20]), "=&v"(r[21]), "=&v"(r[22]), "=&v"(r[23])
+                     : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(a[4]), "v"(a[5]), "v"(a[6]), "v"(a[7])
+                     : "memory");
+    } else {
+        asm volatile("ds_read_u16 %0, %32 offset:0\n" "ds_read_u16 %1, %33 offset:0\n"
+                     "ds_read_u16 %2, %34 offset:0\n" "ds_read_u16 %3, %35 offset:0\n"
+                     "ds_read_u16 %4, %36 offset:0\n" "ds_read_u16 %5, %37 offset:0\n"
+                     "ds_read_u16 %6, %38 offset:0\n" "ds_read_u16 %7, %39 offset:0\n"
+                     "ds_read_u16 %8, %32 offset:64\n" "ds_read_u16 %9, %33 offset:64\n"
+                     "ds_read_u16 %10, %34 offset:64\n" "ds_read_u16 %11, %35 offset:64\n"
+                     "ds_read_u16 %12, %36 offset:64\n" "ds_read_u16 %13, %37 offset:64\n"
+                     "ds_read_u16 %14, %38 offset:64\n" "ds_read_u16 %15, %39 offset:64\n"
+                     "ds_read_u16 %16, %32 offset:128\n" "ds_read_u16 %17, %33 offset:128\n"
+                     "ds_read_u16 %18, %34 offset:128\n" "ds_read_u16 %19, %35 offset:128\n"
+                     "ds_read_u16 %20, %36 offset:128\n" "ds_read_u16 %21, %37 offset:128\n"
+                     "ds_read_u16 %22, %38 offset:128\n" "ds_read_u16 %23, %39 offset:128\n"
+                     "ds_read_u16 %24, %32 offset:192\n" "ds_read_u16 %25, %33 offset:192\n"
+                     "ds_read_u16 %26, %34 offset:192\n" "ds_read_u16 %27, %35 offset:192\n"
+                     "ds_read_u16 %28, %36 offset:192\n" "ds_read_u16 %29, %37 offset:192\n"
+                     "ds_read_u16 %30, %38 offset:192\n" "ds_read_u16 %31, %39 offset:192\n"
+                     " s_waitcnt lgkmcnt(0)"
+                     : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5]), "=&v"(r[6]),
+                       "=&v"(r[7]), "=&v"(r[8]), "=&v"(r[9]), "=&v"(r[10]), "=&v"(r[11]), "=&v"(r[12]),
+                       "=&v"(r[13]), "=&v"(r[14]), "=&v"(r[15]), "=&v"(r[16]), "=&v"(r[17]), "=&v"(r[18]),
+                       "=&v"(r[19]), "=&v"(r[20]), "=&v"(r[21]), "=&v"(r[22]), "=&v"(r[23]), "=&v"(r[24]),
+                       "=&v"(r[25]), "=&v"(r[26]), "=&v"(r[27]), "=&v"(r[28]), "=&v"(r[29]), "=&v"(r[30]),
+                       "=&v"(r[31])
+                     : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(a[4]), "v"(a[5]), "v"(a[6]), "v"(a[7])
+                     : "memory");
+    }
+}
+
 // Causal attention of a prefill chunk: rows 0..M-1 are positions pos0..pos0+M-1
 // of one sequence; row i attends to positions 0..pos0+i of its plane.  A dense
 // contraction, so it runs on MFMA (v_mfma_f32_32x32x16_bf16).
 //
-// Workgroup = (head, 32 rows), 4 waves splitting the keys: the workgroup
-// stages 4 blocks of 32 keys at a time in LDS (K rows as stored, V transposed
-// to dims x keys so both operands read as 16-byte vectors) and wave w takes
-// block w.  Each wave keeps an online softmax state for the 32 rows; the four
-// states are merged through LDS at the end.  Per wave and block:
+// Workgroup = (head, 32 rows), 4 waves splitting the keys in blocks of 32
+// (wave w takes blocks w, w + 4, ...).  Each wave streams its blocks from HBM
+// straight into a private double buffer in LDS with direct loads (K rows with
+// their 16-byte chunks rotated by the key index, so the operand reads of 32
+// rows at one column hit distinct banks; V rows as stored), one block ahead of
+// the one it computes, so no barrier sits in the loop.  Each wave keeps an
+// online softmax state for the 32 rows; the four states are merged through LDS
+// at the end.  Per wave and block:
 //   S^T = K Q^T: A = K rows (keys), B = q (queries), 16 dims per MFMA.  q is
 //     split into bf16 hi + lo parts (two independent MFMA chains), keeping the
 //     scores at about 16 mantissa bits; K is bf16 already.  Lane l ends up
 //     with query l % 32 and 16 of its 32 keys; lane l ^ 32 holds the other 16.
 //   online softmax per query in the exp2 domain (one lane swap per reduction);
-//   O^T += V^T P^T: A = V^T (dims x keys), B = P (keys x queries, regrouped
-//     by one lane swap), P split hi + lo as well.
+//   O^T += V^T P^T: A = V^T (dims x keys, gathered from the key-major rows
+//     with 2-byte LDS reads), B = P (keys x queries, regrouped by one lane
+//     swap), P split hi + lo as well.
 // The output is normalised and written in bf16 fragment layout.
 template <int HD>
 __global__ __launch_bounds__(256) void k_prefill_attn(const float* __restrict__ q, KvTarget kv, int seq, int pos0,
                                                       int M, int H, uint16_t* __restrict__ out, int* err) {
-    constexpr int KB = 32;                         // keys per block
-    constexpr int LD = HD + 8;                     // K row pitch (bf16), 16-byte pad
-    constexpr int LV = KB + 8;                     // V^T row pitch (bf16)
-    constexpr int NDB = HD / 32;                   // 32-dim output blocks
-    constexpr int KBYTES = KB * LD * 2, VBYTES = HD * LV * 2;
-    constexpr int SLOT = KBYTES + VBYTES;          // one block's staging
-    constexpr int PIECES = 4 * 2 * KB * (HD / 8);  // 16-byte pieces of 4 blocks of K and V
-    static_assert(4 * HD * 32 * 4 + 4 * 64 * 4 <= 4 * SLOT, "merge buffers fit the staging area");
-    __shared__ __align__(16) unsigned char smem[4 * SLOT];
-    __shared__ int s_pid[640];                     // page ids of the key range (10240 positions)
+    constexpr int KB = 32;              // keys per block
+    constexpr int CPK = HD / 8;         // 16-byte chunks per key row
+    constexpr int NDB = HD / 32;        // 32-dim output blocks
+    constexpr int BLK = KB * HD * 2;    // bytes of one block of K (or of V)
+    constexpr int WBUF = 2 * 2 * BLK;   // a wave's two buffers of K and V
+    constexpr int NDMA = KB * CPK / 64; // 1 KiB direct loads per block and tensor
+    constexpr int QP = HD + 4;          // q tile row pitch (floats)
+    static_assert(KB * CPK % 64 == 0, "a block is whole 1 KiB loads");
+    static_assert(4 * HD * 32 * 4 + 4 * 64 * 4 <= 4 * WBUF, "merge buffers fit the wave buffers");
+    __shared__ __align__(16) unsigned char smem[4 * WBUF + 32 * QP * 4];
+    __shared__ int s_pid[640];  // page ids of the key range (10240 positions)
     const int head = blockIdx.x;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int d = H * HD;
@@ -56,13 +166,8 @@ __global__ __launch_bounds__(256) void k_prefill_attn(const float* __restrict__ 
         s_pid[i] = pid >= 0 && pid < kv.n_pages ? pid : -1;
         if (s_pid[i] < 0) set_err(err, CDB_DEV_UNMAPPED_PAGE);
     }
-
-    // q tile (32 rows x HD, fp32) through LDS: coalesced 16-byte loads, then
-    // each lane takes its B-operand dims 16t + 8*(lane/32) + e of row lane%32,
-    // scaled and split into bf16 hi + lo
-    constexpr int QP = HD + 4;  // row pitch (floats)
-    static_assert(32 * QP * 4 <= 4 * SLOT, "q tile fits the staging area");
-    float* sq = reinterpret_cast<float*>(smem);
+    // q tile (32 rows x HD, fp32), coalesced 16-byte loads
+    float* sq = reinterpret_cast<float*>(smem + 4 * WBUF);
     for (int i = tid; i < 32 * (HD / 4); i += 256) {
         const int r = i / (HD / 4), c4 = i - r * (HD / 4);
         float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -70,11 +175,41 @@ __global__ __launch_bounds__(256) void k_prefill_attn(const float* __restrict__ 
         *reinterpret_cast<float4*>(sq + r * QP + c4 * 4) = v;
     }
     __syncthreads();  // q tile and page ids
+
+    // block kb (keys kb .. kb + 31) into buffer b: K row `key` keeps chunk c at
+    // position (c + key) % CPK; keys past `last` repeat the last key (masked)
+    unsigned char* wbase = smem + wave * WBUF;
+    auto issue = [&](int kb, int b) {
+        unsigned char* kd = wbase + b * 2 * BLK;
+#pragma unroll
+        for (int i = 0; i < NDMA; ++i) {
+            const int f = i * 64 + lane;  // chunk slot within the block
+            const int key = f / CPK, pos = f - key * CPK;
+            const int rot = key % CPK;
+            const int c = pos >= rot ? pos - rot : pos - rot + CPK;
+            const int kp = min(kb + key, last);
+            const int pid = max(s_pid[kp / kPage], 0);  // unmapped pages were reported above
+            const u32x4* kr = reinterpret_cast<const u32x4*>(
+                kv.pool + kv_offset(kv.layer, pid, kv.n_pages, 0, head, H, kp % kPage, HD));
+            const u32x4* vr = reinterpret_cast<const u32x4*>(
+                kv.pool + kv_offset(kv.layer, pid, kv.n_pages, 1, head, H, kp % kPage, HD));
+            __builtin_amdgcn_global_load_lds(kr + c, (__attribute__((address_space(3))) void*)(kd + i * 1024), 16, 0, 0);
+            __builtin_amdgcn_global_load_lds(vr + pos, (__attribute__((address_space(3))) void*)(kd + BLK + i * 1024),
+                                             16, 0, 0);
+        }
+    };
+    int kb = wave * KB;
+    if (kb <= last) issue(kb, 0);
+
+    // q operands: dims 16t + 8*(lane/32) + e of row lane%32, scaled and split into bf16 hi + lo
     bf16x8 qh[HD / 16], ql[HD / 16];
 #pragma unroll
     for (int t = 0; t < HD / 16; ++t) {
         const float* src = sq + (lane & 31) * QP + t * 16 + (lane >> 5) * 8;
-        const float4 a = *reinterpret_cast<const float4*>(src), b = *reinterpret_cast<const float4*>(src + 4);
+        u32x4 qv[2];
+        const uint32_t qa[2] = {lds_addr(src), lds_addr(src + 4)};
+        lds_read_b128xN(qv, qa);
+        const float4 a = __builtin_bit_cast(float4, qv[0]), b = __builtin_bit_cast(float4, qv[1]);
         const float x[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
         uint32_t hw[4], lw[4];
 #pragma unroll
@@ -95,139 +230,118 @@ __global__ __launch_bounds__(256) void k_prefill_attn(const float* __restrict__ 
 #pragma unroll
         for (int j = 0; j < 16; ++j) o[b][j] = 0.f;
     float m_run = -1e30f, l_run = 0.f;
-    uint16_t* sK = reinterpret_cast<uint16_t*>(smem + wave * SLOT);
-    uint16_t* sVt = reinterpret_cast<uint16_t*>(smem + wave * SLOT + KBYTES);
-    __syncthreads();  // the q tile is read before the staging area is reused
 
-    for (int sb = 0; sb <= last; sb += 4 * KB) {
-        // stage keys sb .. sb + 127: block w in slot w; loads in batches of 4
-        // per thread, issued before their LDS writes
-        constexpr int PPT = PIECES / 256, SB = 4;
-        static_assert(PPT % SB == 0, "staging batches");
-#pragma unroll
-        for (int b0 = 0; b0 < PPT; b0 += SB) {
-            u32x4 v[SB];
-            int slot_off[SB], which_k[SB];
-#pragma unroll
-            for (int i = 0; i < SB; ++i) {
-                const int p = tid + (b0 + i) * 256;
-                const int blk = p / (2 * KB * (HD / 8));
-                const int r0 = p - blk * 2 * KB * (HD / 8);
-                const int which = r0 / (KB * (HD / 8));
-                const int r = r0 - which * KB * (HD / 8);
-                const int key = r / (HD / 8), c8 = r - key * (HD / 8);
-                const int kp = sb + blk * KB + key;
-                v[i] = u32x4{0u, 0u, 0u, 0u};
-                if (kp <= last) {
-                    const int pid = s_pid[kp / kPage];
-                    if (pid >= 0)
-                        v[i] = *reinterpret_cast<const u32x4*>(
-                            kv.pool + kv_offset(kv.layer, pid, kv.n_pages, which, head, H, kp % kPage, HD) + c8 * 8);
-                }
-                slot_off[i] = blk * SLOT + (which == 0 ? (key * LD + c8 * 8) * 2 : KBYTES + (c8 * 8 * LV + key) * 2);
-                which_k[i] = which;
-            }
-#pragma unroll
-            for (int i = 0; i < SB; ++i) {
-                if (which_k[i] == 0) {
-                    *reinterpret_cast<u32x4*>(smem + slot_off[i]) = v[i];
-                } else {
-                    uint16_t* vt = reinterpret_cast<uint16_t*>(smem + slot_off[i]);
-                    const uint32_t w[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) vt[e * LV] = (uint16_t)(w[e >> 1] >> ((e & 1) * 16));
-                }
-            }
+    for (int b = 0; kb <= last; kb += 4 * KB, b ^= 1) {
+        if (kb + 4 * KB <= last) {
+            issue(kb + 4 * KB, b ^ 1);
+            asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * NDMA) : "memory");
+        } else {
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         }
-        __syncthreads();
-        const int kb = sb + wave * KB;
-        if (kb <= last) {
-            // S^T[key][query] for the 32 queries
-            floatx16 sc, sl;
+        const uint16_t* sK = reinterpret_cast<const uint16_t*>(wbase + b * 2 * BLK);
+        const uint16_t* sV = sK + KB * HD;
+        // S^T[key][query] for the 32 queries
+        floatx16 sc, sl;
 #pragma unroll
-            for (int j = 0; j < 16; ++j) {
-                sc[j] = 0.f;
-                sl[j] = 0.f;
-            }
+        for (int j = 0; j < 16; ++j) {
+            sc[j] = 0.f;
+            sl[j] = 0.f;
+        }
+        const int krow = lane & 31;
+        u32x4 ka[HD / 16];
+        uint32_t kaddr[HD / 16];
 #pragma unroll
-            for (int t = 0; t < HD / 16; ++t) {
-                const bf16x8 ka = *reinterpret_cast<const bf16x8*>(sK + (lane & 31) * LD + t * 16 + (lane >> 5) * 8);
-                sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qh[t], sc, 0, 0, 0);
-                sl = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, ql[t], sl, 0, 0, 0);
-            }
-            // causal mask and online softmax; lane holds keys (j/4)*8 + (lane/32)*4 + j%4
-            float mx = -1e30f;
+        for (int t = 0; t < HD / 16; ++t) {
+            const int c = t * 2 + (lane >> 5);
+            const int pos = (c + krow) % CPK;
+            kaddr[t] = lds_addr(sK + (krow * CPK + pos) * 8);
+        }
+        lds_read_b128xN(ka, kaddr);
 #pragma unroll
-            for (int j = 0; j < 16; ++j) {
-                const int kp = kb + (j >> 2) * 8 + (lane >> 5) * 4 + (j & 3);
-                const bool ok = qvalid && kp <= qpos;
-                sc[j] = ok ? sc[j] + sl[j] : -1e30f;
-                mx = fmaxf(mx, sc[j]);
-            }
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
-            const float m_new = fmaxf(m_run, mx);
-            const float corr = exp2f(m_run - m_new);
-            float ls = 0.f;
-            float p[16];
+        for (int t = 0; t < HD / 16; ++t) {
+            const bf16x8 a = __builtin_bit_cast(bf16x8, ka[t]);
+            sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qh[t], sc, 0, 0, 0);
+            sl = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, ql[t], sl, 0, 0, 0);
+        }
+        // causal mask and online softmax; lane holds keys (j/4)*8 + (lane/32)*4 + j%4
+        float mx = -1e30f;
 #pragma unroll
-            for (int j = 0; j < 16; ++j) {
-                p[j] = sc[j] > -1e29f ? exp2f(sc[j] - m_new) : 0.f;
-                ls += p[j];
-            }
-            ls += __shfl_xor(ls, 32);
-            l_run = l_run * corr + ls;
-            m_run = m_new;
+        for (int j = 0; j < 16; ++j) {
+            const int kp = kb + (j >> 2) * 8 + (lane >> 5) * 4 + (j & 3);
+            const bool ok = qvalid && kp <= qpos;
+            sc[j] = ok ? sc[j] + sl[j] : -1e30f;
+            mx = fmaxf(mx, sc[j]);
+        }
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float m_new = fmaxf(m_run, mx);
+        const float corr = exp2f(m_run - m_new);
+        float ls = 0.f;
+        float p[16];
 #pragma unroll
-            for (int b = 0; b < NDB; ++b)
+        for (int j = 0; j < 16; ++j) {
+            p[j] = sc[j] > -1e29f ? exp2f(sc[j] - m_new) : 0.f;
+            ls += p[j];
+        }
+        ls += __shfl_xor(ls, 32);
+        l_run = l_run * corr + ls;
+        m_run = m_new;
 #pragma unroll
-                for (int j = 0; j < 16; ++j) o[b][j] *= corr;
+        for (int b2 = 0; b2 < NDB; ++b2)
+#pragma unroll
+            for (int j = 0; j < 16; ++j) o[b2][j] *= corr;
 
-            // regroup P for the B operand: k step s needs keys 16s + 8*(lane/32) + e
-            const bool lo_half = lane < 32;
-            float mine[8], theirs[8];
+        // regroup P for the B operand: k step st needs keys 16st + 8*(lane/32) + e
+        const bool lo_half = lane < 32;
+        float mine[8], theirs[8];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            mine[e] = lo_half ? p[4 + e] : p[e];  // what the partner lane needs from this lane
+            mine[4 + e] = lo_half ? p[12 + e] : p[8 + e];
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) theirs[e] = __shfl_xor(mine[e], 32);
+#pragma unroll
+        for (int st = 0; st < 2; ++st) {
+            float pk[8];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                mine[e] = lo_half ? p[4 + e] : p[e];  // what the partner lane needs from this lane
-                mine[4 + e] = lo_half ? p[12 + e] : p[8 + e];
+                // lanes < 32: own keys first, then the partner's; lanes >= 32 the reverse
+                pk[e] = lo_half ? p[st * 8 + e] : theirs[st * 4 + e];
+                pk[4 + e] = lo_half ? theirs[st * 4 + e] : p[st * 8 + 4 + e];
             }
+            uint32_t hw[4], lw[4];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) theirs[e] = __shfl_xor(mine[e], 32);
+            for (int e = 0; e < 8; e += 2) {
+                const uint16_t h0 = f2bf(pk[e]), h1 = f2bf(pk[e + 1]);
+                const uint16_t l0 = f2bf(pk[e] - bf2f(h0)), l1 = f2bf(pk[e + 1] - bf2f(h1));
+                hw[e / 2] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+                lw[e / 2] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+            }
+            const bf16x8 ph = __builtin_bit_cast(bf16x8, u32x4{hw[0], hw[1], hw[2], hw[3]});
+            const bf16x8 pl = __builtin_bit_cast(bf16x8, u32x4{lw[0], lw[1], lw[2], lw[3]});
+            // V^T operand: dim 32b + lane%32, keys 16st + 8*(lane/32) .. + 7
+            const uint32_t vcol = lds_addr(sV + (st * 16 + (lane >> 5) * 8) * HD + (lane & 31));
+            uint32_t vaddr[8];
 #pragma unroll
-            for (int st = 0; st < 2; ++st) {
-                float pk[8];
+            for (int e = 0; e < 8; ++e) vaddr[e] = vcol + e * HD * 2;
+            uint32_t vr[32];
+            lds_read_vcols<NDB>(vr, vaddr);
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    // lanes < 32: own keys first, then the partner's; lanes >= 32 the reverse
-                    pk[e] = lo_half ? p[st * 8 + e] : theirs[st * 4 + e];
-                    pk[4 + e] = lo_half ? theirs[st * 4 + e] : p[st * 8 + 4 + e];
-                }
-                uint32_t hw[4], lw[4];
-#pragma unroll
-                for (int e = 0; e < 8; e += 2) {
-                    const uint16_t h0 = f2bf(pk[e]), h1 = f2bf(pk[e + 1]);
-                    const uint16_t l0 = f2bf(pk[e] - bf2f(h0)), l1 = f2bf(pk[e + 1] - bf2f(h1));
-                    hw[e / 2] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-                    lw[e / 2] = (uint32_t)l0 | ((uint32_t)l1 << 16);
-                }
-                const bf16x8 ph = __builtin_bit_cast(bf16x8, u32x4{hw[0], hw[1], hw[2], hw[3]});
-                const bf16x8 pl = __builtin_bit_cast(bf16x8, u32x4{lw[0], lw[1], lw[2], lw[3]});
-                // V^T operand: dims 32b + lane%32, keys 16st + 8*(lane/32) .. + 7
-#pragma unroll
-                for (int b = 0; b < NDB; ++b) {
-                    const bf16x8 va = *reinterpret_cast<const bf16x8*>(sVt + (b * 32 + (lane & 31)) * LV + st * 16 +
-                                                                       (lane >> 5) * 8);
-                    o[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, ph, o[b], 0, 0, 0);
-                    o[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pl, o[b], 0, 0, 0);
-                }
+            for (int b2 = 0; b2 < NDB; ++b2) {
+                const uint32_t* r8 = vr + 8 * b2;
+                const bf16x8 a = __builtin_bit_cast(
+                    bf16x8, u32x4{r8[0] | (r8[1] << 16), r8[2] | (r8[3] << 16), r8[4] | (r8[5] << 16), r8[6] | (r8[7] << 16)});
+                o[b2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, ph, o[b2], 0, 0, 0);
+                o[b2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pl, o[b2], 0, 0, 0);
             }
         }
-        __syncthreads();  // the slots are restaged next
     }
+    __syncthreads();  // every wave is done with its buffers
 
     // merge the four waves' states: O^T[dim][query] with lane holding query
     // lane%32 and dims 32b + (j/4)*8 + (lane/32)*4 + j%4
-    float* sO = reinterpret_cast<float*>(smem);          // [4 waves][HD][32]
-    float* sM = sO + 4 * HD * 32;                         // [4][32] maxima, then [4][32] sums
+    float* sO = reinterpret_cast<float*>(smem);  // [4 waves][HD][32]
+    float* sM = sO + 4 * HD * 32;                // [4][32] maxima, then [4][32] sums
     float* sL = sM + 4 * 32;
 #pragma unroll
     for (int b = 0; b < NDB; ++b)
@@ -275,6 +389,7 @@ hipError_t launch_prefill_attention(const float* q, const KvTarget& kv, int seq,
                                     uint16_t* out, int* err, hipStream_t st) {
     if (M <= 0) return hipSuccess;
     if (pos0 + M > 640 * kPage) return hipErrorInvalidValue;  // page ids of the key range must fit in LDS
+    if (kv.n_pages < 1 || !kv.pool) return hipErrorInvalidValue;
     dim3 grid(H, (M + 31) / 32);
     switch (hd) {
         case 64: k_prefill_attn<64><<<grid, 256, 0, st>>>(q, kv, seq, pos0, M, H, out, err); break;
