@@ -226,6 +226,58 @@ def e2e_decode(shape, dm, kv, n_seqs, prompt, n_decode, seed=3):
     return res
 
 
+def serving_leg(shape, dm, n_req, rate=20.0, max_batch=64, chunk=512, core_pages=24576):
+    """A serving trace of the ouro-shaped model: Poisson arrivals at `rate`
+    requests/s, prompt lengths lognormal (median 300, sigma 1, [16, 4096]),
+    output lengths lognormal (median 400, sigma 1, [16, 2048]), categorical
+    depths; the driver prefills every prompt through cdb_prefill in chunks of
+    512 between loop steps and admits requests at every step while the KV pool
+    (core_pages pages of the depth-indexed cache) has room.  Tokens/s over the
+    whole run and the normalised latency ((finish - arrival) / output tokens)."""
+    import numpy as np
+    import torch
+
+    import cdbgen
+    import paper_2608_09444_amd as cdb
+    from paper_2608_09444_amd import driver as drv
+    wl = cdbgen.WORKLOADS[5]
+    R = shape.r_max
+    plen = cdbgen.lengths(wl.prompt, n_req, seed=cdbgen.PROMPT_SEED, stream=100)
+    olen = cdbgen.lengths(wl.decode, n_req, seed=cdbgen.PROMPT_SEED, stream=101)
+    arrivals = cdbgen.poisson_arrivals(n_req, rate)
+    max_pages = cdbgen.pages_for(int(plen.max() + olen.max()))
+    d = drv.Driver(max_batch=max_batch, max_active=max_batch, r_max=R, max_seqs=n_req, max_pages=max_pages,
+                   core_pages=core_pages, prefill_chunk=chunk)
+    for q in range(n_req):
+        d.add_request(cdbgen.prompt_ids(shape.vocab, 1, int(plen[q]), stream=q)[0],
+                      cdbgen.draw_depths(wl.depth, int(olen[q]), R, stream=1000 + q), arrival=float(arrivals[q]))
+    kv = cdb.PagedKV(shape, n_req, max_pages, 0, core_pages, 0)
+    state = cdb.State(shape, n_req)
+    ws = cdb.Workspace(dm.desc, chunk)
+    scratch = torch.empty(d.scratch_bytes(shape.vocab), dtype=torch.uint8, device="cuda")
+    log(f"serving: {n_req} requests at {rate}/s, {int(plen.sum())} prompt + {int(olen.sum())} output tokens")
+    secs = d.run(dm.model, kv.c, state.c, scratch, None, ws.buf)
+    if cdb.cdb_read_device_error(ws.buf) != 0:
+        raise RuntimeError("device error in the serving run")
+    st = d.stats()
+    lat = d.latencies(n_req)
+    lat = lat[lat >= 0]
+    res = {"workload": f"{n_req} requests, Poisson {rate}/s, prompt lognormal(300, 1) in [16, 4096], output "
+                       f"lognormal(400, 1) in [16, 2048], depths categorical {{1:.3,2:.3,3:.2,4:.2}}, max batch "
+                       f"{max_batch}, prefill chunks of {chunk}, depth-indexed KV of {core_pages} core pages",
+           "seconds": round(secs, 3), "tokens_per_s": round(st["tokens"] / secs, 1),
+           "prompt_tokens_per_s": round(st["prefill_tokens"] / secs, 1),
+           "normalized_latency_s": {"p50": round(float(np.percentile(lat, 50)), 5),
+                                    "p99": round(float(np.percentile(lat, 99)), 5)},
+           "finished": int(len(lat)), "loop_steps": st["loop_steps"], "idle_rows": st["idle_rows"],
+           "prefill_calls": st["prefill_calls"], "coda_calls": st["coda_calls"]}
+    log(f"serving: {st['tokens']} tokens in {secs:.2f}s, p50/p99 normalized latency "
+        f"{res['normalized_latency_s']['p50'] * 1e3:.1f}/{res['normalized_latency_s']['p99'] * 1e3:.1f} ms")
+    del kv, state, ws, scratch
+    torch.cuda.empty_cache()
+    return res
+
+
 def prefill_leg(shape, dm, kv, chunk=512, reps=5):
     """Chunked prefill at full width: one chunk of `chunk` prompt tokens of one
     sequence (positions 0..chunk-1) through cdb_prefill, timed with events on
@@ -278,6 +330,8 @@ def main():
     ap.add_argument("--cpu-sample", type=int, default=16, help="rows in the CPU-oracle sample (0 = skip)")
     ap.add_argument("--no-e2e", action="store_true", help="skip the whole-decode driver runs")
     ap.add_argument("--no-prefill", action="store_true", help="skip the chunked-prefill timing")
+    ap.add_argument("--serving-requests", type=int, default=200,
+                    help="requests in the serving-trace run (0 = skip; 2000 is the full trace)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="run one plain device copy of this many MiB first (a known-size reference for HBM counters)")
     args = ap.parse_args()
@@ -343,6 +397,10 @@ def main():
     if not args.no_prefill:
         prefill = prefill_leg(shape, dm, kv)
 
+    serving = None
+    if args.serving_requests > 0:
+        serving = serving_leg(shape, dm, args.serving_requests)
+
     cpu = None
     if args.cpu_sample > 0:
         threads = min(16, os.cpu_count() or 1)
@@ -379,6 +437,7 @@ def main():
         "cpu_baseline": cpu,
         "e2e": e2e,
         "prefill": prefill,
+        "serving": serving,
     }
     print(json.dumps(res), flush=True)
 

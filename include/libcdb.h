@@ -239,7 +239,9 @@ cdb_status cdb_boundary_coda(const cdb_model* model, const cdb_kv* kv, const cdb
  * (plane 0), r_max core loops over the whole chunk (loop r writes plane r;
  * prompt tokens take every loop), the coda layers (plane r_max + 1), the final
  * RMSNorm and the LM head: logits device fp32 [n_rows][vocab], next_ids device
- * int32 [n_rows] (argmax, lowest index on ties).  Positions < pos0 of the
+ * int32 [n_rows] (argmax, lowest index on ties).  logits may be NULL: then
+ * only the last row's greedy id is produced, in next_ids[0] (the LM head runs
+ * for the 32-row tile holding that row only).  Positions < pos0 of the
  * sequence must already be in the cache (earlier chunks); every plane's pages
  * of positions < pos0 + n_rows must be mapped.  Attention is query-tiled on
  * MFMA; above 256 rows the projections use compute-bound tiles.

@@ -50,6 +50,9 @@ typedef struct {
     int32_t gated;                  /* 1: exits decided on the device by a threshold (cdb_gate) */
     int32_t lookahead;              /* gated: the decision after loop r ends the token after loop r + 1 */
     float threshold;                /* gated: the criterion's threshold */
+    int32_t prefill_chunk;          /* 0: prompts are prefilled by the caller (cdb_driver_add_sequence);
+                                       1..512: prompts of requests added with cdb_driver_add_request run
+                                       through cdb_prefill in chunks of at most this many tokens */
 } cdb_driver_config;
 
 /* Core KV layouts (Section 4.2, App. C.1, Table 1), all by page-table aliasing:
@@ -59,11 +62,14 @@ typedef struct {
  *   FIRST_THEN_SHARED plane 1 private, planes 2..r_max share a second page */
 enum { CDB_KV_FULL = 0, CDB_KV_SHARED = 1, CDB_KV_FIRST_THEN_SHARED = 2 };
 
-enum { CDB_TICK_NONE = 0, CDB_TICK_PRELUDE_FIRST = 1, CDB_TICK_LOOP = 2, CDB_TICK_CODA = 3 };
+enum { CDB_TICK_NONE = 0, CDB_TICK_PRELUDE_FIRST = 1, CDB_TICK_LOOP = 2, CDB_TICK_CODA = 3, CDB_TICK_PREFILL = 4 };
 
 /* One planned stage call (host arrays of up to 256 rows).  For CDB_TICK_CODA
  * the first n_continue rows continue (the prelude of their next input follows
- * in the same tick, at pos + 1); the rest finish their sequence. */
+ * in the same tick, at pos + 1); the rest finish their sequence.  For
+ * CDB_TICK_PREFILL the call is one prompt chunk of sequence seq[0]: n_rows
+ * tokens from position pos[0]; n_continue = 1 when it ends the prompt (its last
+ * row's greedy id is the first decode input). */
 typedef struct {
     int32_t stage;
     int32_t n_rows, n_continue;
@@ -75,6 +81,7 @@ typedef struct {
     int64_t loop_steps, loop_rows, idle_rows;  /* idle_rows: max_batch - rows, summed over loop steps */
     int64_t coda_calls, coda_rows, prelude_calls, prelude_rows;
     int64_t tokens;                            /* decode tokens finished (coda rows) */
+    int64_t prefill_calls, prefill_tokens;     /* prompt chunks run by the driver */
 } cdb_driver_stats;
 
 cdb_driver* cdb_driver_create(const cdb_driver_config* cfg);
@@ -86,6 +93,15 @@ void cdb_driver_destroy(cdb_driver* d);
  * row of the page table and its state slot) or -1. */
 int32_t cdb_driver_add_sequence(cdb_driver* d, int32_t prompt_len, int32_t n_decode, const int32_t* depths,
                                 double arrival);
+
+/* Adds a request whose prompt the driver prefills (prefill_chunk > 0):
+ * prompt_ids (host, prompt_len ids, copied).  Scheduling priority (Section
+ * 4.1): the coda, then prompt chunks (one per call, first admitted first),
+ * then the prelude of first decode inputs, then loop steps.  The first decode
+ * input is the prompt's greedy continuation, passed on the device.  Returns
+ * the sequence id or -1. */
+int32_t cdb_driver_add_request(cdb_driver* d, int32_t prompt_len, const int32_t* prompt_ids, int32_t n_decode,
+                               const int32_t* depths, double arrival);
 
 /* Host page table [max_seqs][r_max + 2][max_pages] as the driver maintains it. */
 const int32_t* cdb_driver_page_table(cdb_driver* d);
@@ -121,7 +137,10 @@ size_t cdb_driver_scratch_bytes(const cdb_driver* d, int32_t vocab);
 /* Runs every added request to completion on the device: plans each call,
  * stages its rows through pinned host memory, enqueues the stage call on
  * `stream`.  first_tokens (host, per sequence) is each sequence's first decode
- * input; later inputs are the coda's greedy ids, passed on device.  The page
+ * input (may be NULL when every request was added with
+ * cdb_driver_add_request: their first inputs come from the prefill); later
+ * inputs are the coda's greedy ids, passed on device.  With prefill_chunk >
+ * 256 the workspace must be sized for prefill_chunk rows.  The page
  * table in kv->page_table (device) is overwritten from the driver's.
  * state needs a slot per sequence (n_slots >= max_seqs).  scratch: device,
  * cdb_driver_scratch_bytes(d, vocab).  tokens_out (device,

@@ -181,7 +181,8 @@ def cdb_boundary_coda(model: cdb_model, kv: cdb_kv, state: cdb_state, rows: cdb_
 
 
 def cdb_prefill(model: cdb_model, kv: cdb_kv, seq: int, pos0: int, tokens, logits, next_ids, ws, stream=None):
-    """tokens: device int32 [n]; logits: device fp32 [n][vocab]; next_ids: device int32 [n]."""
+    """tokens: device int32 [n]; logits: device fp32 [n][vocab], or None (only the
+    last row's greedy id, into next_ids[0]); next_ids: device int32 [n] (or [1])."""
     n = int(tokens.numel())
     _check("cdb_prefill", lib().cdb_prefill(C.byref(model), C.byref(kv), seq, pos0, n, _ptr(tokens), _ptr(logits),
                                             _ptr(next_ids), _ptr(ws), ws.numel(), _stream(stream)))

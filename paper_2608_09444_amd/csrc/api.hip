@@ -2,6 +2,8 @@
 // the launch sequences of the three stage calls.
 #include <string.h>
 
+#include <algorithm>
+
 #include "cdb_internal.h"
 
 namespace cdb {
@@ -101,6 +103,8 @@ WsLayout ws_layout(const cdb_model_desc& d, int rows) {
     off = align256(off + M * 4);
     L.prow = off;  // prefill row arrays: slot, seq, pos
     off = align256(off + 3 * M * 4);
+    L.lm = off;  // prefill without logits: the LM head of the last 32-row tile
+    off = align256(off + (size_t)32 * d.vocab * 4);
     L.total = off;
     return L;
 }
@@ -125,6 +129,7 @@ struct Ctx {
     int32_t* kvpid;
     int32_t* deff;
     int32_t* prow;
+    float* lm;
 };
 
 static Ctx make_ctx(const cdb_model* model, void* ws, int rows) {
@@ -147,6 +152,7 @@ static Ctx make_ctx(const cdb_model* model, void* ws, int rows) {
     c.kvpid = reinterpret_cast<int32_t*>(c.ws + c.L.kvpid);
     c.deff = reinterpret_cast<int32_t*>(c.ws + c.L.deff);
     c.prow = reinterpret_cast<int32_t*>(c.ws + c.L.prow);
+    c.lm = reinterpret_cast<float*>(c.ws + c.L.lm);
     return c;
 }
 
@@ -299,7 +305,11 @@ size_t cdb_kv_page_bytes(const cdb_model_desc* desc, int32_t stage) {
 
 size_t cdb_workspace_bytes(const cdb_model_desc* desc, int32_t max_rows) {
     if (!desc || !desc_supported(*desc) || max_rows < 0 || max_rows > kMaxPrefillRows) return 0;
-    return ws_layout(*desc, max_rows).total;
+    // the layout is not monotonic in the row count (the split-K factor of the
+    // tile GEMM shrinks as its grid grows): the largest one up to max_rows
+    size_t n = ws_layout(*desc, 0).total;
+    for (int r = 1; r <= max_rows; ++r) n = std::max(n, ws_layout(*desc, r).total);
+    return n;
 }
 
 cdb_status cdb_workspace_init(void* ws, size_t ws_bytes, hipStream_t st) {
@@ -390,18 +400,27 @@ cdb_status cdb_boundary_coda(const cdb_model* model, const cdb_kv* kv, const cdb
     s = run_layers(c, d.n_prelude + d.n_core, d.n_coda, t, *rows, true, st);
     if (s != CDB_OK) return s;
     EpiArgs ea{};
-    ea.out = logits;
     ea.ld_out = d.vocab;
     ea.err = c.err;
-    HIPCHK(launch_gemm(EPI_STORE, c.x, wptr(c, c.wl.lm_head), M, c.gm.lm, c.part, ea, st));
-    HIPCHK(launch_argmax(M, d.vocab, logits, next_ids, st));
+    if (logits) {
+        ea.out = logits;
+        HIPCHK(launch_gemm(EPI_STORE, c.x, wptr(c, c.wl.lm_head), M, c.gm.lm, c.part, ea, st));
+        HIPCHK(launch_argmax(M, d.vocab, logits, next_ids, st));
+        return CDB_OK;
+    }
+    // only the last row's greedy id: the LM head over the 32-row tile holding it
+    const int T = (M - 1) / 32, MT = M - 32 * T;
+    const uint16_t* xt = c.x + (size_t)T * (d.d / 16) * 512;  // fragment m-tiles are contiguous
+    ea.out = c.lm;
+    HIPCHK(launch_gemm(EPI_STORE, xt, wptr(c, c.wl.lm_head), MT, gemm_shape(d.vocab, d.d, EPI_STORE), c.part, ea, st));
+    HIPCHK(launch_argmax(1, d.vocab, c.lm + (size_t)(MT - 1) * d.vocab, next_ids, st));
     return CDB_OK;
 }
 
 cdb_status cdb_prefill(const cdb_model* model, const cdb_kv* kv, int32_t seq, int32_t pos0, int32_t n_rows,
                        const int32_t* tokens, float* logits, int32_t* next_ids, void* ws, size_t ws_bytes,
                        hipStream_t st) {
-    if (!model || !kv || !model->packed || !tokens || !logits || !next_ids || !ws) return CDB_ERR_INVALID_ARG;
+    if (!model || !kv || !model->packed || !tokens || !next_ids || !ws) return CDB_ERR_INVALID_ARG;
     const cdb_model_desc& d = model->desc;
     if (!desc_supported(d)) return CDB_ERR_UNSUPPORTED;
     if (n_rows < 1 || n_rows > kMaxPrefillRows) return CDB_ERR_CAPACITY;
@@ -447,11 +466,20 @@ cdb_status cdb_prefill(const cdb_model* model, const cdb_kv* kv, int32_t seq, in
     s = run_layers(c, d.n_prelude + d.n_core, d.n_coda, t, r, true, st, &chunk);
     if (s != CDB_OK) return s;
     EpiArgs ea{};
-    ea.out = logits;
     ea.ld_out = d.vocab;
     ea.err = c.err;
-    HIPCHK(launch_gemm(EPI_STORE, c.x, wptr(c, c.wl.lm_head), M, c.gm.lm, c.part, ea, st));
-    HIPCHK(launch_argmax(M, d.vocab, logits, next_ids, st));
+    if (logits) {
+        ea.out = logits;
+        HIPCHK(launch_gemm(EPI_STORE, c.x, wptr(c, c.wl.lm_head), M, c.gm.lm, c.part, ea, st));
+        HIPCHK(launch_argmax(M, d.vocab, logits, next_ids, st));
+        return CDB_OK;
+    }
+    // only the last row's greedy id: the LM head over the 32-row tile holding it
+    const int T = (M - 1) / 32, MT = M - 32 * T;
+    const uint16_t* xt = c.x + (size_t)T * (d.d / 16) * 512;  // fragment m-tiles are contiguous
+    ea.out = c.lm;
+    HIPCHK(launch_gemm(EPI_STORE, xt, wptr(c, c.wl.lm_head), MT, gemm_shape(d.vocab, d.d, EPI_STORE), c.part, ea, st));
+    HIPCHK(launch_argmax(1, d.vocab, c.lm + (size_t)(MT - 1) * d.vocab, next_ids, st));
     return CDB_OK;
 }
 

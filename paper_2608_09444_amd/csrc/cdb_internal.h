@@ -101,7 +101,7 @@ struct WeightLayout {
 bool weight_layout(const cdb_model_desc& d, WeightLayout* out);
 
 struct WsLayout {
-    size_t err, h, h_in, q, x, act, part, rope, order, kvpid, deff, prow, total;
+    size_t err, h, h_in, q, x, act, part, rope, order, kvpid, deff, prow, lm, total;
 };
 WsLayout ws_layout(const cdb_model_desc& d, int rows);
 

@@ -41,14 +41,18 @@ namespace cdb {
 // defined with the row kernels
 hipError_t launch_scatter_ids(int M, const int32_t* ids, const int32_t* seq, const int32_t* index, int max_seqs,
                               int stride, int32_t* out, hipStream_t st);
+hipError_t launch_gather_ids(int M, const int32_t* seq, const int32_t* src, int max_seqs, int32_t* dst,
+                             hipStream_t st);
 }  // namespace cdb
 
 namespace {
 
-enum SeqState { WAITING = 0, PRELUDE = 1, LOOP = 2, EXITED = 3, DONE = 4 };
+enum SeqState { WAITING = 0, PRELUDE = 1, LOOP = 2, EXITED = 3, DONE = 4, PREFILL = 5 };
 
 struct Seq {
     int32_t prompt_len = 0, n_decode = 0;
+    std::vector<int32_t> prompt;  // ids of a prompt the driver prefills (empty: prefilled by the caller)
+    int32_t prefilled = 0;        // prompt positions done
     std::vector<int32_t> depth;  // per decode input
     double arrival = 0.0;
     int state = WAITING;
@@ -85,6 +89,7 @@ struct cdb_driver {
     size_t next_arrival = 0;  // index into seqs in arrival order (sequences are added in arrival order)
     int32_t active = 0;
     std::deque<int32_t> exited;   // sequences whose token left the core, awaiting the coda
+    std::deque<int32_t> prefillq; // admitted sequences whose prompt is still being prefilled
     std::deque<int32_t> fresh;    // admitted sequences awaiting the prelude of their first input
     std::deque<int32_t> loopq;    // sequences whose token waits for its next loop
     std::vector<int32_t> batch;   // rows of the running loop batch (refill keeps it)
@@ -147,12 +152,18 @@ static bool try_admit(cdb_driver* d, int32_t q) {
         }
     }
     s.pages = need;
-    s.state = PRELUDE;
     s.t = 0;
     s.c = 0;
     s.admit_time = d->now;
     d->active++;
-    d->fresh.push_back(q);
+    if (!s.prompt.empty()) {
+        s.state = PREFILL;
+        s.prefilled = 0;
+        d->prefillq.push_back(q);
+    } else {
+        s.state = PRELUDE;
+        d->fresh.push_back(q);
+    }
     d->table_dirty = true;
     return true;
 }
@@ -204,7 +215,7 @@ extern "C" {
 cdb_driver* cdb_driver_create(const cdb_driver_config* cfg) {
     if (!cfg || cfg->max_batch < 1 || cfg->max_batch > 256 || cfg->r_max < 1 || cfg->max_seqs < 1 ||
         cfg->max_pages < 1 || cfg->max_active < 1 || cfg->min_coda_batch < 1 || cfg->kv_layout < 0 ||
-        cfg->kv_layout > 2 || (cfg->gated && cfg->fixed_depth))
+        cfg->kv_layout > 2 || (cfg->gated && cfg->fixed_depth) || cfg->prefill_chunk < 0 || cfg->prefill_chunk > 512)
         return nullptr;
     cdb_driver* d = new cdb_driver();
     d->cfg = *cfg;
@@ -233,6 +244,14 @@ int32_t cdb_driver_add_sequence(cdb_driver* d, int32_t prompt_len, int32_t n_dec
     s.arrival = arrival;
     d->seqs.push_back(std::move(s));
     return (int32_t)d->seqs.size() - 1;
+}
+
+int32_t cdb_driver_add_request(cdb_driver* d, int32_t prompt_len, const int32_t* prompt_ids, int32_t n_decode,
+                               const int32_t* depths, double arrival) {
+    if (!d || d->cfg.prefill_chunk < 1 || !prompt_ids || prompt_len < 1) return -1;
+    const int32_t q = cdb_driver_add_sequence(d, prompt_len, n_decode, depths, arrival);
+    if (q >= 0) d->seqs[q].prompt.assign(prompt_ids, prompt_ids + prompt_len);
+    return q;
 }
 
 const int32_t* cdb_driver_page_table(cdb_driver* d) { return d ? d->page_table.data() : nullptr; }
@@ -270,10 +289,26 @@ int32_t cdb_driver_next(cdb_driver* d, cdb_driver_tick* t) {
         fill_rows(d, d->batch, t, true, 0);
         return 1;
     };
+    auto prefill_tick = [&]() {
+        const int32_t q = d->prefillq.front();
+        const Seq& s = d->seqs[q];
+        const int32_t n = std::min(d->cfg.prefill_chunk, s.prompt_len - s.prefilled);
+        t->stage = CDB_TICK_PREFILL;
+        t->n_rows = n;
+        t->n_continue = s.prefilled + n == s.prompt_len ? 1 : 0;
+        t->seq[0] = q;
+        t->slot[0] = q;
+        t->pos[0] = s.prefilled;
+        t->c[0] = 0;
+        t->depth[0] = 0;
+        t->decode_index[0] = 0;
+        return 1;
+    };
     if (d->cfg.refill) {
         const bool loop_left = !d->loopq.empty() || !d->batch.empty();
         const int32_t n_exit = (int32_t)d->exited.size();
         if (n_exit > 0 && (n_exit >= d->cfg.min_coda_batch || !loop_left)) return coda_tick();
+        if (!d->prefillq.empty()) return prefill_tick();
         if (!d->fresh.empty()) return prelude_tick();
         if (loop_left) {
             // keep the running rows, fill freed rows from the loop queue
@@ -290,6 +325,7 @@ int32_t cdb_driver_next(cdb_driver* d, cdb_driver_tick* t) {
             d->round_open = false;
         }
         if (!d->exited.empty()) return coda_tick();
+        if (!d->prefillq.empty()) return prefill_tick();
         if (!d->fresh.empty()) return prelude_tick();
         if (!d->loopq.empty()) {
             while ((int32_t)d->batch.size() < d->cfg.max_batch && !d->loopq.empty()) {
@@ -338,6 +374,19 @@ int32_t cdb_driver_complete(cdb_driver* d, const cdb_driver_tick* t) {
         d->stats.prelude_rows += (int64_t)cont.size();
         for (int32_t q : cont) d->loopq.push_back(q);
         if (!d->cfg.refill && d->exited.empty() && d->batch.empty()) d->round_open = false;  // round over
+    } else if (t->stage == CDB_TICK_PREFILL) {
+        const int32_t q = t->seq[0];
+        if (d->prefillq.empty() || d->prefillq.front() != q) return -1;
+        Seq& s = d->seqs[q];
+        if (t->pos[0] != s.prefilled || t->n_rows < 1 || s.prefilled + t->n_rows > s.prompt_len) return -1;
+        s.prefilled += t->n_rows;
+        d->stats.prefill_calls++;
+        d->stats.prefill_tokens += t->n_rows;
+        if (s.prefilled == s.prompt_len) {
+            d->prefillq.pop_front();
+            s.state = PRELUDE;
+            d->fresh.push_back(q);
+        }
     } else if (t->stage == CDB_TICK_PRELUDE_FIRST) {
         for (int32_t i = 0; i < t->n_rows; ++i) {
             const int32_t q = t->seq[i];
@@ -421,9 +470,10 @@ int32_t cdb_driver_latencies(const cdb_driver* d, double* normalized, int32_t n)
 
 // Device scratch: two row sets (6 x 256 int32 each), next ids (256), loop-step
 // outputs (scores, mask, cont, exited, counts, exit_next), the gate's pending
-// flags (max_seqs), logits (256 x vocab fp32).
+// flags (max_seqs), each sequence's first decode input (max_seqs int32),
+// logits (256 x vocab fp32).
 struct ScratchLayout {
-    size_t rows, ids, step, pending, logits, total;
+    size_t rows, ids, step, pending, first, logits, total;
 };
 
 static ScratchLayout scratch_layout(int32_t max_seqs, int32_t vocab) {
@@ -438,6 +488,8 @@ static ScratchLayout scratch_layout(int32_t max_seqs, int32_t vocab) {
     off = (off + 255) & ~(size_t)255;
     L.pending = off;
     off += ((size_t)max_seqs + 255) & ~(size_t)255;
+    L.first = off;
+    off += ((size_t)max_seqs * 4 + 255) & ~(size_t)255;
     L.logits = off;
     off += (size_t)256 * vocab * 4;
     L.total = off;
@@ -451,8 +503,9 @@ size_t cdb_driver_scratch_bytes(const cdb_driver* d, int32_t vocab) {
 int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, const cdb_state* state, void* scratch,
                        size_t scratch_bytes, const int32_t* first_tokens, int32_t* tokens_out,
                        int32_t tokens_stride, void* ws, size_t ws_bytes, hipStream_t stream, double* seconds) {
-    if (!d || !model || !kv || !state || !scratch || !ws || !first_tokens || !kv->page_table)
-        return CDB_ERR_INVALID_ARG;
+    if (!d || !model || !kv || !state || !scratch || !ws || !kv->page_table) return CDB_ERR_INVALID_ARG;
+    for (const Seq& s : d->seqs)
+        if (s.prompt.empty() && !first_tokens) return CDB_ERR_INVALID_ARG;  // its first input must be given
     if (tokens_out) {
         for (const Seq& s : d->seqs)
             if (s.n_decode > tokens_stride) return CDB_ERR_INVALID_ARG;
@@ -465,6 +518,7 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
     int32_t* drows = reinterpret_cast<int32_t*>(base + SL.rows);  // main rows
     int32_t* drows2 = drows + 6 * 256;                            // prelude rows after a coda
     int32_t* dids = reinterpret_cast<int32_t*>(base + SL.ids);
+    int32_t* dfirst = reinterpret_cast<int32_t*>(base + SL.first);  // first decode input per sequence
     float* dlogits = reinterpret_cast<float*>(base + SL.logits);
     cdb_step_out out;
     out.exit_score = reinterpret_cast<float*>(base + SL.step);
@@ -473,6 +527,7 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
     out.exited = out.cont + 256;
     out.counts = out.exited + 256;
     out.exit_next = reinterpret_cast<uint8_t*>(out.counts + 2);
+    int32_t status0 = CDB_OK;
     cdb_gate gate;
     gate.threshold = d->cfg.threshold;
     gate.lookahead = d->cfg.lookahead;
@@ -506,6 +561,17 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
     }
     hipEventCreateWithFlags(&pt_ev, hipEventDisableTiming);
     bool pt_used = false;
+    // the caller's first inputs (prefilled prompts) to the device; the page-table
+    // staging buffer carries them, and its next upload waits for this copy
+    if (first_tokens) {
+        const size_t nb = d->seqs.size() * 4;  // one entry per added sequence
+        memcpy(pinned_pt, first_tokens, nb);
+        if (nb && hipMemcpyAsync(dfirst, pinned_pt, nb, hipMemcpyHostToDevice, stream) !=
+            hipSuccess)
+            status0 = CDB_ERR_HIP;
+        hipEventRecord(pt_ev, stream);
+        pt_used = true;
+    }
     int ring = 0, rb_ring = 0;
     auto stage = [&](const int32_t* slot, const int32_t* seq, const int32_t* pos, const int32_t* c,
                      const int32_t* dep, const int32_t* tok, int32_t n, int32_t* dst) -> hipError_t {
@@ -522,12 +588,21 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
         ring = (ring + 1) % RING;
         return e;
     };
+    auto stage_ids = [&](const int32_t* ids, int32_t n, int32_t* dst) -> hipError_t {
+        hipEventSynchronize(ev[ring]);
+        int32_t* h = pinned + ring * slot_ints;
+        memcpy(h, ids, (size_t)n * 4);
+        hipError_t e = hipMemcpyAsync(dst, h, (size_t)n * 4, hipMemcpyHostToDevice, stream);
+        hipEventRecord(ev[ring], stream);
+        ring = (ring + 1) % RING;
+        return e;
+    };
     // gated: the previous loop tick and the ring slot of its decisions
     cdb_driver_tick prev;
     int prev_rb = -1;
 
     cdb_driver_tick t;
-    int32_t status = CDB_OK;
+    int32_t status = status0;
     std::vector<int32_t> toks(256), npos(256);
     const auto t0 = std::chrono::steady_clock::now();
     while (status == CDB_OK) {
@@ -548,16 +623,39 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
             d->table_dirty = false;
         }
         const int32_t n = t.n_rows;
-        // sixth row array: the first decode input (prelude) or the decode index (coda)
-        for (int32_t i = 0; i < n; ++i)
-            toks[i] = t.stage == CDB_TICK_CODA ? t.decode_index[i] : first_tokens[t.seq[i]];
+        cdb_status s = CDB_OK;
+        if (t.stage == CDB_TICK_PREFILL) {
+            // the chunk's prompt ids through the staging ring; the chunk's last
+            // greedy id lands in the sequence's first-input entry
+            const int32_t q = t.seq[0];
+            if (stage_ids(d->seqs[q].prompt.data() + t.pos[0], n, drows) != hipSuccess) {
+                status = CDB_ERR_HIP;
+                break;
+            }
+            s = cdb_prefill(model, kv, q, t.pos[0], n, drows, nullptr, dfirst + q, ws, ws_bytes, stream);
+            if (s != CDB_OK) {
+                status = s;
+                break;
+            }
+            if (cdb_driver_complete(d, &t) != 0) {
+                status = CDB_ERR_INVALID_ARG;
+                break;
+            }
+            continue;
+        }
+        // sixth row array: the decode index (coda); the prelude of first inputs
+        // gathers its tokens from the first-input entries on the device
+        for (int32_t i = 0; i < n; ++i) toks[i] = t.stage == CDB_TICK_CODA ? t.decode_index[i] : 0;
         if (stage(t.slot, t.seq, t.pos, t.c, t.depth, toks.data(), n, drows) != hipSuccess) {
             status = CDB_ERR_HIP;
             break;
         }
         cdb_rows rows{n, drows, drows + 256, drows + 512, drows + 768, drows + 1024};
-        cdb_status s = CDB_OK;
         if (t.stage == CDB_TICK_PRELUDE_FIRST) {
+            if (cdb::launch_gather_ids(n, drows + 256, dfirst, d->cfg.max_seqs, drows + 1280, stream) != hipSuccess) {
+                status = CDB_ERR_HIP;
+                break;
+            }
             s = cdb_boundary_prelude(model, kv, state, &rows, drows + 1280, ws, ws_bytes, stream);
         } else if (t.stage == CDB_TICK_LOOP) {
             if (!gated) {

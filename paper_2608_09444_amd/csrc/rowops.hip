@@ -533,6 +533,25 @@ hipError_t launch_scatter_ids(int M, const int32_t* ids, const int32_t* seq, con
     return hipGetLastError();
 }
 
+// dst[i] = src[seq[i]]: a batch's first decode inputs from the per-sequence
+// entries the prefill wrote (out-of-range sequences read 0; the row-entry
+// kernels report them).
+__global__ __launch_bounds__(256) void k_gather_ids(int M, const int32_t* __restrict__ seq,
+                                                    const int32_t* __restrict__ src, int max_seqs,
+                                                    int32_t* __restrict__ dst) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= M) return;
+    const int q = seq[i];
+    dst[i] = q >= 0 && q < max_seqs ? src[q] : 0;
+}
+
+hipError_t launch_gather_ids(int M, const int32_t* seq, const int32_t* src, int max_seqs, int32_t* dst,
+                             hipStream_t st) {
+    if (M <= 0) return hipSuccess;
+    k_gather_ids<<<(M + 255) / 256, 256, 0, st>>>(M, seq, src, max_seqs, dst);
+    return hipGetLastError();
+}
+
 __global__ __launch_bounds__(256) void k_prefill_rows(int seq, int pos0, int M, int32_t* __restrict__ rows) {
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= M) return;

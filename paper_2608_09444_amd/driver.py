@@ -13,13 +13,14 @@ import numpy as np
 
 from . import _ptr, _stream, cdb_kv, cdb_model, cdb_state, lib as _lib
 
-EXPORTED = ("cdb_driver_create", "cdb_driver_destroy", "cdb_driver_add_sequence", "cdb_driver_page_table",
+EXPORTED = ("cdb_driver_create", "cdb_driver_destroy", "cdb_driver_add_sequence", "cdb_driver_add_request",
+            "cdb_driver_page_table",
             "cdb_driver_next", "cdb_driver_complete", "cdb_driver_loop_result", "cdb_driver_set_time",
             "cdb_driver_get_stats",
             "cdb_driver_pages_in_use", "cdb_driver_latencies", "cdb_driver_scratch_bytes", "cdb_driver_run")
 
 KV_FULL, KV_SHARED, KV_FIRST_THEN_SHARED = 0, 1, 2
-TICK_NONE, TICK_PRELUDE_FIRST, TICK_LOOP, TICK_CODA = 0, 1, 2, 3
+TICK_NONE, TICK_PRELUDE_FIRST, TICK_LOOP, TICK_CODA, TICK_PREFILL = 0, 1, 2, 3, 4
 MAX_ROWS = 256
 
 
@@ -27,7 +28,7 @@ class cdb_driver_config(C.Structure):
     _fields_ = [(n, C.c_int32) for n in ("max_batch", "max_active", "refill", "fixed_depth", "min_coda_batch",
                                           "r_max", "has_prelude", "has_coda", "max_seqs", "max_pages",
                                           "pre_pages", "core_pages", "coda_pages", "kv_layout", "gated",
-                                          "lookahead")] + [("threshold", C.c_float)]
+                                          "lookahead")] + [("threshold", C.c_float), ("prefill_chunk", C.c_int32)]
 
 
 class cdb_driver_tick(C.Structure):
@@ -38,7 +39,8 @@ class cdb_driver_tick(C.Structure):
 
 class cdb_driver_stats(C.Structure):
     _fields_ = [(n, C.c_int64) for n in ("loop_steps", "loop_rows", "idle_rows", "coda_calls", "coda_rows",
-                                          "prelude_calls", "prelude_rows", "tokens")]
+                                          "prelude_calls", "prelude_rows", "tokens", "prefill_calls",
+                                          "prefill_tokens")]
 
 
 _bound = False
@@ -54,6 +56,7 @@ def lib() -> C.CDLL:
         L.cdb_driver_destroy.argtypes = [P]
         L.cdb_driver_destroy.restype = None
         L.cdb_driver_add_sequence.argtypes = [P, I, I, P, D]
+        L.cdb_driver_add_request.argtypes = [P, I, P, I, P, D]
         L.cdb_driver_page_table.argtypes = [P]
         L.cdb_driver_page_table.restype = C.POINTER(C.c_int32)
         L.cdb_driver_next.argtypes = [P, P]
@@ -67,9 +70,9 @@ def lib() -> C.CDLL:
         L.cdb_driver_scratch_bytes.argtypes = [P, I]
         L.cdb_driver_scratch_bytes.restype = S
         L.cdb_driver_run.argtypes = [P, P, P, P, P, S, P, P, I, P, S, P, P]
-        for f in ("cdb_driver_add_sequence", "cdb_driver_next", "cdb_driver_complete", "cdb_driver_loop_result",
-                  "cdb_driver_get_stats",
-                  "cdb_driver_pages_in_use", "cdb_driver_latencies", "cdb_driver_run"):
+        for f in ("cdb_driver_add_sequence", "cdb_driver_add_request", "cdb_driver_next", "cdb_driver_complete",
+                  "cdb_driver_loop_result", "cdb_driver_get_stats", "cdb_driver_pages_in_use",
+                  "cdb_driver_latencies", "cdb_driver_run"):
             getattr(L, f).restype = C.c_int32
         _bound = True
     return L
@@ -84,10 +87,11 @@ class Driver:
     def __init__(self, max_batch: int, max_active: int, r_max: int, max_seqs: int, max_pages: int,
                  core_pages: int, pre_pages: int = 0, coda_pages: int = 0, has_prelude: bool = False,
                  has_coda: bool = False, refill: bool = True, fixed_depth: bool = False, min_coda_batch: int = 1,
-                 kv_layout: int = KV_FULL, gated: bool = False, lookahead: bool = False, threshold: float = 0.0):
+                 kv_layout: int = KV_FULL, gated: bool = False, lookahead: bool = False, threshold: float = 0.0,
+                 prefill_chunk: int = 0):
         self.cfg = cdb_driver_config(max_batch, max_active, int(refill), int(fixed_depth), min_coda_batch, r_max,
                                      int(has_prelude), int(has_coda), max_seqs, max_pages, pre_pages, core_pages,
-                                     coda_pages, kv_layout, int(gated), int(lookahead), threshold)
+                                     coda_pages, kv_layout, int(gated), int(lookahead), threshold, prefill_chunk)
         self.h = lib().cdb_driver_create(C.byref(self.cfg))
         if not self.h:
             raise ValueError("cdb_driver_create: invalid configuration")
@@ -108,6 +112,19 @@ class Driver:
             q = lib().cdb_driver_add_sequence(self.h, prompt_len, len(dep), dep.ctypes.data, arrival)
         if q < 0:
             raise ValueError("cdb_driver_add_sequence: rejected")
+        return q
+
+    def add_request(self, prompt_ids: Sequence[int], depths: Optional[Sequence[int]], arrival: float = 0.0,
+                    n_decode: Optional[int] = None) -> int:
+        """A request whose prompt the driver prefills (prefill_chunk > 0)."""
+        pr = np.ascontiguousarray(prompt_ids, dtype=np.int32)
+        if depths is None:
+            q = lib().cdb_driver_add_request(self.h, len(pr), pr.ctypes.data, int(n_decode), None, arrival)
+        else:
+            dep = np.ascontiguousarray(depths, dtype=np.int32)
+            q = lib().cdb_driver_add_request(self.h, len(pr), pr.ctypes.data, len(dep), dep.ctypes.data, arrival)
+        if q < 0:
+            raise ValueError("cdb_driver_add_request: rejected")
         return q
 
     def page_table(self) -> np.ndarray:
@@ -168,13 +185,16 @@ class Driver:
     def run(self, model: cdb_model, kv: cdb_kv, state: cdb_state, scratch, first_tokens, ws, tokens_out=None,
             stream=None) -> float:
         """Runs all added requests on the device; returns the wall time in
-        seconds.  tokens_out: optional device int32 [max_seqs][stride]."""
+        seconds.  first_tokens: host ids per sequence, or None when every
+        request was added with add_request.  tokens_out: optional device int32
+        [max_seqs][stride]."""
         from . import CDB_OK, CdbError
-        tok = np.ascontiguousarray(first_tokens, dtype=np.int32)
+        tok = None if first_tokens is None else np.ascontiguousarray(first_tokens, dtype=np.int32)
         secs = C.c_double()
         stride = 0 if tokens_out is None else int(tokens_out.shape[1])
         r = lib().cdb_driver_run(self.h, C.byref(model), C.byref(kv), C.byref(state), _ptr(scratch),
-                                 scratch.numel() * scratch.element_size(), tok.ctypes.data, _ptr(tokens_out), stride,
+                                 scratch.numel() * scratch.element_size(), None if tok is None else tok.ctypes.data,
+                                 _ptr(tokens_out), stride,
                                  _ptr(ws), ws.numel() * ws.element_size(), _stream(stream), C.byref(secs))
         if r != CDB_OK:
             raise CdbError("cdb_driver_run", r)

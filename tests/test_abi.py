@@ -25,7 +25,7 @@ def test_library_exports_every_declared_symbol():
     assert len(names) == 13
     assert set(names) == set(cdb.EXPORTED)
     dnames = declared_functions("libcdb_driver.h")
-    assert len(dnames) == 13
+    assert len(dnames) == 14
     assert set(dnames) == set(cdb_driver.EXPORTED)
     L = cdb.lib()
     for n in names + dnames:
@@ -79,3 +79,13 @@ def test_host_checks_return_errors_without_launching():
     assert L.cdb_boundary_prelude(C.byref(bad), C.byref(kv), C.byref(st), C.byref(rows), 1, 1, 1 << 30,
                                   None) == cdb.CDB_ERR_UNSUPPORTED
     assert cdb.cdb_status_str(cdb.CDB_ERR_CAPACITY) == "capacity exceeded"
+
+
+def test_workspace_size_covers_every_smaller_call():
+    # a workspace sized for max_rows serves every call of fewer rows, although
+    # the per-call layout is not monotonic (the tile GEMM's split-K factor
+    # shrinks as its grid grows)
+    for shape in (cdbgen.TINY, cdbgen.OURO, cdbgen.HUGINN):
+        desc = cdb.make_desc(shape)
+        sizes = [cdb.cdb_workspace_bytes(desc, r) for r in range(1, cdb.MAX_PREFILL_ROWS + 1)]
+        assert all(b >= a for a, b in zip(sizes, sizes[1:])), shape.name

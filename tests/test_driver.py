@@ -11,7 +11,7 @@ import cdbgen
 import paper_2608_09444_amd as cdb
 from paper_2608_09444_amd import cost
 from paper_2608_09444_amd.driver import (KV_FIRST_THEN_SHARED, KV_FULL, KV_SHARED, TICK_CODA, TICK_LOOP,
-                                         TICK_PRELUDE_FIRST, Driver)
+                                         TICK_PREFILL, TICK_PRELUDE_FIRST, Driver)
 
 GOLD = os.path.join(os.path.dirname(__file__), "golden")
 
@@ -234,3 +234,84 @@ def test_flop_bound_at_the_workloads():
     assert cost.flop_bound(cdbgen.OURO, 2.3) == pytest.approx(1.714, abs=2e-3)
     # 50% depth 1, 50% depth 4
     assert cost.flop_bound(cdbgen.OURO, 2.5) == pytest.approx(1.581, abs=2e-3)
+
+
+# ------------------------------------------------------ driver-run prefill
+
+def _prefill_driver(chunk, plens, ndec, arrivals=None, max_active=8, refill=True, r=3):
+    d = Driver(max_batch=4, max_active=max_active, r_max=r, max_seqs=len(plens), max_pages=16,
+               core_pages=16 * r * len(plens), refill=refill, prefill_chunk=chunk)
+    rng = np.random.default_rng(11)
+    for q, (p, n) in enumerate(zip(plens, ndec)):
+        d.add_request(rng.integers(0, 100, p), rng.integers(1, r + 1, n),
+                      arrival=0.0 if arrivals is None else arrivals[q])
+    return d
+
+
+@pytest.mark.parametrize("refill", [True, False])
+def test_prompts_run_as_ordered_chunks_before_their_first_input(refill):
+    plens, ndec, chunk = [37, 5, 16, 64], [3, 4, 2, 5], 16
+    d = _prefill_driver(chunk, plens, ndec, refill=refill)
+    ticks = d.step()
+    done = {q: 0 for q in range(len(plens))}
+    first_prelude = {}
+    for k, t in enumerate(ticks):
+        if t.stage == TICK_PREFILL:
+            q = t.seq[0]
+            assert t.pos[0] == done[q] and 1 <= t.n_rows <= chunk  # chunks in order, none longer than the limit
+            done[q] += t.n_rows
+            assert t.n_continue == int(done[q] == plens[q])
+        elif t.stage == TICK_PRELUDE_FIRST:
+            for i in range(t.n_rows):
+                q = t.seq[i]
+                assert done[q] == plens[q] and t.pos[i] == plens[q]  # the prompt is complete first
+                first_prelude[q] = k
+        elif t.stage == TICK_LOOP:
+            for i in range(t.n_rows):
+                assert t.seq[i] in first_prelude  # no decode work before the first input's prelude
+    assert done == dict(enumerate(plens))
+    st = d.stats()
+    assert st["prefill_tokens"] == sum(plens)
+    assert st["prefill_calls"] == sum(-(-p // chunk) for p in plens)
+    assert st["tokens"] == sum(ndec)
+
+
+def test_prefill_takes_priority_over_loop_steps_but_not_over_the_coda():
+    # a second request arrives while the first decodes: its chunks run before
+    # the next loop step, after any coda that is due
+    d = _prefill_driver(8, [8, 24], [6, 2], arrivals=[0.0, 1.0])
+    seen_second_arrival = False
+    ticks = []
+    while True:
+        t = d.next()
+        if t is None:
+            break
+        if t.stage == 0:
+            d.set_time(t.wait_until)
+            continue
+        if t.stage == TICK_LOOP and not seen_second_arrival and ticks.count(TICK_LOOP) >= 3:
+            d.set_time(1.0)  # the second request is now due
+            seen_second_arrival = True
+        assert d.complete(t) == 0
+        ticks.append(t.stage)
+    # after the arrival time, the three chunks of the second prompt run back to back
+    i = ticks.index(TICK_PREFILL, 1)
+    assert ticks[i:i + 3] == [TICK_PREFILL] * 3
+
+
+def test_prefill_requests_need_the_chunk_setting():
+    d = Driver(max_batch=2, max_active=2, r_max=2, max_seqs=2, max_pages=4, core_pages=16)
+    with pytest.raises(ValueError):
+        d.add_request([1, 2, 3], [1, 2])
+    with pytest.raises(ValueError):
+        Driver(max_batch=2, max_active=2, r_max=2, max_seqs=2, max_pages=4, core_pages=16, prefill_chunk=513)
+
+
+def test_prefill_completion_must_follow_the_plan():
+    d = _prefill_driver(4, [10], [2])
+    t = d.next()
+    assert t.stage == TICK_PREFILL and t.pos[0] == 0 and t.n_rows == 4
+    bad = type(t).from_buffer_copy(t)
+    bad.pos[0] = 4  # a chunk that is not the next one
+    assert d.complete(bad) == -1
+    assert d.complete(t) == 0

@@ -210,3 +210,83 @@ def test_gated_driver_decode_is_schedule_invariant(lookahead):
     assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1]) and a[2] == b[2]
     lo = sum(ndec) * (2 if lookahead else 1)
     assert lo <= a[2] < sum(ndec) * s.r_max  # some tokens exit early, none before the minimum depth
+
+
+def _first_ids_by_prefill(shape, gm, prompts, chunk):
+    """Each prompt through cdb_prefill in the driver's chunking on a pool of its
+    own: the last chunk's greedy id (last-row-only mode) is the first decode
+    input the driver computes (a chunk's rows do not depend on other
+    sequences).  The full-logits mode must give the same id."""
+    R = shape.r_max
+    first = np.zeros(len(prompts), np.int32)
+    for q, p in enumerate(prompts):
+        pages = cdbgen.pages_for(len(p))
+        kv = cdb.PagedKV(shape, 1, pages, pages, pages * R, pages)
+        pt = np.full((1, R + 2, pages), -1, np.int32)
+        for plane in range(R + 2):
+            pt[0, plane, :] = np.arange(pages) + (plane - 1) * pages if 1 <= plane <= R else np.arange(pages)
+        kv.page_table.copy_(torch.from_numpy(pt))
+        ws = cdb.Workspace(gm.desc, chunk)
+        nxt = torch.zeros(chunk, dtype=torch.int32, device="cuda")
+        for p0 in range(0, len(p), chunk):
+            tok = torch.as_tensor(p[p0:p0 + chunk], dtype=torch.int32, device="cuda")
+            cdb.cdb_prefill(gm.model, kv.c, 0, p0, tok, None, nxt, ws.buf)
+        torch.cuda.synchronize()
+        first[q] = int(nxt[0].item())
+        # full logits for the last chunk again (same cache contents): same argmax
+        p0 = (len(p) - 1) // chunk * chunk
+        tok = torch.as_tensor(p[p0:], dtype=torch.int32, device="cuda")
+        lg = torch.empty((len(tok), shape.vocab), dtype=torch.float32, device="cuda")
+        ids = torch.empty(len(tok), dtype=torch.int32, device="cuda")
+        cdb.cdb_prefill(gm.model, kv.c, 0, p0, tok, lg, ids, ws.buf)
+        torch.cuda.synchronize()
+        assert int(ids[-1].item()) == first[q]
+        assert cdb.cdb_read_device_error(ws.buf) == 0
+    return first
+
+
+def _decode_with_driver_prefill(shape, gm, prompts, ndec, depths, chunk, **cfg):
+    R = shape.r_max
+    n = len(prompts)
+    T = [len(p) + k for p, k in zip(prompts, ndec)]
+    max_pages = max(cdbgen.pages_for(t) for t in T)
+    tot = sum(cdbgen.pages_for(t) for t in T)
+    d = drv.Driver(max_seqs=n, max_pages=max_pages, core_pages=tot * R, pre_pages=tot, coda_pages=tot,
+                   has_prelude=shape.n_prelude > 0, has_coda=shape.n_coda > 0, r_max=R, prefill_chunk=chunk, **cfg)
+    for q in range(n):
+        d.add_request(prompts[q], depths[q])
+    kv = cdb.PagedKV(shape, n, max_pages, tot, tot * R, tot)
+    ws = cdb.Workspace(gm.desc, max(256, chunk))
+    state = cdb.State(shape, n)
+    scratch = torch.empty(d.scratch_bytes(shape.vocab), dtype=torch.uint8, device="cuda")
+    out_ids = torch.full((n, max(ndec)), -1, dtype=torch.int32, device="cuda")
+    secs = d.run(gm.model, kv.c, state.c, scratch, None, ws.buf, tokens_out=out_ids)
+    torch.cuda.synchronize()
+    assert cdb.cdb_read_device_error(ws.buf) == 0
+    return out_ids.cpu().numpy(), d.stats(), secs
+
+
+def test_driver_prefill_chunks_decode_like_the_oracle():
+    s = cdbgen.TINY
+    chunk = 16
+    _say(f"[gpu] driver-run prefill {s.name}, chunks of {chunk}")
+    w = cdbgen.model_weights(s)
+    gm = cdb.DeviceModel(s, w)
+    prompts, ndec, depths = _requests(s)
+    n = len(prompts)
+    first = _first_ids_by_prefill(s, gm, prompts, chunk)
+    runs = {}
+    for name, cfg in (("refill", dict(max_batch=4, max_active=n)),
+                      ("no-refill", dict(max_batch=3, max_active=n, refill=False)),
+                      ("two-at-a-time", dict(max_batch=2, max_active=2))):
+        ids, st, secs = _decode_with_driver_prefill(s, gm, prompts, ndec, depths, chunk, **cfg)
+        _say(f"[gpu]   {name}: {st} in {secs * 1e3:.1f} ms")
+        assert st["tokens"] == sum(ndec)
+        assert st["prefill_tokens"] == sum(len(p) for p in prompts)
+        assert st["prefill_calls"] == sum(-(-len(p) // chunk) for p in prompts)
+        runs[name] = ids
+    for name, ids in runs.items():
+        assert np.array_equal(ids, runs["refill"]), name
+    checked = _check_against_oracle(s, w, prompts, ndec, depths, first, runs["refill"], drv.KV_FULL)
+    _say(f"[gpu]   {checked} greedy ids checked against the oracle")
+    assert checked >= 0.3 * (sum(ndec) + n)
