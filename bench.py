@@ -143,6 +143,7 @@ def cpu_baseline(shape, w, rows_np, n_sample, threads, min_s=10.0):
     os.environ["OMP_NUM_THREADS"] = str(threads)
     import cdbgen
     import oracle
+    threads = oracle.set_threads(threads)
     m = oracle.Model(shape, w, bf16_storage=True)
     idx = np.arange(n_sample)
     pos = rows_np["pos"][idx]
@@ -226,7 +227,63 @@ def e2e_decode(shape, dm, kv, n_seqs, prompt, n_decode, seed=3):
     return res
 
 
-def serving_leg(shape, dm, n_req, rate=20.0, max_batch=64, chunk=512, core_pages=24576):
+def batch_sweep(shape, dm, sizes=(16, 32, 64, 128, 256), pos_lo=512, pos_hi=767, steps=10, warmup=3):
+    """cdb_loop_step at several batch sizes on mid-decode refill batches of the
+    same position and depth distributions.  Each row maps its own pages: its
+    loop plane over the whole context plus the page at pos of every deeper
+    plane (copy-on-exit destinations)."""
+    import numpy as np
+    import torch
+
+    import cdbgen
+    import paper_2608_09444_amd as cdb
+    R = shape.r_max
+    out = []
+    for n in sizes:
+        rows_np = cdbgen.decode_snapshot(n, cdbgen.OURO_DEPTHS, R, pos_lo, pos_hi, stream=20 + n)
+        max_pages = cdbgen.pages_for(pos_hi + 1)
+        pt = np.full((n, R + 2, max_pages), -1, np.int32)
+        nxt = 0
+        for i in range(n):
+            plane = int(rows_np["c"][i]) + 1
+            pg = cdbgen.pages_for(int(rows_np["pos"][i]) + 1)
+            pt[i, plane, :pg] = np.arange(nxt, nxt + pg)
+            nxt += pg
+            for pl in range(plane + 1, R + 1):
+                pt[i, pl, pg - 1] = nxt
+                nxt += 1
+        kv = cdb.PagedKV(shape, n, max_pages, 0, nxt, 0, fill="random")
+        kv.core.normal_(0.0, 1.0)
+        kv.page_table.copy_(torch.from_numpy(pt))
+        state = cdb.State(shape, n)
+        state.h.normal_(0.0, 1.0)
+        rows = cdb.Rows(np.arange(n, dtype=np.int32), np.arange(n, dtype=np.int32), rows_np["pos"], rows_np["c"],
+                        rows_np["depth"])
+        so = cdb.StepOut(n)
+        ws = cdb.Workspace(dm.desc, n)
+        st = torch.cuda.current_stream()
+        for _ in range(warmup):
+            cdb.cdb_loop_step(dm.model, kv.c, state.c, rows.c, so.c, ws.buf)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        for _ in range(steps):
+            cdb.cdb_loop_step(dm.model, kv.c, state.c, rows.c, so.c, ws.buf)
+        e1.record(st)
+        e1.synchronize()
+        if cdb.cdb_read_device_error(ws.buf) != 0:
+            raise RuntimeError(f"device error in the {n}-row sweep step")
+        ms = e0.elapsed_time(e1) / steps
+        sb = step_bytes(shape, rows_np)
+        out.append({"rows": n, "ms_per_step": round(ms, 4), "rows_per_s": round(n / (ms * 1e-3), 1),
+                    "hbm_frac": round(sb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)})
+        log(f"sweep {n} rows: {ms:.3f} ms/step, {n / (ms * 1e-3):.0f} rows/s")
+        del kv, state, rows, so, ws
+        torch.cuda.empty_cache()
+    return out
+
+
+def serving_leg(shape, dm, n_req, rate=20.0, max_batch=64, chunk=512, core_pages=24576, fixed_depth=False):
     """A serving trace of the ouro-shaped model: Poisson arrivals at `rate`
     requests/s, prompt lengths lognormal (median 300, sigma 1, [16, 4096]),
     output lengths lognormal (median 400, sigma 1, [16, 2048]), categorical
@@ -247,7 +304,7 @@ def serving_leg(shape, dm, n_req, rate=20.0, max_batch=64, chunk=512, core_pages
     arrivals = cdbgen.poisson_arrivals(n_req, rate)
     max_pages = cdbgen.pages_for(int(plen.max() + olen.max()))
     d = drv.Driver(max_batch=max_batch, max_active=max_batch, r_max=R, max_seqs=n_req, max_pages=max_pages,
-                   core_pages=core_pages, prefill_chunk=chunk)
+                   core_pages=core_pages, prefill_chunk=chunk, fixed_depth=fixed_depth)
     for q in range(n_req):
         d.add_request(cdbgen.prompt_ids(shape.vocab, 1, int(plen[q]), stream=q)[0],
                       cdbgen.draw_depths(wl.depth, int(olen[q]), R, stream=1000 + q), arrival=float(arrivals[q]))
@@ -255,7 +312,8 @@ def serving_leg(shape, dm, n_req, rate=20.0, max_batch=64, chunk=512, core_pages
     state = cdb.State(shape, n_req)
     ws = cdb.Workspace(dm.desc, chunk)
     scratch = torch.empty(d.scratch_bytes(shape.vocab), dtype=torch.uint8, device="cuda")
-    log(f"serving: {n_req} requests at {rate}/s, {int(plen.sum())} prompt + {int(olen.sum())} output tokens")
+    log(f"serving{' (fixed depth)' if fixed_depth else ''}: {n_req} requests at {rate}/s, {int(plen.sum())} prompt + "
+        f"{int(olen.sum())} output tokens")
     secs = d.run(dm.model, kv.c, state.c, scratch, None, ws.buf)
     if cdb.cdb_read_device_error(ws.buf) != 0:
         raise RuntimeError("device error in the serving run")
@@ -330,6 +388,7 @@ def main():
     ap.add_argument("--cpu-sample", type=int, default=16, help="rows in the CPU-oracle sample (0 = skip)")
     ap.add_argument("--no-e2e", action="store_true", help="skip the whole-decode driver runs")
     ap.add_argument("--no-prefill", action="store_true", help="skip the chunked-prefill timing")
+    ap.add_argument("--no-sweep", action="store_true", help="skip the loop-step batch-size sweep")
     ap.add_argument("--serving-requests", type=int, default=200,
                     help="requests in the serving-trace run (0 = skip; 2000 is the full trace)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -389,6 +448,10 @@ def main():
     attn_gbs = ab / (attn_ms * 1e-3) / 1e9
     log(f"attention {attn_ms * 1e3:.1f} us/launch, {ab / 1e6:.1f} MB -> {attn_gbs:.0f} GB/s")
 
+    sweep = None
+    if not args.no_sweep:
+        sweep = batch_sweep(shape, dm)
+
     e2e = None
     if not args.no_e2e:
         e2e = e2e_decode(shape, dm, kv, n_rows, pos_lo, pos_hi + 1 - pos_lo)
@@ -399,13 +462,23 @@ def main():
 
     serving = None
     if args.serving_requests > 0:
-        serving = serving_leg(shape, dm, args.serving_requests)
+        serving = {"cdb_refill": serving_leg(shape, dm, args.serving_requests),
+                   "cb_fixed_depth": serving_leg(shape, dm, args.serving_requests, fixed_depth=True)}
+        a, b = serving["cdb_refill"], serving["cb_fixed_depth"]
+        serving["throughput_ratio"] = round(a["tokens_per_s"] / b["tokens_per_s"], 4)
+        serving["p50_latency_reduction"] = round(1 - a["normalized_latency_s"]["p50"] /
+                                                 b["normalized_latency_s"]["p50"], 4)
+        serving["p99_latency_reduction"] = round(1 - a["normalized_latency_s"]["p99"] /
+                                                 b["normalized_latency_s"]["p99"], 4)
 
     cpu = None
     if args.cpu_sample > 0:
         threads = min(16, os.cpu_count() or 1)
         log(f"cpu baseline on {args.cpu_sample} rows, {threads} threads")
         cpu = cpu_baseline(shape, w, rows_np, args.cpu_sample, threads)
+        log("cpu baseline on 1 row, 1 thread")
+        one = cpu_baseline(shape, w, rows_np, 1, 1, min_s=8.0)
+        cpu["single_core"] = {"value": one["value"], "cores": 1, "sample": one["sample"]}
 
     res = {
         "metric": "mixed-depth loop-step tokens/s (Ouro-1.4B-shaped, bs=64); % HBM/MFMA roofline",
@@ -435,6 +508,7 @@ def main():
                           "frac": round(sb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                           "flops": step_flops(shape, rows_np)},
         "cpu_baseline": cpu,
+        "batch_sweep": sweep,
         "e2e": e2e,
         "prefill": prefill,
         "serving": serving,

@@ -82,6 +82,8 @@ def _declare(L):
     L.orc_loop_step.argtypes = [_P, _P, _P, _P, _P, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]
     L.orc_coda.argtypes = [_P, _P, _P, _P, _I, _I, _P, _P, _P, _P, _P]
     L.orc_exit_compact.argtypes = [_I, _P, _P, _I, _P, _P, _P, _P]
+    L.orc_set_threads.argtypes = [_I]
+    L.orc_set_threads.restype = _I
     L.orc_rmsnorm.argtypes = [_P, _I, C.c_double, _P]
     L.orc_rope.argtypes = [_P, _I, _I, _I, C.c_double]
     L.orc_attend.argtypes = [_P, _P, _P, _I, _I, _P]
@@ -323,3 +325,8 @@ def silu(x: float) -> float:
 
 def to_bf16(x: float) -> float:
     return lib().orc_to_bf16(x)
+
+
+def set_threads(n: int) -> int:
+    """Threads of the oracle's OpenMP loops over rows (for timing runs)."""
+    return int(lib().orc_set_threads(n))

@@ -49,6 +49,7 @@
  *                        scheduler in oracle/executor.py.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -848,3 +849,9 @@ void orc_attend(const double* q, const double* k, const double* v, int32_t n, in
 }
 double orc_silu(double x) { return silu(x); }
 double orc_to_bf16(double x) { return to_bf16(x); }
+
+/* Threads of the OpenMP loops over independent rows (timing runs only). */
+int orc_set_threads(int n) {
+    if (n > 0) omp_set_num_threads(n);
+    return omp_get_max_threads();
+}

@@ -68,6 +68,9 @@ int orc_loop_step(const orc_desc* m, const orc_weights* w, const orc_paged* p, d
 int orc_coda(const orc_desc* m, const orc_weights* w, const orc_paged* p, const double* state_h,
              int32_t n_slots, int32_t n, const int32_t* slot, const int32_t* seq, const int32_t* pos,
              double* logits, int32_t* next_ids);
+/* Threads of the OpenMP loops over rows (timing only); returns the count in use. */
+int orc_set_threads(int n);
+
 int orc_exit_compact(int32_t n, const int32_t* c, const int32_t* depth, int32_t r_max, uint8_t* exit_mask,
                      int32_t* cont, int32_t* exited, int32_t* counts);
 
