@@ -406,7 +406,7 @@ __device__ __forceinline__ void qkv_tile_epilogue(const floatx16 (&acc)[2][2], i
 // buffered in registers.  Each wave owns its outputs, so the epilogue runs from
 // the accumulators: column n's RoPE / SwiGLU partner n ^ 16 is element j ^ 8 of
 // the same lane.
-template <int EPI>
+template <int EPI, bool LDS>
 __global__ __launch_bounds__(256) void k_gemm_mn(GemmArgs ga, EpiArgs ea) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int KS = ga.K >> 4;
@@ -425,49 +425,104 @@ __global__ __launch_bounds__(256) void k_gemm_mn(GemmArgs ga, EpiArgs ea) {
 #pragma unroll
             for (int j = 0; j < 16; ++j) acc[a][b][j] = 0.f;
 
-    // tiles past the matrix re-read the last one (their results are not stored)
-    const u32x4* wsrc[2];
-    const u32x4* xsrc[2];
+    if constexpr (!LDS) {
+        // tiles past the matrix re-read the last one (their results are not stored)
+        const u32x4* wsrc[2];
+        const u32x4* xsrc[2];
+    #pragma unroll
+        for (int a = 0; a < 2; ++a) {
+            wsrc[a] = reinterpret_cast<const u32x4*>(ga.Wp) + (size_t)min(nt0 + a, stripes - 1) * KS * 64 + lane;
+            xsrc[a] = reinterpret_cast<const u32x4*>(ga.X) + (size_t)min(mt0 + a, mtiles - 1) * KS * 64 + lane;
+        }
+        constexpr int CH = 4;
+        u32x4 wa[CH][2], wb[CH][2], xa[CH][2], xb[CH][2];
+        auto load = [&](u32x4 (&w)[CH][2], u32x4 (&x)[CH][2], int c0) {
+    #pragma unroll
+            for (int i = 0; i < CH; ++i) {
+                const int ks = min(c0 + i, k1 - 1);
+    #pragma unroll
+                for (int a = 0; a < 2; ++a) {
+                    w[i][a] = wsrc[a][(size_t)ks * 64];
+                    x[i][a] = xsrc[a][(size_t)ks * 64];
+                }
+            }
+        };
+        auto compute = [&](const u32x4 (&w)[CH][2], const u32x4 (&x)[CH][2], int c0) {
+    #pragma unroll
+            for (int i = 0; i < CH; ++i) {
+                const uint32_t keep = c0 + i < k1 ? 0xffffffffu : 0u;
+    #pragma unroll
+                for (int a = 0; a < 2; ++a) {
+                    const bf16x8 wv = __builtin_bit_cast(bf16x8, w[i][a] & keep);
+    #pragma unroll
+                    for (int b = 0; b < 2; ++b)
+                        acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wv, __builtin_bit_cast(bf16x8, x[i][b]),
+                                                                            acc[a][b], 0, 0, 0);
+                }
+            }
+        };
+        if (k0 < k1) load(wa, xa, k0);
+        for (int c0 = k0; c0 < k1; c0 += 2 * CH) {
+            if (c0 + CH < k1) load(wb, xb, c0 + CH);
+            compute(wa, xa, c0);
+            if (c0 + 2 * CH < k1) load(wa, xa, c0 + 2 * CH);
+            if (c0 + CH < k1) compute(wb, xb, c0 + CH);
+        }
+    } else {
+        // LDS ring of 2 stages of 4 k steps: a stage holds the workgroup's 4
+        // weight tiles and 4 activation tiles of each k step (1 KiB each, lane
+        // order), copied global -> LDS by the waves with direct loads (tile i of a
+        // stage by wave i % 4); each wave then reads its 2 + 2 operands per k step
+        constexpr int CH = 4, NBUF = 2;
+        constexpr int TPS = CH * 8;   // tiles per stage
+        constexpr int LPW = TPS / 4;  // loads per wave per stage
+        extern __shared__ __align__(16) unsigned char lds_ring[];
+        const int ntb = blockIdx.x * 4, mtb = blockIdx.y * 4;
+        const u32x4* Wg = reinterpret_cast<const u32x4*>(ga.Wp);
+        const u32x4* Xg = reinterpret_cast<const u32x4*>(ga.X);
+        const int nst = (k1 - k0 + CH - 1) / CH;
+        auto issue = [&](int st) {
+            unsigned char* base = lds_ring + (size_t)(st % NBUF) * TPS * 1024;
 #pragma unroll
-    for (int a = 0; a < 2; ++a) {
-        wsrc[a] = reinterpret_cast<const u32x4*>(ga.Wp) + (size_t)min(nt0 + a, stripes - 1) * KS * 64 + lane;
-        xsrc[a] = reinterpret_cast<const u32x4*>(ga.X) + (size_t)min(mt0 + a, mtiles - 1) * KS * 64 + lane;
-    }
-    constexpr int CH = 4;
-    u32x4 wa[CH][2], wb[CH][2], xa[CH][2], xb[CH][2];
-    auto load = [&](u32x4 (&w)[CH][2], u32x4 (&x)[CH][2], int c0) {
+            for (int i = 0; i < LPW; ++i) {
+                const int t = wave + 4 * i;  // tile within the stage
+                const int kk = t >> 3, slot = t & 7;
+                const int ks = min(k0 + st * CH + kk, k1 - 1);
+                const u32x4* src = slot < 4 ? Wg + ((size_t)min(ntb + slot, stripes - 1) * KS + ks) * 64
+                                            : Xg + ((size_t)min(mtb + slot - 4, mtiles - 1) * KS + ks) * 64;
+                __builtin_amdgcn_global_load_lds(src + lane, (__attribute__((address_space(3))) void*)(base + t * 1024),
+                                                 16, 0, 0);
+            }
+        };
+        if (nst > 0) issue(0);
+        const int wn = wave & 1, wm = wave >> 1;
+        for (int st = 0; st < nst; ++st) {
+            // this wave's loads of stage st are done; the barrier covers the
+            // other waves' loads and every wave's reads of the stage refilled next
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            __builtin_amdgcn_s_barrier();
+            if (st + 1 < nst) issue(st + 1);
+            const unsigned char* base = lds_ring + (size_t)(st % NBUF) * TPS * 1024 + lane * 16;
 #pragma unroll
-        for (int i = 0; i < CH; ++i) {
-            const int ks = min(c0 + i, k1 - 1);
+            for (int i = 0; i < CH; ++i) {
+                const uint32_t keep = k0 + st * CH + i < k1 ? 0xffffffffu : 0u;
+                u32x4 w[2], x[2];
 #pragma unroll
-            for (int a = 0; a < 2; ++a) {
-                w[i][a] = wsrc[a][(size_t)ks * 64];
-                x[i][a] = xsrc[a][(size_t)ks * 64];
+                for (int a = 0; a < 2; ++a) {
+                    w[a] = *reinterpret_cast<const u32x4*>(base + (i * 8 + wn * 2 + a) * 1024);
+                    x[a] = *reinterpret_cast<const u32x4*>(base + (i * 8 + 4 + wm * 2 + a) * 1024);
+                }
+#pragma unroll
+                for (int a = 0; a < 2; ++a) {
+                    const bf16x8 wv = __builtin_bit_cast(bf16x8, w[a] & keep);
+#pragma unroll
+                    for (int b = 0; b < 2; ++b)
+                        acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wv, __builtin_bit_cast(bf16x8, x[b]),
+                                                                            acc[a][b], 0, 0, 0);
+                }
             }
         }
-    };
-    auto compute = [&](const u32x4 (&w)[CH][2], const u32x4 (&x)[CH][2], int c0) {
-#pragma unroll
-        for (int i = 0; i < CH; ++i) {
-            const uint32_t keep = c0 + i < k1 ? 0xffffffffu : 0u;
-#pragma unroll
-            for (int a = 0; a < 2; ++a) {
-                const bf16x8 wv = __builtin_bit_cast(bf16x8, w[i][a] & keep);
-#pragma unroll
-                for (int b = 0; b < 2; ++b)
-                    acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wv, __builtin_bit_cast(bf16x8, x[i][b]),
-                                                                        acc[a][b], 0, 0, 0);
-            }
-        }
-    };
-    if (k0 < k1) load(wa, xa, k0);
-    for (int c0 = k0; c0 < k1; c0 += 2 * CH) {
-        if (c0 + CH < k1) load(wb, xb, c0 + CH);
-        compute(wa, xa, c0);
-        if (c0 + 2 * CH < k1) load(wa, xa, c0 + 2 * CH);
-        if (c0 + CH < k1) compute(wb, xb, c0 + CH);
     }
-
     if constexpr (EPI == EPI_QKV) {
         qkv_tile_epilogue(acc, nt0, mt0, lane, stripes, ga.M, ea);
         return;
@@ -554,10 +609,25 @@ static hipError_t launch_epi(const GemmArgs& ga, const EpiArgs& ea, int ns, hipS
     }
 }
 
+// The LDS-staged tile path pays off for the wide projections (gate/up and a
+// full-width LM head: 20% faster at 512 rows); q/k/v, O and down keep the
+// direct-load path.
 template <int EPI>
 static hipError_t launch_mn(const GemmArgs& ga, const EpiArgs& ea, hipStream_t st) {
     dim3 grid((ga.N / 32 + 3) / 4, (ga.M + 127) / 128, ga.S);
-    k_gemm_mn<EPI><<<grid, 256, 0, st>>>(ga, ea);
+    const bool lds = EPI == EPI_SWIGLU || (EPI == EPI_STORE && ga.N >= 8192);
+    if (!lds) {
+        k_gemm_mn<EPI, false><<<grid, 256, 0, st>>>(ga, ea);
+        return hipGetLastError();
+    }
+    static bool attr_set = false;
+    if (!attr_set) {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm_mn<EPI, true>),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, 64 * 1024);
+        if (e != hipSuccess) return e;
+        attr_set = true;
+    }
+    k_gemm_mn<EPI, true><<<grid, 256, 2 * 4 * 8 * 1024, st>>>(ga, ea);
     return hipGetLastError();
 }
 
