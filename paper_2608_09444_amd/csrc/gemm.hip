@@ -333,65 +333,70 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs ga, EpiArgs ea) {
     stripe_epilogue<EPI>(fin, fld, nt, NS, mcap, s, tid, nthr, ga, ea, qs);
 }
 
-// q/k/v epilogue of a wave's 2 x 2 accumulator tiles.  Every input the stores
-// need (each row's write page and slot, the RoPE factors of the lane's 8
-// rotary pairs per stripe and m-tile) is loaded before the first store.
-// Lane l holds column n = (j/4)*8 + (l/32)*4 + j%4 of a stripe in element j:
-// rotary pair jj = n % 16, first half for j < 8, its partner in element j + 8.
-__device__ __forceinline__ void qkv_tile_epilogue(const floatx16 (&acc)[2][2], int nt0, int mt0, int lane,
-                                                  int stripes, int M, const EpiArgs& ea) {
+// q/k/v epilogue of a wave's 64-row x 64-column block (stripes nt0, nt0 + 1;
+// rows m0 .. m0 + 63) staged in LDS as fin[n][m - m0] (pitch fld): each lane
+// takes a run of consecutive dims of one row, so the stores are 16-byte
+// vectors (4 fp32 q values, or 8 bf16 K/V values) instead of one column of 32
+// rows per instruction.  Same arithmetic per element as epilogue_elem.
+__device__ __forceinline__ void qkv_block_epilogue(const float* fin, int fld, int nt0, int stripes, int m0, int M,
+                                                   int lane, const EpiArgs& ea) {
     const int gph = ea.hd >> 5, hg = ea.H * gph, half_hd = ea.hd >> 1;
-    int m[2], pid[2], tok[2];
-#pragma unroll
-    for (int b = 0; b < 2; ++b) {
-        m[b] = (mt0 + b) * 32 + (lane & 31);
-        const bool ok = m[b] < M;
-        pid[b] = ok ? ea.kvpid[m[b]] : -1;
-        tok[b] = ok ? ea.pos[m[b]] % kPage : 0;
-    }
-    float2 cs[2][2][8];
-#pragma unroll
-    for (int a = 0; a < 2; ++a) {
-        const int g = min(nt0 + a, stripes - 1);
-        const int part = g / hg, gi = (g - part * hg) % gph;
-#pragma unroll
-        for (int b = 0; b < 2; ++b)
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const int jj = (j >> 2) * 8 + (lane >> 5) * 4 + (j & 3);
-                cs[a][b][j] = (part < 2 && m[b] < M) ? ea.rope[(size_t)m[b] * half_hd + gi * 16 + jj]
-                                                     : make_float2(1.f, 0.f);
-            }
-    }
 #pragma unroll
     for (int a = 0; a < 2; ++a) {
         const int g = nt0 + a;
-        if (g >= stripes) continue;
+        if (g >= stripes) break;
         const int part = g / hg, rem = g - part * hg;
         const int head = rem / gph, gi = rem - head * gph;
+        const float* f = fin + a * 32 * fld;
+        if (part == 0) {
+            for (int e = lane; e < 64 * 8; e += 64) {  // (row, half, 4-pair run)
+                const int ml = e >> 3, half = (e >> 2) & 1, j4 = (e & 3) * 4;
+                const int m = m0 + ml;
+                if (m >= M) continue;
+                const float2* cs = ea.rope + (size_t)m * half_hd + gi * 16 + j4;
+                float o[4];
 #pragma unroll
-        for (int b = 0; b < 2; ++b) {
-            if (m[b] >= M) continue;
+                for (int i = 0; i < 4; ++i) {
+                    const int jj = j4 + i;
+                    const float val = f[(half * 16 + jj) * fld + ml], partner = f[((half ^ 1) * 16 + jj) * fld + ml];
+                    const float2 c = cs[i];
+                    const float xf = half ? partner : val, xs = half ? val : partner;
+                    o[i] = half ? (xs * c.x + xf * c.y) : (xf * c.x - xs * c.y);
+                }
+                float* dst = ea.q + (size_t)m * (ea.H * ea.hd) + head * ea.hd + gi * 16 + j4 + half * half_hd;
+                *reinterpret_cast<float4*>(dst) = make_float4(o[0], o[1], o[2], o[3]);
+            }
+        } else {
+            for (int e = lane; e < 64 * 4; e += 64) {  // (row, half, 8-pair run)
+                const int ml = e >> 2, half = (e >> 1) & 1, j8 = (e & 1) * 8;
+                const int m = m0 + ml;
+                if (m >= M) continue;
+                const int pid = ea.kvpid[m];  // -1: unmapped (reported by the row-entry kernel)
+                if (pid < 0) continue;
+                const int tok = ea.pos[m] % kPage;
+                uint32_t w[4];
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const int jj = (j >> 2) * 8 + (lane >> 5) * 4 + (j & 3);
-                const float x1 = acc[a][b][j], x2 = acc[a][b][j + 8];  // dims jj and jj + hd/2 of the pair
-                float y1 = x1, y2 = x2;
-                if (part < 2) {
-                    y1 = x1 * cs[a][b][j].x - x2 * cs[a][b][j].y;
-                    y2 = x2 * cs[a][b][j].x + x1 * cs[a][b][j].y;
+                for (int i = 0; i < 8; i += 2) {
+                    float o2[2];
+#pragma unroll
+                    for (int b = 0; b < 2; ++b) {
+                        const int jj = j8 + i + b;
+                        const float val = f[(half * 16 + jj) * fld + ml];
+                        float outv = val;
+                        if (part == 1) {
+                            const float partner = f[((half ^ 1) * 16 + jj) * fld + ml];
+                            const float2 c = ea.rope[(size_t)m * half_hd + gi * 16 + jj];
+                            const float xf = half ? partner : val, xs = half ? val : partner;
+                            outv = half ? (xs * c.x + xf * c.y) : (xf * c.x - xs * c.y);
+                        }
+                        o2[b] = outv;
+                    }
+                    w[i / 2] = (uint32_t)f2bf(o2[0]) | ((uint32_t)f2bf(o2[1]) << 16);
                 }
-                const int d1 = gi * 16 + jj, d2 = d1 + half_hd;
-                if (part == 0) {
-                    float* qrow = ea.q + (size_t)m[b] * (ea.H * ea.hd) + head * ea.hd;
-                    qrow[d1] = y1;
-                    qrow[d2] = y2;
-                } else if (pid[b] >= 0) {
-                    uint16_t* dst = ea.kv.pool + kv_offset(ea.kv.layer, pid[b], ea.kv.n_pages, part - 1, head, ea.H,
-                                                           tok[b], ea.hd);
-                    dst[d1] = f2bf(y1);
-                    dst[d2] = f2bf(y2);
-                }
+                const KvTarget& kv = ea.kv;
+                uint16_t* dst = kv.pool + kv_offset(kv.layer, pid, kv.n_pages, part - 1, head, ea.H, tok, ea.hd) +
+                                gi * 16 + j8 + half * half_hd;
+                *reinterpret_cast<u32x4*>(dst) = u32x4{w[0], w[1], w[2], w[3]};
             }
         }
     }
@@ -524,7 +529,20 @@ __global__ __launch_bounds__(256) void k_gemm_mn(GemmArgs ga, EpiArgs ea) {
         }
     }
     if constexpr (EPI == EPI_QKV) {
-        qkv_tile_epilogue(acc, nt0, mt0, lane, stripes, ga.M, ea);
+        // the wave's block through its own LDS region (64 columns x 65-float rows)
+        extern __shared__ __align__(16) unsigned char lds_ring[];
+        constexpr int fld = 65;
+        float* fin = reinterpret_cast<float*>(lds_ring) + wave * 64 * fld;
+#pragma unroll
+        for (int a = 0; a < 2; ++a)
+#pragma unroll
+            for (int b = 0; b < 2; ++b)
+#pragma unroll
+                for (int j = 0; j < 16; ++j) {
+                    const int n = a * 32 + (j >> 2) * 8 + (lane >> 5) * 4 + (j & 3);
+                    fin[n * fld + b * 32 + (lane & 31)] = acc[a][b][j];
+                }
+        qkv_block_epilogue(fin, fld, nt0, stripes, mt0 * 32, ga.M, lane, ea);
         return;
     }
     const QkvStage qs{};
@@ -617,7 +635,17 @@ static hipError_t launch_mn(const GemmArgs& ga, const EpiArgs& ea, hipStream_t s
     dim3 grid((ga.N / 32 + 3) / 4, (ga.M + 127) / 128, ga.S);
     const bool lds = EPI == EPI_SWIGLU || (EPI == EPI_STORE && ga.N >= 8192);
     if (!lds) {
-        k_gemm_mn<EPI, false><<<grid, 256, 0, st>>>(ga, ea);
+        // the q/k/v epilogue stages each wave's 64 x 64 block in LDS
+        if constexpr (EPI == EPI_QKV) {
+            static bool qkv_attr = false;
+            if (!qkv_attr) {
+                hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm_mn<EPI, false>),
+                                                   hipFuncAttributeMaxDynamicSharedMemorySize, 4 * 64 * 65 * 4);
+                if (e != hipSuccess) return e;
+                qkv_attr = true;
+            }
+        }
+        k_gemm_mn<EPI, false><<<grid, 256, EPI == EPI_QKV ? 4 * 64 * 65 * 4 : 0, st>>>(ga, ea);
         return hipGetLastError();
     }
     static bool attr_set = false;
