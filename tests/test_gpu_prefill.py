@@ -164,3 +164,14 @@ def test_prefill_huginn_width_head_dim_96():
     _say(f"[gpu] prefill Huginn widths (2-1-2, r_max 2): chunks 24 + 16")
     err = run_prefill(s, w, prompt, [24, 16], sensitivity=True)
     _say(f"[gpu]   {err}")
+
+
+def test_prefill_ouro_width_second_chunk_over_earlier_context():
+    # the second chunk's rows attend to 320 earlier positions and to each
+    # other: key blocks stream from two chunks' pages, every wave takes several
+    s, w = _core_prefix(cdbgen.OURO, cdbgen.model_weights(cdbgen.OURO), 2)
+    prompt = cdbgen.prompt_ids(s.vocab, 1, 620, seed=84)[0]
+    _say(f"[gpu] prefill Ouro widths, 2 core layers: chunks 320 + 300")
+    err = run_prefill(s, w, prompt, [320, 300], check_rows=[0, 319, 320, 321, 400, 511, 512, 600, 619],
+                      sensitivity=True)
+    _say(f"[gpu]   {err}")
