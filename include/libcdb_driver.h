@@ -150,7 +150,8 @@ size_t cdb_driver_scratch_bytes(const cdb_driver* d, int32_t vocab);
  * exit decisions are copied back after every loop step and fed to the
  * scheduler (one step late with lookahead); CDB_ERR_INVALID_ARG if they ever
  * disagree with the exits applied.  Returns a cdb_status; *seconds = wall
- * time including the final synchronisation. */
+ * time including the final synchronisation.  With the environment variable
+ * CDB_DRIVER_PROGRESS set, a progress line goes to stderr every 10 s. */
 int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, const cdb_state* state, void* scratch,
                        size_t scratch_bytes, const int32_t* first_tokens, int32_t* tokens_out,
                        int32_t tokens_stride, void* ws, size_t ws_bytes, hipStream_t stream, double* seconds);

@@ -27,6 +27,8 @@
 // prelude's tokens for the next tick without any host round trip.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+#include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <algorithm>
@@ -604,9 +606,18 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
     cdb_driver_tick t;
     int32_t status = status0;
     std::vector<int32_t> toks(256), npos(256);
+    // CDB_DRIVER_PROGRESS set: a line on stderr every 10 s of a long run
+    const bool progress = getenv("CDB_DRIVER_PROGRESS") != nullptr;
+    double next_report = 10.0;
     const auto t0 = std::chrono::steady_clock::now();
     while (status == CDB_OK) {
         d->now = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+        if (progress && d->now >= next_report) {
+            fprintf(stderr, "[driver] %.0f s: %lld tokens, %lld loop steps, %lld prompt tokens, %d active\n", d->now,
+                    (long long)d->stats.tokens, (long long)d->stats.loop_steps, (long long)d->stats.prefill_tokens,
+                    d->active);
+            next_report += 10.0;
+        }
         const int32_t r = cdb_driver_next(d, &t);
         if (r == 0) break;
         if (r < 0) continue;  // the next request has not arrived yet
