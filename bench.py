@@ -224,6 +224,29 @@ def e2e_decode(shape, dm, kv, n_seqs, prompt, n_decode, seed=3):
     cb = res["cb_fixed_depth"]["tokens_per_s"]
     res["speedup_refill_vs_cb"] = round(res["cdb_refill"]["tokens_per_s"] / cb, 4)
     res["speedup_no_refill_vs_cb"] = round(res["cdb_no_refill"]["tokens_per_s"] / cb, 4)
+
+    # device-decided exits (gate score >= 0.5): with the lookahead the host
+    # plans each loop step from decisions one step old; without it every loop
+    # step waits for its own decisions (the GPU idles for the round trip)
+    def run_gated(lookahead):
+        d = drv.Driver(max_batch=64, max_active=n_seqs, r_max=R, max_seqs=n_seqs, max_pages=max_pages,
+                       core_pages=kv.c.core_pages, gated=True, lookahead=lookahead, threshold=0.5)
+        for q in range(n_seqs):
+            d.add_sequence(prompt, None, n_decode=n_decode)
+        scratch = torch.empty(d.scratch_bytes(shape.vocab), dtype=torch.uint8, device="cuda")
+        secs = d.run(dm.model, kv.c, state.c, scratch, first, ws.buf, tokens_out=out_ids)
+        if cdb.cdb_read_device_error(ws.buf) != 0:
+            raise RuntimeError("device error in the gated driver run")
+        st = d.stats()
+        return {"tokens_per_s": round(st["tokens"] / secs, 1), "seconds": round(secs, 4),
+                "loop_steps": st["loop_steps"], "mean_depth": round(st["loop_rows"] / st["tokens"], 4),
+                "ms_per_loop_step": round(secs * 1e3 / st["loop_steps"], 4)}
+
+    ga, gs = run_gated(True), run_gated(False)
+    res["gated"] = {"lookahead": ga, "synchronous": gs,
+                    "idle_fraction_removed": round(1 - ga["ms_per_loop_step"] / gs["ms_per_loop_step"], 4)}
+    log(f"e2e gated: lookahead {ga['ms_per_loop_step']:.3f} ms/step (depth {ga['mean_depth']}), synchronous "
+        f"{gs['ms_per_loop_step']:.3f} ms/step (depth {gs['mean_depth']})")
     return res
 
 
