@@ -243,10 +243,18 @@ def e2e_decode(shape, dm, kv, n_seqs, prompt, n_decode, seed=3):
                 "ms_per_loop_step": round(secs * 1e3 / st["loop_steps"], 4)}
 
     ga, gs = run_gated(True), run_gated(False)
-    res["gated"] = {"lookahead": ga, "synchronous": gs,
-                    "idle_fraction_removed": round(1 - ga["ms_per_loop_step"] / gs["ms_per_loop_step"], 4)}
-    log(f"e2e gated: lookahead {ga['ms_per_loop_step']:.3f} ms/step (depth {ga['mean_depth']}), synchronous "
-        f"{gs['ms_per_loop_step']:.3f} ms/step (depth {gs['mean_depth']})")
+    res["gated"] = {"threshold": 0.5, "lookahead": ga, "synchronous": gs}
+    log(f"e2e gated: lookahead {ga['tokens_per_s']} tokens/s (depth {ga['mean_depth']}), synchronous "
+        f"{gs['tokens_per_s']} tokens/s (depth {gs['mean_depth']})")
+    # the same replayed refill run with the runner waiting after every loop
+    # step: the device idles for each round trip and planning (what planning
+    # one step ahead removes)
+    secs_sync, st_sync = run(n_seqs, n_decode, sync_steps=True)
+    a = res["cdb_refill"]["seconds"]
+    res["sync_ablation"] = {"async_seconds": a, "sync_seconds": round(secs_sync, 4),
+                            "idle_us_per_loop_step": round((secs_sync - a) / st_sync["loop_steps"] * 1e6, 2),
+                            "slowdown": round(secs_sync / a, 4)}
+    log(f"e2e sync ablation: {secs_sync:.3f}s vs {a:.3f}s asynchronous")
     return res
 
 

@@ -53,6 +53,8 @@ typedef struct {
     int32_t prefill_chunk;          /* 0: prompts are prefilled by the caller (cdb_driver_add_sequence);
                                        1..512: prompts of requests added with cdb_driver_add_request run
                                        through cdb_prefill in chunks of at most this many tokens */
+    int32_t sync_steps;             /* 1: the runner waits for every loop step before planning the next
+                                       (the synchronous scheduler, for comparison); 0: never waits */
 } cdb_driver_config;
 
 /* Core KV layouts (Section 4.2, App. C.1, Table 1), all by page-table aliasing:

@@ -729,6 +729,10 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
             status = CDB_ERR_INVALID_ARG;
             break;
         }
+        if (d->cfg.sync_steps && t.stage == CDB_TICK_LOOP && hipStreamSynchronize(stream) != hipSuccess) {
+            status = CDB_ERR_HIP;
+            break;
+        }
     }
     if (hipStreamSynchronize(stream) != hipSuccess && status == CDB_OK) status = CDB_ERR_HIP;
     const double secs = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();

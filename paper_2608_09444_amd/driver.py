@@ -28,7 +28,8 @@ class cdb_driver_config(C.Structure):
     _fields_ = [(n, C.c_int32) for n in ("max_batch", "max_active", "refill", "fixed_depth", "min_coda_batch",
                                           "r_max", "has_prelude", "has_coda", "max_seqs", "max_pages",
                                           "pre_pages", "core_pages", "coda_pages", "kv_layout", "gated",
-                                          "lookahead")] + [("threshold", C.c_float), ("prefill_chunk", C.c_int32)]
+                                          "lookahead")] + [("threshold", C.c_float), ("prefill_chunk", C.c_int32),
+                                                           ("sync_steps", C.c_int32)]
 
 
 class cdb_driver_tick(C.Structure):
@@ -88,10 +89,11 @@ class Driver:
                  core_pages: int, pre_pages: int = 0, coda_pages: int = 0, has_prelude: bool = False,
                  has_coda: bool = False, refill: bool = True, fixed_depth: bool = False, min_coda_batch: int = 1,
                  kv_layout: int = KV_FULL, gated: bool = False, lookahead: bool = False, threshold: float = 0.0,
-                 prefill_chunk: int = 0):
+                 prefill_chunk: int = 0, sync_steps: bool = False):
         self.cfg = cdb_driver_config(max_batch, max_active, int(refill), int(fixed_depth), min_coda_batch, r_max,
                                      int(has_prelude), int(has_coda), max_seqs, max_pages, pre_pages, core_pages,
-                                     coda_pages, kv_layout, int(gated), int(lookahead), threshold, prefill_chunk)
+                                     coda_pages, kv_layout, int(gated), int(lookahead), threshold, prefill_chunk,
+                                     int(sync_steps))
         self.h = lib().cdb_driver_create(C.byref(self.cfg))
         if not self.h:
             raise ValueError("cdb_driver_create: invalid configuration")
