@@ -314,6 +314,75 @@ def batch_sweep(shape, dm, sizes=(16, 32, 64, 128, 256), pos_lo=512, pos_hi=767,
     return out
 
 
+def graph_leg(dm, kv, state, rows, out, ws, steps, reps=3):
+    """cdb_loop_step captured once in a HIP graph and replayed: the replay time
+    per step, and each of `reps` replays checked bit for bit against an eager
+    step from the same saved state (eager work and synchronisation between the
+    replays)."""
+    import torch
+
+    import paper_2608_09444_amd as cdb
+    st = torch.cuda.current_stream()
+    h0 = state.h.clone()
+
+    def outputs():
+        return state.h.clone(), out.score.clone(), out.mask.clone(), out.cont.clone()
+
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(st)
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(g, stream=side):
+            cdb.cdb_loop_step(dm.model, kv.c, state.c, rows.c, out.c, ws.buf)
+    st.wait_stream(side)
+    torch.cuda.synchronize()
+    ok = True
+    for _ in range(reps):
+        state.h.copy_(h0)
+        cdb.cdb_loop_step(dm.model, kv.c, state.c, rows.c, out.c, ws.buf)
+        torch.cuda.synchronize()
+        ref = outputs()
+        state.h.copy_(h0)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        got = outputs()
+        ok &= all(torch.equal(a, b) for a, b in zip(ref, got))
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(st)
+    for _ in range(steps):
+        g.replay()
+    e1.record(st)
+    e1.synchronize()
+    if cdb.cdb_read_device_error(ws.buf) != 0:
+        raise RuntimeError("device error in the graph replays")
+    ms = e0.elapsed_time(e1) / steps
+    log(f"graph replay: {ms:.3f} ms/step, replays {'identical to' if ok else 'DIFFERENT from'} eager steps")
+    return {"ms_per_step": round(ms, 4), "replays_match_eager": bool(ok)}
+
+
+def copy_peak(gib=4, reps=5):
+    """A plain device-to-device copy of `gib` GiB: the HBM rate a simple stream
+    reaches on this part (read + write bytes per second)."""
+    import torch
+    n = gib << 28
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    e1.synchronize()
+    gbs = 2.0 * n * 4 * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del src, dst
+    torch.cuda.empty_cache()
+    log(f"copy of {gib} GiB: {gbs:.0f} GB/s")
+    return round(gbs, 1)
+
+
 def serving_leg(shape, dm, n_req, rate=20.0, max_batch=64, chunk=512, core_pages=24576, fixed_depth=False):
     """A serving trace of the ouro-shaped model: Poisson arrivals at `rate`
     requests/s, prompt lengths lognormal (median 300, sigma 1, [16, 4096]),
@@ -474,6 +543,12 @@ def main():
     sb = step_bytes(shape, rows_np)
     log(f"{ms:.3f} ms/step, {value:.0f} rows/s, step bytes {sb / 1e9:.2f} GB -> {sb / (ms * 1e-3) / 1e9:.0f} GB/s")
 
+    try:
+        graph = graph_leg(dm, kv, state, rows, out, ws, args.steps)
+    except RuntimeError as e:  # a capture the runtime refuses is reported, not fatal
+        graph = {"error": str(e)}
+    copy_gbs = copy_peak()
+
     attn_ms = time_attention(shape, kv, rows, n_rows, args.steps * shape.n_core)
     ab = attention_bytes(shape, rows_np["pos"])
     attn_gbs = ab / (attn_ms * 1e-3) / 1e9
@@ -534,6 +609,8 @@ def main():
                      "achieved": round(attn_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(attn_gbs / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
                      "algorithmic_bytes": ab},
+        "graph_replay": graph,
+        "hbm_copy_gbs": copy_gbs,
         "step_roofline": {"bound": "hbm", "algorithmic_bytes": sb, "achieved": round(sb / (ms * 1e-3) / 1e9, 1),
                           "peak": HBM_PEAK_GBS, "unit": "GB/s",
                           "frac": round(sb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
