@@ -122,7 +122,7 @@ __device__ __forceinline__ void stripe_epilogue(const float* fin, int fld, int n
                 const float g0 = f[(c8 + i) * fld], u0 = f[(16 + c8 + i) * fld];
                 const float g1 = f[(c8 + i + 1) * fld], u1 = f[(16 + c8 + i + 1) * fld];
                 const float s0 = g0 / (1.0f + __expf(-g0)), s1 = g1 / (1.0f + __expf(-g1));
-                w[i / 2] = (uint32_t)f2bf(s0 * u0) | ((uint32_t)f2bf(s1 * u1) << 16);
+                w[i / 2] = pack_bf16(s0 * u0, s1 * u1);
             }
             const int feat = (nt + ns) * 16 + c8;
             *reinterpret_cast<u32x4*>(ea.act + frag_index(m, feat, ea.ld_act)) = u32x4{w[0], w[1], w[2], w[3]};
@@ -173,7 +173,7 @@ __device__ __forceinline__ void stripe_epilogue(const float* fin, int fld, int n
                         }
                         o2[b] = outv;
                     }
-                    w[i / 2] = (uint32_t)f2bf(o2[0]) | ((uint32_t)f2bf(o2[1]) << 16);
+                    w[i / 2] = pack_bf16(o2[0], o2[1]);
                 }
                 const KvTarget& kv = ea.kv;
                 uint16_t* dst = kv.pool + kv_offset(kv.layer, pid, kv.n_pages, part - 1, head, ea.H, tok, ea.hd) +
@@ -391,7 +391,7 @@ __device__ __forceinline__ void qkv_block_epilogue(const float* fin, int fld, in
                         }
                         o2[b] = outv;
                     }
-                    w[i / 2] = (uint32_t)f2bf(o2[0]) | ((uint32_t)f2bf(o2[1]) << 16);
+                    w[i / 2] = pack_bf16(o2[0], o2[1]);
                 }
                 const KvTarget& kv = ea.kv;
                 uint16_t* dst = kv.pool + kv_offset(kv.layer, pid, kv.n_pages, part - 1, head, ea.H, tok, ea.hd) +

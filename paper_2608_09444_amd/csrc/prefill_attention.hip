@@ -215,10 +215,9 @@ __global__ __launch_bounds__(256) void k_prefill_attn(const float* __restrict__ 
 #pragma unroll
         for (int e = 0; e < 8; e += 2) {
             const float x0 = x[e] * qscale, x1 = x[e + 1] * qscale;
-            const uint16_t h0 = f2bf(x0), h1 = f2bf(x1);
-            const uint16_t l0 = f2bf(x0 - bf2f(h0)), l1 = f2bf(x1 - bf2f(h1));
-            hw[e / 2] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-            lw[e / 2] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+            const uint32_t h = pack_bf16(x0, x1);
+            hw[e / 2] = h;
+            lw[e / 2] = pack_bf16(x0 - bflo(h), x1 - bfhi(h));
         }
         qh[t] = __builtin_bit_cast(bf16x8, u32x4{hw[0], hw[1], hw[2], hw[3]});
         ql[t] = __builtin_bit_cast(bf16x8, u32x4{lw[0], lw[1], lw[2], lw[3]});
@@ -312,10 +311,9 @@ __global__ __launch_bounds__(256) void k_prefill_attn(const float* __restrict__ 
             uint32_t hw[4], lw[4];
 #pragma unroll
             for (int e = 0; e < 8; e += 2) {
-                const uint16_t h0 = f2bf(pk[e]), h1 = f2bf(pk[e + 1]);
-                const uint16_t l0 = f2bf(pk[e] - bf2f(h0)), l1 = f2bf(pk[e + 1] - bf2f(h1));
-                hw[e / 2] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-                lw[e / 2] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+                const uint32_t h = pack_bf16(pk[e], pk[e + 1]);
+                hw[e / 2] = h;
+                lw[e / 2] = pack_bf16(pk[e] - bflo(h), pk[e + 1] - bfhi(h));
             }
             const bf16x8 ph = __builtin_bit_cast(bf16x8, u32x4{hw[0], hw[1], hw[2], hw[3]});
             const bf16x8 pl = __builtin_bit_cast(bf16x8, u32x4{lw[0], lw[1], lw[2], lw[3]});
@@ -378,8 +376,7 @@ __global__ __launch_bounds__(256) void k_prefill_attn(const float* __restrict__ 
                 num[0] += f[w] * sO[(w * HD + c8 * 8 + i) * 32 + qq];
                 num[1] += f[w] * sO[(w * HD + c8 * 8 + i + 1) * 32 + qq];
             }
-            pk[i / 2] = (uint32_t)f2bf(den > 0.f ? num[0] / den : 0.f) |
-                        ((uint32_t)f2bf(den > 0.f ? num[1] / den : 0.f) << 16);
+            pk[i / 2] = pack_bf16(den > 0.f ? num[0] / den : 0.f, den > 0.f ? num[1] / den : 0.f);
         }
         *reinterpret_cast<u32x4*>(out + frag_index(row, head * HD + c8 * 8, d)) = u32x4{pk[0], pk[1], pk[2], pk[3]};
     }

@@ -77,10 +77,10 @@ __global__ __launch_bounds__(256) void k_gather(int d, int r_max, int n_slots, i
         if (xcat) {  // adapter input [h; e], fragment layout with K = 2d
             float4 e = ok ? *reinterpret_cast<const float4*>(se + (size_t)sl * d + k) : make_float4(0.f, 0.f, 0.f, 0.f);
             uint2 ph, pe;
-            ph.x = (uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16);
-            ph.y = (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16);
-            pe.x = (uint32_t)f2bf(e.x) | ((uint32_t)f2bf(e.y) << 16);
-            pe.y = (uint32_t)f2bf(e.z) | ((uint32_t)f2bf(e.w) << 16);
+            ph.x = pack_bf16(v.x, v.y);
+            ph.y = pack_bf16(v.z, v.w);
+            pe.x = pack_bf16(e.x, e.y);
+            pe.y = pack_bf16(e.z, e.w);
             *reinterpret_cast<uint2*>(xcat + frag_index(i, k, 2 * d)) = ph;
             *reinterpret_cast<uint2*>(xcat + frag_index(i, d + k, 2 * d)) = pe;
         }
@@ -149,8 +149,8 @@ __global__ __launch_bounds__(1024) void k_resid_norm(float* __restrict__ h, cons
         const int k = (threadIdx.x + u * blockDim.x) * 4;
         if (k >= d) continue;
         uint2 pk;
-        pk.x = (uint32_t)f2bf(v[u].x * inv) | ((uint32_t)f2bf(v[u].y * inv) << 16);
-        pk.y = (uint32_t)f2bf(v[u].z * inv) | ((uint32_t)f2bf(v[u].w * inv) << 16);
+        pk.x = pack_bf16(v[u].x * inv, v[u].y * inv);
+        pk.y = pack_bf16(v[u].z * inv, v[u].w * inv);
         *reinterpret_cast<uint2*>(out + frag_index(i, k, d)) = pk;  // 4 consecutive k share one 8-slot run
     }
 }
@@ -587,10 +587,10 @@ __global__ __launch_bounds__(256) void k_concat_frag(int d, const float* __restr
         const float4 a = *reinterpret_cast<const float4*>(h + (size_t)m * d + k);
         const float4 b = *reinterpret_cast<const float4*>(e + (size_t)m * d + k);
         uint2 pa, pb;
-        pa.x = (uint32_t)f2bf(a.x) | ((uint32_t)f2bf(a.y) << 16);
-        pa.y = (uint32_t)f2bf(a.z) | ((uint32_t)f2bf(a.w) << 16);
-        pb.x = (uint32_t)f2bf(b.x) | ((uint32_t)f2bf(b.y) << 16);
-        pb.y = (uint32_t)f2bf(b.z) | ((uint32_t)f2bf(b.w) << 16);
+        pa.x = pack_bf16(a.x, a.y);
+        pa.y = pack_bf16(a.z, a.w);
+        pb.x = pack_bf16(b.x, b.y);
+        pb.y = pack_bf16(b.z, b.w);
         *reinterpret_cast<uint2*>(xcat + frag_index(m, k, 2 * d)) = pa;
         *reinterpret_cast<uint2*>(xcat + frag_index(m, d + k, 2 * d)) = pb;
     }
