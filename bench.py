@@ -32,16 +32,24 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_attn_ouro_bs64_hbm_traffic.json")
-ATTN_SRC = os.path.join(ROOT, "paper_2608_09444_amd", "csrc", "attention.hip")
+# the decode attention kernel's source: its file and the device helpers it includes
+ATTN_SRC = [os.path.join(ROOT, "paper_2608_09444_amd", "csrc", f) for f in ("attention.hip", "cdb_internal.h")]
+
+
+def attention_source_sha256():
+    import hashlib
+    h = hashlib.sha256()
+    for f in ATTN_SRC:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()
 
 
 def measured_traffic():
     """HBM bytes per attention launch from the committed FETCH_SIZE / WRITE_SIZE
     passes, if they were taken on the attention source as it stands."""
-    import hashlib
     try:
         rec = json.load(open(TRAFFIC_FILE))
-        if rec["attention_source_sha256"] != hashlib.sha256(open(ATTN_SRC, "rb").read()).hexdigest():
+        if rec["attention_source_sha256"] != attention_source_sha256():
             return None
         return int(rec["hbm_bytes_per_launch"])
     except (OSError, KeyError, ValueError):
