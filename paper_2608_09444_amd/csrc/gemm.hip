@@ -337,10 +337,62 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs ga, EpiArgs ea) {
 // rows m0 .. m0 + 63) staged in LDS as fin[n][m - m0] (pitch fld): each lane
 // takes a run of consecutive dims of one row, so the stores are 16-byte
 // vectors (4 fp32 q values, or 8 bf16 K/V values) instead of one column of 32
-// rows per instruction.  Same arithmetic per element as epilogue_elem.
-__device__ __forceinline__ void qkv_block_epilogue(const float* fin, int fld, int nt0, int stripes, int m0, int M,
-                                                   int lane, const EpiArgs& ea) {
+// rows per instruction.  A q stripe gives a lane 8 runs (rows lane/8 + 8i,
+// 4 dims), a K/V stripe 4 runs (rows lane/4 + 16i, 8 dims).  The global loads
+// (RoPE factors, page ids, positions; qkv_block_loads) are issued before the
+// GEMM's main loop: the stores may alias them, so loads left between stores
+// would wait one by one.  Same arithmetic per element as epilogue_elem.
+struct QkvBlockInputs {
+    float4 rc[2][16];  // (cos, sin) pairs of each run, two per float4
+    int pid[2][4], tok[2][4];
+};
+
+__device__ __forceinline__ void qkv_block_loads(QkvBlockInputs& in, int nt0, int stripes, int m0, int M, int lane,
+                                                const EpiArgs& ea) {
     const int gph = ea.hd >> 5, hg = ea.H * gph, half_hd = ea.hd >> 1;
+    float4 (&rc)[2][16] = in.rc;
+    int (&pid)[2][4] = in.pid;
+    int (&tok)[2][4] = in.tok;
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+        const int g = nt0 + a;
+        if (g >= stripes) break;
+        const int part = g / hg, gi = (g - part * hg) % gph;
+        if (part == 0) {
+#pragma unroll
+            for (int it = 0; it < 8; ++it) {
+                const int m = min(m0 + (lane >> 3) + 8 * it, M - 1);
+                const float4* cs = reinterpret_cast<const float4*>(ea.rope + (size_t)m * half_hd + gi * 16 + (lane & 3) * 4);
+                rc[a][2 * it] = cs[0];
+                rc[a][2 * it + 1] = cs[1];
+            }
+        } else {
+#pragma unroll
+            for (int it = 0; it < 4; ++it) {
+                const int m = min(m0 + (lane >> 2) + 16 * it, M - 1);
+                pid[a][it] = ea.kvpid[m];
+                tok[a][it] = ea.pos[m] % kPage;
+                if (part == 1) {
+                    const float4* cs = reinterpret_cast<const float4*>(ea.rope + (size_t)m * half_hd + gi * 16 + (lane & 1) * 8);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) rc[a][4 * it + i] = cs[i];
+                }
+            }
+        }
+    }
+}
+
+__device__ __forceinline__ void qkv_block_epilogue(const QkvBlockInputs& in, const float* fin, int fld, int nt0,
+                                                   int stripes, int m0, int M, int lane, const EpiArgs& ea) {
+    const int gph = ea.hd >> 5, hg = ea.H * gph, half_hd = ea.hd >> 1;
+    const float4 (&rc)[2][16] = in.rc;
+    const int (&pid)[2][4] = in.pid;
+    const int (&tok)[2][4] = in.tok;
+    // pair t of a run from its float4s
+    auto cpair = [](const float4* r, int t) {
+        const float4 v = r[t >> 1];
+        return (t & 1) ? make_float2(v.z, v.w) : make_float2(v.x, v.y);
+    };
 #pragma unroll
     for (int a = 0; a < 2; ++a) {
         const int g = nt0 + a;
@@ -349,17 +401,17 @@ __device__ __forceinline__ void qkv_block_epilogue(const float* fin, int fld, in
         const int head = rem / gph, gi = rem - head * gph;
         const float* f = fin + a * 32 * fld;
         if (part == 0) {
-            for (int e = lane; e < 64 * 8; e += 64) {  // (row, half, 4-pair run)
-                const int ml = e >> 3, half = (e >> 2) & 1, j4 = (e & 3) * 4;
+#pragma unroll
+            for (int it = 0; it < 8; ++it) {
+                const int ml = (lane >> 3) + 8 * it, half = (lane >> 2) & 1, j4 = (lane & 3) * 4;
                 const int m = m0 + ml;
                 if (m >= M) continue;
-                const float2* cs = ea.rope + (size_t)m * half_hd + gi * 16 + j4;
                 float o[4];
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int jj = j4 + i;
                     const float val = f[(half * 16 + jj) * fld + ml], partner = f[((half ^ 1) * 16 + jj) * fld + ml];
-                    const float2 c = cs[i];
+                    const float2 c = cpair(&rc[a][2 * it], i);
                     const float xf = half ? partner : val, xs = half ? val : partner;
                     o[i] = half ? (xs * c.x + xf * c.y) : (xf * c.x - xs * c.y);
                 }
@@ -367,13 +419,12 @@ __device__ __forceinline__ void qkv_block_epilogue(const float* fin, int fld, in
                 *reinterpret_cast<float4*>(dst) = make_float4(o[0], o[1], o[2], o[3]);
             }
         } else {
-            for (int e = lane; e < 64 * 4; e += 64) {  // (row, half, 8-pair run)
-                const int ml = e >> 2, half = (e >> 1) & 1, j8 = (e & 1) * 8;
+#pragma unroll
+            for (int it = 0; it < 4; ++it) {
+                const int ml = (lane >> 2) + 16 * it, half = (lane >> 1) & 1, j8 = (lane & 1) * 8;
                 const int m = m0 + ml;
-                if (m >= M) continue;
-                const int pid = ea.kvpid[m];  // -1: unmapped (reported by the row-entry kernel)
-                if (pid < 0) continue;
-                const int tok = ea.pos[m] % kPage;
+                // pid -1: unmapped (reported by the row-entry kernel)
+                if (m >= M || pid[a][it] < 0) continue;
                 uint32_t w[4];
 #pragma unroll
                 for (int i = 0; i < 8; i += 2) {
@@ -385,7 +436,7 @@ __device__ __forceinline__ void qkv_block_epilogue(const float* fin, int fld, in
                         float outv = val;
                         if (part == 1) {
                             const float partner = f[((half ^ 1) * 16 + jj) * fld + ml];
-                            const float2 c = ea.rope[(size_t)m * half_hd + gi * 16 + jj];
+                            const float2 c = cpair(&rc[a][4 * it], i + b);
                             const float xf = half ? partner : val, xs = half ? val : partner;
                             outv = half ? (xs * c.x + xf * c.y) : (xf * c.x - xs * c.y);
                         }
@@ -394,7 +445,7 @@ __device__ __forceinline__ void qkv_block_epilogue(const float* fin, int fld, in
                     w[i / 2] = pack_bf16(o2[0], o2[1]);
                 }
                 const KvTarget& kv = ea.kv;
-                uint16_t* dst = kv.pool + kv_offset(kv.layer, pid, kv.n_pages, part - 1, head, ea.H, tok, ea.hd) +
+                uint16_t* dst = kv.pool + kv_offset(kv.layer, pid[a][it], kv.n_pages, part - 1, head, ea.H, tok[a][it], ea.hd) +
                                 gi * 16 + j8 + half * half_hd;
                 *reinterpret_cast<u32x4*>(dst) = u32x4{w[0], w[1], w[2], w[3]};
             }
@@ -429,6 +480,8 @@ __global__ __launch_bounds__(256) void k_gemm_mn(GemmArgs ga, EpiArgs ea) {
         for (int b = 0; b < 2; ++b)
 #pragma unroll
             for (int j = 0; j < 16; ++j) acc[a][b][j] = 0.f;
+    QkvBlockInputs qin;
+    if constexpr (EPI == EPI_QKV) qkv_block_loads(qin, nt0, stripes, mt0 * 32, ga.M, lane, ea);
 
     if constexpr (!LDS) {
         // tiles past the matrix re-read the last one (their results are not stored)
@@ -542,7 +595,7 @@ __global__ __launch_bounds__(256) void k_gemm_mn(GemmArgs ga, EpiArgs ea) {
                     const int n = a * 32 + (j >> 2) * 8 + (lane >> 5) * 4 + (j & 3);
                     fin[n * fld + b * 32 + (lane & 31)] = acc[a][b][j];
                 }
-        qkv_block_epilogue(fin, fld, nt0, stripes, mt0 * 32, ga.M, lane, ea);
+        qkv_block_epilogue(qin, fin, fld, nt0, stripes, mt0 * 32, ga.M, lane, ea);
         return;
     }
     const QkvStage qs{};
