@@ -333,12 +333,12 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs ga, EpiArgs ea) {
     stripe_epilogue<EPI>(fin, fld, nt, NS, mcap, s, tid, nthr, ga, ea, qs);
 }
 
-// q/k/v epilogue of a wave's 64-row x 64-column block (stripes nt0, nt0 + 1;
-// rows m0 .. m0 + 63) staged in LDS as fin[n][m - m0] (pitch fld): each lane
-// takes a run of consecutive dims of one row, so the stores are 16-byte
-// vectors (4 fp32 q values, or 8 bf16 K/V values) instead of one column of 32
-// rows per instruction.  A q stripe gives a lane 8 runs (rows lane/8 + 8i,
-// 4 dims), a K/V stripe 4 runs (rows lane/4 + 16i, 8 dims).  The global loads
+// q/k/v epilogue of a wave's (32 WM)-row x 64-column block (stripes nt0,
+// nt0 + 1; rows m0 .. m0 + 32 WM - 1) staged in LDS as fin[n][m - m0] (pitch
+// fld): each lane takes a run of consecutive dims of one row, so the stores
+// are 16-byte vectors (4 fp32 q values, or 8 bf16 K/V values) instead of one
+// column of 32 rows per instruction.  A q stripe gives a lane 4 WM runs (rows
+// lane/8 + 8i, 4 dims), a K/V stripe 2 WM runs (rows lane/4 + 16i, 8 dims).  The global loads
 // (RoPE factors, page ids, positions; qkv_block_loads) are issued before the
 // GEMM's main loop: the stores may alias them, so loads left between stores
 // would wait one by one.  Same arithmetic per element as epilogue_elem.
@@ -347,6 +347,7 @@ struct QkvBlockInputs {
     int pid[2][4], tok[2][4];
 };
 
+template <int WM>
 __device__ __forceinline__ void qkv_block_loads(QkvBlockInputs& in, int nt0, int stripes, int m0, int M, int lane,
                                                 const EpiArgs& ea) {
     const int gph = ea.hd >> 5, hg = ea.H * gph, half_hd = ea.hd >> 1;
@@ -360,7 +361,7 @@ __device__ __forceinline__ void qkv_block_loads(QkvBlockInputs& in, int nt0, int
         const int part = g / hg, gi = (g - part * hg) % gph;
         if (part == 0) {
 #pragma unroll
-            for (int it = 0; it < 8; ++it) {
+            for (int it = 0; it < 4 * WM; ++it) {
                 const int m = min(m0 + (lane >> 3) + 8 * it, M - 1);
                 const float4* cs = reinterpret_cast<const float4*>(ea.rope + (size_t)m * half_hd + gi * 16 + (lane & 3) * 4);
                 rc[a][2 * it] = cs[0];
@@ -368,7 +369,7 @@ __device__ __forceinline__ void qkv_block_loads(QkvBlockInputs& in, int nt0, int
             }
         } else {
 #pragma unroll
-            for (int it = 0; it < 4; ++it) {
+            for (int it = 0; it < 2 * WM; ++it) {
                 const int m = min(m0 + (lane >> 2) + 16 * it, M - 1);
                 pid[a][it] = ea.kvpid[m];
                 tok[a][it] = ea.pos[m] % kPage;
@@ -382,6 +383,7 @@ __device__ __forceinline__ void qkv_block_loads(QkvBlockInputs& in, int nt0, int
     }
 }
 
+template <int WM>
 __device__ __forceinline__ void qkv_block_epilogue(const QkvBlockInputs& in, const float* fin, int fld, int nt0,
                                                    int stripes, int m0, int M, int lane, const EpiArgs& ea) {
     const int gph = ea.hd >> 5, hg = ea.H * gph, half_hd = ea.hd >> 1;
@@ -402,7 +404,7 @@ __device__ __forceinline__ void qkv_block_epilogue(const QkvBlockInputs& in, con
         const float* f = fin + a * 32 * fld;
         if (part == 0) {
 #pragma unroll
-            for (int it = 0; it < 8; ++it) {
+            for (int it = 0; it < 4 * WM; ++it) {
                 const int ml = (lane >> 3) + 8 * it, half = (lane >> 2) & 1, j4 = (lane & 3) * 4;
                 const int m = m0 + ml;
                 if (m >= M) continue;
@@ -420,7 +422,7 @@ __device__ __forceinline__ void qkv_block_epilogue(const QkvBlockInputs& in, con
             }
         } else {
 #pragma unroll
-            for (int it = 0; it < 4; ++it) {
+            for (int it = 0; it < 2 * WM; ++it) {
                 const int ml = (lane >> 2) + 16 * it, half = (lane >> 1) & 1, j8 = (lane & 1) * 8;
                 const int m = m0 + ml;
                 // pid -1: unmapped (reported by the row-entry kernel)
@@ -454,16 +456,18 @@ __device__ __forceinline__ void qkv_block_epilogue(const QkvBlockInputs& in, con
 }
 
 // Large-M GEMM (prefill chunks of up to 512 rows), where the product is
-// compute-bound (about M FLOP per weight byte).  A workgroup owns a 128-row x
-// 128-column output tile and one K split: 4 waves in 2 x 2, each 64 rows x 64
-// columns (2 m-tiles x 2 stripes, 4 MFMAs per 16-wide k step), operands read
-// straight from the packed weights and the fragment-layout activations (each
-// tile feeds two waves; the second read is served by the caches), double-
-// buffered in registers.  Each wave owns its outputs, so the epilogue runs from
-// the accumulators: column n's RoPE / SwiGLU partner n ^ 16 is element j ^ 8 of
-// the same lane.
-template <int EPI, bool LDS>
+// compute-bound (about M FLOP per weight byte).  A workgroup owns a
+// (64 WM)-row x 128-column output tile and one K split: 4 waves in 2 x 2, each
+// 32 WM rows x 64 columns (WM m-tiles x 2 stripes, 2 WM MFMAs per 16-wide k
+// step), operands read straight from the packed weights and the fragment-
+// layout activations (each tile feeds two waves; the second read is served by
+// the caches), double-buffered in registers.  Each wave owns its outputs, so
+// the epilogue runs from the accumulators: column n's RoPE / SwiGLU partner
+// n ^ 16 is element j ^ 8 of the same lane.
+template <int EPI, bool LDS, int WM>
 __global__ __launch_bounds__(256) void k_gemm_mn(GemmArgs ga, EpiArgs ea) {
+    static_assert(WM == 1 || WM == 2, "one or two m-tiles per wave");
+    static_assert(!LDS || WM == 2, "the LDS ring stages 4 m-tiles per k step");
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int KS = ga.K >> 4;
     const int stripes = ga.N >> 5;
@@ -471,41 +475,41 @@ __global__ __launch_bounds__(256) void k_gemm_mn(GemmArgs ga, EpiArgs ea) {
     const int s = blockIdx.z;
     const int k0 = (int)(((long)s * KS) / ga.S), k1 = (int)(((long)(s + 1) * KS) / ga.S);
     const int nt0 = blockIdx.x * 4 + (wave & 1) * 2;   // first stripe of this wave
-    const int mt0 = blockIdx.y * 4 + (wave >> 1) * 2;  // first m-tile of this wave
+    const int mt0 = blockIdx.y * 2 * WM + (wave >> 1) * WM;  // first m-tile of this wave
 
-    floatx16 acc[2][2];
+    floatx16 acc[2][WM];
 #pragma unroll
     for (int a = 0; a < 2; ++a)
 #pragma unroll
-        for (int b = 0; b < 2; ++b)
+        for (int b = 0; b < WM; ++b)
 #pragma unroll
             for (int j = 0; j < 16; ++j) acc[a][b][j] = 0.f;
     QkvBlockInputs qin;
-    if constexpr (EPI == EPI_QKV) qkv_block_loads(qin, nt0, stripes, mt0 * 32, ga.M, lane, ea);
+    if constexpr (EPI == EPI_QKV) qkv_block_loads<WM>(qin, nt0, stripes, mt0 * 32, ga.M, lane, ea);
 
     if constexpr (!LDS) {
         // tiles past the matrix re-read the last one (their results are not stored)
         const u32x4* wsrc[2];
-        const u32x4* xsrc[2];
+        const u32x4* xsrc[WM];
     #pragma unroll
-        for (int a = 0; a < 2; ++a) {
+        for (int a = 0; a < 2; ++a)
             wsrc[a] = reinterpret_cast<const u32x4*>(ga.Wp) + (size_t)min(nt0 + a, stripes - 1) * KS * 64 + lane;
-            xsrc[a] = reinterpret_cast<const u32x4*>(ga.X) + (size_t)min(mt0 + a, mtiles - 1) * KS * 64 + lane;
-        }
+    #pragma unroll
+        for (int b = 0; b < WM; ++b)
+            xsrc[b] = reinterpret_cast<const u32x4*>(ga.X) + (size_t)min(mt0 + b, mtiles - 1) * KS * 64 + lane;
         constexpr int CH = 4;
-        u32x4 wa[CH][2], wb[CH][2], xa[CH][2], xb[CH][2];
-        auto load = [&](u32x4 (&w)[CH][2], u32x4 (&x)[CH][2], int c0) {
+        u32x4 wa[CH][2], wb[CH][2], xa[CH][WM], xb[CH][WM];
+        auto load = [&](u32x4 (&w)[CH][2], u32x4 (&x)[CH][WM], int c0) {
     #pragma unroll
             for (int i = 0; i < CH; ++i) {
                 const int ks = min(c0 + i, k1 - 1);
     #pragma unroll
-                for (int a = 0; a < 2; ++a) {
-                    w[i][a] = wsrc[a][(size_t)ks * 64];
-                    x[i][a] = xsrc[a][(size_t)ks * 64];
-                }
+                for (int a = 0; a < 2; ++a) w[i][a] = wsrc[a][(size_t)ks * 64];
+    #pragma unroll
+                for (int b = 0; b < WM; ++b) x[i][b] = xsrc[b][(size_t)ks * 64];
             }
         };
-        auto compute = [&](const u32x4 (&w)[CH][2], const u32x4 (&x)[CH][2], int c0) {
+        auto compute = [&](const u32x4 (&w)[CH][2], const u32x4 (&x)[CH][WM], int c0) {
     #pragma unroll
             for (int i = 0; i < CH; ++i) {
                 const uint32_t keep = c0 + i < k1 ? 0xffffffffu : 0u;
@@ -513,7 +517,7 @@ __global__ __launch_bounds__(256) void k_gemm_mn(GemmArgs ga, EpiArgs ea) {
                 for (int a = 0; a < 2; ++a) {
                     const bf16x8 wv = __builtin_bit_cast(bf16x8, w[i][a] & keep);
     #pragma unroll
-                    for (int b = 0; b < 2; ++b)
+                    for (int b = 0; b < WM; ++b)
                         acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wv, __builtin_bit_cast(bf16x8, x[i][b]),
                                                                             acc[a][b], 0, 0, 0);
                 }
@@ -582,20 +586,20 @@ __global__ __launch_bounds__(256) void k_gemm_mn(GemmArgs ga, EpiArgs ea) {
         }
     }
     if constexpr (EPI == EPI_QKV) {
-        // the wave's block through its own LDS region (64 columns x 65-float rows)
+        // the wave's block through its own LDS region (64 columns x (32 WM + 1)-float rows)
         extern __shared__ __align__(16) unsigned char lds_ring[];
-        constexpr int fld = 65;
+        constexpr int fld = 32 * WM + 1;
         float* fin = reinterpret_cast<float*>(lds_ring) + wave * 64 * fld;
 #pragma unroll
         for (int a = 0; a < 2; ++a)
 #pragma unroll
-            for (int b = 0; b < 2; ++b)
+            for (int b = 0; b < WM; ++b)
 #pragma unroll
                 for (int j = 0; j < 16; ++j) {
                     const int n = a * 32 + (j >> 2) * 8 + (lane >> 5) * 4 + (j & 3);
                     fin[n * fld + b * 32 + (lane & 31)] = acc[a][b][j];
                 }
-        qkv_block_epilogue(qin, fin, fld, nt0, stripes, mt0 * 32, ga.M, lane, ea);
+        qkv_block_epilogue<WM>(qin, fin, fld, nt0, stripes, mt0 * 32, ga.M, lane, ea);
         return;
     }
     const QkvStage qs{};
@@ -603,7 +607,7 @@ __global__ __launch_bounds__(256) void k_gemm_mn(GemmArgs ga, EpiArgs ea) {
     for (int a = 0; a < 2; ++a) {
         if (nt0 + a >= stripes) continue;
 #pragma unroll
-        for (int b = 0; b < 2; ++b) {
+        for (int b = 0; b < WM; ++b) {
             const int m = (mt0 + b) * 32 + (lane & 31);
             if (m >= ga.M) continue;
 #pragma unroll
@@ -615,10 +619,27 @@ __global__ __launch_bounds__(256) void k_gemm_mn(GemmArgs ga, EpiArgs ea) {
     }
 }
 
+// Which tile-kernel path a projection takes: the LDS-staged one pays off for
+// the wide projections (gate/up and a full-width LM head: 20% faster at 512
+// rows); q/k/v, O and down are faster with direct loads.
+static bool mn_lds(int epi, int N) { return epi == EPI_SWIGLU || (epi == EPI_STORE && N >= 8192); }
+
+// m-tiles per wave of the tile kernel: 2 (128-row workgroup tiles), or 1
+// (64-row tiles) for q/k/v when that grid still runs in one round on the 256
+// CUs.  Its workgroups take one CU each (register bound), so at 257-320 rows of
+// the Ouro-shaped q/k/v the 64-row tiles use 240 CUs instead of 144 (29 -> 22
+// us); above that they would take two rounds.  O and down are as fast or
+// faster with 128-row tiles at every size from 272 to 512 rows but 480-512.
+static int mn_wave_mtiles(int epi, int N, int M) {
+    if (mn_lds(epi, N)) return 2;
+    return epi == EPI_QKV && ((M + 63) / 64) * ((N / 32 + 3) / 4) <= 256 ? 1 : 2;
+}
+
 // Launch shape for M > kMaxRows rows (k_gemm_mn): K split only for the
 // split-K partial epilogue, until the grid covers the chip.
 GemmShape gemm_shape_mn(int N, int K, int M, int epi) {
-    const int tiles = ((N / 32 + 3) / 4) * ((M + 127) / 128);
+    const int rows_per_tile = 64 * mn_wave_mtiles(epi, N, M);
+    const int tiles = ((N / 32 + 3) / 4) * ((M + rows_per_tile - 1) / rows_per_tile);
     const int KS = K / 16;
     int S = 1;
     if (epi == EPI_PARTIAL)
@@ -680,36 +701,31 @@ static hipError_t launch_epi(const GemmArgs& ga, const EpiArgs& ea, int ns, hipS
     }
 }
 
-// The LDS-staged tile path pays off for the wide projections (gate/up and a
-// full-width LM head: 20% faster at 512 rows); q/k/v, O and down keep the
-// direct-load path.
+template <int EPI, bool LDS, int WM>
+static hipError_t launch_mn_wm(const GemmArgs& ga, const EpiArgs& ea, hipStream_t st) {
+    dim3 grid((ga.N / 32 + 3) / 4, (ga.M + 64 * WM - 1) / (64 * WM), ga.S);
+    // dynamic LDS: the ring of the LDS path, the q/k/v epilogue's staging blocks
+    constexpr size_t ring = LDS ? 2 * 4 * 8 * 1024 : 0;
+    constexpr size_t stage = EPI == EPI_QKV ? 4 * 64 * (32 * WM + 1) * 4 : 0;
+    constexpr size_t smem = ring > stage ? ring : stage;
+    if constexpr (smem > 48 * 1024) {
+        static bool attr_set = false;
+        if (!attr_set) {
+            hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm_mn<EPI, LDS, WM>),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+            if (e != hipSuccess) return e;
+            attr_set = true;
+        }
+    }
+    k_gemm_mn<EPI, LDS, WM><<<grid, 256, smem, st>>>(ga, ea);
+    return hipGetLastError();
+}
+
 template <int EPI>
 static hipError_t launch_mn(const GemmArgs& ga, const EpiArgs& ea, hipStream_t st) {
-    dim3 grid((ga.N / 32 + 3) / 4, (ga.M + 127) / 128, ga.S);
-    const bool lds = EPI == EPI_SWIGLU || (EPI == EPI_STORE && ga.N >= 8192);
-    if (!lds) {
-        // the q/k/v epilogue stages each wave's 64 x 64 block in LDS
-        if constexpr (EPI == EPI_QKV) {
-            static bool qkv_attr = false;
-            if (!qkv_attr) {
-                hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm_mn<EPI, false>),
-                                                   hipFuncAttributeMaxDynamicSharedMemorySize, 4 * 64 * 65 * 4);
-                if (e != hipSuccess) return e;
-                qkv_attr = true;
-            }
-        }
-        k_gemm_mn<EPI, false><<<grid, 256, EPI == EPI_QKV ? 4 * 64 * 65 * 4 : 0, st>>>(ga, ea);
-        return hipGetLastError();
-    }
-    static bool attr_set = false;
-    if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm_mn<EPI, true>),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, 64 * 1024);
-        if (e != hipSuccess) return e;
-        attr_set = true;
-    }
-    k_gemm_mn<EPI, true><<<grid, 256, 2 * 4 * 8 * 1024, st>>>(ga, ea);
-    return hipGetLastError();
+    if (mn_lds(EPI, ga.N)) return launch_mn_wm<EPI, true, 2>(ga, ea, st);
+    if (mn_wave_mtiles(EPI, ga.N, ga.M) == 1) return launch_mn_wm<EPI, false, 1>(ga, ea, st);
+    return launch_mn_wm<EPI, false, 2>(ga, ea, st);
 }
 
 hipError_t launch_gemm(int epi, const uint16_t* X, const uint16_t* Wp, int M, GemmShape g, float* part,

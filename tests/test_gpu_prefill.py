@@ -26,6 +26,13 @@ ODD = cdbgen.ModelShape(name="odd-1-2-1-inj", d=192, n_heads=3, head_dim=64, d_f
                         n_core=2, n_coda=1, r_max=3, injection=1, exit_kind=1)
 
 
+# head_dim 96 with 5 heads: 15 stripes per q/k/v part, an odd count, so one
+# wave's stripe pair in the tile kernel straddles the q/k boundary (the
+# Huginn-shaped 55 x 96 heads have 165 per part)
+HD96 = cdbgen.ModelShape(name="hd96-1-2-1-inj", d=480, n_heads=5, head_dim=96, d_ff=256, vocab=320, n_prelude=1,
+                         n_core=2, n_coda=1, r_max=2, injection=1, exit_kind=1)
+
+
 def _say(msg):
     print(msg, flush=True)
     sys.stdout.flush()
@@ -174,4 +181,23 @@ def test_prefill_ouro_width_second_chunk_over_earlier_context():
     _say(f"[gpu] prefill Ouro widths, 2 core layers: chunks 320 + 300")
     err = run_prefill(s, w, prompt, [320, 300], check_rows=[0, 319, 320, 321, 400, 511, 512, 600, 619],
                       sensitivity=True)
+    _say(f"[gpu]   {err}")
+
+
+def test_prefill_ouro_width_full_chunk_then_short_chunk():
+    # the largest chunk (128-row q/k/v tiles), then a skinny chunk over its 512 positions
+    s, w = _core_prefix(cdbgen.OURO, cdbgen.model_weights(cdbgen.OURO), 2)
+    prompt = cdbgen.prompt_ids(s.vocab, 1, 552, seed=85)[0]
+    _say(f"[gpu] prefill Ouro widths, 2 core layers: chunks 512 + 40")
+    err = run_prefill(s, w, prompt, [512, 40], check_rows=[0, 1, 127, 128, 255, 256, 383, 384, 500, 511, 512, 530, 551],
+                      sensitivity=True)
+    _say(f"[gpu]   {err}")
+
+
+def test_prefill_head_dim_96_odd_stripes_per_part():
+    s = HD96
+    w = cdbgen.model_weights(s)
+    prompt = cdbgen.prompt_ids(s.vocab, 1, 300, seed=86)[0]
+    _say(f"[gpu] prefill {s.name}: chunks 264 (tile GEMMs) + 36")
+    err = run_prefill(s, w, prompt, [264, 36])
     _say(f"[gpu]   {err}")
