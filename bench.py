@@ -266,6 +266,47 @@ def e2e_decode(shape, dm, kv, n_seqs, prompt, n_decode, seed=3):
     return res
 
 
+def own_pages(shape, rows_np, max_pages):
+    """Page table [rows][r_max + 2][max_pages] of a loop-step snapshot in which
+    every row maps its own pages: its loop plane over the whole context plus the
+    page at pos of every deeper plane (copy-on-exit destinations).  Returns the
+    table and the number of core pages it uses."""
+    import numpy as np
+    import cdbgen
+    R = shape.r_max
+    n = len(rows_np["pos"])
+    pt = np.full((n, R + 2, max_pages), -1, np.int32)
+    nxt = 0
+    for i in range(n):
+        plane = int(rows_np["c"][i]) + 1
+        pg = cdbgen.pages_for(int(rows_np["pos"][i]) + 1)
+        pt[i, plane, :pg] = np.arange(nxt, nxt + pg)
+        nxt += pg
+        for pl in range(plane + 1, R + 1):
+            pt[i, pl, pg - 1] = nxt
+            nxt += 1
+    return pt, nxt
+
+
+def time_loop_step(dm, kv, state, rows, so, ws, steps, warmup):
+    """Milliseconds per cdb_loop_step on one batch, timed with events."""
+    import torch
+    import paper_2608_09444_amd as cdb
+    st = torch.cuda.current_stream()
+    for _ in range(warmup):
+        cdb.cdb_loop_step(dm.model, kv.c, state.c, rows.c, so.c, ws.buf)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(st)
+    for _ in range(steps):
+        cdb.cdb_loop_step(dm.model, kv.c, state.c, rows.c, so.c, ws.buf)
+    e1.record(st)
+    e1.synchronize()
+    if cdb.cdb_read_device_error(ws.buf) != 0:
+        raise RuntimeError("device error in a timed loop step")
+    return e0.elapsed_time(e1) / steps
+
+
 def batch_sweep(shape, dm, sizes=(16, 32, 64, 128, 256), pos_lo=512, pos_hi=767, steps=10, warmup=3):
     """cdb_loop_step at several batch sizes on mid-decode refill batches of the
     same position and depth distributions.  Each row maps its own pages: its
@@ -281,16 +322,7 @@ def batch_sweep(shape, dm, sizes=(16, 32, 64, 128, 256), pos_lo=512, pos_hi=767,
     for n in sizes:
         rows_np = cdbgen.decode_snapshot(n, cdbgen.OURO_DEPTHS, R, pos_lo, pos_hi, stream=20 + n)
         max_pages = cdbgen.pages_for(pos_hi + 1)
-        pt = np.full((n, R + 2, max_pages), -1, np.int32)
-        nxt = 0
-        for i in range(n):
-            plane = int(rows_np["c"][i]) + 1
-            pg = cdbgen.pages_for(int(rows_np["pos"][i]) + 1)
-            pt[i, plane, :pg] = np.arange(nxt, nxt + pg)
-            nxt += pg
-            for pl in range(plane + 1, R + 1):
-                pt[i, pl, pg - 1] = nxt
-                nxt += 1
+        pt, nxt = own_pages(shape, rows_np, max_pages)
         kv = cdb.PagedKV(shape, n, max_pages, 0, nxt, 0, fill="random")
         kv.core.normal_(0.0, 1.0)
         kv.page_table.copy_(torch.from_numpy(pt))
@@ -300,19 +332,7 @@ def batch_sweep(shape, dm, sizes=(16, 32, 64, 128, 256), pos_lo=512, pos_hi=767,
                         rows_np["depth"])
         so = cdb.StepOut(n)
         ws = cdb.Workspace(dm.desc, n)
-        st = torch.cuda.current_stream()
-        for _ in range(warmup):
-            cdb.cdb_loop_step(dm.model, kv.c, state.c, rows.c, so.c, ws.buf)
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(st)
-        for _ in range(steps):
-            cdb.cdb_loop_step(dm.model, kv.c, state.c, rows.c, so.c, ws.buf)
-        e1.record(st)
-        e1.synchronize()
-        if cdb.cdb_read_device_error(ws.buf) != 0:
-            raise RuntimeError(f"device error in the {n}-row sweep step")
-        ms = e0.elapsed_time(e1) / steps
+        ms = time_loop_step(dm, kv, state, rows, so, ws, steps, warmup)
         sb = step_bytes(shape, rows_np)
         out.append({"rows": n, "ms_per_step": round(ms, 4), "rows_per_s": round(n / (ms * 1e-3), 1),
                     "hbm_frac": round(sb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)})
@@ -320,6 +340,115 @@ def batch_sweep(shape, dm, sizes=(16, 32, 64, 128, 256), pos_lo=512, pos_hi=767,
         del kv, state, rows, so, ws
         torch.cuda.empty_cache()
     return out
+
+
+def huginn_leg(n_decode, steps=20, warmup=3):
+    """The Huginn-shaped model (prelude 2, recurrent block of 4 layers with the
+    input-injection adapter looped up to 32 times, coda 2; d 5280, 55 x 96
+    heads): the loop step at its mid-decode refill batch (128 rows at positions
+    U[256, 767], lognormal depths, median 12, clipped to [4, 32]), and whole
+    decodes through the host driver, CDB refill against fixed-depth continuous
+    batching.  The decodes use the shared KV layout (one core plane per
+    position, as in the paper's own runs): the depth-indexed layout of 128
+    requests of 768 positions would take 274 GB.  The boundary stages wait for
+    32 rows (or for the loop work to run out), the minimum boundary batch the
+    paper sets for this model (Section 6.1): each prelude + coda pass streams
+    more weight bytes (4 layers and a 65536-row LM head) than the core."""
+    import numpy as np
+    import torch
+
+    import cdbgen
+    import paper_2608_09444_amd as cdb
+    from paper_2608_09444_amd import cost
+    from paper_2608_09444_amd import driver as drv
+    shape = cdbgen.HUGINN
+    wl = cdbgen.WORKLOADS[3]
+    R = shape.r_max
+    t0 = time.time()
+    w = cdbgen.model_weights(shape)
+    dm = cdb.DeviceModel(shape, w)
+    del w
+    log(f"huginn: weights in {time.time() - t0:.1f}s")
+    n_rows, pos_lo, pos_hi = wl.n_seqs, wl.prompt, wl.prompt + wl.decode - 1
+    rows_np = cdbgen.decode_snapshot(n_rows, wl.depth, R, pos_lo, pos_hi, stream=30)
+    max_pages = cdbgen.pages_for(pos_hi + 1)
+    pt, n_pages = own_pages(shape, rows_np, max_pages)
+    kv = cdb.PagedKV(shape, n_rows, max_pages, 0, n_pages, 0, fill="random")
+    kv.core.normal_(0.0, 1.0)
+    kv.page_table.copy_(torch.from_numpy(pt))
+    state = cdb.State(shape, n_rows)
+    state.h.normal_(0.0, 1.0)
+    state.e.normal_(0.0, 1.0)
+    rows = cdb.Rows(np.arange(n_rows, dtype=np.int32), np.arange(n_rows, dtype=np.int32), rows_np["pos"],
+                    rows_np["c"], rows_np["depth"])
+    so = cdb.StepOut(n_rows)
+    ws = cdb.Workspace(dm.desc, n_rows)
+    ms = time_loop_step(dm, kv, state, rows, so, ws, steps, warmup)
+    sb = step_bytes(shape, rows_np)
+    attn_ms = time_attention(shape, kv, rows, n_rows, steps * shape.n_core)
+    ab = attention_bytes(shape, rows_np["pos"])
+    log(f"huginn loop step: {ms:.3f} ms, {n_rows / (ms * 1e-3):.0f} rows/s; attention {attn_ms * 1e3:.1f} us")
+    res = {"loop_step": {
+        "workload": f"huginn-3.5b-shaped looped LM, mixed-depth decode loop step: {n_rows} rows at positions "
+                    f"U[{pos_lo},{pos_hi}] (prompt {wl.prompt} + decode {wl.decode}), depths lognormal median 12, "
+                    f"sigma 0.5, clipped to [4, 32]",
+        "rows": n_rows, "ms_per_step": round(ms, 4), "tokens_per_s": round(n_rows / (ms * 1e-3), 1),
+        "mean_context": float(np.mean(rows_np["pos"] + 1)),
+        "exits_per_step": int((rows_np["c"] + 1 == rows_np["depth"]).sum()),
+        "step_roofline": {"bound": "hbm", "algorithmic_bytes": sb, "achieved": round(sb / (ms * 1e-3) / 1e9, 1),
+                          "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                          "frac": round(sb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                          "flops": step_flops(shape, rows_np)},
+        "attention_roofline": {"bound": "hbm", "kernel": "k_attn<96> (paged decode attention, one layer)",
+                               "achieved": round(ab / (attn_ms * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS,
+                               "unit": "GB/s", "frac": round(ab / (attn_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                               "algorithmic_bytes": ab, "us_per_launch": round(attn_ms * 1e3, 2)}}}
+    del kv, state, rows, so, ws
+    torch.cuda.empty_cache()
+
+    # whole decodes, shared layout: one core page per 16 positions and stage
+    n_seqs, prompt = wl.n_seqs, wl.prompt
+    depths = [cdbgen.draw_depths(wl.depth, n_decode, R, seed=3, stream=q) for q in range(n_seqs)]
+    mean_depth = float(np.mean(np.concatenate(depths)))
+    first = cdbgen.prompt_ids(shape.vocab, 1, n_seqs, seed=4)[0]
+    max_pages = cdbgen.pages_for(prompt + n_decode)
+    pages = n_seqs * max_pages
+    kv = cdb.PagedKV(shape, n_seqs, max_pages, pages, pages, pages, fill="random")
+    kv.core.normal_(0.0, 1.0)
+    kv.pre.normal_(0.0, 1.0)
+    kv.coda.normal_(0.0, 1.0)
+    state = cdb.State(shape, n_seqs)
+    ws = cdb.Workspace(dm.desc, 256)
+    out_ids = torch.empty((n_seqs, n_decode), dtype=torch.int32, device="cuda")
+
+    def run(n, nd, **mode):
+        d = drv.Driver(max_batch=wl.max_batch, max_active=n, r_max=R, max_seqs=n_seqs, max_pages=max_pages,
+                       core_pages=pages, pre_pages=pages, coda_pages=pages, has_prelude=True, has_coda=True,
+                       kv_layout=drv.KV_SHARED, min_coda_batch=32, **mode)
+        for q in range(n):
+            d.add_sequence(prompt, depths[q][:nd])
+        scratch = torch.empty(d.scratch_bytes(shape.vocab), dtype=torch.uint8, device="cuda")
+        secs = d.run(dm.model, kv.c, state.c, scratch, first, ws.buf, tokens_out=out_ids)
+        if cdb.cdb_read_device_error(ws.buf) != 0:
+            raise RuntimeError("device error in the huginn driver run")
+        return secs, d.stats()
+
+    run(4, 4)  # first use of the boundary kernels at this shape
+    e2e = {"workload": f"{n_seqs} requests, prompt {prompt} (KV synthesized), {n_decode} decode tokens each, depths "
+                       f"lognormal median 12, sigma 0.5, clipped to [4, 32], max batch {wl.max_batch}, shared KV, "
+                       f"minimum boundary batch 32",
+           "mean_depth": round(mean_depth, 4), "flop_bound": round(cost.flop_bound(shape, mean_depth), 4)}
+    for name, mode in (("cdb_refill", {}), ("cb_fixed_depth", {"fixed_depth": True})):
+        secs, st = run(n_seqs, n_decode, **mode)
+        e2e[name] = {"tokens_per_s": round(st["tokens"] / secs, 1), "seconds": round(secs, 4),
+                     "loop_steps": st["loop_steps"], "loop_rows": st["loop_rows"], "idle_rows": st["idle_rows"],
+                     "coda_calls": st["coda_calls"], "prelude_calls": st["prelude_calls"]}
+        log(f"huginn e2e {name}: {st['tokens']} tokens in {secs:.3f}s, {st['loop_steps']} loop steps")
+    e2e["speedup_refill_vs_cb"] = round(e2e["cdb_refill"]["tokens_per_s"] / e2e["cb_fixed_depth"]["tokens_per_s"], 4)
+    res["e2e"] = e2e
+    del kv, state, ws, dm
+    torch.cuda.empty_cache()
+    return res
 
 
 def graph_leg(dm, kv, state, rows, out, ws, steps, reps=3):
@@ -499,6 +628,9 @@ def main():
     ap.add_argument("--no-sweep", action="store_true", help="skip the loop-step batch-size sweep")
     ap.add_argument("--serving-requests", type=int, default=200,
                     help="requests in the serving-trace run (0 = skip; 2000 is the full trace)")
+    ap.add_argument("--huginn-decode", type=int, default=64,
+                    help="decode tokens per request in the Huginn-shaped whole-decode runs (0 = skip the Huginn leg; "
+                         "512 is the full workload)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="run one plain device copy of this many MiB first (a known-size reference for HBM counters)")
     args = ap.parse_args()
@@ -585,6 +717,12 @@ def main():
         serving["p99_latency_reduction"] = round(1 - a["normalized_latency_s"]["p99"] /
                                                  b["normalized_latency_s"]["p99"], 4)
 
+    huginn = None
+    if args.huginn_decode > 0:
+        del kv, state, rows, out, ws
+        torch.cuda.empty_cache()
+        huginn = huginn_leg(args.huginn_decode)
+
     cpu = None
     if args.cpu_sample > 0:
         threads = min(16, os.cpu_count() or 1)
@@ -628,6 +766,7 @@ def main():
         "e2e": e2e,
         "prefill": prefill,
         "serving": serving,
+        "huginn": huginn,
     }
     print(json.dumps(res), flush=True)
 

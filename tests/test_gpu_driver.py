@@ -134,6 +134,35 @@ def test_driver_decode_is_schedule_invariant_and_follows_oracle(kv_layout):
     assert checked >= 0.3 * (sum(ndec) + n)  # not vacuous: about half the positions have a clear gap
 
 
+# the Huginn-shaped features at small widths: the input-injection adapter
+# (W_a [h; e] before every core pass) and the convergence exit score
+INJ = cdbgen.ModelShape(name="inj-1-2-1", d=192, n_heads=3, head_dim=64, d_ff=256, vocab=160, n_prelude=1,
+                        n_core=2, n_coda=1, r_max=3, injection=1, exit_kind=1)
+
+
+@pytest.mark.parametrize("kv_layout", [drv.KV_FULL, drv.KV_SHARED], ids=["full", "shared"])
+def test_driver_decode_with_injection_is_schedule_invariant_and_follows_oracle(kv_layout):
+    s = INJ
+    _say(f"[gpu] driver decode {s.name} layout {kv_layout}")
+    w = cdbgen.model_weights(s)
+    gm = cdb.DeviceModel(s, w)
+    prompts, ndec, depths = _requests(s, seed=44)
+    n = len(prompts)
+    runs = {}
+    for name, cfg in (("refill", dict(max_batch=4, max_active=n)),
+                      ("no-refill", dict(max_batch=5, max_active=n, refill=False))):
+        first, ids, st, secs = _decode_on_gpu(s, gm, prompts, ndec, depths, kv_layout, **cfg)
+        _say(f"[gpu]   {name}: {st} in {secs * 1e3:.1f} ms")
+        assert st["tokens"] == sum(ndec)
+        assert st["loop_rows"] == sum(int(x.sum()) for x in depths)
+        runs[name] = (first, ids)
+    assert np.array_equal(runs["refill"][0], runs["no-refill"][0])
+    assert np.array_equal(runs["refill"][1], runs["no-refill"][1])
+    checked = _check_against_oracle(s, w, prompts, ndec, depths, *runs["refill"], kv_layout)
+    _say(f"[gpu]   {checked} greedy ids checked against the oracle")
+    assert checked >= 0.3 * (sum(ndec) + n)
+
+
 @pytest.mark.parametrize("kv_layout", [1, 2], ids=["shared", "first-then-shared"])
 def test_shared_layouts_call_by_call(kv_layout):
     from lockstep import Lockstep
