@@ -306,11 +306,16 @@ __global__ __launch_bounds__(256) void k_compact(int M, const uint8_t* __restric
 
 // Last-exited cache: for each exiting row (depth < r_max), copy its K/V at pos
 // from plane depth to planes depth+1..r_max, for the core layer blockIdx.y.
+// The destination page ids are read into LDS first and each chunk of the
+// source entry (up to 8 16-byte vectors per thread) is loaded once, before
+// any store: source and destinations share the pool, so a load left after a
+// store would wait for it, one round trip per vector and plane.
 __global__ __launch_bounds__(256) void k_copy_on_exit(int H, int hd, int r_max, KvTarget kv,
                                                       const int32_t* __restrict__ seq, const int32_t* __restrict__ pos,
                                                       const int32_t* __restrict__ depth,
                                                       const int32_t* __restrict__ exited,
                                                       const int32_t* __restrict__ counts, int* err) {
+    __shared__ int s_dst[64];  // destination page of plane dep + 1 + k, -1 if unmapped (r_max <= 64)
     const int j = blockIdx.x;
     if (j >= counts[1]) return;
     const int i = exited[j];
@@ -328,23 +333,45 @@ __global__ __launch_bounds__(256) void k_copy_on_exit(int H, int hd, int r_max, 
         if (threadIdx.x == 0) set_err(err, CDB_DEV_UNMAPPED_PAGE);
         return;
     }
+    const int n_dst = r_max - dep;
+    if (threadIdx.x < n_dst) {
+        const int dst = pt[(size_t)(dep + 1 + threadIdx.x) * kv.max_pages + pg];
+        const bool ok = dst >= 0 && dst < kv.n_pages;
+        if (!ok) set_err(err, CDB_DEV_UNMAPPED_PAGE);
+        s_dst[threadIdx.x] = ok ? dst : -1;
+    }
+    __syncthreads();
     const int vec_per_head = hd / 8;  // 16-byte vectors per (kv, head) entry
     const int nvec = 2 * H * vec_per_head;
-    int prev = src;  // aliased planes (shared layouts) map one page: copy it once
-    for (int pl = dep + 1; pl <= r_max; ++pl) {
-        const int dst = pt[(size_t)pl * kv.max_pages + pg];
-        if (dst < 0 || dst >= kv.n_pages) {
-            if (threadIdx.x == 0) set_err(err, CDB_DEV_UNMAPPED_PAGE);
-            continue;
+    const int tok = ps % kPage;
+    // vector v = (kv * H + head, 8-element run e) of the entry: its offset from
+    // kv_offset(l, page, ..., kv 0, head 0, tok 0) is the same on every page
+    auto in_page = [&](int v) {
+        const int kvh = v / vec_per_head, e = v - kvh * vec_per_head;
+        return ((size_t)kvh * kPage + tok) * hd + e * 8;
+    };
+    const uint16_t* src_base = kv.pool + kv_offset(l, src, kv.n_pages, 0, 0, H, 0, hd);
+    constexpr int VPT = 8;  // vectors per thread per chunk
+    for (int base = 0; base < nvec; base += VPT * 256) {
+        uint4 buf[VPT];
+        size_t off[VPT];
+#pragma unroll
+        for (int u = 0; u < VPT; ++u) {
+            const int v = base + threadIdx.x + u * 256;
+            off[u] = v < nvec ? in_page(v) : 0;
+            if (v < nvec) buf[u] = *reinterpret_cast<const uint4*>(src_base + off[u]);
         }
-        if (dst == src || dst == prev) continue;
-        prev = dst;
-        for (int v = threadIdx.x; v < nvec; v += 256) {
-            const int kvh = v / vec_per_head, e = v - kvh * vec_per_head;  // kvh = kv*H + head
-            const int kvi = kvh / H, hh = kvh - kvi * H;
-            const size_t so = kv_offset(l, src, kv.n_pages, kvi, hh, H, ps % kPage, hd) + e * 8;
-            const size_t dof = kv_offset(l, dst, kv.n_pages, kvi, hh, H, ps % kPage, hd) + e * 8;
-            *reinterpret_cast<uint4*>(kv.pool + dof) = *reinterpret_cast<const uint4*>(kv.pool + so);
+        int prev = src;  // aliased planes (shared layouts) map one page: copy it once
+        for (int k = 0; k < n_dst; ++k) {
+            const int dst = s_dst[k];
+            if (dst < 0 || dst == src || dst == prev) continue;
+            prev = dst;
+            uint16_t* dst_base = kv.pool + kv_offset(l, dst, kv.n_pages, 0, 0, H, 0, hd);
+#pragma unroll
+            for (int u = 0; u < VPT; ++u) {
+                const int v = base + threadIdx.x + u * 256;
+                if (v < nvec) *reinterpret_cast<uint4*>(dst_base + off[u]) = buf[u];
+            }
         }
     }
 }
