@@ -245,7 +245,8 @@ cdb_status cdb_boundary_coda(const cdb_model* model, const cdb_kv* kv, const cdb
  * sequence must already be in the cache (earlier chunks); every plane's pages
  * of positions < pos0 + n_rows must be mapped.  Attention is query-tiled on
  * MFMA; above 256 rows the projections use compute-bound tiles.
- * n_rows <= 512; the workspace must be sized for n_rows. */
+ * 1 <= n_rows <= 512, else CDB_ERR_CAPACITY (an empty chunk has no last row to
+ * take an id from); the workspace must be sized for n_rows. */
 cdb_status cdb_prefill(const cdb_model* model, const cdb_kv* kv, int32_t seq, int32_t pos0, int32_t n_rows,
                        const int32_t* tokens, float* logits, int32_t* next_ids, void* ws, size_t ws_bytes,
                        hipStream_t stream);

@@ -1,0 +1,174 @@
+"""GPU: edge cases of the stage calls.
+
+* Empty calls are no-ops (a loop step over zero rows still reports zero counts);
+  an empty prefill chunk is refused.
+* Row counts that leave ragged 32-row tiles in every skinny-GEMM tile size
+  (1, 31, 33, 100, 255 rows) at the Ouro widths, checked like the full-batch
+  parity tests: integer outputs for the whole batch, sampled rows against the
+  oracle.
+* Degenerate exit patterns: every row exits (depth = c + 1, depths 1..r_max, so
+  every exiting row below r_max copies its entry into the deeper planes), and no
+  row exits.
+* Conditions the device detects are reported through the sticky error word and
+  never make a kernel touch memory outside its buffers: an unmapped page inside a
+  row's context, an unmapped write page, a slot outside the state pool.  They are
+  forced from the host through the page table and the row arrays.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import cdbgen
+import paper_2608_09444_amd as cdb
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def _ouro_two_layers():
+    s = cdbgen.shrink(cdbgen.OURO, n_core=2)
+    w = cdbgen.model_weights(cdbgen.OURO)
+    w = dict(w, layers=w["layers"][:2])
+    return s, w
+
+
+def _sample_rows(rows_np, r_max):
+    c, dep, pos = rows_np["c"], rows_np["depth"], rows_np["pos"]
+    ex = [i for i in range(len(c)) if c[i] + 1 == dep[i] and dep[i] < r_max]
+    co = [i for i in range(len(c)) if c[i] + 1 < dep[i]]
+    picks = []
+    for cand in (ex[:1], co[:1], [int(np.argmax(pos))], [len(c) - 1]):
+        for i in cand:
+            if i not in picks:
+                picks.append(i)
+    return picks
+
+
+def test_empty_stage_calls():
+    s = cdbgen.TINY
+    R = s.r_max
+    gm = cdb.DeviceModel(s, cdbgen.model_weights(s))
+    kv = cdb.PagedKV(s, 2, 4, 8, 8 * R, 8, fill="random")
+    pt = np.arange(2 * (R + 2) * 4, dtype=np.int32).reshape(2, R + 2, 4) % 8
+    kv.page_table.copy_(torch.from_numpy(pt))
+    state = cdb.State(s, 2)
+    state.h.normal_(0.0, 1.0)
+    pools = [kv.pre.clone(), kv.core.clone(), kv.coda.clone()]
+    h0 = state.h.clone()
+    ws = cdb.Workspace(gm.desc, 4)
+    empty = np.zeros(0, np.int32)
+    rows = cdb.Rows(empty, empty, empty, empty, empty)
+    out = cdb.StepOut(1)
+    out.counts.fill_(7)
+    tokens = torch.zeros(1, dtype=torch.int32, device="cuda")
+    logits = torch.zeros((1, s.vocab), dtype=torch.float32, device="cuda")
+    ids = torch.zeros(1, dtype=torch.int32, device="cuda")
+    _say("[gpu] empty prelude / loop step / coda / attention calls on the tiny model")
+    cdb.cdb_boundary_prelude(gm.model, kv.c, state.c, rows.c, tokens, ws.buf)
+    cdb.cdb_loop_step(gm.model, kv.c, state.c, rows.c, out.c, ws.buf)
+    cdb.cdb_boundary_coda(gm.model, kv.c, state.c, rows.c, logits, ids, ws.buf)
+    q = torch.zeros((1, s.d), dtype=torch.float32, device="cuda")
+    o = torch.zeros((1, s.d), dtype=torch.bfloat16, device="cuda")
+    cdb.cdb_paged_attention(gm.desc, kv.c, rows.c, 1, 0, q, o, ws.buf)
+    torch.cuda.synchronize()
+    assert out.counts.cpu().tolist() == [0, 0]
+    assert torch.equal(state.h, h0)
+    for a, b in zip(pools, (kv.pre, kv.core, kv.coda)):
+        assert torch.equal(a, b)
+    assert cdb.cdb_read_device_error(ws.buf) == cdb.CDB_DEV_OK
+    with pytest.raises(cdb.CdbError):
+        cdb.cdb_prefill(gm.model, kv.c, 0, 0, tokens[:0], logits, ids, ws.buf)
+
+
+@pytest.mark.parametrize("n_rows", [1, 31, 33, 100, 255])
+def test_ragged_row_counts_at_ouro_width(n_rows):
+    from lockstep import injected_loop_step
+    s, w = _ouro_two_layers()
+    rows = cdbgen.decode_snapshot(n_rows, cdbgen.OURO_DEPTHS, s.r_max, 512, 767, stream=60 + n_rows)
+    sample = _sample_rows(rows, s.r_max)
+    _say(f"[gpu] Ouro widths, 2 core layers, {n_rows} rows; sampled rows {sample}")
+    err = injected_loop_step(s, w, rows, sample, sensitivity=True)
+    _say(f"[gpu]   errors {err}")
+
+
+@pytest.mark.parametrize("pattern", ["all_exit", "none_exit"])
+def test_degenerate_exit_patterns(pattern):
+    from lockstep import injected_loop_step
+    s, w = _ouro_two_layers()
+    R = s.r_max
+    rows = cdbgen.decode_snapshot(64, cdbgen.OURO_DEPTHS, R, 512, 767, stream=70)
+    g = np.random.default_rng(5)
+    if pattern == "all_exit":
+        rows["c"] = g.integers(0, R, 64).astype(np.int32)
+        rows["depth"] = rows["c"] + 1
+    else:
+        rows["depth"] = np.full(64, R, np.int32)
+        rows["c"] = g.integers(0, R - 1, 64).astype(np.int32)
+    sample = _sample_rows(rows, R)
+    _say(f"[gpu] {pattern}: c {rows['c'][:8]} depth {rows['depth'][:8]}; sampled rows {sample}")
+    err = injected_loop_step(s, w, rows, sample, sensitivity=True)
+    _say(f"[gpu]   errors {err}")
+
+
+def _tiny_step_setup(n=4, seed=3):
+    s = cdbgen.TINY
+    R = s.r_max
+    gm = cdb.DeviceModel(s, cdbgen.model_weights(s))
+    pos = np.array([40, 47, 52, 60], np.int32)[:n]
+    c = np.array([0, 1, 2, 3], np.int32)[:n]
+    depth = np.array([1, 3, 4, 4], np.int32)[:n]
+    max_pages = cdbgen.pages_for(int(pos.max()) + 1)
+    n_pages = n * max_pages * R
+    pt = np.full((n, R + 2, max_pages), -1, np.int32)
+    pt[:, 1:R + 1, :] = np.arange(n_pages, dtype=np.int32).reshape(n, R, max_pages)
+    kv = cdb.PagedKV(s, n, max_pages, 0, n_pages, 0, fill="random")
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    kv.core.normal_(0.0, 1.0, generator=g)
+    state = cdb.State(s, n)
+    state.h.normal_(0.0, 1.0, generator=g)
+    return s, gm, kv, pt, state, pos, c, depth
+
+
+@pytest.mark.parametrize("case", ["context_page", "write_page"])
+def test_unmapped_page_is_reported(case):
+    s, gm, kv, pt, state, pos, c, depth = _tiny_step_setup()
+    i = 2
+    if case == "context_page":
+        pt[i, c[i] + 1, 1] = -1  # positions 16..31 of row 2's plane
+    else:
+        pt[i, c[i] + 1, pos[i] // 16] = -1  # the page row 2 writes its new entry to
+    kv.page_table.copy_(torch.from_numpy(pt))
+    n = len(pos)
+    rows = cdb.Rows(np.arange(n, dtype=np.int32), np.arange(n, dtype=np.int32), pos, c, depth)
+    out = cdb.StepOut(n)
+    ws = cdb.Workspace(gm.desc, n)
+    _say(f"[gpu] tiny loop step with an unmapped {case.replace('_', ' ')} in row {i}")
+    cdb.cdb_loop_step(gm.model, kv.c, state.c, rows.c, out.c, ws.buf)
+    torch.cuda.synchronize()
+    assert cdb.cdb_read_device_error(ws.buf) == cdb.CDB_DEV_UNMAPPED_PAGE
+    assert out.counts.cpu().tolist() == [int((c + 1 < depth).sum()), int((c + 1 == depth).sum())]
+
+
+def test_slot_outside_the_pool_is_reported():
+    s, gm, kv, pt, state, pos, c, depth = _tiny_step_setup()
+    kv.page_table.copy_(torch.from_numpy(pt))
+    n = len(pos)
+    slots = np.arange(n, dtype=np.int32)
+    slots[1] = n + 5
+    h0 = state.h.clone()
+    rows = cdb.Rows(slots, np.arange(n, dtype=np.int32), pos, c, depth)
+    out = cdb.StepOut(n)
+    ws = cdb.Workspace(gm.desc, n)
+    _say("[gpu] tiny loop step with a slot outside the state pool")
+    cdb.cdb_loop_step(gm.model, kv.c, state.c, rows.c, out.c, ws.buf)
+    torch.cuda.synchronize()
+    assert cdb.cdb_read_device_error(ws.buf) == cdb.CDB_DEV_BAD_INDEX
+    # the valid rows' states were written, the pool has no row for the bad one
+    assert not torch.equal(state.h[0], h0[0])
