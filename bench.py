@@ -451,6 +451,75 @@ def huginn_leg(n_decode, steps=20, warmup=3):
     return res
 
 
+def long_context_leg(shape, dm, headroom_gib=16):
+    """Config 4: 256 requests with prompts uniform in [2048, 4096] (KV
+    synthesized as zeros), 128 decode tokens each, half of the tokens exiting at
+    loop 1 and half at loop 4.  The depth-indexed cache of all 256 would take
+    ≈ 630 GB, so under the full layout the driver admits requests while core
+    pages last (KV-capacity admission) and the resident batch is what fits; the
+    shared layout (one plane per position) holds all of them.  Each layout runs
+    CDB refill against fixed-depth continuous batching on the same pool."""
+    import numpy as np
+    import torch
+
+    import cdbgen
+    import paper_2608_09444_amd as cdb
+    from paper_2608_09444_amd import cost
+    from paper_2608_09444_amd import driver as drv
+    wl = cdbgen.WORKLOADS[4]
+    R = shape.r_max
+    n_seqs, n_decode = wl.n_seqs, wl.decode
+    plen = cdbgen.lengths(wl.prompt, n_seqs, seed=cdbgen.PROMPT_SEED, stream=400)
+    depths = [cdbgen.draw_depths(wl.depth, n_decode, R, stream=400 + q) for q in range(n_seqs)]
+    mean_depth = float(np.mean(np.concatenate(depths)))
+    first = cdbgen.prompt_ids(shape.vocab, 1, n_seqs, seed=5)[0]
+    max_pages = cdbgen.pages_for(int(plen.max()) + n_decode)
+    page_bytes = shape.n_core * 2 * shape.n_heads * cdbgen.PAGE_TOKENS * shape.head_dim * 2
+    torch.cuda.empty_cache()
+    free, _ = torch.cuda.mem_get_info()
+    budget_pages = int((free - (headroom_gib << 30)) // page_bytes)
+    state = cdb.State(shape, n_seqs)
+    ws = cdb.Workspace(dm.desc, 256)
+    out_ids = torch.empty((n_seqs, n_decode), dtype=torch.int32, device="cuda")
+    res = {"workload": f"{n_seqs} requests, prompts uniform in [2048, 4096] (KV synthesized), {n_decode} decode tokens "
+                       f"each, depths 50% 1 / 50% 4 per token, max batch {wl.max_batch}",
+           "mean_depth": round(mean_depth, 4), "flop_bound": round(cost.flop_bound(shape, mean_depth), 4),
+           "prompt_tokens": int(plen.sum())}
+    for lname, layout, planes in (("full", drv.KV_FULL, R), ("shared", drv.KV_SHARED, 1)):
+        need = int(sum(cdbgen.pages_for(int(p) + n_decode) for p in plen)) * planes
+        core_pages = min(need, budget_pages)
+        kv = cdb.PagedKV(shape, n_seqs, max_pages, 0, core_pages, 0)
+        torch.cuda.synchronize()
+        log(f"long context, {lname} layout: {core_pages} core pages ({core_pages * page_bytes / 1e9:.0f} GB of "
+            f"{need * page_bytes / 1e9:.0f} GB for all requests)")
+        entry = {"core_pages": core_pages, "pool_gb": round(core_pages * page_bytes / 1e9, 1),
+                 "all_requests_gb": round(need * page_bytes / 1e9, 1)}
+        for name, mode in (("cdb_refill", {}), ("cb_fixed_depth", {"fixed_depth": True})):
+            d = drv.Driver(max_batch=wl.max_batch, max_active=n_seqs, r_max=R, max_seqs=n_seqs, max_pages=max_pages,
+                           core_pages=core_pages, kv_layout=layout, **mode)
+            for q in range(n_seqs):
+                d.add_sequence(int(plen[q]), depths[q])
+            scratch = torch.empty(d.scratch_bytes(shape.vocab), dtype=torch.uint8, device="cuda")
+            secs = d.run(dm.model, kv.c, state.c, scratch, first, ws.buf, tokens_out=out_ids)
+            if cdb.cdb_read_device_error(ws.buf) != 0:
+                raise RuntimeError("device error in the long-context driver run")
+            st = d.stats()
+            entry[name] = {"tokens_per_s": round(st["tokens"] / secs, 1), "seconds": round(secs, 3),
+                           "loop_steps": st["loop_steps"], "loop_rows": st["loop_rows"],
+                           "mean_rows_per_loop_step": round(st["loop_rows"] / max(st["loop_steps"], 1), 1),
+                           "idle_rows": st["idle_rows"], "coda_calls": st["coda_calls"]}
+            log(f"long context, {lname} layout, {name}: {st['tokens']} tokens in {secs:.2f}s, {st['loop_steps']} loop "
+                f"steps, {st['loop_rows'] / max(st['loop_steps'], 1):.1f} rows per step")
+        entry["speedup_refill_vs_cb"] = round(entry["cdb_refill"]["tokens_per_s"] /
+                                              entry["cb_fixed_depth"]["tokens_per_s"], 4)
+        res[lname] = entry
+        del kv
+        torch.cuda.empty_cache()
+    del state, ws, out_ids
+    torch.cuda.empty_cache()
+    return res
+
+
 def graph_leg(dm, kv, state, rows, out, ws, steps, reps=3):
     """cdb_loop_step captured once in a HIP graph and replayed: the replay time
     per step, and each of `reps` replays checked bit for bit against an eager
@@ -631,6 +700,8 @@ def main():
     ap.add_argument("--huginn-decode", type=int, default=64,
                     help="decode tokens per request in the Huginn-shaped whole-decode runs (0 = skip the Huginn leg; "
                          "512 is the full workload)")
+    ap.add_argument("--long-context", action="store_true",
+                    help="also run config 4's long-context decodes (about 250 GB of KV pools, ≈ 3 minutes)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="run one plain device copy of this many MiB first (a known-size reference for HBM counters)")
     args = ap.parse_args()
@@ -718,9 +789,13 @@ def main():
                                                  b["normalized_latency_s"]["p99"], 4)
 
     huginn = None
-    if args.huginn_decode > 0:
+    long_ctx = None
+    if args.huginn_decode > 0 or args.long_context:
         del kv, state, rows, out, ws
         torch.cuda.empty_cache()
+    if args.long_context:
+        long_ctx = long_context_leg(shape, dm)
+    if args.huginn_decode > 0:
         huginn = huginn_leg(args.huginn_decode)
 
     cpu = None
@@ -767,6 +842,7 @@ def main():
         "prefill": prefill,
         "serving": serving,
         "huginn": huginn,
+        "long_context": long_ctx,
     }
     print(json.dumps(res), flush=True)
 
