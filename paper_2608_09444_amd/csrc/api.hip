@@ -64,12 +64,12 @@ static ModelGemms model_gemms(const cdb_model_desc& d, int M = 0) {
         g.lm = gemm_shape_mn(d.vocab, d.d, M, EPI_STORE);
         return g;
     }
-    g.qkv = gemm_shape(3 * d.d, d.d, EPI_QKV);
-    g.o = gemm_shape(d.d, d.d, EPI_PARTIAL);
-    g.gu = gemm_shape(2 * d.d_ff, d.d, EPI_SWIGLU);
-    g.down = gemm_shape(d.d, d.d_ff, EPI_PARTIAL);
-    g.adapter = gemm_shape(d.d, 2 * d.d, EPI_STORE);
-    g.lm = gemm_shape(d.vocab, d.d, EPI_STORE);
+    g.qkv = gemm_shape(3 * d.d, d.d, EPI_QKV, M);
+    g.o = gemm_shape(d.d, d.d, EPI_PARTIAL, M);
+    g.gu = gemm_shape(2 * d.d_ff, d.d, EPI_SWIGLU, M);
+    g.down = gemm_shape(d.d, d.d_ff, EPI_PARTIAL, M);
+    g.adapter = gemm_shape(d.d, 2 * d.d, EPI_STORE, M);
+    g.lm = gemm_shape(d.vocab, d.d, EPI_STORE, M);
     return g;
 }
 
@@ -412,7 +412,7 @@ cdb_status cdb_boundary_coda(const cdb_model* model, const cdb_kv* kv, const cdb
     const int T = (M - 1) / 32, MT = M - 32 * T;
     const uint16_t* xt = c.x + (size_t)T * (d.d / 16) * 512;  // fragment m-tiles are contiguous
     ea.out = c.lm;
-    HIPCHK(launch_gemm(EPI_STORE, xt, wptr(c, c.wl.lm_head), MT, gemm_shape(d.vocab, d.d, EPI_STORE), c.part, ea, st));
+    HIPCHK(launch_gemm(EPI_STORE, xt, wptr(c, c.wl.lm_head), MT, gemm_shape(d.vocab, d.d, EPI_STORE, MT), c.part, ea, st));
     HIPCHK(launch_argmax(1, d.vocab, c.lm + (size_t)(MT - 1) * d.vocab, next_ids, st));
     return CDB_OK;
 }
@@ -478,7 +478,7 @@ cdb_status cdb_prefill(const cdb_model* model, const cdb_kv* kv, int32_t seq, in
     const int T = (M - 1) / 32, MT = M - 32 * T;
     const uint16_t* xt = c.x + (size_t)T * (d.d / 16) * 512;  // fragment m-tiles are contiguous
     ea.out = c.lm;
-    HIPCHK(launch_gemm(EPI_STORE, xt, wptr(c, c.wl.lm_head), MT, gemm_shape(d.vocab, d.d, EPI_STORE), c.part, ea, st));
+    HIPCHK(launch_gemm(EPI_STORE, xt, wptr(c, c.wl.lm_head), MT, gemm_shape(d.vocab, d.d, EPI_STORE, MT), c.part, ea, st));
     HIPCHK(launch_argmax(1, d.vocab, c.lm + (size_t)(MT - 1) * d.vocab, next_ids, st));
     return CDB_OK;
 }

@@ -107,7 +107,7 @@ struct WsLayout {
 };
 WsLayout ws_layout(const cdb_model_desc& d, int rows);
 
-GemmShape gemm_shape(int N, int K, int epi);
+GemmShape gemm_shape(int N, int K, int epi, int M);  // M <= kMaxRows
 GemmShape gemm_shape_mn(int N, int K, int M, int epi);  // M > kMaxRows
 bool desc_supported(const cdb_model_desc& d);
 

@@ -96,6 +96,7 @@ __device__ __forceinline__ void stripe_epilogue(const float* fin, int fld, int n
         const int ld = EPI == EPI_PARTIAL ? ga.N : ea.ld_out;
         for (int e = tid; e < NS * per; e += nthr) {
             const int ns = e / per, r = e - ns * per;
+            if (nt + ns >= (ga.N >> 5)) break;
             const int m = r >> 3, c4 = (r & 7) * 4;
             const float* f = fin + ns * 32 * fld + c4 * fld + m;
             const float4 v = make_float4(f[0], f[fld], f[2 * fld], f[3 * fld]);
@@ -114,6 +115,7 @@ __device__ __forceinline__ void stripe_epilogue(const float* fin, int fld, int n
         const int per = mcap * 2;
         for (int e = tid; e < NS * per; e += nthr) {
             const int ns = e / per, r = e - ns * per;
+            if (nt + ns >= (ga.N >> 5)) break;
             const int m = r >> 1, c8 = (r & 1) * 8;
             const float* f = fin + ns * 32 * fld + m;
             uint32_t w[4];
@@ -208,7 +210,13 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs ga, EpiArgs ea) {
 #pragma unroll
             for (int j = 0; j < 16; ++j) acc[ns][t][j] = 0.f;
 
-    const u32x4* wsrc = reinterpret_cast<const u32x4*>(ga.Wp) + (size_t)nt * KS * 64 + lane;
+    // a workgroup's last stripes may lie past the matrix (an odd stripe count
+    // with NS = 2): they re-read the last stripe and their results are not stored
+    const int stripes = ga.N >> 5;
+    const u32x4* wsrc[NS];
+#pragma unroll
+    for (int ns = 0; ns < NS; ++ns)
+        wsrc[ns] = reinterpret_cast<const u32x4*>(ga.Wp) + (size_t)min(nt + ns, stripes - 1) * KS * 64 + lane;
     // X is in fragment layout: the operand of m-tile t at k step k is the 1 KiB tile (t, k)
     const u32x4* xsrc = reinterpret_cast<const u32x4*>(ga.X) + lane;
     // k steps per load batch (register budget: two batches of NS + MT operands)
@@ -226,7 +234,7 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs ga, EpiArgs ea) {
         for (int i = 0; i < CH; ++i) {
             const int ks = min(c0 + i, ks1 - 1);
 #pragma unroll
-            for (int ns = 0; ns < NS; ++ns) w[i][ns] = wsrc[((size_t)ns * KS + ks) * 64];
+            for (int ns = 0; ns < NS; ++ns) w[i][ns] = wsrc[ns][(size_t)ks * 64];
 #pragma unroll
             for (int t = 0; t < MT; ++t) x[i][t] = xsrc[((size_t)t * KS + ks) * 64];
         }
@@ -647,21 +655,34 @@ GemmShape gemm_shape_mn(int N, int K, int M, int epi) {
     return GemmShape{N, K, S, 4, 4};
 }
 
-GemmShape gemm_shape(int N, int K, int epi) {
+GemmShape gemm_shape(int N, int K, int epi, int M) {
     const int stripes = N / 32;
     const int KS = K / 16;
+    const int MT = M <= 32 ? 1 : (M <= 64 ? 2 : (M <= 128 ? 4 : 8));  // 32-row tiles per pass
+    // K split until the grid covers the chip, keeping at least min_ks k steps per
+    // workgroup: at 33-64 rows 64 (the 4-way split of a 2048-long K loses more to
+    // each workgroup's fixed costs than its extra workgroups gain: 6.4 -> 5.8 us
+    // for Ouro's O projection at 2-way), elsewhere 32
+    const int min_ks = MT == 2 ? 64 : 32;
     int S = 1;
     if (epi == EPI_PARTIAL) {
-        while (stripes * S < 256 && KS / (S * 2) >= 32) S *= 2;
+        while (stripes * S < 256 && KS / (S * 2) >= min_ks) S *= 2;
     }
     // waves per workgroup: 8 (more weight bytes in flight per CU) while the
     // grid fits the chip in one round, else 4
     int KW = 4;
     if (stripes * S <= 256 && KS / S >= 32) KW = 8;
-    // wide projections without a K split (gate/up, LM head): two stripes per
-    // workgroup share the activation loads, with 8 waves
     int NS = 1;
-    if (epi != EPI_QKV && S == 1 && stripes > 256 && stripes % 2 == 0 && KS >= 64) {
+    // wide projections without a K split (gate/up, LM head): two stripes per
+    // workgroup share the activation loads (256-row passes hold one stripe)
+    if (epi != EPI_QKV && MT < 8 && S == 1 && stripes > 256 && stripes % 2 == 0 && KS >= 64) {
+        NS = 2;
+        KW = stripes / 2 <= 256 ? 8 : 4;
+    }
+    // 65-128 rows read 4 activation bytes from L2 per weight byte; over long K
+    // ranges that stream bounds the kernel, and two stripes per workgroup halve
+    // it (Huginn-shaped O and down: 36 -> 28 and 99 -> 69 us)
+    if (epi == EPI_PARTIAL && MT == 4 && KS / S >= 128) {
         NS = 2;
         KW = 8;
     }
@@ -679,7 +700,7 @@ static hipError_t launch_mt(const GemmArgs& ga, const EpiArgs& ea, hipStream_t s
     }
     size_t lds = ((size_t)ga.KW * 1024 + (size_t)NS * 32 * (MT * 32 + 1)) * 4;
     if (EPI == EPI_QKV) lds += (size_t)MT * 32 * 16 * 8 + (size_t)MT * 32 * 2 * 4;
-    dim3 grid(ga.N / (32 * NS), ga.S);
+    dim3 grid((ga.N / 32 + NS - 1) / NS, ga.S);
     k_gemm<EPI, MT, NS><<<grid, ga.KW * 64, lds, st>>>(ga, ea);
     return hipGetLastError();
 }
@@ -742,7 +763,7 @@ hipError_t launch_gemm(int epi, const uint16_t* X, const uint16_t* Wp, int M, Ge
             default: return launch_mn<EPI_STORE>(ga, ea, st);
         }
     }
-    if (g.KW < 1 || g.KW > kMaxKw || (g.NS != 1 && g.NS != 2) || g.N % (32 * g.NS)) return hipErrorInvalidValue;
+    if (g.KW < 1 || g.KW > kMaxKw || (g.NS != 1 && g.NS != 2)) return hipErrorInvalidValue;
     if (epi == EPI_QKV && (g.KW < 4 || g.NS != 1)) return hipErrorInvalidValue;  // epilogue staging: >= 256 threads
     switch (epi) {
         case EPI_QKV: return launch_epi<EPI_QKV>(ga, ea, g.NS, st);
