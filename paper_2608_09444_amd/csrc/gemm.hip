@@ -656,36 +656,37 @@ GemmShape gemm_shape_mn(int N, int K, int M, int epi) {
 }
 
 GemmShape gemm_shape(int N, int K, int epi, int M) {
+    // S and KW fix every wave's K range and so the summation order of each
+    // output: they depend on (N, K, epi) only, which keeps a row's result
+    // independent of the rows that share its call.  NS (stripes per
+    // workgroup) only regroups whole stripes, and follows the row count.
     const int stripes = N / 32;
     const int KS = K / 16;
     const int MT = M <= 32 ? 1 : (M <= 64 ? 2 : (M <= 128 ? 4 : 8));  // 32-row tiles per pass
-    // K split until the grid covers the chip, keeping at least min_ks k steps per
-    // workgroup: at 33-64 rows 64 (the 4-way split of a 2048-long K loses more to
-    // each workgroup's fixed costs than its extra workgroups gain: 6.4 -> 5.8 us
-    // for Ouro's O projection at 2-way), elsewhere 32
-    const int min_ks = MT == 2 ? 64 : 32;
+    // K split until the grid covers the chip, keeping at least 64 k steps per
+    // workgroup (a 4-way split of a 2048-long K loses more to each workgroup's
+    // fixed costs than its extra workgroups gain: Ouro's O at 64 rows 6.4 ->
+    // 5.8 us with 2 ways)
     int S = 1;
     if (epi == EPI_PARTIAL) {
-        while (stripes * S < 256 && KS / (S * 2) >= min_ks) S *= 2;
+        while (stripes * S < 256 && KS / (S * 2) >= 64) S *= 2;
     }
+    // Two stripes per workgroup share every activation load.  Wide projections
+    // without a K split (gate/up, LM head) take them at up to 128 rows (a
+    // 256-row pass holds one stripe); split-K projections over long K ranges
+    // take them at 65-128 rows, where each weight byte brings 4 activation
+    // bytes from L2 and that stream bounds the kernel (Huginn-shaped O and
+    // down: 36 -> 28 and 99 -> 69 us), but not below (shorter K ranges lose
+    // more workgroups than they save).
+    const bool pair_wide = epi != EPI_QKV && epi != EPI_PARTIAL && S == 1 && stripes > 256 && stripes % 2 == 0 &&
+                           KS >= 64;
+    const bool pair_long = epi == EPI_PARTIAL && KS / S >= 128;
+    const int NS = (pair_wide && MT < 8) || (pair_long && MT == 4) ? 2 : 1;
     // waves per workgroup: 8 (more weight bytes in flight per CU) while the
-    // grid fits the chip in one round, else 4
-    int KW = 4;
-    if (stripes * S <= 256 && KS / S >= 32) KW = 8;
-    int NS = 1;
-    // wide projections without a K split (gate/up, LM head): two stripes per
-    // workgroup share the activation loads (256-row passes hold one stripe)
-    if (epi != EPI_QKV && MT < 8 && S == 1 && stripes > 256 && stripes % 2 == 0 && KS >= 64) {
-        NS = 2;
-        KW = stripes / 2 <= 256 ? 8 : 4;
-    }
-    // 65-128 rows read 4 activation bytes from L2 per weight byte; over long K
-    // ranges that stream bounds the kernel, and two stripes per workgroup halve
-    // it (Huginn-shaped O and down: 36 -> 28 and 99 -> 69 us)
-    if (epi == EPI_PARTIAL && MT == 4 && KS / S >= 128) {
-        NS = 2;
-        KW = 8;
-    }
+    // grid fits the chip in one round, counted with the stripe pairs where
+    // they may be used, else 4
+    const int groups = (pair_wide || pair_long) ? (stripes + 1) / 2 : stripes;
+    const int KW = groups * S <= 256 && KS / S >= 32 ? 8 : 4;
     return GemmShape{N, K, S, KW, NS};
 }
 

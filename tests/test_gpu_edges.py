@@ -172,3 +172,73 @@ def test_slot_outside_the_pool_is_reported():
     assert cdb.cdb_read_device_error(ws.buf) == cdb.CDB_DEV_BAD_INDEX
     # the valid rows' states were written, the pool has no row for the bad one
     assert not torch.equal(state.h[0], h0[0])
+
+
+def _own_pages(shape, rows_np):
+    R = shape.r_max
+    n = len(rows_np["pos"])
+    max_pages = cdbgen.pages_for(int(rows_np["pos"].max()) + 1)
+    pt = np.full((n, R + 2, max_pages), -1, np.int32)
+    nxt = 0
+    for i in range(n):
+        plane = int(rows_np["c"][i]) + 1
+        pg = cdbgen.pages_for(int(rows_np["pos"][i]) + 1)
+        pt[i, plane, :pg] = np.arange(nxt, nxt + pg)
+        nxt += pg
+        for pl in range(plane + 1, R + 1):
+            pt[i, pl, pg - 1] = nxt
+            nxt += 1
+    return pt, max_pages, nxt
+
+
+def _batch_invariance(shape, w, rows_np, n_small):
+    """The first n_small rows run alone give bit-identical states and exit scores
+    to the same rows run inside the whole batch (same pages, same inputs)."""
+    n = len(rows_np["pos"])
+    gm = cdb.DeviceModel(shape, w)
+    pt, max_pages, n_pages = _own_pages(shape, rows_np)
+    kv = cdb.PagedKV(shape, n, max_pages, 0, n_pages, 0, fill="random")
+    g = torch.Generator(device="cuda")
+    g.manual_seed(21)
+    kv.core.normal_(0.0, 1.0, generator=g)
+    kv.page_table.copy_(torch.from_numpy(pt))
+    state = cdb.State(shape, n)
+    state.h.normal_(0.0, 1.0, generator=g)
+    if shape.injection:
+        state.e.normal_(0.0, 1.0, generator=g)
+    h0 = state.h.clone()
+    ws = cdb.Workspace(gm.desc, n)
+    results = {}
+    for m in (n, n_small):
+        state.h.copy_(h0)
+        sl = {k: rows_np[k][:m] for k in ("pos", "c", "depth")}
+        rows = cdb.Rows(np.arange(m, dtype=np.int32), np.arange(m, dtype=np.int32), sl["pos"], sl["c"], sl["depth"])
+        out = cdb.StepOut(m)
+        cdb.cdb_loop_step(gm.model, kv.c, state.c, rows.c, out.c, ws.buf)
+        torch.cuda.synchronize()
+        assert cdb.cdb_read_device_error(ws.buf) == 0
+        results[m] = (state.h[:n_small].clone(), out.score[:n_small].clone())
+    hb, sb = results[n]
+    hs, ss = results[n_small]
+    diff = float((hb - hs).abs().max())
+    _say(f"[gpu]   {n} vs {n_small} rows: max |h difference| {diff}")
+    assert torch.equal(hb, hs) and torch.equal(sb, ss)
+
+
+def test_row_results_do_not_depend_on_the_batch_ouro_width():
+    s, w = _ouro_two_layers()
+    rows = cdbgen.decode_snapshot(100, cdbgen.OURO_DEPTHS, s.r_max, 512, 767, stream=80)
+    _say("[gpu] batch invariance, Ouro widths, 2 core layers: 100 rows (4 row tiles) vs their first 30 (1)")
+    _batch_invariance(s, w, rows, 30)
+
+
+def test_row_results_do_not_depend_on_the_batch_huginn_width():
+    # O and down take two stripes per workgroup at 128 rows and one at 50
+    s = cdbgen.shrink(cdbgen.HUGINN, n_core=1)
+    w = cdbgen.model_weights(cdbgen.HUGINN)
+    P = cdbgen.HUGINN.n_prelude
+    w = dict(w, layers=w["layers"][:P + 1] + w["layers"][P + cdbgen.HUGINN.n_core:])
+    wl = cdbgen.WORKLOADS[3]
+    rows = cdbgen.decode_snapshot(128, wl.depth, s.r_max, 256, 767, stream=81)
+    _say("[gpu] batch invariance, Huginn widths, 1 core layer: 128 rows vs their first 50")
+    _batch_invariance(s, w, rows, 50)
