@@ -129,11 +129,16 @@ __device__ __forceinline__ void stripe_epilogue(const float* fin, int fld, int n
             const int feat = (nt + ns) * 16 + c8;
             *reinterpret_cast<u32x4*>(ea.act + frag_index(m, feat, ea.ld_act)) = u32x4{w[0], w[1], w[2], w[3]};
         }
-    } else {  // EPI_QKV, one stripe: 16 rotary pairs (dims gi*16 + jj and + hd/2) of one head
-        const int g = nt, gph = ea.hd >> 5, hg = ea.H * gph;
+    } else {  // EPI_QKV: a stripe holds 16 rotary pairs (dims gi*16 + jj and + hd/2) of one head
+      const int mrows = fld - 1;  // rows of a stripe's staged RoPE table
+      for (int ns = 0; ns < NS; ++ns) {
+        const int g = nt + ns, gph = ea.hd >> 5, hg = ea.H * gph;
+        if (g >= (ga.N >> 5)) break;
         const int part = g / hg, rem = g - part * hg;
         const int head = rem / gph, gi = rem - head * gph;
         const int half_hd = ea.hd >> 1;
+        const float* fs = fin + ns * 32 * fld;
+        const float2* srope = qs.rope ? qs.rope + (size_t)ns * mrows * 16 : nullptr;
         if (part == 0) {
             // (m, half, 4-pair run) -> 4 consecutive fp32 q values
             for (int e = tid; e < mcap * 8; e += nthr) {
@@ -142,8 +147,8 @@ __device__ __forceinline__ void stripe_epilogue(const float* fin, int fld, int n
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int jj = j4 + i;
-                    const float val = fin[(half * 16 + jj) * fld + m], partner = fin[((half ^ 1) * 16 + jj) * fld + m];
-                    const float2 cs = qs.rope ? qs.rope[m * 16 + jj] : ea.rope[(size_t)m * half_hd + gi * 16 + jj];
+                    const float val = fs[(half * 16 + jj) * fld + m], partner = fs[((half ^ 1) * 16 + jj) * fld + m];
+                    const float2 cs = srope ? srope[m * 16 + jj] : ea.rope[(size_t)m * half_hd + gi * 16 + jj];
                     const float xf = half ? partner : val, xs = half ? val : partner;
                     o[i] = half ? (xs * cs.x + xf * cs.y) : (xf * cs.x - xs * cs.y);
                 }
@@ -164,12 +169,12 @@ __device__ __forceinline__ void stripe_epilogue(const float* fin, int fld, int n
 #pragma unroll
                     for (int b = 0; b < 2; ++b) {
                         const int jj = j8 + i + b;
-                        const float val = fin[(half * 16 + jj) * fld + m];
+                        const float val = fs[(half * 16 + jj) * fld + m];
                         float outv = val;
                         if (part == 1) {
-                            const float partner = fin[((half ^ 1) * 16 + jj) * fld + m];
+                            const float partner = fs[((half ^ 1) * 16 + jj) * fld + m];
                             const float2 cs =
-                                qs.rope ? qs.rope[m * 16 + jj] : ea.rope[(size_t)m * half_hd + gi * 16 + jj];
+                                srope ? srope[m * 16 + jj] : ea.rope[(size_t)m * half_hd + gi * 16 + jj];
                             const float xf = half ? partner : val, xs = half ? val : partner;
                             outv = half ? (xs * cs.x + xf * cs.y) : (xf * cs.x - xs * cs.y);
                         }
@@ -183,6 +188,7 @@ __device__ __forceinline__ void stripe_epilogue(const float* fin, int fld, int n
                 *reinterpret_cast<u32x4*>(dst) = u32x4{w[0], w[1], w[2], w[3]};
             }
         }
+      }
     }
 }
 
@@ -190,7 +196,6 @@ __device__ __forceinline__ void stripe_epilogue(const float* fin, int fld, int n
 // 32-column stripes per workgroup (they share every activation load).
 template <int EPI, int MT, int NS>
 __global__ __launch_bounds__(512) void k_gemm(GemmArgs ga, EpiArgs ea) {
-    static_assert(EPI != EPI_QKV || NS == 1, "the q/k/v epilogue stages one stripe");
     extern __shared__ __align__(16) float smem[];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int KW = ga.KW;
@@ -264,12 +269,13 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs ga, EpiArgs ea) {
     constexpr int RP = MT <= 2 ? MT * 2 : 1;  // MT <= 2: >= mcap * 16 / nthr, as nthr >= 256
     float2 pf_rope[RP];
     int pf_pid = -1, pf_tok = 0;
-    int q_part = 0, q_gi = 0;
+    int q_part = 0, q_gi = 0, q_part_last = 0;
     if constexpr (EPI == EPI_QKV) {
         const int gph = ea.hd >> 5, hg = ea.H * gph;
         q_part = nt / hg;
         q_gi = (nt - q_part * hg) % gph;
-        if (MT <= 2 && q_part < 2) {
+        q_part_last = min(nt + NS - 1, stripes - 1) / hg;
+        if (MT <= 2 && NS == 1 && q_part < 2) {
 #pragma unroll
             for (int r = 0; r < RP; ++r) {
                 const int idx = tid + r * nthr;
@@ -277,7 +283,7 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs ga, EpiArgs ea) {
                     pf_rope[r] = ea.rope[(size_t)(idx >> 4) * (ea.hd >> 1) + q_gi * 16 + (idx & 15)];
             }
         }
-        if (q_part > 0 && tid < mcap) {
+        if (q_part_last > 0 && tid < mcap) {  // a K or V stripe
             pf_pid = ea.kvpid[tid];
             pf_tok = ea.pos[tid] % kPage;
         }
@@ -298,19 +304,26 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs ga, EpiArgs ea) {
     const int fld = MT * 32 + 1;
     QkvStage qs{};
     if constexpr (EPI == EPI_QKV) {
-        float2* s_rope = reinterpret_cast<float2*>(fin + NS * 32 * fld);  // [MT*32][16]; 32 * fld is even
-        int* s_pid = reinterpret_cast<int*>(s_rope + MT * 32 * 16);
+        // per stripe a [MT*32][16] RoPE table; 32 * fld is even
+        float2* s_rope = reinterpret_cast<float2*>(fin + NS * 32 * fld);
+        int* s_pid = reinterpret_cast<int*>(s_rope + NS * MT * 32 * 16);
         int* s_tok = s_pid + MT * 32;
-        if (q_part < 2) {
-            if (MT <= 2) {
+        if (MT <= 2 && NS == 1) {
+            if (q_part < 2) {
 #pragma unroll
                 for (int r = 0; r < RP; ++r) {
                     const int idx = tid + r * nthr;
                     if (idx < mcap * 16) s_rope[idx] = pf_rope[r];
                 }
-            } else {
+            }
+        } else {
+            const int gph = ea.hd >> 5, hg = ea.H * gph;
+            for (int ns = 0; ns < NS; ++ns) {
+                const int g = min(nt + ns, stripes - 1);
+                if (g / hg >= 2) continue;  // V: no rotation
+                const int gi = (g % hg) % gph;
                 for (int idx = tid; idx < mcap * 16; idx += nthr)
-                    s_rope[idx] = ea.rope[(size_t)(idx >> 4) * (ea.hd >> 1) + q_gi * 16 + (idx & 15)];
+                    s_rope[ns * MT * 32 * 16 + idx] = ea.rope[(size_t)(idx >> 4) * (ea.hd >> 1) + gi * 16 + (idx & 15)];
             }
         }
         if (tid < mcap) {
@@ -674,13 +687,14 @@ GemmShape gemm_shape(int N, int K, int epi, int M) {
     // Two stripes per workgroup share every activation load.  Wide projections
     // without a K split (gate/up, LM head) take them at up to 128 rows (a
     // 256-row pass holds one stripe); split-K projections over long K ranges
-    // take them at 65-128 rows, where each weight byte brings 4 activation
-    // bytes from L2 and that stream bounds the kernel (Huginn-shaped O and
-    // down: 36 -> 28 and 99 -> 69 us), but not below (shorter K ranges lose
-    // more workgroups than they save).
+    // (and q/k/v, whose epilogue handles a pair) take them at 65-128 rows, where
+    // each weight byte brings 4 activation bytes from L2 and that stream bounds
+    // the kernel: with at least 160 k steps per workgroup (Huginn-shaped O,
+    // down and q/k/v: 36 -> 28, 99 -> 69 and 75 -> 54 us), not with 128 or fewer
+    // (Ouro-shaped q/k/v: 15 -> 22 us), nor below 65 rows.
     const bool pair_wide = epi != EPI_QKV && epi != EPI_PARTIAL && S == 1 && stripes > 256 && stripes % 2 == 0 &&
                            KS >= 64;
-    const bool pair_long = epi == EPI_PARTIAL && KS / S >= 128;
+    const bool pair_long = (epi == EPI_PARTIAL || epi == EPI_QKV) && KS / S >= 160;
     const int NS = (pair_wide && MT < 8) || (pair_long && MT == 4) ? 2 : 1;
     // waves per workgroup: 8 (more weight bytes in flight per CU) while the
     // grid fits the chip in one round, counted with the stripe pairs where
@@ -700,7 +714,7 @@ static hipError_t launch_mt(const GemmArgs& ga, const EpiArgs& ea, hipStream_t s
         attr_set = true;
     }
     size_t lds = ((size_t)ga.KW * 1024 + (size_t)NS * 32 * (MT * 32 + 1)) * 4;
-    if (EPI == EPI_QKV) lds += (size_t)MT * 32 * 16 * 8 + (size_t)MT * 32 * 2 * 4;
+    if (EPI == EPI_QKV) lds += (size_t)NS * MT * 32 * 16 * 8 + (size_t)MT * 32 * 2 * 4;
     dim3 grid((ga.N / 32 + NS - 1) / NS, ga.S);
     k_gemm<EPI, MT, NS><<<grid, ga.KW * 64, lds, st>>>(ga, ea);
     return hipGetLastError();
@@ -716,11 +730,7 @@ static hipError_t launch_ns(const GemmArgs& ga, const EpiArgs& ea, hipStream_t s
 
 template <int EPI>
 static hipError_t launch_epi(const GemmArgs& ga, const EpiArgs& ea, int ns, hipStream_t st) {
-    if constexpr (EPI == EPI_QKV) {
-        return launch_ns<EPI, 1>(ga, ea, st);
-    } else {
-        return ns == 2 ? launch_ns<EPI, 2>(ga, ea, st) : launch_ns<EPI, 1>(ga, ea, st);
-    }
+    return ns == 2 ? launch_ns<EPI, 2>(ga, ea, st) : launch_ns<EPI, 1>(ga, ea, st);
 }
 
 template <int EPI, bool LDS, int WM>
@@ -765,7 +775,7 @@ hipError_t launch_gemm(int epi, const uint16_t* X, const uint16_t* Wp, int M, Ge
         }
     }
     if (g.KW < 1 || g.KW > kMaxKw || (g.NS != 1 && g.NS != 2)) return hipErrorInvalidValue;
-    if (epi == EPI_QKV && (g.KW < 4 || g.NS != 1)) return hipErrorInvalidValue;  // epilogue staging: >= 256 threads
+    if (epi == EPI_QKV && g.KW < 4) return hipErrorInvalidValue;  // epilogue staging: >= 256 threads
     switch (epi) {
         case EPI_QKV: return launch_epi<EPI_QKV>(ga, ea, g.NS, st);
         case EPI_SWIGLU: return launch_epi<EPI_SWIGLU>(ga, ea, g.NS, st);
