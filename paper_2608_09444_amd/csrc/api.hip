@@ -177,7 +177,8 @@ static cdb_status run_layers(const Ctx& c, int first, int count, KvTarget kv, co
     const cdb_model_desc& d = *c.md;
     const int M = r.n_rows;
     int pending = 0;  // split-K partials of the previous down projection not yet added to h
-    if (count > 0 && !chunk) HIPCHK(launch_row_order(r.pos, M, c.order, st));
+    // the attention's row order (c.order) was written by the call's row-entry
+    // kernel (gather, embed or state load); prefill chunks need none
     for (int l = 0; l < count; ++l) {
         const size_t lb = (size_t)(first + l) * c.wl.layer_stride;
         kv.layer = l;
@@ -329,7 +330,8 @@ cdb_status cdb_boundary_prelude(const cdb_model* model, const cdb_kv* kv, const 
     if (rows->n_rows == 0) return CDB_OK;
     Ctx c = make_ctx(model, ws, rows->n_rows);
     const KvTarget t = stage_target(d, *kv, 0);
-    HIPCHK(launch_embed(d, wptr(c, c.wl.embed), tokens, *rows, *kv, t, state->n_slots, c.h, c.rope, c.kvpid, c.err,
+    HIPCHK(launch_embed(d, wptr(c, c.wl.embed), tokens, *rows, *kv, t, state->n_slots, c.h, c.rope, c.kvpid, c.order,
+                        c.err,
                         st));
     s = run_layers(c, 0, d.n_prelude, t, *rows, false, st);
     if (s != CDB_OK) return s;
@@ -355,7 +357,8 @@ static cdb_status loop_step(const cdb_model* model, const cdb_kv* kv, const cdb_
     if (M > 0) {
         KvTarget t = stage_target(d, *kv, 1);
         t.c_row = r.c;
-        HIPCHK(launch_gather(d, *state, r, *kv, t, c.h, c.h_in, d.injection ? c.x : nullptr, c.rope, c.kvpid, c.err,
+        HIPCHK(launch_gather(d, *state, r, *kv, t, c.h, c.h_in, d.injection ? c.x : nullptr, c.rope, c.kvpid, c.order,
+                             c.err,
                              st));
         if (d.injection) {
             EpiArgs ea{};
@@ -368,8 +371,8 @@ static cdb_status loop_step(const cdb_model* model, const cdb_kv* kv, const cdb_
         if (s != CDB_OK) return s;
         HIPCHK(launch_exit(d, r, c.h, c.h_in, wptr(c, c.wl.w_exit), state->h, state->n_slots, *out, gate, c.deff, st));
     }
-    HIPCHK(launch_compact(M, out->exit_mask, out->cont, out->exited, out->counts, st));
-    if (M > 0) HIPCHK(launch_copy_on_exit(d, *kv, r, c.deff, out->exited, out->counts, c.err, st));
+    // copy-on-exit, with the stable compaction in its first workgroup
+    HIPCHK(launch_copy_on_exit(d, *kv, r, c.deff, out->exit_mask, out->cont, out->exited, out->counts, c.err, st));
     return CDB_OK;
 }
 
@@ -396,6 +399,7 @@ cdb_status cdb_boundary_coda(const cdb_model* model, const cdb_kv* kv, const cdb
     Ctx c = make_ctx(model, ws, M);
     const KvTarget t = stage_target(d, *kv, 2);
     HIPCHK(launch_load_state(d, M, rows->slot, rows->seq, rows->pos, t, state->h, state->n_slots, c.h, c.rope, c.kvpid,
+                             c.order,
                              c.err, st));
     s = run_layers(c, d.n_prelude + d.n_core, d.n_coda, t, *rows, true, st);
     if (s != CDB_OK) return s;
@@ -440,7 +444,7 @@ cdb_status cdb_prefill(const cdb_model* model, const cdb_kv* kv, int32_t seq, in
     HIPCHK(launch_prefill_rows(seq, pos0, M, c.prow, st));
     // prelude (plane 0): embedding, RoPE table, write pages
     KvTarget t = stage_target(d, *kv, 0);
-    HIPCHK(launch_embed(d, wptr(c, c.wl.embed), tokens, r, *kv, t, M, c.h, c.rope, c.kvpid, c.err, st));
+    HIPCHK(launch_embed(d, wptr(c, c.wl.embed), tokens, r, *kv, t, M, c.h, c.rope, c.kvpid, nullptr, c.err, st));
     cdb_status s = run_layers(c, 0, d.n_prelude, t, r, false, st, &chunk);
     if (s != CDB_OK) return s;
     if (d.injection) HIPCHK(hipMemcpyAsync(c.h_in, c.h, (size_t)M * d.d * 4, hipMemcpyDeviceToDevice, st));  // e

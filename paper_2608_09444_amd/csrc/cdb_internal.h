@@ -130,25 +130,29 @@ hipError_t launch_resid_norm(float* h, const float* part, int S, int M, int d, f
 // table rope[M][hd/2] = (cos, sin) of pos * base^(-2j/hd), angles in fp64,
 // and kvpid[M], the page of the stage's pool that receives each row's K/V
 // (the page table looked up once per call; -1 and a device error if unmapped).
+// the row-entry kernels (gather, embed, state load) also write the attention's
+// row order when `order` is non-null (at most kMaxRows rows)
 hipError_t launch_gather(const cdb_model_desc& md, const cdb_state& s, const cdb_rows& r, const cdb_kv& kv,
                          const KvTarget& kt, float* h, float* h_in, uint16_t* xcat, float2* rope, int32_t* kvpid,
-                         int* err, hipStream_t st);
+                         int32_t* order, int* err, hipStream_t st);
 hipError_t launch_embed(const cdb_model_desc& md, const uint16_t* embed, const int32_t* tokens, const cdb_rows& r,
                         const cdb_kv& kv, const KvTarget& kt, int n_slots, float* h, float2* rope, int32_t* kvpid,
-                        int* err, hipStream_t st);
+                        int32_t* order, int* err, hipStream_t st);
 hipError_t launch_store_state(int M, int d, int n_slots, const int32_t* slot, const float* h, float* state_h,
                               float* state_e, hipStream_t st);
 hipError_t launch_load_state(const cdb_model_desc& md, int M, const int32_t* slot, const int32_t* seq,
                              const int32_t* pos, const KvTarget& kt, const float* state_h, int n_slots, float* h,
-                             float2* rope, int32_t* kvpid, int* err, hipStream_t st);
+                             float2* rope, int32_t* kvpid, int32_t* order, int* err, hipStream_t st);
 // gate: NULL replays rows.depth; deff[M] receives each exiting row's depth.
 hipError_t launch_exit(const cdb_model_desc& md, const cdb_rows& r, const float* h, const float* h_in,
                        const uint16_t* w_exit, float* state_h, int n_slots, const cdb_step_out& o,
                        const cdb_gate* gate, int32_t* deff, hipStream_t st);
 hipError_t launch_compact(int M, const uint8_t* mask, int32_t* cont, int32_t* exited, int32_t* counts,
                           hipStream_t st);
+// copy-on-exit for the rows with deff > 0, and the step's stable compaction
 hipError_t launch_copy_on_exit(const cdb_model_desc& md, const cdb_kv& kv, const cdb_rows& r, const int32_t* deff,
-                               const int32_t* exited, const int32_t* counts, int* err, hipStream_t st);
+                               const uint8_t* mask, int32_t* cont, int32_t* exited, int32_t* counts, int* err,
+                               hipStream_t st);
 hipError_t launch_argmax(int M, int V, const float* logits, int32_t* ids, hipStream_t st);
 // prefill: row arrays slot = i, seq, pos = pos0 + i in rows[0..3M); per-row
 // write pages of a fixed plane; adapter input [h; e] in fragment layout

@@ -30,6 +30,26 @@ __device__ __forceinline__ void rope_row(int pos, int hd, float base, float2* ou
     }
 }
 
+// ------------------------------------------------------------------ row order
+// order[rank] = row, ranked by descending position (ties by row index), for
+// the paged attention's row pairing.  Run by every thread of one workgroup;
+// M <= kMaxRows.  The stage calls run it in the first workgroup of their
+// row-entry kernel instead of a launch of its own.
+__device__ __forceinline__ void row_order_block(const int32_t* __restrict__ pos, int M, int32_t* __restrict__ order) {
+    __shared__ int s_pos[kMaxRows];
+    for (int i = threadIdx.x; i < M; i += blockDim.x) s_pos[i] = pos[i];
+    __syncthreads();
+    for (int i = threadIdx.x; i < M; i += blockDim.x) {
+        const int pi = s_pos[i];
+        int rank = 0;
+        for (int j = 0; j < M; ++j) {
+            const int pj = s_pos[j];
+            rank += (pj > pi) || (pj == pi && j < i);
+        }
+        order[rank] = i;
+    }
+}
+
 // ------------------------------------------------------------------ gather
 // h[i] = state.h[slot[i]]; h_in[i] = h[i] (exit score of the L2 criterion);
 // xcat[i] = bf16([h; e]) for the input-injection adapter.  Validates the row.
@@ -58,8 +78,9 @@ __global__ __launch_bounds__(256) void k_gather(int d, int r_max, int n_slots, i
                                                 const float* __restrict__ sh, const float* __restrict__ se,
                                                 float* __restrict__ h, float* __restrict__ h_in,
                                                 uint16_t* __restrict__ xcat, float2* __restrict__ rope, KvTarget kt,
-                                                int32_t* __restrict__ kvpid, int* err) {
+                                                int32_t* __restrict__ kvpid, int32_t* __restrict__ order, int* err) {
     const int i = blockIdx.x;
+    if (order && i == 0 && gridDim.x <= kMaxRows) row_order_block(pos, gridDim.x, order);
     const int sl = slot[i];
     rope_row(pos[i], hd, base, rope + (size_t)i * (hd / 2));
     if (threadIdx.x == 0) {
@@ -92,8 +113,10 @@ __global__ __launch_bounds__(256) void k_load_state(int d, int n_slots, int hd, 
                                                     const int32_t* __restrict__ slot, const int32_t* __restrict__ seq,
                                                     const int32_t* __restrict__ pos, KvTarget kt,
                                                     const float* __restrict__ sh, float* __restrict__ h,
-                                                    float2* __restrict__ rope, int32_t* __restrict__ kvpid, int* err) {
+                                                    float2* __restrict__ rope, int32_t* __restrict__ kvpid,
+                                                    int32_t* __restrict__ order, int* err) {
     const int i = blockIdx.x;
+    if (order && i == 0 && gridDim.x <= kMaxRows) row_order_block(pos, gridDim.x, order);
     const int sl = slot[i];
     rope_row(pos[i], hd, base, rope + (size_t)i * (hd / 2));
     const bool ok = sl >= 0 && sl < n_slots;
@@ -161,8 +184,9 @@ __global__ __launch_bounds__(256) void k_embed(int d, int vocab, int n_slots, in
                                                const int32_t* __restrict__ tok, const int32_t* __restrict__ slot,
                                                const int32_t* __restrict__ seq, const int32_t* __restrict__ pos,
                                                float* __restrict__ h, float2* __restrict__ rope, KvTarget kt,
-                                               int32_t* __restrict__ kvpid, int* err) {
+                                               int32_t* __restrict__ kvpid, int32_t* __restrict__ order, int* err) {
     const int i = blockIdx.x;
+    if (order && i == 0 && gridDim.x <= kMaxRows) row_order_block(pos, gridDim.x, order);
     rope_row(pos[i], hd, base, rope + (size_t)i * (hd / 2));
     const int t = tok[i];
     const bool ok = t >= 0 && t < vocab;
@@ -268,8 +292,11 @@ __global__ __launch_bounds__(256) void k_exit(int d, float eps, int exit_kind, i
         for (int k = threadIdx.x * 4; k < d; k += 1024)
             *reinterpret_cast<float4*>(sh + (size_t)sl * d + k) = *reinterpret_cast<const float4*>(x + k);
 }
-__global__ __launch_bounds__(256) void k_compact(int M, const uint8_t* __restrict__ mask, int32_t* __restrict__ cont,
-                                                 int32_t* __restrict__ exited, int32_t* __restrict__ counts) {
+// Stable compaction of one step's rows: cont / exited list the continuing and
+// exiting rows in batch order, counts = {continuing, exiting}.  Run by every
+// thread of one 256-thread workgroup.
+__device__ __forceinline__ void compact_block(int M, const uint8_t* __restrict__ mask, int32_t* __restrict__ cont,
+                                              int32_t* __restrict__ exited, int32_t* __restrict__ counts) {
     __shared__ int s_scan[256];
     __shared__ int s_base;
     if (threadIdx.x == 0) s_base = 0;
@@ -304,8 +331,15 @@ __global__ __launch_bounds__(256) void k_compact(int M, const uint8_t* __restric
     }
 }
 
+__global__ __launch_bounds__(256) void k_compact(int M, const uint8_t* __restrict__ mask, int32_t* __restrict__ cont,
+                                                 int32_t* __restrict__ exited, int32_t* __restrict__ counts) {
+    compact_block(M, mask, cont, exited, counts);
+}
+
 // Last-exited cache: for each exiting row (depth < r_max), copy its K/V at pos
-// from plane depth to planes depth+1..r_max, for the core layer blockIdx.y.
+// from plane depth to planes depth+1..r_max, for the core layer blockIdx.y;
+// depth is the row's exit depth, 0 for a continuing row.  Workgroup (0, 0)
+// also runs the step's stable compaction (the copy needs none of its output).
 // The destination page ids are read into LDS first and each chunk of the
 // source entry (up to 8 16-byte vectors per thread) is loaded once, before
 // any store: source and destinations share the pool, so a load left after a
@@ -313,12 +347,12 @@ __global__ __launch_bounds__(256) void k_compact(int M, const uint8_t* __restric
 __global__ __launch_bounds__(256) void k_copy_on_exit(int H, int hd, int r_max, KvTarget kv,
                                                       const int32_t* __restrict__ seq, const int32_t* __restrict__ pos,
                                                       const int32_t* __restrict__ depth,
-                                                      const int32_t* __restrict__ exited,
-                                                      const int32_t* __restrict__ counts, int* err) {
+                                                      const uint8_t* __restrict__ mask, int32_t* __restrict__ cont,
+                                                      int32_t* __restrict__ exited, int32_t* __restrict__ counts,
+                                                      int* err) {
     __shared__ int s_dst[64];  // destination page of plane dep + 1 + k, -1 if unmapped (r_max <= 64)
-    const int j = blockIdx.x;
-    if (j >= counts[1]) return;
-    const int i = exited[j];
+    if (blockIdx.x == 0 && blockIdx.y == 0) compact_block(gridDim.x, mask, cont, exited, counts);
+    const int i = blockIdx.x;
     const int dep = depth[i];
     if (dep >= r_max || dep < 1) return;
     const int sq = seq[i], ps = pos[i], pg = ps / kPage;
@@ -456,20 +490,22 @@ static int page_cap(const cdb_kv& kv) { return kv.max_pages * kPage; }
 
 hipError_t launch_gather(const cdb_model_desc& md, const cdb_state& s, const cdb_rows& r, const cdb_kv& kv,
                          const KvTarget& kt, float* h, float* h_in, uint16_t* xcat, float2* rope, int32_t* kvpid,
-                         int* err, hipStream_t st) {
+                         int32_t* order, int* err, hipStream_t st) {
     if (r.n_rows <= 0) return hipSuccess;
+    if (order && r.n_rows > kMaxRows) return hipErrorInvalidValue;
     k_gather<<<r.n_rows, 256, 0, st>>>(md.d, md.r_max, s.n_slots, kv.max_seqs, page_cap(kv), md.head_dim, md.rope_base,
                                         r.slot, r.seq, r.pos, r.c, r.depth, s.h, s.e, h, h_in, xcat, rope, kt, kvpid,
-                                        err);
+                                        order, err);
     return hipGetLastError();
 }
 
 hipError_t launch_load_state(const cdb_model_desc& md, int M, const int32_t* slot, const int32_t* seq,
                              const int32_t* pos, const KvTarget& kt, const float* state_h, int n_slots, float* h,
-                             float2* rope, int32_t* kvpid, int* err, hipStream_t st) {
+                             float2* rope, int32_t* kvpid, int32_t* order, int* err, hipStream_t st) {
     if (M <= 0) return hipSuccess;
+    if (order && M > kMaxRows) return hipErrorInvalidValue;
     k_load_state<<<M, 256, 0, st>>>(md.d, n_slots, md.head_dim, md.rope_base, slot, seq, pos, kt, state_h, h, rope,
-                                    kvpid, err);
+                                    kvpid, order, err);
     return hipGetLastError();
 }
 
@@ -492,10 +528,11 @@ hipError_t launch_resid_norm(float* h, const float* part, int S, int M, int d, f
 
 hipError_t launch_embed(const cdb_model_desc& md, const uint16_t* embed, const int32_t* tokens, const cdb_rows& r,
                         const cdb_kv& kv, const KvTarget& kt, int n_slots, float* h, float2* rope, int32_t* kvpid,
-                        int* err, hipStream_t st) {
+                        int32_t* order, int* err, hipStream_t st) {
     if (r.n_rows <= 0) return hipSuccess;
+    if (order && r.n_rows > kMaxRows) return hipErrorInvalidValue;
     k_embed<<<r.n_rows, 256, 0, st>>>(md.d, md.vocab, n_slots, kv.max_seqs, page_cap(kv), md.head_dim, md.rope_base,
-                                       embed, tokens, r.slot, r.seq, r.pos, h, rope, kt, kvpid, err);
+                                       embed, tokens, r.slot, r.seq, r.pos, h, rope, kt, kvpid, order, err);
     return hipGetLastError();
 }
 
@@ -524,8 +561,9 @@ hipError_t launch_compact(int M, const uint8_t* mask, int32_t* cont, int32_t* ex
 }
 
 hipError_t launch_copy_on_exit(const cdb_model_desc& md, const cdb_kv& kv, const cdb_rows& r, const int32_t* deff,
-                               const int32_t* exited, const int32_t* counts, int* err, hipStream_t st) {
-    if (r.n_rows <= 0 || md.n_core <= 0) return hipSuccess;
+                               const uint8_t* mask, int32_t* cont, int32_t* exited, int32_t* counts, int* err,
+                               hipStream_t st) {
+    if (r.n_rows <= 0 || md.n_core <= 0) return launch_compact(r.n_rows > 0 ? r.n_rows : 0, mask, cont, exited, counts, st);
     KvTarget t{};
     t.pool = static_cast<uint16_t*>(kv.core_pool);
     t.n_pages = kv.core_pages;
@@ -535,8 +573,8 @@ hipError_t launch_copy_on_exit(const cdb_model_desc& md, const cdb_kv& kv, const
     t.max_pages = kv.max_pages;
     t.n_planes = md.r_max + 2;
     dim3 grid(r.n_rows, md.n_core);
-    k_copy_on_exit<<<grid, 256, 0, st>>>(md.n_heads, md.head_dim, md.r_max, t, r.seq, r.pos, deff, exited, counts,
-                                         err);
+    k_copy_on_exit<<<grid, 256, 0, st>>>(md.n_heads, md.head_dim, md.r_max, t, r.seq, r.pos, deff, mask, cont, exited,
+                                         counts, err);
     return hipGetLastError();
 }
 
