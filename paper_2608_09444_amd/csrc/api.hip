@@ -48,8 +48,10 @@ bool weight_layout(const cdb_model_desc& d, WeightLayout* w) {
 }
 
 // The four per-layer GEMMs and the adapter / LM head, with their split counts.
+// The loop step's adapter writes split-K partials that the first core layer's
+// residual + norm sums (adapter_part); the prefill's writes its result (adapter).
 struct ModelGemms {
-    GemmShape qkv, o, gu, down, adapter, lm;
+    GemmShape qkv, o, gu, down, adapter, adapter_part, lm;
 };
 // Launch shapes of the model's projections for calls of M rows: the skinny
 // weight-streaming kernel up to kMaxRows rows, the tile kernel above.
@@ -61,6 +63,7 @@ static ModelGemms model_gemms(const cdb_model_desc& d, int M = 0) {
         g.gu = gemm_shape_mn(2 * d.d_ff, d.d, M, EPI_SWIGLU);
         g.down = gemm_shape_mn(d.d, d.d_ff, M, EPI_PARTIAL);
         g.adapter = gemm_shape_mn(d.d, 2 * d.d, M, EPI_STORE);
+        g.adapter_part = g.adapter;  // the loop step never has more than kMaxRows rows
         g.lm = gemm_shape_mn(d.vocab, d.d, M, EPI_STORE);
         return g;
     }
@@ -69,6 +72,7 @@ static ModelGemms model_gemms(const cdb_model_desc& d, int M = 0) {
     g.gu = gemm_shape(2 * d.d_ff, d.d, EPI_SWIGLU, M);
     g.down = gemm_shape(d.d, d.d_ff, EPI_PARTIAL, M);
     g.adapter = gemm_shape(d.d, 2 * d.d, EPI_STORE, M);
+    g.adapter_part = gemm_shape(d.d, 2 * d.d, EPI_PARTIAL, M);
     g.lm = gemm_shape(d.vocab, d.d, EPI_STORE, M);
     return g;
 }
@@ -77,7 +81,8 @@ WsLayout ws_layout(const cdb_model_desc& d, int rows) {
     WsLayout L;
     const size_t D = d.d, F = d.d_ff, M = rows, M32 = gemm_rows(rows);
     const ModelGemms g = model_gemms(d, rows);
-    const size_t part = (size_t)(g.o.S > g.down.S ? g.o.S : g.down.S) * D;  // split-K partials of O / down
+    // split-K partials of O, down and the loop step's adapter
+    const size_t part = (size_t)std::max({g.o.S, g.down.S, d.injection ? g.adapter_part.S : 0}) * D;
     size_t off = 0;
     L.err = off;
     off = 256;
@@ -173,10 +178,12 @@ struct Chunk {
 // ctx.x its RMSNorm when `norm_out` is set.  With `chunk` the rows are a
 // prefill chunk and attention runs query-tiled on MFMA.
 static cdb_status run_layers(const Ctx& c, int first, int count, KvTarget kv, const cdb_rows& r, bool norm_out,
-                             hipStream_t st, const Chunk* chunk = nullptr) {
+                             hipStream_t st, const Chunk* chunk = nullptr, int pending_in = 0) {
     const cdb_model_desc& d = *c.md;
     const int M = r.n_rows;
-    int pending = 0;  // split-K partials of the previous down projection not yet added to h
+    // split-K partials not yet added to h: the previous down projection's, or at
+    // the start those of the loop step's adapter (h then holds zeros)
+    int pending = pending_in;
     // the attention's row order (c.order) was written by the call's row-entry
     // kernel (gather, embed or state load); prefill chunks need none
     for (int l = 0; l < count; ++l) {
@@ -360,14 +367,14 @@ static cdb_status loop_step(const cdb_model* model, const cdb_kv* kv, const cdb_
         HIPCHK(launch_gather(d, *state, r, *kv, t, c.h, c.h_in, d.injection ? c.x : nullptr, c.rope, c.kvpid, c.order,
                              c.err,
                              st));
+        // injection models: the gather zeroed h; the adapter's split-K
+        // partials become the first layer's input in its residual + norm
         if (d.injection) {
             EpiArgs ea{};
-            ea.out = c.h;
-            ea.ld_out = d.d;
             ea.err = c.err;
-            HIPCHK(launch_gemm(EPI_STORE, c.x, wptr(c, c.wl.adapter), M, c.gm.adapter, c.part, ea, st));
+            HIPCHK(launch_gemm(EPI_PARTIAL, c.x, wptr(c, c.wl.adapter), M, c.gm.adapter_part, c.part, ea, st));
         }
-        s = run_layers(c, d.n_prelude, d.n_core, t, r, false, st);
+        s = run_layers(c, d.n_prelude, d.n_core, t, r, false, st, nullptr, d.injection ? c.gm.adapter_part.S : 0);
         if (s != CDB_OK) return s;
         HIPCHK(launch_exit(d, r, c.h, c.h_in, wptr(c, c.wl.w_exit), state->h, state->n_slots, *out, gate, c.deff, st));
     }

@@ -51,8 +51,9 @@ __device__ __forceinline__ void row_order_block(const int32_t* __restrict__ pos,
 }
 
 // ------------------------------------------------------------------ gather
-// h[i] = state.h[slot[i]]; h_in[i] = h[i] (exit score of the L2 criterion);
-// xcat[i] = bf16([h; e]) for the input-injection adapter.  Validates the row.
+// h[i] = state.h[slot[i]] (zeros with the adapter); h_in[i] = state.h[slot[i]]
+// (exit score of the L2 criterion); xcat[i] = bf16([h; e]) for the
+// input-injection adapter.  Validates the row.
 // kvpid[i]: the page of the stage pool that receives row i's K/V (plane c+1 of
 // the core, or the stage's fixed plane); -1 when the stage has no layers.
 __device__ __forceinline__ void write_page(const KvTarget& kt, int i, int sq, int ps, const int32_t* c_row,
@@ -93,7 +94,8 @@ __global__ __launch_bounds__(256) void k_gather(int d, int r_max, int n_slots, i
     const bool ok = sl >= 0 && sl < n_slots;
     for (int k = threadIdx.x * 4; k < d; k += 256 * 4) {
         float4 v = ok ? *reinterpret_cast<const float4*>(sh + (size_t)sl * d + k) : make_float4(0.f, 0.f, 0.f, 0.f);
-        *reinterpret_cast<float4*>(h + (size_t)i * d + k) = v;
+        // with the adapter, h starts at zero: the adapter's split-K partials are added to it
+        *reinterpret_cast<float4*>(h + (size_t)i * d + k) = xcat ? make_float4(0.f, 0.f, 0.f, 0.f) : v;
         *reinterpret_cast<float4*>(h_in + (size_t)i * d + k) = v;
         if (xcat) {  // adapter input [h; e], fragment layout with K = 2d
             float4 e = ok ? *reinterpret_cast<const float4*>(se + (size_t)sl * d + k) : make_float4(0.f, 0.f, 0.f, 0.f);
