@@ -488,7 +488,6 @@ __device__ __forceinline__ void qkv_block_epilogue(const QkvBlockInputs& in, con
 template <int EPI, bool LDS, int WM>
 __global__ __launch_bounds__(256) void k_gemm_mn(GemmArgs ga, EpiArgs ea) {
     static_assert(WM == 1 || WM == 2, "one or two m-tiles per wave");
-    static_assert(!LDS || WM == 2, "the LDS ring stages 4 m-tiles per k step");
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int KS = ga.K >> 4;
     const int stripes = ga.N >> 5;
@@ -553,14 +552,17 @@ __global__ __launch_bounds__(256) void k_gemm_mn(GemmArgs ga, EpiArgs ea) {
         }
     } else {
         // LDS ring of 2 stages of 4 k steps: a stage holds the workgroup's 4
-        // weight tiles and 4 activation tiles of each k step (1 KiB each, lane
-        // order), copied global -> LDS by the waves with direct loads (tile i of a
-        // stage by wave i % 4); each wave then reads its 2 + 2 operands per k step
+        // weight tiles and 2 WM activation tiles of each k step (1 KiB each,
+        // lane order), copied global -> LDS by the waves with direct loads (tile
+        // i of a stage by wave i % 4); each wave then reads its 2 + WM operands
+        // per k step
         constexpr int CH = 4, NBUF = 2;
-        constexpr int TPS = CH * 8;   // tiles per stage
-        constexpr int LPW = TPS / 4;  // loads per wave per stage
+        constexpr int TPK = 4 + 2 * WM;  // tiles per k step
+        constexpr int TPS = CH * TPK;    // tiles per stage
+        constexpr int LPW = TPS / 4;     // loads per wave per stage
+        static_assert(TPS % 4 == 0, "a stage's tiles split evenly over the 4 waves");
         extern __shared__ __align__(16) unsigned char lds_ring[];
-        const int ntb = blockIdx.x * 4, mtb = blockIdx.y * 4;
+        const int ntb = blockIdx.x * 4, mtb = blockIdx.y * 2 * WM;
         const u32x4* Wg = reinterpret_cast<const u32x4*>(ga.Wp);
         const u32x4* Xg = reinterpret_cast<const u32x4*>(ga.X);
         const int nst = (k1 - k0 + CH - 1) / CH;
@@ -569,7 +571,7 @@ __global__ __launch_bounds__(256) void k_gemm_mn(GemmArgs ga, EpiArgs ea) {
 #pragma unroll
             for (int i = 0; i < LPW; ++i) {
                 const int t = wave + 4 * i;  // tile within the stage
-                const int kk = t >> 3, slot = t & 7;
+                const int kk = t / TPK, slot = t - kk * TPK;
                 const int ks = min(k0 + st * CH + kk, k1 - 1);
                 const u32x4* src = slot < 4 ? Wg + ((size_t)min(ntb + slot, stripes - 1) * KS + ks) * 64
                                             : Xg + ((size_t)min(mtb + slot - 4, mtiles - 1) * KS + ks) * 64;
@@ -589,17 +591,18 @@ __global__ __launch_bounds__(256) void k_gemm_mn(GemmArgs ga, EpiArgs ea) {
 #pragma unroll
             for (int i = 0; i < CH; ++i) {
                 const uint32_t keep = k0 + st * CH + i < k1 ? 0xffffffffu : 0u;
-                u32x4 w[2], x[2];
+                u32x4 w[2], x[WM];
 #pragma unroll
-                for (int a = 0; a < 2; ++a) {
-                    w[a] = *reinterpret_cast<const u32x4*>(base + (i * 8 + wn * 2 + a) * 1024);
-                    x[a] = *reinterpret_cast<const u32x4*>(base + (i * 8 + 4 + wm * 2 + a) * 1024);
-                }
+                for (int a = 0; a < 2; ++a)
+                    w[a] = *reinterpret_cast<const u32x4*>(base + (i * TPK + wn * 2 + a) * 1024);
+#pragma unroll
+                for (int b = 0; b < WM; ++b)
+                    x[b] = *reinterpret_cast<const u32x4*>(base + (i * TPK + 4 + wm * WM + b) * 1024);
 #pragma unroll
                 for (int a = 0; a < 2; ++a) {
                     const bf16x8 wv = __builtin_bit_cast(bf16x8, w[a] & keep);
 #pragma unroll
-                    for (int b = 0; b < 2; ++b)
+                    for (int b = 0; b < WM; ++b)
                         acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wv, __builtin_bit_cast(bf16x8, x[b]),
                                                                             acc[a][b], 0, 0, 0);
                 }
@@ -645,14 +648,17 @@ __global__ __launch_bounds__(256) void k_gemm_mn(GemmArgs ga, EpiArgs ea) {
 // rows); q/k/v, O and down are faster with direct loads.
 static bool mn_lds(int epi, int N) { return epi == EPI_SWIGLU || (epi == EPI_STORE && N >= 8192); }
 
-// m-tiles per wave of the tile kernel: 2 (128-row workgroup tiles), or 1
-// (64-row tiles) for q/k/v when that grid still runs in one round on the 256
-// CUs.  Its workgroups take one CU each (register bound), so at 257-320 rows of
-// the Ouro-shaped q/k/v the 64-row tiles use 240 CUs instead of 144 (29 -> 22
-// us); above that they would take two rounds.  O and down are as fast or
-// faster with 128-row tiles at every size from 272 to 512 rows but 480-512.
+// m-tiles per wave of the tile kernel: 2 (128-row workgroup tiles) or 1 (64-row
+// tiles; the sums are the same either way).  Direct loads: 1 for q/k/v when
+// that grid still runs in one round on the 256 CUs; its workgroups take one
+// CU each (register bound), so at 257-320 rows of the Ouro-shaped q/k/v the
+// 64-row tiles use 240 CUs instead of 144 (29 -> 22 us); above that they would
+// take two rounds.  O and down are as fast or faster with 128-row tiles at
+// every size from 272 to 512 rows but 480-512.  LDS-staged: 1 when the rows
+// span an odd number of 64-row tiles, which 128-row tiles would pad by 64 rows
+// (gate/up at 300 rows: 36.0 -> 30.1 us; at 512 rows 64-row tiles gain nothing).
 static int mn_wave_mtiles(int epi, int N, int M) {
-    if (mn_lds(epi, N)) return 2;
+    if (mn_lds(epi, N)) return ((M + 63) / 64) % 2 ? 1 : 2;
     return epi == EPI_QKV && ((M + 63) / 64) * ((N / 32 + 3) / 4) <= 256 ? 1 : 2;
 }
 
@@ -737,10 +743,10 @@ template <int EPI, bool LDS, int WM>
 static hipError_t launch_mn_wm(const GemmArgs& ga, const EpiArgs& ea, hipStream_t st) {
     dim3 grid((ga.N / 32 + 3) / 4, (ga.M + 64 * WM - 1) / (64 * WM), ga.S);
     // dynamic LDS: the ring of the LDS path, the q/k/v epilogue's staging blocks
-    constexpr size_t ring = LDS ? 2 * 4 * 8 * 1024 : 0;
+    constexpr size_t ring = LDS ? 2 * 4 * (4 + 2 * WM) * 1024 : 0;
     constexpr size_t stage = EPI == EPI_QKV ? 4 * 64 * (32 * WM + 1) * 4 : 0;
     constexpr size_t smem = ring > stage ? ring : stage;
-    if constexpr (smem > 48 * 1024) {
+    if constexpr (smem > 0) {
         static bool attr_set = false;
         if (!attr_set) {
             hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm_mn<EPI, LDS, WM>),
@@ -755,7 +761,9 @@ static hipError_t launch_mn_wm(const GemmArgs& ga, const EpiArgs& ea, hipStream_
 
 template <int EPI>
 static hipError_t launch_mn(const GemmArgs& ga, const EpiArgs& ea, hipStream_t st) {
-    if (mn_lds(EPI, ga.N)) return launch_mn_wm<EPI, true, 2>(ga, ea, st);
+    if (mn_lds(EPI, ga.N))
+        return mn_wave_mtiles(EPI, ga.N, ga.M) == 1 ? launch_mn_wm<EPI, true, 1>(ga, ea, st)
+                                                    : launch_mn_wm<EPI, true, 2>(ga, ea, st);
     if (mn_wave_mtiles(EPI, ga.N, ga.M) == 1) return launch_mn_wm<EPI, false, 1>(ga, ea, st);
     return launch_mn_wm<EPI, false, 2>(ga, ea, st);
 }
