@@ -820,11 +820,11 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": "ouro-1.4b-shaped looped LM, mixed-depth decode loop step: 64 rows at positions "
-                               "U[512,767] (prompt 512 + decode 256), depths categorical {1:.3,2:.3,3:.2,4:.2}",
-                   "rows": n_rows, "d": shape.d, "heads": shape.n_heads, "head_dim": shape.head_dim,
-                   "d_ff": shape.d_ff, "core_layers": shape.n_core, "r_max": shape.r_max,
-                   "mean_context": float(np.mean(rows_np["pos"] + 1)),
+        "config": {"workload": f"mixed-depth decode loop step of an ouro-1.4b-shaped looped LM (d {shape.d}, "
+                               f"{shape.n_heads} heads x {shape.head_dim}, SwiGLU {shape.d_ff}, {shape.n_core} core "
+                               f"layers looped up to {shape.r_max} times): {n_rows} rows at positions U[512,767] "
+                               f"(prompt 512 + decode 256), depths categorical {{1:.3,2:.3,3:.2,4:.2}}",
+                   "rows": n_rows, "mean_context": float(np.mean(rows_np["pos"] + 1)),
                    "exits_per_step": int((rows_np["c"] + 1 == rows_np["depth"]).sum())},
         "roofline": {"bound": "hbm", "kernel": "k_attn<128> (paged decode attention, one layer)",
                      "achieved": round(attn_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
