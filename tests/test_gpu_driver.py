@@ -319,3 +319,28 @@ def test_driver_prefill_chunks_decode_like_the_oracle():
     checked = _check_against_oracle(s, w, prompts, ndec, depths, first, runs["refill"], drv.KV_FULL)
     _say(f"[gpu]   {checked} greedy ids checked against the oracle")
     assert checked >= 0.3 * (sum(ndec) + n)
+
+
+def test_driver_decode_at_ouro_width_follows_oracle():
+    # the real projection widths (d 2048, 16 x 128 heads, SwiGLU 5632) with a
+    # 2-layer core: skinny GEMMs of every row count the schedule produces
+    s = cdbgen.shrink(cdbgen.OURO, n_core=2)
+    w = cdbgen.model_weights(cdbgen.OURO)
+    w = dict(w, layers=w["layers"][:2])
+    _say(f"[gpu] driver decode at Ouro widths, 2 core layers")
+    gm = cdb.DeviceModel(s, w)
+    plens, ndec = [12, 5, 20, 9], [6, 8, 5, 7]
+    prompts = [cdbgen.prompt_ids(s.vocab, 1, p, seed=46, stream=q)[0] for q, p in enumerate(plens)]
+    depths = [cdbgen.draw_depths(cdbgen.OURO_DEPTHS, n, s.r_max, seed=47, stream=q) for q, n in enumerate(ndec)]
+    runs = {}
+    for name, cfg in (("refill", dict(max_batch=3, max_active=4)), ("no-refill", dict(max_batch=4, max_active=4,
+                                                                                        refill=False))):
+        first, ids, st, secs = _decode_on_gpu(s, gm, prompts, ndec, depths, drv.KV_FULL, **cfg)
+        _say(f"[gpu]   {name}: {st} in {secs * 1e3:.1f} ms")
+        assert st["tokens"] == sum(ndec)
+        runs[name] = (first, ids)
+    assert np.array_equal(runs["refill"][0], runs["no-refill"][0])
+    assert np.array_equal(runs["refill"][1], runs["no-refill"][1])
+    checked = _check_against_oracle(s, w, prompts, ndec, depths, *runs["refill"], drv.KV_FULL)
+    _say(f"[gpu]   {checked} greedy ids checked against the oracle")
+    assert checked >= 0.3 * (sum(ndec) + len(plens))
