@@ -451,6 +451,63 @@ def huginn_leg(n_decode, steps=20, warmup=3):
     return res
 
 
+def long_context_step(shape, dm, steps=5, warmup=2):
+    """The loop step at config 4's full batch: 256 rows at positions
+    U[2048, 4223] (prompt U[2048, 4096] + decode 128), half of the tokens
+    exiting at loop 1 and half at loop 4, drawn size-biased over the loop work.
+    Each row maps its own pages (its loop plane over its context, plus the
+    copy-on-exit destination page of every deeper plane): ≈ 160 GB of K/V, which
+    one GPU holds although the whole depth-indexed cache of the config does not."""
+    import numpy as np
+    import torch
+
+    import cdbgen
+    import paper_2608_09444_amd as cdb
+    wl = cdbgen.WORKLOADS[4]
+    R = shape.r_max
+    n_rows = wl.max_batch
+    pos_lo, pos_hi = wl.prompt[0], wl.prompt[1] + wl.decode - 1
+    rows_np = cdbgen.decode_snapshot(n_rows, wl.depth, R, pos_lo, pos_hi, stream=40)
+    max_pages = cdbgen.pages_for(pos_hi + 1)
+    pt, n_pages = own_pages(shape, rows_np, max_pages)
+    kv = cdb.PagedKV(shape, n_rows, max_pages, 0, n_pages, 0, fill="random")
+    g = torch.Generator(device="cuda")
+    g.manual_seed(1234)
+    kv.core.normal_(0.0, 1.0, generator=g)
+    kv.page_table.copy_(torch.from_numpy(pt))
+    state = cdb.State(shape, n_rows)
+    state.h.normal_(0.0, 1.0, generator=g)
+    rows = cdb.Rows(np.arange(n_rows, dtype=np.int32), np.arange(n_rows, dtype=np.int32), rows_np["pos"],
+                    rows_np["c"], rows_np["depth"])
+    so = cdb.StepOut(n_rows)
+    ws = cdb.Workspace(dm.desc, n_rows)
+    log(f"long context loop step: {n_rows} rows, {n_pages} core pages "
+        f"({kv.core.numel() * 2 / 1e9:.0f} GB)")
+    ms = time_loop_step(dm, kv, state, rows, so, ws, steps, warmup)
+    if cdb.cdb_read_device_error(ws.buf) != 0:
+        raise RuntimeError("device error in the long-context loop step")
+    sb = step_bytes(shape, rows_np)
+    attn_ms = time_attention(shape, kv, rows, n_rows, steps * shape.n_core)
+    ab = attention_bytes(shape, rows_np["pos"])
+    log(f"long context loop step: {ms:.3f} ms, {n_rows / (ms * 1e-3):.0f} rows/s; attention {attn_ms * 1e3:.1f} us")
+    res = {"workload": f"ouro-shaped mixed-depth decode loop step: {n_rows} rows at positions U[{pos_lo},{pos_hi}] "
+                       f"(prompt U[{wl.prompt[0]},{wl.prompt[1]}] + decode {wl.decode}), depths 50% 1 / 50% 4 per token",
+           "rows": n_rows, "ms_per_step": round(ms, 4), "tokens_per_s": round(n_rows / (ms * 1e-3), 1),
+           "mean_context": float(np.mean(rows_np["pos"] + 1)),
+           "exits_per_step": int((rows_np["c"] + 1 == rows_np["depth"]).sum()),
+           "step_roofline": {"bound": "hbm", "algorithmic_bytes": sb, "achieved": round(sb / (ms * 1e-3) / 1e9, 1),
+                             "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                             "frac": round(sb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                             "flops": step_flops(shape, rows_np)},
+           "attention_roofline": {"bound": "hbm", "kernel": "k_attn<128> (paged decode attention, one layer)",
+                                  "achieved": round(ab / (attn_ms * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS,
+                                  "unit": "GB/s", "frac": round(ab / (attn_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                                  "algorithmic_bytes": ab, "us_per_launch": round(attn_ms * 1e3, 2)}}
+    del kv, state, rows, so, ws
+    torch.cuda.empty_cache()
+    return res
+
+
 def long_context_leg(shape, dm, headroom_gib=16):
     """Config 4: 256 requests with prompts uniform in [2048, 4096] (KV
     synthesized as zeros), 128 decode tokens each, half of the tokens exiting at
@@ -485,6 +542,7 @@ def long_context_leg(shape, dm, headroom_gib=16):
                        f"each, depths 50% 1 / 50% 4 per token, max batch {wl.max_batch}",
            "mean_depth": round(mean_depth, 4), "flop_bound": round(cost.flop_bound(shape, mean_depth), 4),
            "prompt_tokens": int(plen.sum())}
+    res["loop_step"] = long_context_step(shape, dm)
     for lname, layout, planes in (("full", drv.KV_FULL, R), ("shared", drv.KV_SHARED, 1)):
         need = int(sum(cdbgen.pages_for(int(p) + n_decode) for p in plen)) * planes
         core_pages = min(need, budget_pages)
