@@ -16,12 +16,14 @@
 // workgroups of a launch are resident at once, so one workgroup per row would
 // leave the chip idle while the longest rows finish.  A workgroup therefore
 // takes two rows -- the p-th longest and the p-th shortest, from the order
-// k_row_order wrote at the start of the stage call -- and deals the pages of
-// both to its 4 waves.  Each wave keeps one softmax state per row.  With pairs,
-// mixed and equal context lengths run at the same bandwidth.  The partial
-// states are merged through LDS in an order fixed by the row alone, so every
-// row's output is bit-identical whatever else shares the batch; the output is
-// written in the fragment layout the output projection reads.
+// ranked at the start of the stage call (by the first workgroup of its
+// row-entry kernel, or by k_row_order for a standalone attention call) -- and
+// deals the pages of both to its 4 waves.  Each wave keeps one softmax state
+// per row.  With pairs, mixed and equal context lengths run at the same
+// bandwidth.  The partial states are merged through LDS in an order fixed by
+// the row alone, so every row's output is bit-identical whatever else shares
+// the batch; the output is written in the fragment layout the output
+// projection reads.
 #include "cdb_internal.h"
 
 namespace cdb {

@@ -23,10 +23,10 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
 __device__ __forceinline__ float bflo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bfhi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
-// fp32 -> bf16, round to nearest even, by the gfx950 conversion instruction
-// (v_cvt_pk_bf16_f32; fp32 denormals are kept, NaN stays NaN).
 typedef float floatx2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+// fp32 -> bf16, round to nearest even, by the gfx950 conversion instruction
+// (v_cvt_pk_bf16_f32; fp32 denormals are kept, NaN stays NaN).
 __device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
 // Two values in one instruction: a in the low half, b in the high half.
 __device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
@@ -42,9 +42,9 @@ __host__ __device__ __forceinline__ size_t frag_index(int m, int k, int K) {
     return ((((size_t)(m >> 5) * (K >> 4) + (k >> 4)) * 64 + (m & 31) + 32 * ((k & 15) >> 3)) << 3) + (k & 7);
 }
 __host__ __device__ __forceinline__ int round32(int m) { return (m + 31) & ~31; }
-// Rows a GEMM input buffer must hold for M rows: the GEMM covers M with 1, 2, 4
-// or 8 tiles of 32 rows and reads every row of them.
-// rows a fragment-layout activation buffer holds for m rows (whole tiles of the GEMM that reads it)
+// Rows a fragment-layout activation buffer must hold for m rows: every row of
+// the tiles the GEMM that reads it covers m with (1, 2, 4 or 8 tiles of 32 rows
+// up to 256 rows, whole 128-row tiles above).
 __host__ __device__ __forceinline__ int gemm_rows(int m) {
     return m <= 32 ? 32 : m <= 64 ? 64 : m <= 128 ? 128 : ((m + 127) / 128) * 128;
 }
@@ -114,7 +114,8 @@ bool desc_supported(const cdb_model_desc& d);
 // ---------------------------------------------------------------- launchers
 hipError_t launch_gemm(int epi, const uint16_t* X, const uint16_t* Wp, int M, GemmShape g, float* part,
                        const EpiArgs& ea, hipStream_t st);
-// order: the call's rows ranked by descending position (launch_row_order)
+// order: the call's rows ranked by descending position (by the row-entry
+// kernels of a stage call, or by launch_row_order)
 hipError_t launch_attention(const float* q, const KvTarget& kv, const int32_t* seq, const int32_t* pos,
                             const int32_t* order, int M, int H, int hd, uint16_t* out, int* err, hipStream_t st);
 hipError_t launch_row_order(const int32_t* pos, int M, int32_t* order, hipStream_t st);
@@ -130,8 +131,8 @@ hipError_t launch_resid_norm(float* h, const float* part, int S, int M, int d, f
 // table rope[M][hd/2] = (cos, sin) of pos * base^(-2j/hd), angles in fp64,
 // and kvpid[M], the page of the stage's pool that receives each row's K/V
 // (the page table looked up once per call; -1 and a device error if unmapped).
-// the row-entry kernels (gather, embed, state load) also write the attention's
-// row order when `order` is non-null (at most kMaxRows rows)
+// They (gather, embed, state load) also write the attention's row order when
+// `order` is non-null (at most kMaxRows rows).
 hipError_t launch_gather(const cdb_model_desc& md, const cdb_state& s, const cdb_rows& r, const cdb_kv& kv,
                          const KvTarget& kt, float* h, float* h_in, uint16_t* xcat, float2* rope, int32_t* kvpid,
                          int32_t* order, int* err, hipStream_t st);

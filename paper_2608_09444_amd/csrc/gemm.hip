@@ -8,8 +8,8 @@
 //    operand, coalesced; the tiles of one 32-column stripe are contiguous
 //    along K.  A 32-wide stripe halves the activation (B operand) traffic per
 //    weight byte compared with a 16-wide one.
-//  * A workgroup owns one 32-column stripe and one K split; its KW waves split
-//    that K range further.  Each wave streams its weight tiles and the matching
+//  * A workgroup owns NS (1 or 2) 32-column stripes and one K split; its KW
+//    waves split that K range further.  Each wave streams its weight tiles and the matching
 //    activation fragments (L2-resident) in batches, double-buffered in
 //    registers so one batch is in flight while the previous one feeds the
 //    MFMAs.  The KW partial tiles are summed in LDS in wave order.
