@@ -207,11 +207,11 @@ def e2e_decode(shape, dm, kv, n_seqs, prompt, n_decode, seed=3):
     ws = cdb.Workspace(dm.desc, 256)
     out_ids = torch.empty((n_seqs, n_decode), dtype=torch.int32, device="cuda")
 
-    def run(n, nd, **mode):
+    def run(n, nd, dep=None, **mode):
         d = drv.Driver(max_batch=64, max_active=n, r_max=R, max_seqs=n_seqs, max_pages=max_pages,
                        core_pages=kv.c.core_pages, **mode)
         for q in range(n):
-            d.add_sequence(prompt, depths[q][:nd])
+            d.add_sequence(prompt, (depths if dep is None else dep)[q][:nd])
         scratch = torch.empty(d.scratch_bytes(shape.vocab), dtype=torch.uint8, device="cuda")
         secs = d.run(dm.model, kv.c, state.c, scratch, first, ws.buf, tokens_out=out_ids)
         if cdb.cdb_read_device_error(ws.buf) != 0:
@@ -232,6 +232,13 @@ def e2e_decode(shape, dm, kv, n_seqs, prompt, n_decode, seed=3):
     cb = res["cb_fixed_depth"]["tokens_per_s"]
     res["speedup_refill_vs_cb"] = round(res["cdb_refill"]["tokens_per_s"] / cb, 4)
     res["speedup_no_refill_vs_cb"] = round(res["cdb_no_refill"]["tokens_per_s"] / cb, 4)
+    # no early exits (every token at r_max): CDB can gain nothing, so its ratio
+    # to fixed depth is the scheduler's own overhead (Section 6.2)
+    secs_nx, st_nx = run(n_seqs, n_decode, dep=[np.full(n_decode, R, np.int32)] * n_seqs)
+    res["no_exit"] = {"cdb_refill_tokens_per_s": round(st_nx["tokens"] / secs_nx, 1), "seconds": round(secs_nx, 4),
+                      "loop_steps": st_nx["loop_steps"],
+                      "ratio_vs_cb": round(st_nx["tokens"] / secs_nx / cb, 4)}
+    log(f"e2e no exits: {st_nx['tokens']} tokens in {secs_nx:.3f}s, {st_nx['loop_steps']} loop steps")
 
     # device-decided exits (gate score >= 0.5): with the lookahead the host
     # plans each loop step from decisions one step old; without it every loop
