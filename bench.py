@@ -349,6 +349,54 @@ def batch_sweep(shape, dm, sizes=(16, 32, 64, 128, 256), pos_lo=512, pos_hi=767,
     return out
 
 
+def latency_model(shape, dm, sizes=(16, 32, 64, 128, 256), contexts=(128, 512, 2048), steps=10, warmup=3):
+    """The recurrent-step latency model of the paper's Appendix A on this
+    kernel set: cdb_loop_step over B equal-length rows (every row at context L,
+    loop index 0, no exit), timed on a grid of B and L and fitted by least
+    squares to t = delta + gamma * N_b + alpha * N_c, with N_b = B rows and N_c
+    = B * L context tokens.  Each row maps its own pages."""
+    import numpy as np
+    import torch
+
+    import cdbgen
+    import paper_2608_09444_amd as cdb
+    R = shape.r_max
+    pts = []
+    for L in contexts:
+        for n in sizes:
+            rows_np = {"pos": np.full(n, L - 1, np.int32), "c": np.zeros(n, np.int32),
+                       "depth": np.full(n, R, np.int32)}
+            max_pages = cdbgen.pages_for(L)
+            pt, nxt = own_pages(shape, rows_np, max_pages)
+            kv = cdb.PagedKV(shape, n, max_pages, 0, nxt, 0, fill="random")
+            kv.core.normal_(0.0, 1.0)
+            kv.page_table.copy_(torch.from_numpy(pt))
+            state = cdb.State(shape, n)
+            state.h.normal_(0.0, 1.0)
+            rows = cdb.Rows(np.arange(n, dtype=np.int32), np.arange(n, dtype=np.int32), rows_np["pos"],
+                            rows_np["c"], rows_np["depth"])
+            so = cdb.StepOut(n)
+            ws = cdb.Workspace(dm.desc, n)
+            ms = time_loop_step(dm, kv, state, rows, so, ws, steps, warmup)
+            pts.append({"rows": n, "context": L, "ms_per_step": round(ms, 4)})
+            del kv, state, rows, so, ws
+            torch.cuda.empty_cache()
+        log(f"latency model, context {L}: " + ", ".join(f"{p['rows']} rows {p['ms_per_step']:.3f} ms"
+                                                         for p in pts if p["context"] == L))
+    A = np.array([[1.0, p["rows"], p["rows"] * p["context"]] for p in pts])
+    t = np.array([p["ms_per_step"] for p in pts])
+    coef, *_ = np.linalg.lstsq(A, t, rcond=None)
+    fit = A @ coef
+    r2 = 1.0 - float(np.sum((t - fit) ** 2) / np.sum((t - t.mean()) ** 2))
+    delta, gamma, alpha = (float(x) for x in coef)
+    res = {"points": pts, "delta_ms": round(delta, 4), "gamma_us_per_row": round(gamma * 1e3, 3),
+           "alpha_ns_per_context_token": round(alpha * 1e6, 3), "r2": round(r2, 5),
+           "saturation_batch": {str(L): round(delta / (gamma + alpha * L), 1) for L in (128, 8192)}}
+    log(f"latency model: delta {delta:.3f} ms, gamma {gamma * 1e3:.2f} us/row, alpha {alpha * 1e6:.2f} ns/token, "
+        f"R2 {r2:.4f}")
+    return res
+
+
 def huginn_leg(n_decode, steps=20, warmup=3):
     """The Huginn-shaped model (prelude 2, recurrent block of 4 layers with the
     input-injection adapter looped up to 32 times, coda 2; d 5280, 55 x 96
@@ -759,7 +807,7 @@ def main():
     ap.add_argument("--cpu-sample", type=int, default=16, help="rows in the CPU-oracle sample (0 = skip)")
     ap.add_argument("--no-e2e", action="store_true", help="skip the whole-decode driver runs")
     ap.add_argument("--no-prefill", action="store_true", help="skip the chunked-prefill timing")
-    ap.add_argument("--no-sweep", action="store_true", help="skip the loop-step batch-size sweep")
+    ap.add_argument("--no-sweep", action="store_true", help="skip the loop-step batch-size sweep and the latency-model grid")
     ap.add_argument("--serving-requests", type=int, default=200,
                     help="requests in the serving-trace run (0 = skip; 2000 is the full trace)")
     ap.add_argument("--huginn-decode", type=int, default=64,
@@ -830,9 +878,10 @@ def main():
     attn_gbs = ab / (attn_ms * 1e-3) / 1e9
     log(f"attention {attn_ms * 1e3:.1f} us/launch, {ab / 1e6:.1f} MB -> {attn_gbs:.0f} GB/s")
 
-    sweep = None
+    sweep = lat = None
     if not args.no_sweep:
         sweep = batch_sweep(shape, dm)
+        lat = latency_model(shape, dm)
 
     e2e = None
     if not args.no_e2e:
@@ -902,7 +951,7 @@ def main():
                           "frac": round(sb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                           "flops": step_flops(shape, rows_np)},
         "cpu_baseline": cpu,
-        "batch_sweep": sweep,
+        "batch_sweep": sweep, "latency_model": lat,
         "e2e": e2e,
         "prefill": prefill,
         "serving": serving,
