@@ -349,6 +349,58 @@ def batch_sweep(shape, dm, sizes=(16, 32, 64, 128, 256), pos_lo=512, pos_hi=767,
     return out
 
 
+def batch_e2e(shape, dm, sizes=(16, 32, 64, 128), n_seqs=384, prompt=512, n_decode=32, seed=5):
+    """Whole decodes of the same 384 requests (prompt 512 with synthesized KV,
+    32 decode tokens each, config 2's categorical depths) at several maximum
+    batch sizes, with as many sequences in flight as the batch holds (so at
+    least 3 batches' worth of requests wait at every size): CDB refill and
+    no-refill against fixed-depth continuous batching (the paper's batch-size
+    sweep, Section 6.2).  The pool holds the pages of the sequences in flight."""
+    import numpy as np
+    import torch
+
+    import cdbgen
+    import paper_2608_09444_amd as cdb
+    from paper_2608_09444_amd import driver as drv
+    R = shape.r_max
+    depths = [cdbgen.draw_depths(cdbgen.OURO_DEPTHS, n_decode, R, seed=seed, stream=q) for q in range(n_seqs)]
+    first = cdbgen.prompt_ids(shape.vocab, 1, n_seqs, seed=seed + 1)[0]
+    max_pages = cdbgen.pages_for(prompt + n_decode)
+    core_pages = max(sizes) * max_pages * R
+    kv = cdb.PagedKV(shape, n_seqs, max_pages, 0, core_pages, 0, fill="random")
+    kv.core.normal_(0.0, 1.0)
+    state = cdb.State(shape, n_seqs)
+    ws = cdb.Workspace(dm.desc, 256)
+    out_ids = torch.empty((n_seqs, n_decode), dtype=torch.int32, device="cuda")
+    res = {"workload": f"{n_seqs} requests, prompt {prompt} (KV synthesized), {n_decode} decode tokens each, depths "
+                       f"categorical {{1:.3,2:.3,3:.2,4:.2}}, sequences in flight = max batch, full depth-indexed KV",
+           "points": []}
+    for B in sizes:
+        e = {"max_batch": B}
+        for name, mode in (("cdb_refill", {}), ("cdb_no_refill", {"refill": False}),
+                           ("cb_fixed_depth", {"fixed_depth": True})):
+            d = drv.Driver(max_batch=B, max_active=B, r_max=R, max_seqs=n_seqs, max_pages=max_pages,
+                           core_pages=core_pages, **mode)
+            for q in range(n_seqs):
+                d.add_sequence(prompt, depths[q])
+            scratch = torch.empty(d.scratch_bytes(shape.vocab), dtype=torch.uint8, device="cuda")
+            secs = d.run(dm.model, kv.c, state.c, scratch, first, ws.buf, tokens_out=out_ids)
+            if cdb.cdb_read_device_error(ws.buf) != 0:
+                raise RuntimeError("device error in the batch-size sweep")
+            st = d.stats()
+            e[name] = {"tokens_per_s": round(st["tokens"] / secs, 1), "seconds": round(secs, 4),
+                       "loop_steps": st["loop_steps"]}
+        cb = e["cb_fixed_depth"]["tokens_per_s"]
+        e["speedup_refill_vs_cb"] = round(e["cdb_refill"]["tokens_per_s"] / cb, 4)
+        e["speedup_no_refill_vs_cb"] = round(e["cdb_no_refill"]["tokens_per_s"] / cb, 4)
+        res["points"].append(e)
+        log(f"batch e2e, max batch {B}: refill {e['speedup_refill_vs_cb']}x, no-refill "
+            f"{e['speedup_no_refill_vs_cb']}x ({cb:.0f} tokens/s fixed depth)")
+    del kv, state, ws, out_ids
+    torch.cuda.empty_cache()
+    return res
+
+
 def latency_model(shape, dm, sizes=(16, 32, 64, 128, 256), contexts=(128, 512, 2048), steps=10, warmup=3):
     """The recurrent-step latency model of the paper's Appendix A on this
     kernel set: cdb_loop_step over B equal-length rows (every row at context L,
@@ -886,6 +938,7 @@ def main():
     e2e = None
     if not args.no_e2e:
         e2e = e2e_decode(shape, dm, kv, n_rows, pos_lo, pos_hi + 1 - pos_lo)
+        e2e["batch_sweep"] = batch_e2e(shape, dm)
 
     prefill = None
     if not args.no_prefill:
