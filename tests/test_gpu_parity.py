@@ -117,6 +117,25 @@ def test_config4_long_context_256_rows_sampled():
     _say(f"[gpu] config 4 errors {err}")
 
 
+def test_config4_loop_step_as_benched_sampled_rows():
+    """The long-context loop step exactly as the benchmark times it: 256 rows,
+    every one at a position drawn from [2048, 4223] (prompt U[2048, 4096] +
+    decode 128), each row on its own pages (≈ 155 GB of K/V); two rows checked
+    against the oracle, integer outputs for the whole batch."""
+    import torch
+    from lockstep import injected_loop_step
+    s = cdbgen.OURO
+    wl = cdbgen.WORKLOADS[4]
+    rows = cdbgen.decode_snapshot(wl.max_batch, wl.depth, s.r_max, wl.prompt[0], wl.prompt[1] + wl.decode - 1,
+                                  stream=40)
+    sample = _sample_rows(rows, s.r_max, k=2)
+    _say(f"[gpu] config 4 as benched, 256 rows at mean context {rows['pos'].mean() + 1:.0f}, sampled rows "
+         f"{sample}: pos {rows['pos'][sample]} c {rows['c'][sample]}")
+    err = injected_loop_step(s, cdbgen.model_weights(s), rows, sample, sensitivity=True)
+    torch.cuda.empty_cache()
+    _say(f"[gpu] config 4 as benched errors {err}")
+
+
 def test_config2_reduced_length_end_to_end():
     """Ouro widths with a 2-layer core, 2 sequences, prompt 16, decode 6, batch
     2; every call checked from the oracle's states (resync)."""
