@@ -872,7 +872,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the loop step shards by sequence with no exchange between GPUs, "
-              "and this build runs and reports the single-GPU path (use --gpus 1).", file=sys.stderr)
+              "and this benchmark runs and reports the single-GPU path (use --gpus 1).", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
