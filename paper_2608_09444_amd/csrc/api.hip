@@ -177,10 +177,16 @@ struct Chunk {
 // rows in ctx.h, with K/V in `kv`.  On return ctx.h holds the stage output and
 // ctx.x its RMSNorm when `norm_out` is set.  With `chunk` the rows are a
 // prefill chunk and attention runs query-tiled on MFMA.
+// x_ready: c.x already holds the first layer's input (the loop step's gather
+// wrote it), so its residual + norm is skipped.  pending_out: the last down
+// projection's partials are left for the caller (the loop step's exit kernel
+// adds them) instead of a closing residual kernel; not with norm_out.
 static cdb_status run_layers(const Ctx& c, int first, int count, KvTarget kv, const cdb_rows& r, bool norm_out,
-                             hipStream_t st, const Chunk* chunk = nullptr, int pending_in = 0) {
+                             hipStream_t st, const Chunk* chunk = nullptr, int pending_in = 0, bool x_ready = false,
+                             int* pending_out = nullptr) {
     const cdb_model_desc& d = *c.md;
     const int M = r.n_rows;
+    if ((x_ready && pending_in) || (pending_out && norm_out)) return CDB_ERR_INVALID_ARG;
     // split-K partials not yet added to h: the previous down projection's, or at
     // the start those of the loop step's adapter (h then holds zeros)
     int pending = pending_in;
@@ -201,7 +207,7 @@ static cdb_status run_layers(const Ctx& c, int first, int count, KvTarget kv, co
         ea.act = c.act;
         ea.ld_act = d.d_ff;
         // attention half: h += down partials; x = RMSNorm(h); q/k/v + RoPE + K/V write
-        HIPCHK(launch_resid_norm(c.h, c.part, pending, M, d.d, d.rms_eps, c.x, st));
+        if (l > 0 || !x_ready) HIPCHK(launch_resid_norm(c.h, c.part, pending, M, d.d, d.rms_eps, c.x, st));
         HIPCHK(launch_gemm(EPI_QKV, c.x, wptr(c, lb + c.wl.qkv), M, c.gm.qkv, c.part, ea, st));
         if (chunk)
             HIPCHK(launch_prefill_attention(c.q, kv, chunk->seq, chunk->pos0, M, d.n_heads, d.head_dim, c.x, c.err,
@@ -215,7 +221,9 @@ static cdb_status run_layers(const Ctx& c, int first, int count, KvTarget kv, co
         HIPCHK(launch_gemm(EPI_PARTIAL, c.act, wptr(c, lb + c.wl.down), M, c.gm.down, c.part, ea, st));
         pending = c.gm.down.S;
     }
-    if (pending || norm_out)
+    if (pending_out)
+        *pending_out = pending;
+    else if (pending || norm_out)
         HIPCHK(launch_resid_norm(c.h, c.part, pending, M, d.d, d.rms_eps, norm_out ? c.x : nullptr, st));
     return CDB_OK;
 }
@@ -364,9 +372,10 @@ static cdb_status loop_step(const cdb_model* model, const cdb_kv* kv, const cdb_
     if (M > 0) {
         KvTarget t = stage_target(d, *kv, 1);
         t.c_row = r.c;
+        // the gather also writes the first core layer's input (the adapter's
+        // input for injection models)
         HIPCHK(launch_gather(d, *state, r, *kv, t, c.h, c.h_in, d.injection ? c.x : nullptr, c.rope, c.kvpid, c.order,
-                             c.err,
-                             st));
+                             d.injection ? nullptr : c.x, c.err, st));
         // injection models: the gather zeroed h; the adapter's split-K
         // partials become the first layer's input in its residual + norm
         if (d.injection) {
@@ -374,9 +383,13 @@ static cdb_status loop_step(const cdb_model* model, const cdb_kv* kv, const cdb_
             ea.err = c.err;
             HIPCHK(launch_gemm(EPI_PARTIAL, c.x, wptr(c, c.wl.adapter), M, c.gm.adapter_part, c.part, ea, st));
         }
-        s = run_layers(c, d.n_prelude, d.n_core, t, r, false, st, nullptr, d.injection ? c.gm.adapter_part.S : 0);
+        int pending = 0;
+        s = run_layers(c, d.n_prelude, d.n_core, t, r, false, st, nullptr, d.injection ? c.gm.adapter_part.S : 0,
+                       !d.injection, &pending);
         if (s != CDB_OK) return s;
-        HIPCHK(launch_exit(d, r, c.h, c.h_in, wptr(c, c.wl.w_exit), state->h, state->n_slots, *out, gate, c.deff, st));
+        // the exit kernel adds the last down projection's partials to h first
+        HIPCHK(launch_exit(d, r, c.h, c.part, pending, c.h_in, wptr(c, c.wl.w_exit), state->h, state->n_slots, *out,
+                           gate, c.deff, st));
     }
     // copy-on-exit, with the stable compaction in its first workgroup
     HIPCHK(launch_copy_on_exit(d, *kv, r, c.deff, out->exit_mask, out->cont, out->exited, out->counts, c.err, st));

@@ -132,10 +132,12 @@ hipError_t launch_resid_norm(float* h, const float* part, int S, int M, int d, f
 // and kvpid[M], the page of the stage's pool that receives each row's K/V
 // (the page table looked up once per call; -1 and a device error if unmapped).
 // They (gather, embed, state load) also write the attention's row order when
-// `order` is non-null (at most kMaxRows rows).
+// `order` is non-null (at most kMaxRows rows).  The gather writes either the
+// adapter input xcat = [h; e] or, with xn set, the first core layer's input
+// xn = bf16(RMSNorm(h)), both in fragment layout.
 hipError_t launch_gather(const cdb_model_desc& md, const cdb_state& s, const cdb_rows& r, const cdb_kv& kv,
                          const KvTarget& kt, float* h, float* h_in, uint16_t* xcat, float2* rope, int32_t* kvpid,
-                         int32_t* order, int* err, hipStream_t st);
+                         int32_t* order, uint16_t* xn, int* err, hipStream_t st);
 hipError_t launch_embed(const cdb_model_desc& md, const uint16_t* embed, const int32_t* tokens, const cdb_rows& r,
                         const cdb_kv& kv, const KvTarget& kt, int n_slots, float* h, float2* rope, int32_t* kvpid,
                         int32_t* order, int* err, hipStream_t st);
@@ -144,9 +146,10 @@ hipError_t launch_store_state(int M, int d, int n_slots, const int32_t* slot, co
 hipError_t launch_load_state(const cdb_model_desc& md, int M, const int32_t* slot, const int32_t* seq,
                              const int32_t* pos, const KvTarget& kt, const float* state_h, int n_slots, float* h,
                              float2* rope, int32_t* kvpid, int32_t* order, int* err, hipStream_t st);
-// gate: NULL replays rows.depth; deff[M] receives each exiting row's depth.
-hipError_t launch_exit(const cdb_model_desc& md, const cdb_rows& r, const float* h, const float* h_in,
-                       const uint16_t* w_exit, float* state_h, int n_slots, const cdb_step_out& o,
+// h += the S split-K partials in part (split order) first; gate: NULL replays
+// rows.depth; deff[M] receives each exiting row's depth.
+hipError_t launch_exit(const cdb_model_desc& md, const cdb_rows& r, float* h, const float* part, int S,
+                       const float* h_in, const uint16_t* w_exit, float* state_h, int n_slots, const cdb_step_out& o,
                        const cdb_gate* gate, int32_t* deff, hipStream_t st);
 hipError_t launch_compact(int M, const uint8_t* mask, int32_t* cont, int32_t* exited, int32_t* counts,
                           hipStream_t st);

@@ -79,7 +79,9 @@ __global__ __launch_bounds__(256) void k_gather(int d, int r_max, int n_slots, i
                                                 const float* __restrict__ sh, const float* __restrict__ se,
                                                 float* __restrict__ h, float* __restrict__ h_in,
                                                 uint16_t* __restrict__ xcat, float2* __restrict__ rope, KvTarget kt,
-                                                int32_t* __restrict__ kvpid, int32_t* __restrict__ order, int* err) {
+                                                int32_t* __restrict__ kvpid, int32_t* __restrict__ order, float eps,
+                                                uint16_t* __restrict__ xn, int* err) {
+    __shared__ float red[4];
     const int i = blockIdx.x;
     if (order && i == 0 && gridDim.x <= kMaxRows) row_order_block(pos, gridDim.x, order);
     const int sl = slot[i];
@@ -106,6 +108,22 @@ __global__ __launch_bounds__(256) void k_gather(int d, int r_max, int n_slots, i
             pe.y = pack_bf16(e.z, e.w);
             *reinterpret_cast<uint2*>(xcat + frag_index(i, k, 2 * d)) = ph;
             *reinterpret_cast<uint2*>(xcat + frag_index(i, d + k, 2 * d)) = pe;
+        }
+    }
+    if (xn) {  // no adapter: the first core layer's input bf16(RMSNorm(h)), fragment layout
+        float ss = 0.f;
+        for (int k = threadIdx.x * 4; k < d; k += 256 * 4) {
+            const float4 v = *reinterpret_cast<const float4*>(h + (size_t)i * d + k);
+            ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+        }
+        ss = block_sum(ss, red);
+        const float inv = 1.0f / sqrtf(ss / d + eps);
+        for (int k = threadIdx.x * 4; k < d; k += 256 * 4) {
+            const float4 v = *reinterpret_cast<const float4*>(h + (size_t)i * d + k);
+            uint2 pk;
+            pk.x = pack_bf16(v.x * inv, v.y * inv);
+            pk.y = pack_bf16(v.z * inv, v.w * inv);
+            *reinterpret_cast<uint2*>(xn + frag_index(i, k, d)) = pk;
         }
     }
 }
@@ -222,8 +240,9 @@ __global__ __launch_bounds__(256) void k_store_state(int d, int n_slots, const i
 }
 
 // ------------------------------------------------------------------ exit
-// score: sigmoid(w_exit . RMSNorm(h)) or ||h - h_in||_2; exit = (c + 1 == depth);
-// state.h[slot] = h.
+// h += sum_s part[s] (the last down projection's split-K partials, split order
+// 0..S-1, as the residual + norm kernel adds them); score: sigmoid(w_exit .
+// RMSNorm(h)) or ||h - h_in||_2; exit = (c + 1 == depth); state.h[slot] = h.
 // Exit score and decision of every row.  Replayed depths (gated == 0):
 // exit = (c + 1 == depth).  Threshold gate (gated == 1, Section 4.3; App. C.2):
 // the criterion (score >= threshold, or for convergence distance < threshold
@@ -232,7 +251,8 @@ __global__ __launch_bounds__(256) void k_store_state(int d, int n_slots, const i
 // the exiting row's depth (c + 1), 0 for continuing rows.
 __global__ __launch_bounds__(256) void k_exit(int d, float eps, int exit_kind, int r_max, int n_slots,
                                               const int32_t* __restrict__ slot, const int32_t* __restrict__ c,
-                                              const int32_t* __restrict__ depth, const float* __restrict__ h,
+                                              const int32_t* __restrict__ depth, float* __restrict__ h,
+                                              const float* __restrict__ part, int S, int M,
                                               const float* __restrict__ h_in, const uint16_t* __restrict__ w_exit,
                                               float* __restrict__ sh, float* __restrict__ score,
                                               uint8_t* __restrict__ mask, uint8_t* __restrict__ exit_next,
@@ -240,11 +260,21 @@ __global__ __launch_bounds__(256) void k_exit(int d, float eps, int exit_kind, i
                                               uint8_t* __restrict__ pending) {
     __shared__ float red[4];
     const int i = blockIdx.x;
-    const float* x = h + (size_t)i * d;
+    float* x = h + (size_t)i * d;
     const float* x0 = h_in + (size_t)i * d;
     float a = 0.f, b = 0.f;
     for (int k = threadIdx.x * 4; k < d; k += 1024) {
-        const float4 v = *reinterpret_cast<const float4*>(x + k);
+        float4 v = *reinterpret_cast<const float4*>(x + k);
+        if (S > 0) {
+            for (int s0 = 0; s0 < S; ++s0) {
+                const float4 p = *reinterpret_cast<const float4*>(part + ((size_t)s0 * M + i) * d + k);
+                v.x += p.x;
+                v.y += p.y;
+                v.z += p.z;
+                v.w += p.w;
+            }
+            *reinterpret_cast<float4*>(x + k) = v;
+        }
         if (exit_kind == 1) {
             const float4 u = *reinterpret_cast<const float4*>(x0 + k);
             const float dx = v.x - u.x, dy = v.y - u.y, dz = v.z - u.z, dw = v.w - u.w;
@@ -492,12 +522,13 @@ static int page_cap(const cdb_kv& kv) { return kv.max_pages * kPage; }
 
 hipError_t launch_gather(const cdb_model_desc& md, const cdb_state& s, const cdb_rows& r, const cdb_kv& kv,
                          const KvTarget& kt, float* h, float* h_in, uint16_t* xcat, float2* rope, int32_t* kvpid,
-                         int32_t* order, int* err, hipStream_t st) {
+                         int32_t* order, uint16_t* xn, int* err, hipStream_t st) {
     if (r.n_rows <= 0) return hipSuccess;
     if (order && r.n_rows > kMaxRows) return hipErrorInvalidValue;
+    if (xcat && xn) return hipErrorInvalidValue;
     k_gather<<<r.n_rows, 256, 0, st>>>(md.d, md.r_max, s.n_slots, kv.max_seqs, page_cap(kv), md.head_dim, md.rope_base,
                                         r.slot, r.seq, r.pos, r.c, r.depth, s.h, s.e, h, h_in, xcat, rope, kt, kvpid,
-                                        order, err);
+                                        order, md.rms_eps, xn, err);
     return hipGetLastError();
 }
 
@@ -546,12 +577,13 @@ hipError_t launch_store_state(int M, int d, int n_slots, const int32_t* slot, co
     return hipGetLastError();
 }
 
-hipError_t launch_exit(const cdb_model_desc& md, const cdb_rows& r, const float* h, const float* h_in,
-                       const uint16_t* w_exit, float* state_h, int n_slots, const cdb_step_out& o,
+hipError_t launch_exit(const cdb_model_desc& md, const cdb_rows& r, float* h, const float* part, int S,
+                       const float* h_in, const uint16_t* w_exit, float* state_h, int n_slots, const cdb_step_out& o,
                        const cdb_gate* gate, int32_t* deff, hipStream_t st) {
     if (r.n_rows <= 0) return hipSuccess;
+    if (S < 0 || (S > 0 && !part)) return hipErrorInvalidValue;
     k_exit<<<r.n_rows, 256, 0, st>>>(md.d, md.rms_eps, md.exit_kind, md.r_max, n_slots, r.slot, r.c, r.depth, h,
-                                      h_in, w_exit, state_h, o.exit_score, o.exit_mask, o.exit_next, deff,
+                                      part, S, r.n_rows, h_in, w_exit, state_h, o.exit_score, o.exit_mask, o.exit_next, deff,
                                       gate ? 1 : 0, gate ? gate->threshold : 0.f, gate ? gate->lookahead : 0,
                                       gate ? gate->pending : nullptr);
     return hipGetLastError();
