@@ -9,6 +9,8 @@
 * Degenerate exit patterns: every row exits (depth = c + 1, depths 1..r_max, so
   every exiting row below r_max copies its entry into the deeper planes), and no
   row exits.
+* The benchmark's loop step run twice from the same state and cache is
+  bit-identical (determinism).
 * Conditions the device detects are reported through the sticky error word and
   never make a kernel touch memory outside its buffers: an unmapped page inside a
   row's context, an unmapped write page, a slot outside the state pool.  They are
@@ -242,3 +244,40 @@ def test_row_results_do_not_depend_on_the_batch_huginn_width():
     rows = cdbgen.decode_snapshot(128, wl.depth, s.r_max, 256, 767, stream=81)
     _say("[gpu] batch invariance, Huginn widths, 1 core layer: 128 rows vs their first 50")
     _batch_invariance(s, w, rows, 50)
+
+
+def test_loop_step_is_deterministic_as_benched():
+    """The benchmark's batch (64 mixed-depth rows of the 24-layer Ouro-shaped
+    model at positions 512..767) run twice from the same state and cache: the
+    states, exit scores, integer outputs and every written K/V entry are
+    bit-identical between the runs."""
+    s = cdbgen.OURO
+    rows_np = cdbgen.decode_snapshot(64, cdbgen.OURO_DEPTHS, s.r_max, 512, 767, stream=7)
+    n = 64
+    gm = cdb.DeviceModel(s, cdbgen.model_weights(s))
+    pt, max_pages, n_pages = _own_pages(s, rows_np)
+    kv = cdb.PagedKV(s, n, max_pages, 0, n_pages, 0, fill="random")
+    g = torch.Generator(device="cuda")
+    g.manual_seed(23)
+    kv.core.normal_(0.0, 1.0, generator=g)
+    kv.page_table.copy_(torch.from_numpy(pt))
+    state = cdb.State(s, n)
+    state.h.normal_(0.0, 1.0, generator=g)
+    h0 = state.h.clone()
+    rows = cdb.Rows(np.arange(n, dtype=np.int32), np.arange(n, dtype=np.int32), rows_np["pos"], rows_np["c"],
+                    rows_np["depth"])
+    ws = cdb.Workspace(gm.desc, n)
+    _say("[gpu] determinism: the benchmark's 64-row, 24-layer loop step twice")
+    runs = []
+    for _ in range(2):
+        state.h.copy_(h0)
+        out = cdb.StepOut(n)
+        cdb.cdb_loop_step(gm.model, kv.c, state.c, rows.c, out.c, ws.buf)
+        torch.cuda.synchronize()
+        assert cdb.cdb_read_device_error(ws.buf) == 0
+        runs.append((state.h.clone(), out.score.clone(), out.mask.clone(), out.cont.clone(), out.exited.clone(),
+                     out.counts.clone(), kv.core.clone()))
+    for a, b in zip(runs[0], runs[1]):
+        assert torch.equal(a, b)
+    del runs
+    torch.cuda.empty_cache()
