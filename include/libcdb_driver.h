@@ -92,7 +92,11 @@ void cdb_driver_destroy(cdb_driver* d);
 /* Adds a request in arrival order: its prompt (already prefilled: its KV must
  * be present when the sequence is admitted) and the exit depth of each of its
  * n_decode decode inputs (NULL in gated mode).  Returns the sequence id (= its
- * row of the page table and its state slot) or -1. */
+ * row of the page table and its state slot) or -1: a bad argument, max_seqs
+ * reached, an arrival before the previous one, a depth outside [1, r_max], or
+ * a sequence that could never be admitted (prompt_len + n_decode positions
+ * need more pages per plane than max_pages, or more pages than a pool holds
+ * in all). */
 int32_t cdb_driver_add_sequence(cdb_driver* d, int32_t prompt_len, int32_t n_decode, const int32_t* depths,
                                 double arrival);
 

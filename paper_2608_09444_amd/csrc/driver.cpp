@@ -239,6 +239,11 @@ int32_t cdb_driver_add_sequence(cdb_driver* d, int32_t prompt_len, int32_t n_dec
     if (depths)
         for (int32_t i = 0; i < n_decode; ++i)
             if (depths[i] < 1 || depths[i] > d->cfg.r_max) return -1;
+    // a sequence no pool state could ever admit would stall the queue behind it
+    const int64_t need = ((int64_t)prompt_len + n_decode + 15) / 16;  // pages per plane
+    if (need > d->cfg.max_pages || need * core_slots(d) > d->cfg.core_pages ||
+        (d->cfg.has_prelude && need > d->cfg.pre_pages) || (d->cfg.has_coda && need > d->cfg.coda_pages))
+        return -1;
     Seq s;
     s.prompt_len = prompt_len;
     s.n_decode = n_decode;

@@ -315,3 +315,29 @@ def test_prefill_completion_must_follow_the_plan():
     bad.pos[0] = 4  # a chunk that is not the next one
     assert d.complete(bad) == -1
     assert d.complete(t) == 0
+
+
+def test_add_sequence_rejects_what_could_never_run():
+    """Bad depths, a zero-length prompt, too many sequences, out-of-order
+    arrivals, and sequences longer than the page table or the pool are refused
+    when added (a sequence that could never be admitted would stall the queue)."""
+    d = Driver(max_batch=2, max_active=2, r_max=2, max_seqs=2, max_pages=2, core_pages=8)
+    for prompt, depths in ((4, [0, 1]), (4, [1, 3]), (0, [1]), (4, [])):
+        with pytest.raises(ValueError):
+            d.add_sequence(prompt, depths)
+    with pytest.raises(ValueError):
+        d.add_sequence(30, [1, 2, 1])  # 33 positions: 3 pages > max_pages 2
+    assert d.add_sequence(30, [1, 2]) == 0  # 32 positions fit 2 pages
+    small = Driver(max_batch=2, max_active=2, r_max=4, max_seqs=2, max_pages=4, core_pages=7)
+    with pytest.raises(ValueError):
+        small.add_sequence(20, [1])  # 2 pages x 4 planes = 8 > 7 core pages
+    shared = Driver(max_batch=2, max_active=2, r_max=4, max_seqs=2, max_pages=4, core_pages=7, kv_layout=KV_SHARED)
+    assert shared.add_sequence(20, [1]) == 0  # 2 pages when all planes share one
+    one = Driver(max_batch=2, max_active=2, r_max=2, max_seqs=1, max_pages=4, core_pages=16)
+    one.add_sequence(4, [1], arrival=1.0)
+    with pytest.raises(ValueError):
+        one.add_sequence(4, [1], arrival=2.0)  # beyond max_seqs
+    two = Driver(max_batch=2, max_active=2, r_max=2, max_seqs=2, max_pages=4, core_pages=16)
+    two.add_sequence(4, [1], arrival=1.0)
+    with pytest.raises(ValueError):
+        two.add_sequence(4, [1], arrival=0.5)  # before the previous arrival
