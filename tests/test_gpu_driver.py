@@ -7,6 +7,7 @@ the shared core KV layouts call by call against the oracle.
 * The greedy tokens must follow the oracle's wherever the history agrees and
   the oracle's top-2 logit gap is clear of the tolerance.
 """
+import dataclasses
 import sys
 
 import numpy as np
@@ -194,17 +195,22 @@ def test_driver_rejects_short_token_table():
 
 
 def _gate_threshold(shape, w, prompts):
-    """A threshold the tiny model's gate scores straddle: the median of the
-    loop-1 scores of the first prompt under the oracle."""
+    """A threshold the model's exit scores straddle: the median, over the first
+    prompt under the oracle, of the loop-1 gate scores, or for the convergence
+    criterion (first applied after loop 2) of the loop-2 distances."""
     m = oracle.Model(shape, w, bf16_storage=True)
     p = prompts[0]
     ref = m.ref_sequence(p, np.full(len(p), shape.r_max, np.int32))
-    return float(np.median(ref["scores"][:, 0]))
+    return float(np.median(ref["scores"][:, 1 if shape.exit_kind == 1 else 0]))
 
 
-def test_lookahead_gate_call_by_call():
+# the learned gate (the tiny model) and the convergence criterion (the d = 192
+# model with the adapter, at r_max 4 so that its earliest lookahead exit, after
+# loop 3, comes before r_max)
+@pytest.mark.parametrize("shape_name", ["tiny", "inj"], ids=["tiny-gate", "inj-convergence"])
+def test_lookahead_gate_call_by_call(shape_name):
     from lockstep import Lockstep
-    s = cdbgen.TINY
+    s = cdbgen.TINY if shape_name == "tiny" else dataclasses.replace(INJ, name="inj-1-2-1-r4", r_max=4)
     w = cdbgen.model_weights(s)
     prompts, ndec, depths = _requests(s, seed=70)
     thr = _gate_threshold(s, w, prompts)
