@@ -243,7 +243,10 @@ cdb_status cdb_boundary_coda(const cdb_model* model, const cdb_kv* kv, const cdb
  * only the last row's greedy id is produced, in next_ids[0] (the LM head runs
  * for the 32-row tile holding that row only).  Positions < pos0 of the
  * sequence must already be in the cache (earlier chunks); every plane's pages
- * of positions < pos0 + n_rows must be mapped.  Attention is query-tiled on
+ * of positions < pos0 + n_rows must be mapped.  Earlier positions are read from
+ * what each plane's page holds: with aliased planes (the shared layouts) that
+ * is an earlier chunk's last loop, so chunking matches one whole-prompt block
+ * under the full layout only.  Attention is query-tiled on
  * MFMA; above 256 rows the projections use compute-bound tiles.
  * 1 <= n_rows <= 512, else CDB_ERR_CAPACITY (an empty chunk has no last row to
  * take an id from); the workspace must be sized for n_rows. */
