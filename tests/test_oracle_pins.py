@@ -94,11 +94,20 @@ def test_silu_identities():
 
 # ------------------------------------------------ textbook unrolled transformer
 
-def unrolled_reference(shape, w, tokens):
+def unrolled_reference(shape, w, tokens, bf16=False):
     """Fixed depth r_max as a plain weight-tied transformer over the whole
     sequence at once: layers [prelude, (adapter,) core x r_max, coda], causal
-    library attention, complex-number RoPE.  Returns logits, per-loop states."""
+    library attention, complex-number RoPE.  Returns logits, per-loop states.
+
+    bf16: round to bf16 (torch's own conversion, through fp32 as a device that
+    computes in fp32 does) exactly where the model keeps values in bf16: the
+    normalised input of every projection (q/k/v, gate/up, LM head), K and V
+    after RoPE, the attention output, the SwiGLU product and the adapter input
+    [h; e].  Everything else stays fp64."""
     s = shape
+
+    def st(x):
+        return x.to(torch.float32).to(torch.bfloat16).to(torch.float64) if bf16 else x
     T = len(tokens)
     d, H, hd = s.d, s.n_heads, s.head_dim
     pos = torch.arange(T, dtype=torch.float64)
@@ -115,14 +124,14 @@ def unrolled_reference(shape, w, tokens):
 
     def layer(x, L):
         lw = {k: f64(v) for k, v in w["layers"][L].items()}
-        n = rms(x)
+        n = st(rms(x))
         q = rope((n @ lw["q"].T).view(T, H, hd)).transpose(0, 1)
-        k = rope((n @ lw["k"].T).view(T, H, hd)).transpose(0, 1)
-        v = (n @ lw["v"].T).view(T, H, hd).transpose(0, 1)
-        o = F.scaled_dot_product_attention(q, k, v, is_causal=True).transpose(0, 1).reshape(T, d)
+        k = st(rope((n @ lw["k"].T).view(T, H, hd))).transpose(0, 1)
+        v = st((n @ lw["v"].T).view(T, H, hd)).transpose(0, 1)
+        o = st(F.scaled_dot_product_attention(q, k, v, is_causal=True).transpose(0, 1).reshape(T, d))
         x = x + o @ lw["o"].T
-        n = rms(x)
-        return x + (F.silu(n @ lw["gate"].T) * (n @ lw["up"].T)) @ lw["down"].T
+        n = st(rms(x))
+        return x + st(F.silu(n @ lw["gate"].T) * (n @ lw["up"].T)) @ lw["down"].T
 
     x = f64(w["embed"])[torch.as_tensor(tokens, dtype=torch.long)]
     for L in range(s.n_prelude):
@@ -130,14 +139,14 @@ def unrolled_reference(shape, w, tokens):
     e = x
     states = [x]
     for _ in range(s.r_max):
-        u = x if not s.injection else torch.cat([x, e], dim=-1) @ f64(w["adapter"]).T
+        u = x if not s.injection else st(torch.cat([x, e], dim=-1)) @ f64(w["adapter"]).T
         for l in range(s.n_core):
             u = layer(u, s.n_prelude + l)
         x = u
         states.append(x)
     for l in range(s.n_coda):
         x = layer(x, s.n_prelude + s.n_core + l)
-    logits = rms(x) @ f64(w["lm_head"]).T
+    logits = st(rms(x)) @ f64(w["lm_head"]).T
     return logits.numpy(), [t.numpy() for t in states]
 
 
@@ -160,6 +169,49 @@ def test_fixed_depth_equals_unrolled_weight_tied_transformer(shape):
             n = F.rms_norm(torch.from_numpy(states[r]), (shape.d,), eps=shape.rms_eps).numpy()
             want = 1.0 / (1.0 + np.exp(-(n @ cdbgen.bf16_to_f32(w["w_exit"]).astype(np.float64))))
         assert np.allclose(got["scores"][:, r - 1], want, rtol=1e-10, atol=1e-12)
+
+
+@pytest.mark.parametrize("shape", [SMALL, SMALL_INJ], ids=lambda s: s.name)
+def test_bf16_storage_rounds_where_the_unrolled_transformer_does(shape):
+    """The oracle's bf16-storage mode (the mode the device is graded against)
+    equals the unrolled transformer with torch's bf16 conversion applied at the
+    model's storage points, and differs from the unrounded model: a rounding
+    point dropped from or added to the oracle moves its logits by ~1e-3."""
+    w = weights(shape)
+    T = 11
+    tokens = cdbgen.prompt_ids(shape.vocab, 1, T, seed=5)[0]
+    depth = np.full(T, shape.r_max, dtype=np.int32)
+    got = oracle.Model(shape, w, bf16_storage=True).ref_sequence(tokens, depth)
+    logits, states = unrolled_reference(shape, w, tokens, bf16=True)
+    assert np.abs(got["logits"] - logits).max() <= 1e-10
+    assert np.abs(got["h"] - states[-1]).max() <= 1e-10
+    exact, _ = unrolled_reference(shape, w, tokens, bf16=False)
+    assert np.abs(got["logits"] - exact).max() > 1e-4
+
+
+def test_argmax_takes_the_lowest_index_on_ties():
+    """Greedy ties: copying the winning LM-head row to a lower and a higher
+    index makes an exact three-way tie; the oracle's greedy id is the lowest
+    of them, as numpy's argmax (first occurrence) gives."""
+    shape = SMALL
+    w = weights(shape)
+    T = 6
+    tokens = cdbgen.prompt_ids(shape.vocab, 1, T, seed=14)[0]
+    depth = np.full(T, shape.r_max, dtype=np.int32)
+    ids = oracle.Model(shape, w, bf16_storage=True).ref_sequence(tokens, depth)["logits"].argmax(axis=1)
+    for t in range(T - 1):
+        win = int(ids[t])
+        lo, hi = (win - 1 - t) % shape.vocab, (win + 1 + t) % shape.vocab
+        lm = w["lm_head"].copy()
+        lm[lo] = lm[win]
+        lm[hi] = lm[win]
+        ww = dict(w, lm_head=lm)
+        # positions <= t given, so the states are those of the first run; id t + 1 is greedy
+        res = oracle.Model(shape, ww, bf16_storage=True).ref_sequence(tokens, depth, n_given=t + 1)
+        row = res["logits"][t]
+        tied = np.flatnonzero(row == row.max()).tolist()
+        assert tied == sorted({lo, win, hi})
+        assert res["tokens"][t + 1] == tied[0] == int(np.argmax(row))
 
 
 def test_fixed_depth_bf16_storage_stays_near_exact():
