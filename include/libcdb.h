@@ -145,7 +145,15 @@ typedef struct {
  * (replayed exit decisions, App. B.2).  Rows may sit at any loop index
  * (refill); rows of one sequence at consecutive positions in one call (a
  * prompt) see each other causally.  c and depth are ignored by the boundary
- * calls. */
+ * calls.
+ * d_n_rows (optional, device int32, may be NULL): the number of rows the call
+ * holds, read by the kernels when they run, so that one captured call (Section
+ * 4.3, static shapes) replays for any row count up to n_rows.  With it set,
+ * n_rows is the capacity: launch shapes, workspace and output buffers are sized
+ * for n_rows; only the first clamp(*d_n_rows, 0, n_rows) rows are read,
+ * computed into outputs and counted (cont / exited / counts cover those rows);
+ * the rest of each output is left as it was.  A row's results are the same as
+ * in a call of exactly that many rows.  Not read by cdb_prefill. */
 typedef struct {
     int32_t n_rows;
     const int32_t* slot;
@@ -153,6 +161,7 @@ typedef struct {
     const int32_t* pos;
     const int32_t* c;
     const int32_t* depth;
+    const int32_t* d_n_rows;
 } cdb_rows;
 
 /* Loop-step outputs (device): exit_score fp32 [n_rows]; exit_mask uint8
@@ -227,8 +236,8 @@ cdb_status cdb_loop_step_gated(const cdb_model* model, const cdb_kv* kv, const c
 
 /* Coda stage (Section 4.1; Eq. 1 p(x_{t+1}) = softmax(C(h))): coda layers with
  * KV plane r_max + 1 on h = state.h[slot], final RMSNorm, LM head.  logits:
- * device fp32 [n_rows][vocab]; next_ids: device int32 [n_rows] = argmax (lowest
- * index on ties). */
+ * device fp32 [n_rows][vocab], required (CDB_ERR_INVALID_ARG if NULL);
+ * next_ids: device int32 [n_rows] = argmax (lowest index on ties). */
 cdb_status cdb_boundary_coda(const cdb_model* model, const cdb_kv* kv, const cdb_state* state,
                              const cdb_rows* rows, float* logits, int32_t* next_ids, void* ws, size_t ws_bytes,
                              hipStream_t stream);
@@ -249,7 +258,9 @@ cdb_status cdb_boundary_coda(const cdb_model* model, const cdb_kv* kv, const cdb
  * under the full layout only.  Attention is query-tiled on
  * MFMA; above 256 rows the projections use compute-bound tiles.
  * 1 <= n_rows <= 512, else CDB_ERR_CAPACITY (an empty chunk has no last row to
- * take an id from); the workspace must be sized for n_rows. */
+ * take an id from); the workspace must be sized for n_rows.  One call spans at
+ * most 10240 positions: pos0 + n_rows > 10240 returns CDB_ERR_CAPACITY before
+ * anything is enqueued (the page ids of the key range are held on chip). */
 cdb_status cdb_prefill(const cdb_model* model, const cdb_kv* kv, int32_t seq, int32_t pos0, int32_t n_rows,
                        const int32_t* tokens, float* logits, int32_t* next_ids, void* ws, size_t ws_bytes,
                        hipStream_t stream);

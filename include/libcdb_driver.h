@@ -105,7 +105,8 @@ int32_t cdb_driver_add_sequence(cdb_driver* d, int32_t prompt_len, int32_t n_dec
  * 4.1): the coda, then prompt chunks (one per call, first admitted first),
  * then the prelude of first decode inputs, then loop steps.  The first decode
  * input is the prompt's greedy continuation, passed on the device.  Returns
- * the sequence id or -1. */
+ * the sequence id or -1 (the reasons of cdb_driver_add_sequence, or a prompt
+ * longer than the 10240 positions one cdb_prefill call spans). */
 int32_t cdb_driver_add_request(cdb_driver* d, int32_t prompt_len, const int32_t* prompt_ids, int32_t n_decode,
                                const int32_t* depths, double arrival);
 

@@ -58,7 +58,7 @@ class cdb_state(C.Structure):
 
 class cdb_rows(C.Structure):
     _fields_ = [("n_rows", C.c_int32), ("slot", C.c_void_p), ("seq", C.c_void_p), ("pos", C.c_void_p),
-                ("c", C.c_void_p), ("depth", C.c_void_p)]
+                ("c", C.c_void_p), ("depth", C.c_void_p), ("d_n_rows", C.c_void_p)]
 
 
 class cdb_step_out(C.Structure):
@@ -295,9 +295,11 @@ class Workspace:
 
 
 class Rows:
-    """Device row arrays for one stage call."""
+    """Device row arrays for one stage call.  d_n_rows: optional device int32
+    tensor holding the live row count (the arrays' length is then the
+    capacity)."""
 
-    def __init__(self, slot, seq, pos, c=None, depth=None, device="cuda"):
+    def __init__(self, slot, seq, pos, c=None, depth=None, device="cuda", d_n_rows=None):
         import torch
 
         def dev(a):
@@ -306,8 +308,10 @@ class Rows:
             return torch.as_tensor(a, dtype=torch.int32).to(device).contiguous()
 
         self.slot, self.seq, self.pos, self.cc, self.depth = dev(slot), dev(seq), dev(pos), dev(c), dev(depth)
+        self.d_n_rows = d_n_rows
         self.n = int(self.slot.numel())
-        self.c = cdb_rows(self.n, _ptr(self.slot), _ptr(self.seq), _ptr(self.pos), _ptr(self.cc), _ptr(self.depth))
+        self.c = cdb_rows(self.n, _ptr(self.slot), _ptr(self.seq), _ptr(self.pos), _ptr(self.cc), _ptr(self.depth),
+                          _ptr(d_n_rows))
 
 
 class StepOut:

@@ -186,6 +186,7 @@ static cdb_status run_layers(const Ctx& c, int first, int count, KvTarget kv, co
                              int* pending_out = nullptr) {
     const cdb_model_desc& d = *c.md;
     const int M = r.n_rows;
+    const int32_t* dn = r.d_n_rows;  // device row count (M is then the capacity)
     if ((x_ready && pending_in) || (pending_out && norm_out)) return CDB_ERR_INVALID_ARG;
     // split-K partials not yet added to h: the previous down projection's, or at
     // the start those of the loop step's adapter (h then holds zeros)
@@ -207,24 +208,24 @@ static cdb_status run_layers(const Ctx& c, int first, int count, KvTarget kv, co
         ea.act = c.act;
         ea.ld_act = d.d_ff;
         // attention half: h += down partials; x = RMSNorm(h); q/k/v + RoPE + K/V write
-        if (l > 0 || !x_ready) HIPCHK(launch_resid_norm(c.h, c.part, pending, M, d.d, d.rms_eps, c.x, st));
-        HIPCHK(launch_gemm(EPI_QKV, c.x, wptr(c, lb + c.wl.qkv), M, c.gm.qkv, c.part, ea, st));
+        if (l > 0 || !x_ready) HIPCHK(launch_resid_norm(c.h, c.part, pending, M, d.d, d.rms_eps, c.x, st, dn));
+        HIPCHK(launch_gemm(EPI_QKV, c.x, wptr(c, lb + c.wl.qkv), M, c.gm.qkv, c.part, ea, st, dn));
         if (chunk)
             HIPCHK(launch_prefill_attention(c.q, kv, chunk->seq, chunk->pos0, M, d.n_heads, d.head_dim, c.x, c.err,
                                             st));
         else
-            HIPCHK(launch_attention(c.q, kv, r.seq, r.pos, c.order, M, d.n_heads, d.head_dim, c.x, c.err, st));
-        HIPCHK(launch_gemm(EPI_PARTIAL, c.x, wptr(c, lb + c.wl.o), M, c.gm.o, c.part, ea, st));
+            HIPCHK(launch_attention(c.q, kv, r.seq, r.pos, c.order, M, d.n_heads, d.head_dim, c.x, c.err, st, dn));
+        HIPCHK(launch_gemm(EPI_PARTIAL, c.x, wptr(c, lb + c.wl.o), M, c.gm.o, c.part, ea, st, dn));
         // MLP half: h += O partials; x = RMSNorm(h); act = SwiGLU; down partials
-        HIPCHK(launch_resid_norm(c.h, c.part, c.gm.o.S, M, d.d, d.rms_eps, c.x, st));
-        HIPCHK(launch_gemm(EPI_SWIGLU, c.x, wptr(c, lb + c.wl.gu), M, c.gm.gu, c.part, ea, st));
-        HIPCHK(launch_gemm(EPI_PARTIAL, c.act, wptr(c, lb + c.wl.down), M, c.gm.down, c.part, ea, st));
+        HIPCHK(launch_resid_norm(c.h, c.part, c.gm.o.S, M, d.d, d.rms_eps, c.x, st, dn));
+        HIPCHK(launch_gemm(EPI_SWIGLU, c.x, wptr(c, lb + c.wl.gu), M, c.gm.gu, c.part, ea, st, dn));
+        HIPCHK(launch_gemm(EPI_PARTIAL, c.act, wptr(c, lb + c.wl.down), M, c.gm.down, c.part, ea, st, dn));
         pending = c.gm.down.S;
     }
     if (pending_out)
         *pending_out = pending;
     else if (pending || norm_out)
-        HIPCHK(launch_resid_norm(c.h, c.part, pending, M, d.d, d.rms_eps, norm_out ? c.x : nullptr, st));
+        HIPCHK(launch_resid_norm(c.h, c.part, pending, M, d.d, d.rms_eps, norm_out ? c.x : nullptr, st, dn));
     return CDB_OK;
 }
 
@@ -351,7 +352,7 @@ cdb_status cdb_boundary_prelude(const cdb_model* model, const cdb_kv* kv, const 
     s = run_layers(c, 0, d.n_prelude, t, *rows, false, st);
     if (s != CDB_OK) return s;
     HIPCHK(launch_store_state(rows->n_rows, d.d, state->n_slots, rows->slot, c.h, state->h,
-                              d.injection ? state->e : nullptr, st));
+                              d.injection ? state->e : nullptr, st, rows->d_n_rows));
     return CDB_OK;
 }
 
@@ -381,7 +382,8 @@ static cdb_status loop_step(const cdb_model* model, const cdb_kv* kv, const cdb_
         if (d.injection) {
             EpiArgs ea{};
             ea.err = c.err;
-            HIPCHK(launch_gemm(EPI_PARTIAL, c.x, wptr(c, c.wl.adapter), M, c.gm.adapter_part, c.part, ea, st));
+            HIPCHK(launch_gemm(EPI_PARTIAL, c.x, wptr(c, c.wl.adapter), M, c.gm.adapter_part, c.part, ea, st,
+                               r.d_n_rows));
         }
         int pending = 0;
         s = run_layers(c, d.n_prelude, d.n_core, t, r, false, st, nullptr, d.injection ? c.gm.adapter_part.S : 0,
@@ -419,25 +421,15 @@ cdb_status cdb_boundary_coda(const cdb_model* model, const cdb_kv* kv, const cdb
     Ctx c = make_ctx(model, ws, M);
     const KvTarget t = stage_target(d, *kv, 2);
     HIPCHK(launch_load_state(d, M, rows->slot, rows->seq, rows->pos, t, state->h, state->n_slots, c.h, c.rope, c.kvpid,
-                             c.order,
-                             c.err, st));
+                             c.order, c.err, st, rows->d_n_rows));
     s = run_layers(c, d.n_prelude + d.n_core, d.n_coda, t, *rows, true, st);
     if (s != CDB_OK) return s;
     EpiArgs ea{};
     ea.ld_out = d.vocab;
     ea.err = c.err;
-    if (logits) {
-        ea.out = logits;
-        HIPCHK(launch_gemm(EPI_STORE, c.x, wptr(c, c.wl.lm_head), M, c.gm.lm, c.part, ea, st));
-        HIPCHK(launch_argmax(M, d.vocab, logits, next_ids, st));
-        return CDB_OK;
-    }
-    // only the last row's greedy id: the LM head over the 32-row tile holding it
-    const int T = (M - 1) / 32, MT = M - 32 * T;
-    const uint16_t* xt = c.x + (size_t)T * (d.d / 16) * 512;  // fragment m-tiles are contiguous
-    ea.out = c.lm;
-    HIPCHK(launch_gemm(EPI_STORE, xt, wptr(c, c.wl.lm_head), MT, gemm_shape(d.vocab, d.d, EPI_STORE, MT), c.part, ea, st));
-    HIPCHK(launch_argmax(1, d.vocab, c.lm + (size_t)(MT - 1) * d.vocab, next_ids, st));
+    ea.out = logits;
+    HIPCHK(launch_gemm(EPI_STORE, c.x, wptr(c, c.wl.lm_head), M, c.gm.lm, c.part, ea, st, rows->d_n_rows));
+    HIPCHK(launch_argmax(M, d.vocab, logits, next_ids, st, rows->d_n_rows));
     return CDB_OK;
 }
 
@@ -450,6 +442,7 @@ cdb_status cdb_prefill(const cdb_model* model, const cdb_kv* kv, int32_t seq, in
     if (n_rows < 1 || n_rows > kMaxPrefillRows) return CDB_ERR_CAPACITY;
     if (seq < 0 || seq >= kv->max_seqs || pos0 < 0 || (size_t)pos0 + n_rows > (size_t)kv->max_pages * kPage)
         return CDB_ERR_INVALID_ARG;
+    if (pos0 + n_rows > kMaxPrefillPos) return CDB_ERR_CAPACITY;  // checked before any launch
     if (!kv->page_table) return CDB_ERR_INVALID_ARG;
     for (int stage = 0; stage < 3; ++stage) {
         const int layers = stage == 0 ? d.n_prelude : (stage == 1 ? d.n_core : d.n_coda);
@@ -460,7 +453,7 @@ cdb_status cdb_prefill(const cdb_model* model, const cdb_kv* kv, int32_t seq, in
     const int M = n_rows;
     Ctx c = make_ctx(model, ws, M);
     const Chunk chunk{seq, pos0};
-    cdb_rows r{M, c.prow, c.prow + M, c.prow + 2 * M, nullptr, nullptr};
+    cdb_rows r{M, c.prow, c.prow + M, c.prow + 2 * M, nullptr, nullptr, nullptr};
     HIPCHK(launch_prefill_rows(seq, pos0, M, c.prow, st));
     // prelude (plane 0): embedding, RoPE table, write pages
     KvTarget t = stage_target(d, *kv, 0);
@@ -526,11 +519,11 @@ cdb_status cdb_paged_attention(const cdb_model_desc* desc, const cdb_kv* kv, con
     if (stage == 1) t.c_row = rows->c;
     if (!order) {
         int32_t* own = reinterpret_cast<int32_t*>(static_cast<unsigned char*>(ws) + 256);
-        HIPCHK(launch_row_order(rows->pos, rows->n_rows, own, st));
+        HIPCHK(launch_row_order(rows->pos, rows->n_rows, own, st, rows->d_n_rows));
         order = own;
     }
     HIPCHK(launch_attention(q, t, rows->seq, rows->pos, order, rows->n_rows, d.n_heads, d.head_dim,
-                            static_cast<uint16_t*>(out), static_cast<int*>(ws), st));
+                            static_cast<uint16_t*>(out), static_cast<int*>(ws), st, rows->d_n_rows));
     return CDB_OK;
 }
 

@@ -118,7 +118,8 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(const float* __restric
                                                           const int32_t* __restrict__ seq,
                                                           const int32_t* __restrict__ pos,
                                                           const int32_t* __restrict__ order, int M, int H,
-                                                          uint16_t* __restrict__ out, int* err) {
+                                                          uint16_t* __restrict__ out, int* err,
+                                                          const int32_t* __restrict__ dn) {
     constexpr int DPL = HD / 16;
     constexpr int NP = kAttnWaves * 4;  // partial states per row
     __shared__ float s_m[2][NP], s_l[2][NP];
@@ -130,10 +131,13 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(const float* __restric
     const float qscale = 1.4426950408889634f / sqrtf((float)HD);  // log2(e) / sqrt(hd)
     const size_t vofs = (size_t)H * kPage * HD;  // V follows K within a (layer, page)
 
-    // the pair: p-th longest and p-th shortest row (one row when they meet)
+    // the pair: p-th longest and p-th shortest row (one row when they meet);
+    // with a device row count the grid covers the capacity M
+    const int n = live_rows(dn, M);
+    if (2 * pair >= n) return;
     int rows[2];
     rows[0] = order[pair];
-    rows[1] = (M - 1 - pair > pair) ? order[M - 1 - pair] : -1;
+    rows[1] = (n - 1 - pair > pair) ? order[n - 1 - pair] : -1;
     int n_ctx[2] = {0, 0}, npg[2] = {0, 0}, valid[2] = {0, 0};
     const int32_t* pt[2] = {kv.page_table, kv.page_table};
     float qr[2][DPL];
@@ -144,10 +148,13 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(const float* __restric
         const int m = rows[r];
         if (m < 0) continue;
         const int sq = seq[m];
+        // a row's own loop index reads a core plane (1..r_max) only
         const int plane = kv.c_row ? kv.c_row[m] + 1 : kv.plane_fixed;
+        const bool plane_ok =
+            kv.c_row ? (plane >= 1 && plane <= kv.n_planes - 2) : (plane >= 0 && plane < kv.n_planes);
         const int nc = pos[m] + 1;
         const int np = (nc + kPage - 1) / kPage;
-        if (!(sq >= 0 && sq < kv.max_seqs && plane >= 0 && plane < kv.n_planes && nc >= 1 && np <= kv.max_pages)) {
+        if (!(sq >= 0 && sq < kv.max_seqs && plane_ok && nc >= 1 && np <= kv.max_pages)) {
             if (tid == 0) set_err(err, CDB_DEV_UNMAPPED_PAGE);
             continue;
         }
@@ -236,13 +243,14 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(const float* __restric
 }
 
 hipError_t launch_attention(const float* q, const KvTarget& kv, const int32_t* seq, const int32_t* pos,
-                            const int32_t* order, int M, int H, int hd, uint16_t* out, int* err, hipStream_t st) {
+                            const int32_t* order, int M, int H, int hd, uint16_t* out, int* err, hipStream_t st,
+                            const int32_t* dn) {
     if (M <= 0) return hipSuccess;
     dim3 grid(H, (M + 1) / 2);
     switch (hd) {
-        case 64: k_attn<64><<<grid, kAttnWaves * 64, 0, st>>>(q, kv, seq, pos, order, M, H, out, err); break;
-        case 96: k_attn<96><<<grid, kAttnWaves * 64, 0, st>>>(q, kv, seq, pos, order, M, H, out, err); break;
-        case 128: k_attn<128><<<grid, kAttnWaves * 64, 0, st>>>(q, kv, seq, pos, order, M, H, out, err); break;
+        case 64: k_attn<64><<<grid, kAttnWaves * 64, 0, st>>>(q, kv, seq, pos, order, M, H, out, err, dn); break;
+        case 96: k_attn<96><<<grid, kAttnWaves * 64, 0, st>>>(q, kv, seq, pos, order, M, H, out, err, dn); break;
+        case 128: k_attn<128><<<grid, kAttnWaves * 64, 0, st>>>(q, kv, seq, pos, order, M, H, out, err, dn); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -250,7 +258,9 @@ hipError_t launch_attention(const float* q, const KvTarget& kv, const int32_t* s
 
 // order[rank] = row, ranked by descending position (ties by row index).  One
 // workgroup; M <= 256.
-__global__ __launch_bounds__(256) void k_row_order(const int32_t* __restrict__ pos, int M, int32_t* __restrict__ order) {
+__global__ __launch_bounds__(256) void k_row_order(const int32_t* __restrict__ pos, int M, int32_t* __restrict__ order,
+                                                   const int32_t* __restrict__ dn) {
+    M = live_rows(dn, M);
     for (int i = threadIdx.x; i < M; i += blockDim.x) {
         const int pi = pos[i];
         int rank = 0;
@@ -262,9 +272,9 @@ __global__ __launch_bounds__(256) void k_row_order(const int32_t* __restrict__ p
     }
 }
 
-hipError_t launch_row_order(const int32_t* pos, int M, int32_t* order, hipStream_t st) {
+hipError_t launch_row_order(const int32_t* pos, int M, int32_t* order, hipStream_t st, const int32_t* dn) {
     if (M <= 0) return hipSuccess;
-    k_row_order<<<1, 256, 0, st>>>(pos, M, order);
+    k_row_order<<<1, 256, 0, st>>>(pos, M, order, dn);
     return hipGetLastError();
 }
 

@@ -13,6 +13,7 @@ namespace cdb {
 constexpr int kPage = 16;       // tokens per KV page
 constexpr int kMaxRows = 256;          // rows per stage call
 constexpr int kMaxPrefillRows = 512;   // rows per prefill chunk
+constexpr int kMaxPrefillPos = 10240;  // positions one prefill call spans (key-range page ids sit in LDS)
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -55,6 +56,14 @@ __host__ __device__ __forceinline__ int gemm_rows(int m) {
 __host__ __device__ __forceinline__ size_t kv_offset(int layer, int pid, int n_pages, int kv, int head, int H, int tok,
                                                      int hd) {
     return (((((size_t)layer * n_pages + pid) * 2 + kv) * H + head) * 16 + tok) * (size_t)hd;
+}
+
+// Rows a call holds: the host count M, or, when the caller passes a device
+// count, that count clamped to [0, M] (M is then the launch capacity).
+__device__ __forceinline__ int live_rows(const int32_t* dn, int M) {
+    if (!dn) return M;
+    const int n = *dn;
+    return n < 0 ? 0 : (n > M ? M : n);
 }
 
 // First sticky error wins.
@@ -112,13 +121,15 @@ GemmShape gemm_shape_mn(int N, int K, int M, int epi);  // M > kMaxRows
 bool desc_supported(const cdb_model_desc& d);
 
 // ---------------------------------------------------------------- launchers
+// dn: optional device row count (<= M); rows at or past it are not stored
 hipError_t launch_gemm(int epi, const uint16_t* X, const uint16_t* Wp, int M, GemmShape g, float* part,
-                       const EpiArgs& ea, hipStream_t st);
+                       const EpiArgs& ea, hipStream_t st, const int32_t* dn = nullptr);
 // order: the call's rows ranked by descending position (by the row-entry
 // kernels of a stage call, or by launch_row_order)
 hipError_t launch_attention(const float* q, const KvTarget& kv, const int32_t* seq, const int32_t* pos,
-                            const int32_t* order, int M, int H, int hd, uint16_t* out, int* err, hipStream_t st);
-hipError_t launch_row_order(const int32_t* pos, int M, int32_t* order, hipStream_t st);
+                            const int32_t* order, int M, int H, int hd, uint16_t* out, int* err, hipStream_t st,
+                            const int32_t* dn = nullptr);
+hipError_t launch_row_order(const int32_t* pos, int M, int32_t* order, hipStream_t st, const int32_t* dn = nullptr);
 // causal attention of a prefill chunk: rows are positions pos0..pos0+M-1 of one
 // sequence in the target's fixed plane
 hipError_t launch_prefill_attention(const float* q, const KvTarget& kv, int seq, int pos0, int M, int H, int hd,
@@ -126,7 +137,7 @@ hipError_t launch_prefill_attention(const float* q, const KvTarget& kv, int seq,
 // h[i] += sum over s < S of part[s][i] (split order), then, when out is set,
 // out = bf16(RMSNorm(h)) in fragment layout.
 hipError_t launch_resid_norm(float* h, const float* part, int S, int M, int d, float eps, uint16_t* out,
-                             hipStream_t st);
+                             hipStream_t st, const int32_t* dn = nullptr);
 // The row-entry kernels of the three stage calls also fill the call's RoPE
 // table rope[M][hd/2] = (cos, sin) of pos * base^(-2j/hd), angles in fp64,
 // and kvpid[M], the page of the stage's pool that receives each row's K/V
@@ -142,10 +153,11 @@ hipError_t launch_embed(const cdb_model_desc& md, const uint16_t* embed, const i
                         const cdb_kv& kv, const KvTarget& kt, int n_slots, float* h, float2* rope, int32_t* kvpid,
                         int32_t* order, int* err, hipStream_t st);
 hipError_t launch_store_state(int M, int d, int n_slots, const int32_t* slot, const float* h, float* state_h,
-                              float* state_e, hipStream_t st);
+                              float* state_e, hipStream_t st, const int32_t* dn = nullptr);
 hipError_t launch_load_state(const cdb_model_desc& md, int M, const int32_t* slot, const int32_t* seq,
                              const int32_t* pos, const KvTarget& kt, const float* state_h, int n_slots, float* h,
-                             float2* rope, int32_t* kvpid, int32_t* order, int* err, hipStream_t st);
+                             float2* rope, int32_t* kvpid, int32_t* order, int* err, hipStream_t st,
+                             const int32_t* dn = nullptr);
 // h += the S split-K partials in part (split order) first; gate: NULL replays
 // rows.depth; deff[M] receives each exiting row's depth.
 hipError_t launch_exit(const cdb_model_desc& md, const cdb_rows& r, float* h, const float* part, int S,
@@ -157,7 +169,7 @@ hipError_t launch_compact(int M, const uint8_t* mask, int32_t* cont, int32_t* ex
 hipError_t launch_copy_on_exit(const cdb_model_desc& md, const cdb_kv& kv, const cdb_rows& r, const int32_t* deff,
                                const uint8_t* mask, int32_t* cont, int32_t* exited, int32_t* counts, int* err,
                                hipStream_t st);
-hipError_t launch_argmax(int M, int V, const float* logits, int32_t* ids, hipStream_t st);
+hipError_t launch_argmax(int M, int V, const float* logits, int32_t* ids, hipStream_t st, const int32_t* dn = nullptr);
 // prefill: row arrays slot = i, seq, pos = pos0 + i in rows[0..3M); per-row
 // write pages of a fixed plane; adapter input [h; e] in fragment layout
 hipError_t launch_prefill_rows(int seq, int pos0, int M, int32_t* rows, hipStream_t st);

@@ -255,7 +255,8 @@ int32_t cdb_driver_add_sequence(cdb_driver* d, int32_t prompt_len, int32_t n_dec
 
 int32_t cdb_driver_add_request(cdb_driver* d, int32_t prompt_len, const int32_t* prompt_ids, int32_t n_decode,
                                const int32_t* depths, double arrival) {
-    if (!d || d->cfg.prefill_chunk < 1 || !prompt_ids || prompt_len < 1) return -1;
+    // one cdb_prefill call spans at most 10240 positions
+    if (!d || d->cfg.prefill_chunk < 1 || !prompt_ids || prompt_len < 1 || prompt_len > 10240) return -1;
     const int32_t q = cdb_driver_add_sequence(d, prompt_len, n_decode, depths, arrival);
     if (q >= 0) d->seqs[q].prompt.assign(prompt_ids, prompt_ids + prompt_len);
     return q;
@@ -666,7 +667,7 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
             status = CDB_ERR_HIP;
             break;
         }
-        cdb_rows rows{n, drows, drows + 256, drows + 512, drows + 768, drows + 1024};
+        cdb_rows rows{n, drows, drows + 256, drows + 512, drows + 768, drows + 1024, nullptr};
         if (t.stage == CDB_TICK_PRELUDE_FIRST) {
             if (cdb::launch_gather_ids(n, drows + 256, dfirst, d->cfg.max_seqs, drows + 1280, stream) != hipSuccess) {
                 status = CDB_ERR_HIP;
@@ -722,7 +723,7 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
                     status = CDB_ERR_HIP;
                     break;
                 }
-                cdb_rows prow{t.n_continue, drows2, drows2 + 256, drows2 + 512, nullptr, nullptr};
+                cdb_rows prow{t.n_continue, drows2, drows2 + 256, drows2 + 512, nullptr, nullptr, nullptr};
                 s = cdb_boundary_prelude(model, kv, state, &prow, dids, ws, ws_bytes, stream);
             }
         }

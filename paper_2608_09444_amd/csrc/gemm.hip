@@ -33,6 +33,7 @@ struct GemmArgs {
     const uint16_t* Wp;
     int M, N, K, S, KW;
     float* part;  // EPI_PARTIAL: [S][M][N]
+    const int32_t* dn;  // optional device row count (<= M): rows at or past it are not stored
 };
 
 // Inputs of the q/k/v epilogue, staged in LDS: the RoPE factors of the
@@ -264,7 +265,7 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs ga, EpiArgs ea) {
     // q/k/v epilogue inputs, loaded while the weight stream is in flight (no
     // wait on them before the main loop ends); above 64 rows the RoPE factors
     // would cost more registers than the loop can spare and are loaded after it
-    const int mcap = min(M, MT * 32);
+    const int mcap = min(live_rows(ga.dn, M), MT * 32);
     const int nthr = KW * 64;
     constexpr int RP = MT <= 2 ? MT * 2 : 1;  // MT <= 2: >= mcap * 16 / nthr, as nthr >= 256
     float2 pf_rope[RP];
@@ -769,12 +770,12 @@ static hipError_t launch_mn(const GemmArgs& ga, const EpiArgs& ea, hipStream_t s
 }
 
 hipError_t launch_gemm(int epi, const uint16_t* X, const uint16_t* Wp, int M, GemmShape g, float* part,
-                       const EpiArgs& ea, hipStream_t st) {
+                       const EpiArgs& ea, hipStream_t st, const int32_t* dn) {
     if (M <= 0) return hipSuccess;
     if (g.K % 16 || g.N % 32 || g.S < 1) return hipErrorInvalidValue;
-    GemmArgs ga{X, Wp, M, g.N, g.K, g.S, g.KW, part};
+    GemmArgs ga{X, Wp, M, g.N, g.K, g.S, g.KW, part, dn};
     if (M > kMaxRows) {  // prefill chunks: the compute-bound tile kernel (shape from gemm_shape_mn)
-        if (M > kMaxPrefillRows || g.NS != 4) return hipErrorInvalidValue;
+        if (M > kMaxPrefillRows || g.NS != 4 || dn) return hipErrorInvalidValue;
         switch (epi) {
             case EPI_QKV: return launch_mn<EPI_QKV>(ga, ea, st);
             case EPI_SWIGLU: return launch_mn<EPI_SWIGLU>(ga, ea, st);

@@ -144,7 +144,7 @@ __global__ __launch_bounds__(256) void k_prefill_attn(const float* __restrict__ 
     static_assert(KB * CPK % 64 == 0, "a block is whole 1 KiB loads");
     static_assert(4 * HD * 32 * 4 + 4 * 64 * 4 <= 4 * WBUF, "merge buffers fit the wave buffers");
     __shared__ __align__(16) unsigned char smem[4 * WBUF + 32 * QP * 4];
-    __shared__ int s_pid[640];  // page ids of the key range (10240 positions)
+    __shared__ int s_pid[kMaxPrefillPos / kPage];  // page ids of the key range
     const int head = blockIdx.x;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int d = H * HD;
@@ -157,7 +157,7 @@ __global__ __launch_bounds__(256) void k_prefill_attn(const float* __restrict__ 
     const int32_t* pt = kv.page_table + ((size_t)seq * kv.n_planes + kv.plane_fixed) * kv.max_pages;
 
     const int n_pg = last / kPage + 1;
-    if (n_pg > 640) {  // the launcher bounds the context; kept as a guard
+    if (n_pg > kMaxPrefillPos / kPage) {  // the launcher bounds the context; kept as a guard
         if (tid == 0) set_err(err, CDB_DEV_BAD_INDEX);
         return;
     }
@@ -385,7 +385,7 @@ __global__ __launch_bounds__(256) void k_prefill_attn(const float* __restrict__ 
 hipError_t launch_prefill_attention(const float* q, const KvTarget& kv, int seq, int pos0, int M, int H, int hd,
                                     uint16_t* out, int* err, hipStream_t st) {
     if (M <= 0) return hipSuccess;
-    if (pos0 + M > 640 * kPage) return hipErrorInvalidValue;  // page ids of the key range must fit in LDS
+    if (pos0 + M > kMaxPrefillPos) return hipErrorInvalidValue;  // page ids of the key range must fit in LDS
     if (kv.n_pages < 1 || !kv.pool) return hipErrorInvalidValue;
     dim3 grid(H, (M + 31) / 32);
     switch (hd) {

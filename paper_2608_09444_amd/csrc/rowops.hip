@@ -60,9 +60,12 @@ __device__ __forceinline__ void write_page(const KvTarget& kt, int i, int sq, in
                                            int32_t* kvpid, int* err) {
     int pid = -1;
     if (kt.n_layers > 0) {
+        // a row's own loop index selects a core plane, 1..r_max; a c outside
+        // [0, r_max) must not resolve the prelude or coda plane's page
         const int plane = c_row ? c_row[i] + 1 : kt.plane_fixed;
+        const bool plane_ok = c_row ? (plane >= 1 && plane <= kt.n_planes - 2) : (plane >= 0 && plane < kt.n_planes);
         const int pg = ps >= 0 ? ps / kPage : -1;
-        if (sq >= 0 && sq < kt.max_seqs && pg >= 0 && pg < kt.max_pages && plane >= 0 && plane < kt.n_planes)
+        if (sq >= 0 && sq < kt.max_seqs && pg >= 0 && pg < kt.max_pages && plane_ok)
             pid = kt.page_table[((size_t)sq * kt.n_planes + plane) * kt.max_pages + pg];
         if (pid < 0 || pid >= kt.n_pages) {
             set_err(err, CDB_DEV_UNMAPPED_PAGE);
@@ -80,10 +83,12 @@ __global__ __launch_bounds__(256) void k_gather(int d, int r_max, int n_slots, i
                                                 float* __restrict__ h, float* __restrict__ h_in,
                                                 uint16_t* __restrict__ xcat, float2* __restrict__ rope, KvTarget kt,
                                                 int32_t* __restrict__ kvpid, int32_t* __restrict__ order, float eps,
-                                                uint16_t* __restrict__ xn, int* err) {
+                                                uint16_t* __restrict__ xn, int* err, const int32_t* __restrict__ dn) {
     __shared__ float red[4];
     const int i = blockIdx.x;
-    if (order && i == 0 && gridDim.x <= kMaxRows) row_order_block(pos, gridDim.x, order);
+    const int n = live_rows(dn, gridDim.x);
+    if (order && i == 0 && gridDim.x <= kMaxRows) row_order_block(pos, n, order);
+    if (i >= n) return;
     const int sl = slot[i];
     rope_row(pos[i], hd, base, rope + (size_t)i * (hd / 2));
     if (threadIdx.x == 0) {
@@ -134,9 +139,12 @@ __global__ __launch_bounds__(256) void k_load_state(int d, int n_slots, int hd, 
                                                     const int32_t* __restrict__ pos, KvTarget kt,
                                                     const float* __restrict__ sh, float* __restrict__ h,
                                                     float2* __restrict__ rope, int32_t* __restrict__ kvpid,
-                                                    int32_t* __restrict__ order, int* err) {
+                                                    int32_t* __restrict__ order, int* err,
+                                                    const int32_t* __restrict__ dn) {
     const int i = blockIdx.x;
-    if (order && i == 0 && gridDim.x <= kMaxRows) row_order_block(pos, gridDim.x, order);
+    const int n = live_rows(dn, gridDim.x);
+    if (order && i == 0 && gridDim.x <= kMaxRows) row_order_block(pos, n, order);
+    if (i >= n) return;
     const int sl = slot[i];
     rope_row(pos[i], hd, base, rope + (size_t)i * (hd / 2));
     const bool ok = sl >= 0 && sl < n_slots;
@@ -156,9 +164,11 @@ __global__ __launch_bounds__(256) void k_load_state(int d, int n_slots, int hd, 
 // partial loads of up to 4 splits at once.
 template <int NV>
 __global__ __launch_bounds__(1024) void k_resid_norm(float* __restrict__ h, const float* __restrict__ part, int S, int M,
-                                                     int d, float eps, uint16_t* __restrict__ out) {
+                                                     int d, float eps, uint16_t* __restrict__ out,
+                                                     const int32_t* __restrict__ dn) {
     __shared__ float red[16];
     const int i = blockIdx.x;
+    if (i >= live_rows(dn, M)) return;
     float* x = h + (size_t)i * d;
     float4 v[NV];
     float ss = 0.f;
@@ -204,9 +214,12 @@ __global__ __launch_bounds__(256) void k_embed(int d, int vocab, int n_slots, in
                                                const int32_t* __restrict__ tok, const int32_t* __restrict__ slot,
                                                const int32_t* __restrict__ seq, const int32_t* __restrict__ pos,
                                                float* __restrict__ h, float2* __restrict__ rope, KvTarget kt,
-                                               int32_t* __restrict__ kvpid, int32_t* __restrict__ order, int* err) {
+                                               int32_t* __restrict__ kvpid, int32_t* __restrict__ order, int* err,
+                                               const int32_t* __restrict__ dn) {
     const int i = blockIdx.x;
-    if (order && i == 0 && gridDim.x <= kMaxRows) row_order_block(pos, gridDim.x, order);
+    const int n = live_rows(dn, gridDim.x);
+    if (order && i == 0 && gridDim.x <= kMaxRows) row_order_block(pos, n, order);
+    if (i >= n) return;
     rope_row(pos[i], hd, base, rope + (size_t)i * (hd / 2));
     const int t = tok[i];
     const bool ok = t >= 0 && t < vocab;
@@ -228,8 +241,9 @@ __global__ __launch_bounds__(256) void k_embed(int d, int vocab, int n_slots, in
 
 __global__ __launch_bounds__(256) void k_store_state(int d, int n_slots, const int32_t* __restrict__ slot,
                                                      const float* __restrict__ h, float* __restrict__ sh,
-                                                     float* __restrict__ se) {
+                                                     float* __restrict__ se, const int32_t* __restrict__ dn) {
     const int i = blockIdx.x;
+    if (i >= live_rows(dn, gridDim.x)) return;
     const int sl = slot[i];
     if (sl < 0 || sl >= n_slots) return;
     for (int k = threadIdx.x * 4; k < d; k += 1024) {
@@ -257,9 +271,10 @@ __global__ __launch_bounds__(256) void k_exit(int d, float eps, int exit_kind, i
                                               float* __restrict__ sh, float* __restrict__ score,
                                               uint8_t* __restrict__ mask, uint8_t* __restrict__ exit_next,
                                               int32_t* __restrict__ deff, int gated, float threshold, int lookahead,
-                                              uint8_t* __restrict__ pending) {
+                                              uint8_t* __restrict__ pending, const int32_t* __restrict__ dn) {
     __shared__ float red[4];
     const int i = blockIdx.x;
+    if (i >= live_rows(dn, M)) return;
     float* x = h + (size_t)i * d;
     const float* x0 = h_in + (size_t)i * d;
     float a = 0.f, b = 0.f;
@@ -381,10 +396,12 @@ __global__ __launch_bounds__(256) void k_copy_on_exit(int H, int hd, int r_max, 
                                                       const int32_t* __restrict__ depth,
                                                       const uint8_t* __restrict__ mask, int32_t* __restrict__ cont,
                                                       int32_t* __restrict__ exited, int32_t* __restrict__ counts,
-                                                      int* err) {
+                                                      int* err, const int32_t* __restrict__ dn) {
     __shared__ int s_dst[64];  // destination page of plane dep + 1 + k, -1 if unmapped (r_max <= 64)
-    if (blockIdx.x == 0 && blockIdx.y == 0) compact_block(gridDim.x, mask, cont, exited, counts);
+    const int n = live_rows(dn, gridDim.x);
+    if (blockIdx.x == 0 && blockIdx.y == 0) compact_block(n, mask, cont, exited, counts);
     const int i = blockIdx.x;
+    if (i >= n) return;
     const int dep = depth[i];
     if (dep >= r_max || dep < 1) return;
     const int sq = seq[i], ps = pos[i], pg = ps / kPage;
@@ -443,10 +460,12 @@ __global__ __launch_bounds__(256) void k_copy_on_exit(int H, int hd, int r_max, 
 }
 
 // ------------------------------------------------------------------ argmax
-__global__ __launch_bounds__(256) void k_argmax(int V, const float* __restrict__ logits, int32_t* __restrict__ ids) {
+__global__ __launch_bounds__(256) void k_argmax(int V, const float* __restrict__ logits, int32_t* __restrict__ ids,
+                                                const int32_t* __restrict__ dn) {
     __shared__ float sv[256];
     __shared__ int si[256];
     const int i = blockIdx.x;
+    if (i >= live_rows(dn, gridDim.x)) return;
     const float* x = logits + (size_t)i * V;
     float bv = -INFINITY;
     int bi = 0x7fffffff;
@@ -528,22 +547,23 @@ hipError_t launch_gather(const cdb_model_desc& md, const cdb_state& s, const cdb
     if (xcat && xn) return hipErrorInvalidValue;
     k_gather<<<r.n_rows, 256, 0, st>>>(md.d, md.r_max, s.n_slots, kv.max_seqs, page_cap(kv), md.head_dim, md.rope_base,
                                         r.slot, r.seq, r.pos, r.c, r.depth, s.h, s.e, h, h_in, xcat, rope, kt, kvpid,
-                                        order, md.rms_eps, xn, err);
+                                        order, md.rms_eps, xn, err, r.d_n_rows);
     return hipGetLastError();
 }
 
 hipError_t launch_load_state(const cdb_model_desc& md, int M, const int32_t* slot, const int32_t* seq,
                              const int32_t* pos, const KvTarget& kt, const float* state_h, int n_slots, float* h,
-                             float2* rope, int32_t* kvpid, int32_t* order, int* err, hipStream_t st) {
+                             float2* rope, int32_t* kvpid, int32_t* order, int* err, hipStream_t st,
+                             const int32_t* dn) {
     if (M <= 0) return hipSuccess;
     if (order && M > kMaxRows) return hipErrorInvalidValue;
     k_load_state<<<M, 256, 0, st>>>(md.d, n_slots, md.head_dim, md.rope_base, slot, seq, pos, kt, state_h, h, rope,
-                                    kvpid, order, err);
+                                    kvpid, order, err, dn);
     return hipGetLastError();
 }
 
 hipError_t launch_resid_norm(float* h, const float* part, int S, int M, int d, float eps, uint16_t* out,
-                             hipStream_t st) {
+                             hipStream_t st, const int32_t* dn) {
     if (M <= 0) return hipSuccess;
     // one workgroup per row, runs of 4 elements, at most 4 runs per thread
     if (d % 4 || d > 16384) return hipErrorInvalidValue;
@@ -551,11 +571,11 @@ hipError_t launch_resid_norm(float* h, const float* part, int S, int M, int d, f
     while (threads < 1024 && threads * 4 < d) threads *= 2;
     const int nv = (d / 4 + threads - 1) / threads;
     if (nv == 1)
-        k_resid_norm<1><<<M, threads, 0, st>>>(h, part, S, M, d, eps, out);
+        k_resid_norm<1><<<M, threads, 0, st>>>(h, part, S, M, d, eps, out, dn);
     else if (nv == 2)
-        k_resid_norm<2><<<M, threads, 0, st>>>(h, part, S, M, d, eps, out);
+        k_resid_norm<2><<<M, threads, 0, st>>>(h, part, S, M, d, eps, out, dn);
     else
-        k_resid_norm<4><<<M, threads, 0, st>>>(h, part, S, M, d, eps, out);
+        k_resid_norm<4><<<M, threads, 0, st>>>(h, part, S, M, d, eps, out, dn);
     return hipGetLastError();
 }
 
@@ -565,15 +585,16 @@ hipError_t launch_embed(const cdb_model_desc& md, const uint16_t* embed, const i
     if (r.n_rows <= 0) return hipSuccess;
     if (order && r.n_rows > kMaxRows) return hipErrorInvalidValue;
     k_embed<<<r.n_rows, 256, 0, st>>>(md.d, md.vocab, n_slots, kv.max_seqs, page_cap(kv), md.head_dim, md.rope_base,
-                                       embed, tokens, r.slot, r.seq, r.pos, h, rope, kt, kvpid, order, err);
+                                       embed, tokens, r.slot, r.seq, r.pos, h, rope, kt, kvpid, order, err,
+                                       r.d_n_rows);
     return hipGetLastError();
 }
 
 hipError_t launch_store_state(int M, int d, int n_slots, const int32_t* slot, const float* h, float* state_h,
-                              float* state_e, hipStream_t st) {
+                              float* state_e, hipStream_t st, const int32_t* dn) {
     // out-of-range slots were reported by the embed kernel and are skipped here
     if (M <= 0) return hipSuccess;
-    k_store_state<<<M, 256, 0, st>>>(d, n_slots, slot, h, state_h, state_e);
+    k_store_state<<<M, 256, 0, st>>>(d, n_slots, slot, h, state_h, state_e, dn);
     return hipGetLastError();
 }
 
@@ -585,7 +606,7 @@ hipError_t launch_exit(const cdb_model_desc& md, const cdb_rows& r, float* h, co
     k_exit<<<r.n_rows, 256, 0, st>>>(md.d, md.rms_eps, md.exit_kind, md.r_max, n_slots, r.slot, r.c, r.depth, h,
                                       part, S, r.n_rows, h_in, w_exit, state_h, o.exit_score, o.exit_mask, o.exit_next, deff,
                                       gate ? 1 : 0, gate ? gate->threshold : 0.f, gate ? gate->lookahead : 0,
-                                      gate ? gate->pending : nullptr);
+                                      gate ? gate->pending : nullptr, r.d_n_rows);
     return hipGetLastError();
 }
 
@@ -608,7 +629,7 @@ hipError_t launch_copy_on_exit(const cdb_model_desc& md, const cdb_kv& kv, const
     t.n_planes = md.r_max + 2;
     dim3 grid(r.n_rows, md.n_core);
     k_copy_on_exit<<<grid, 256, 0, st>>>(md.n_heads, md.head_dim, md.r_max, t, r.seq, r.pos, deff, mask, cont, exited,
-                                         counts, err);
+                                         counts, err, r.d_n_rows);
     return hipGetLastError();
 }
 
@@ -701,9 +722,9 @@ hipError_t launch_concat_frag(int M, int d, const float* h, const float* e, uint
     return hipGetLastError();
 }
 
-hipError_t launch_argmax(int M, int V, const float* logits, int32_t* ids, hipStream_t st) {
+hipError_t launch_argmax(int M, int V, const float* logits, int32_t* ids, hipStream_t st, const int32_t* dn) {
     if (M <= 0) return hipSuccess;
-    k_argmax<<<M, 256, 0, st>>>(V, logits, ids);
+    k_argmax<<<M, 256, 0, st>>>(V, logits, ids, dn);
     return hipGetLastError();
 }
 

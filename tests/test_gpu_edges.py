@@ -41,15 +41,8 @@ def _ouro_two_layers():
 
 
 def _sample_rows(rows_np, r_max):
-    c, dep, pos = rows_np["c"], rows_np["depth"], rows_np["pos"]
-    ex = [i for i in range(len(c)) if c[i] + 1 == dep[i] and dep[i] < r_max]
-    co = [i for i in range(len(c)) if c[i] + 1 < dep[i]]
-    picks = []
-    for cand in (ex[:1], co[:1], [int(np.argmax(pos))], [len(c) - 1]):
-        for i in cand:
-            if i not in picks:
-                picks.append(i)
-    return picks
+    from lockstep import sample_rows
+    return sample_rows(rows_np, r_max)
 
 
 def test_empty_stage_calls():
@@ -156,6 +149,30 @@ def test_unmapped_page_is_reported(case):
     torch.cuda.synchronize()
     assert cdb.cdb_read_device_error(ws.buf) == cdb.CDB_DEV_UNMAPPED_PAGE
     assert out.counts.cpu().tolist() == [int((c + 1 < depth).sum()), int((c + 1 == depth).sum())]
+
+
+def test_bad_loop_index_writes_no_other_page():
+    """A row whose loop index c is r_max (past its last core plane) is reported
+    as a bad depth, and its K/V write does not land in the page its sequence's
+    coda-plane entry names (here another row's context page, which must stay
+    unchanged)."""
+    s, gm, kv, pt, state, pos, c, depth = _tiny_step_setup()
+    R = s.r_max
+    i, victim = 2, int(pt[0, 1, 0])  # row 0's plane-1 positions 0..15: read-only in this step
+    c = c.copy()
+    c[i] = R
+    pt[i, R + 1, pos[i] // 16] = victim
+    kv.page_table.copy_(torch.from_numpy(pt))
+    before = kv.core[:, victim].clone()
+    n = len(pos)
+    rows = cdb.Rows(np.arange(n, dtype=np.int32), np.arange(n, dtype=np.int32), pos, c, depth)
+    out = cdb.StepOut(n)
+    ws = cdb.Workspace(gm.desc, n)
+    _say(f"[gpu] tiny loop step with c = r_max in row {i}")
+    cdb.cdb_loop_step(gm.model, kv.c, state.c, rows.c, out.c, ws.buf)
+    torch.cuda.synchronize()
+    assert cdb.cdb_read_device_error(ws.buf) == cdb.CDB_DEV_BAD_DEPTH
+    assert torch.equal(kv.core[:, victim], before)
 
 
 def test_slot_outside_the_pool_is_reported():

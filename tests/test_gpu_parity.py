@@ -1,11 +1,13 @@
 """GPU parity: the HIP stage calls against the CPU oracle, element by element,
 on identical seeded inputs.  Integer outputs (exit masks, compaction lists,
 counts) must match exactly.  Hidden states, exit scores and logits must lie
-within max-abs 2e-2 / mean-abs 2e-3, or, where larger, within twice the
-distance between the oracle and the same oracle run with fp32 accumulators on
-the same inputs (deep random-init cores amplify rounding-level differences
-through bf16 rounding flips; an fp32 implementation cannot be expected to sit
-closer than that).  K/V entries must agree within one bf16 step or that bound."""
+within max-abs 2e-2 / mean-abs 2e-3, or, where larger, within 1.25 times the
+largest distance of fp32-level realizations of the oracle from the fp64 oracle
+on the same inputs (a random-init core turns rounding-level differences into
+bf16 rounding flips that cascade from layer to layer; an fp32 implementation
+cannot be expected to sit closer than that).  Every test prints its errors,
+relative errors ||dh||/||h|| and the ratio of each error to its bound.  K/V
+entries must agree within one bf16 step or that bound."""
 import sys
 
 import numpy as np
@@ -44,18 +46,9 @@ def test_config1_tiny_end_to_end():
     assert ls.calls["loop"] > wl.decode
 
 
-def _sample_rows(rows_np, r_max, k=3):
-    """Rows to check with the oracle: an exiting row with copy-on-exit (depth <
-    r_max), a continuing row, and the row with the longest context."""
-    c, dep, pos = rows_np["c"], rows_np["depth"], rows_np["pos"]
-    ex = [i for i in range(len(c)) if c[i] + 1 == dep[i] and dep[i] < r_max]
-    co = [i for i in range(len(c)) if c[i] + 1 < dep[i]]
-    picks = []
-    for cand in (ex[:1], co[:1], [int(np.argmax(pos))]):
-        for i in cand:
-            if i not in picks:
-                picks.append(i)
-    return picks[:k]
+def _sample_rows(rows_np, r_max, k=16):
+    from lockstep import sample_rows
+    return sample_rows(rows_np, r_max, k=k)
 
 
 def _core_prefix(shape, w, n_core):
@@ -71,9 +64,8 @@ def _core_prefix(shape, w, n_core):
 @pytest.mark.parametrize("n_core", [2, 24])
 def test_config2_loop_step_full_batch_sampled_rows(n_core):
     """The benchmark's launch: 64 mixed-depth rows of the Ouro-shaped model at
-    decode positions 512..767; three rows checked against the oracle.  With 2
-    core layers the absolute bound applies; with all 24 the bound is twice the
-    oracle's fp32-vs-fp64 drift on the same inputs."""
+    decode positions 512..767; 16 rows checked against the oracle (both rows of
+    four attention pairs, every loop index, exiting and continuing rows)."""
     from lockstep import injected_loop_step
     s, w = _core_prefix(cdbgen.OURO, cdbgen.model_weights(cdbgen.OURO), n_core)
     rows = cdbgen.decode_snapshot(64, cdbgen.OURO_DEPTHS, s.r_max, 512, 767, stream=7)
@@ -87,8 +79,7 @@ def test_config2_loop_step_full_batch_sampled_rows(n_core):
 @pytest.mark.parametrize("n_core", [1, 4])
 def test_config3_huginn_loop_step_full_batch_sampled_rows(n_core):
     """128 rows of the Huginn-shaped model (adapter, 55 heads x 96, r_max 32) at
-    decode positions 256..767; three rows checked against the oracle (absolute
-    bound with 1 core layer, sensitivity bound with all 4)."""
+    decode positions 256..767; 16 rows checked against the oracle."""
     from lockstep import injected_loop_step
     s, w = _core_prefix(cdbgen.HUGINN, cdbgen.model_weights(cdbgen.HUGINN), n_core)
     wl = cdbgen.WORKLOADS[3]
@@ -103,13 +94,13 @@ def test_config3_huginn_loop_step_full_batch_sampled_rows(n_core):
 def test_config4_long_context_256_rows_sampled():
     """256 rows (the config's batch), 50/50 exits at loop 1 and 4; sampled rows
     sit at long contexts 2048..4223, the others at short ones to bound memory.
-    Full 24-layer core, sensitivity bound."""
+    Full 24-layer core."""
     from lockstep import injected_loop_step
     s = cdbgen.OURO
     wl = cdbgen.WORKLOADS[4]
     rows = cdbgen.decode_snapshot(256, wl.depth, s.r_max, 16, 200, stream=11)
     g = np.random.default_rng(3)
-    sample = _sample_rows(rows, s.r_max, k=2)
+    sample = _sample_rows(rows, s.r_max, k=16)
     for i in sample:
         rows["pos"][i] = int(g.integers(2048, 4224))
     _say(f"[gpu] config 4, 256 rows, sampled rows {sample}: pos {rows['pos'][sample]} c {rows['c'][sample]}")
@@ -120,7 +111,7 @@ def test_config4_long_context_256_rows_sampled():
 def test_config4_loop_step_as_benched_sampled_rows():
     """The long-context loop step exactly as the benchmark times it: 256 rows,
     every one at a position drawn from [2048, 4223] (prompt U[2048, 4096] +
-    decode 128), each row on its own pages (≈ 155 GB of K/V); two rows checked
+    decode 128), each row on its own pages (≈ 155 GB of K/V); 16 rows checked
     against the oracle, integer outputs for the whole batch."""
     import torch
     from lockstep import injected_loop_step
@@ -128,7 +119,7 @@ def test_config4_loop_step_as_benched_sampled_rows():
     wl = cdbgen.WORKLOADS[4]
     rows = cdbgen.decode_snapshot(wl.max_batch, wl.depth, s.r_max, wl.prompt[0], wl.prompt[1] + wl.decode - 1,
                                   stream=40)
-    sample = _sample_rows(rows, s.r_max, k=2)
+    sample = _sample_rows(rows, s.r_max, k=16)
     _say(f"[gpu] config 4 as benched, 256 rows at mean context {rows['pos'].mean() + 1:.0f}, sampled rows "
          f"{sample}: pos {rows['pos'][sample]} c {rows['c'][sample]}")
     err = injected_loop_step(s, cdbgen.model_weights(s), rows, sample, sensitivity=True)
@@ -161,4 +152,31 @@ def test_config3_reduced_depth_end_to_end():
     ls = Lockstep(s, w, [6, 6], max_batch=2, resync=True, sensitivity=True)
     ls.run(prompts, [3, 3], depths)
     _say(f"[gpu] config 3 reduced errors {ls.errors} oracle self {ls.self_diff} calls {ls.calls}")
+    assert ls.device_error() == 0
+
+
+@pytest.mark.parametrize("case", ["ouro2", "ouro24"])
+def test_config2_free_running_decode_at_full_depth(case):
+    """Whole decodes at Ouro widths with no resync: 2 sequences, prompt 16,
+    decode 6, config 2's depth distribution, states from the embedding of real
+    token ids (teacher-forced with the oracle's greedy ids).  ouro24 is the full
+    24-layer core at r_max 4.  Each call is bounded by the stored envelope of
+    the oracle's own fp32-level realizations run free over the same decode
+    (tests/golden/drift_<case>.json, written by make_drift_envelope.py from the
+    oracle alone)."""
+    import json
+    import os
+    from lockstep import Lockstep
+    from oracle_side import free_run_case
+    s, w, prompts, depths, n_dec, max_batch = free_run_case(case)
+    env = json.load(open(os.path.join(os.path.dirname(__file__), "golden", f"drift_{case}.json")))
+    assert env["depths"] == [d.tolist() for d in depths]
+    _say(f"[gpu] free-running {case}: {s.n_core} core layers, depths {[d[16:].tolist() for d in depths]}")
+    ls = Lockstep(s, w, [len(p) + n for p, n in zip(prompts, n_dec)], max_batch=max_batch, envelope=env)
+    toks = ls.run(prompts, n_dec, depths)
+    assert [t.tolist() for t in toks] == env["tokens"]
+    _say(f"[gpu] free-running {case} errors {ls.errors} ratio to bound {ls.ratio} calls {ls.calls} "
+         f"argmax checked {ls.argmax_checked}; oracle fp32 realizations: h {env['run_h_max']:.4g} / "
+         f"{env['run_h_mean']:.4g} rel {env['run_h_rel']:.4g}, logits {env['run_logit_max']:.4g} / "
+         f"{env['run_logit_mean']:.4g}")
     assert ls.device_error() == 0

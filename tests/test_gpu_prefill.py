@@ -3,7 +3,7 @@ the same prompt as one block (prelude, r_max loop steps at full depth, coda).
 Under the full KV layout a prompt split into chunks reads exactly what the
 single block reads, so chunks and block must agree.  Logits within the
 tolerance, greedy ids where the top-2 gap is clear, K/V of every plane within
-one bf16 step.  For real widths the bounds widen to twice the distance
+one bf16 step.  For real widths the bounds widen to 1.25 times the distance
 between the oracle and its fp32-accumulator build on the same prompt, as in
 the loop-step parity tests (deep random-init cores amplify rounding)."""
 import sys
@@ -19,6 +19,7 @@ import paper_2608_09444_amd as cdb
 pytestmark = pytest.mark.gpu
 
 TOL_MAX, TOL_MEAN = 2e-2, 2e-3
+DRIFT_FACTOR = 1.25  # bound: this times the fp32-accumulator oracle's distance from the fp64 oracle
 
 # 18 q/k/v stripes, 6 output stripes, 5 vocabulary stripes: tiles that do not
 # divide the 128-column workgroup tile; adapter and convergence score
@@ -81,8 +82,9 @@ def run_prefill(shape, w, prompt, chunks, check_rows=None, sensitivity=False):
     if sensitivity:
         op32, ol32, _ = oracle_block(shape, w, prompt, acc32=True)
         dl = np.abs(ol32 - ologits)
-        tol_max, tol_mean = max(TOL_MAX, 2 * float(dl.max())), max(TOL_MEAN, 2 * float(dl.mean()))
-        kv_tol = max(TOL_MAX, 2 * max(float(np.abs(a - b).max()) for a, b in
+        tol_max = max(TOL_MAX, DRIFT_FACTOR * float(dl.max()))
+        tol_mean = max(TOL_MEAN, DRIFT_FACTOR * float(dl.mean()))
+        kv_tol = max(TOL_MAX, DRIFT_FACTOR * max(float(np.abs(a - b).max()) for a, b in
                                         ((op32.pre, op.pre), (op32.core, op.core), (op32.coda, op.coda))))
     gkv = cdb.PagedKV(shape, 1, pages, pages, pages * R, pages)
     gkv.page_table.copy_(torch.from_numpy(op.page_table))
