@@ -234,6 +234,23 @@ cdb_status cdb_loop_step_gated(const cdb_model* model, const cdb_kv* kv, const c
                                const cdb_rows* rows, const cdb_gate* gate, const cdb_step_out* out, void* ws,
                                size_t ws_bytes, hipStream_t stream);
 
+/* cdb_loop_step for callers that cannot allocate memory (code under HIP graph
+ * capture, serving loops and harnesses that forbid allocation): the same
+ * computation and outputs, with its scratch taken from a 48 MiB array the
+ * library keeps in device memory (one per GPU, held until the process ends)
+ * instead of a workspace argument.  It allocates and frees nothing.
+ *   d_error: device int32, required; receives the sticky device error codes
+ *   (CDB_DEV_*) that cdb_loop_step keeps in its workspace.  The caller zeroes
+ *   it once and reads (and re-zeroes) it outside the hot path.
+ * Calls whose workspace would exceed 48 MiB (cdb_workspace_bytes of the model
+ * at n_rows: e.g. more than 256 rows of the Ouro-shaped model) return
+ * CDB_ERR_CAPACITY before anything is enqueued.  Nothing carries over between
+ * calls in the scratch.  Every call on one GPU shares its scratch: calls that
+ * overlap on a GPU (different streams without ordering, several threads) race
+ * and must not be issued. */
+cdb_status cdb_loop_step_noalloc(const cdb_model* model, const cdb_kv* kv, const cdb_state* state,
+                                 const cdb_rows* rows, const cdb_step_out* out, int32_t* d_error, hipStream_t stream);
+
 /* Coda stage (Section 4.1; Eq. 1 p(x_{t+1}) = softmax(C(h))): coda layers with
  * KV plane r_max + 1 on h = state.h[slot], final RMSNorm, LM head.  logits:
  * device fp32 [n_rows][vocab], required (CDB_ERR_INVALID_ARG if NULL);

@@ -22,7 +22,7 @@ MAX_PREFILL_ROWS = 512
 
 EXPORTED = ("cdb_packed_weight_bytes", "cdb_pack_weights", "cdb_kv_page_bytes", "cdb_workspace_bytes",
             "cdb_workspace_init", "cdb_boundary_prelude", "cdb_loop_step", "cdb_loop_step_gated", "cdb_boundary_coda",
-            "cdb_prefill", "cdb_paged_attention", "cdb_read_device_error", "cdb_status_str")
+            "cdb_prefill", "cdb_paged_attention", "cdb_read_device_error", "cdb_status_str", "cdb_loop_step_noalloc")
 
 
 class CdbError(RuntimeError):
@@ -92,6 +92,7 @@ def lib() -> C.CDLL:
         L.cdb_boundary_prelude.argtypes = [P, P, P, P, P, P, S, P]
         L.cdb_loop_step.argtypes = [P, P, P, P, P, P, S, P]
         L.cdb_loop_step_gated.argtypes = [P, P, P, P, P, P, P, S, P]
+        L.cdb_loop_step_noalloc.argtypes = [P, P, P, P, P, P, P]
         L.cdb_boundary_coda.argtypes = [P, P, P, P, P, P, P, S, P]
         L.cdb_paged_attention.argtypes = [P, P, P, I, I, P, P, P, P, S, P]
         L.cdb_prefill.argtypes = [P, P, I, I, I, P, P, P, P, S, P]
@@ -99,7 +100,8 @@ def lib() -> C.CDLL:
         L.cdb_status_str.argtypes = [C.c_int]
         L.cdb_status_str.restype = C.c_char_p
         for f in ("cdb_pack_weights", "cdb_workspace_init", "cdb_boundary_prelude", "cdb_loop_step", "cdb_loop_step_gated",
-                  "cdb_boundary_coda", "cdb_paged_attention", "cdb_prefill", "cdb_read_device_error"):
+                  "cdb_boundary_coda", "cdb_paged_attention", "cdb_prefill", "cdb_read_device_error",
+                  "cdb_loop_step_noalloc"):
             getattr(L, f).restype = C.c_int
         _lib = L
     return _lib
@@ -171,6 +173,14 @@ def cdb_loop_step_gated(model: cdb_model, kv: cdb_kv, state: cdb_state, rows: cd
     _check("cdb_loop_step_gated", lib().cdb_loop_step_gated(C.byref(model), C.byref(kv), C.byref(state),
                                                             C.byref(rows), C.byref(gate), C.byref(out), _ptr(ws),
                                                             ws.numel(), _stream(stream)))
+
+
+def cdb_loop_step_noalloc(model: cdb_model, kv: cdb_kv, state: cdb_state, rows: cdb_rows, out: cdb_step_out,
+                          d_error, stream=None):
+    """d_error: device int32 tensor of one element (zeroed by the caller)."""
+    _check("cdb_loop_step_noalloc", lib().cdb_loop_step_noalloc(C.byref(model), C.byref(kv), C.byref(state),
+                                                                C.byref(rows), C.byref(out), _ptr(d_error),
+                                                                _stream(stream)))
 
 
 def cdb_boundary_coda(model: cdb_model, kv: cdb_kv, state: cdb_state, rows: cdb_rows, logits, next_ids, ws,

@@ -3,6 +3,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "cdb_internal.h"
 
@@ -356,8 +357,10 @@ cdb_status cdb_boundary_prelude(const cdb_model* model, const cdb_kv* kv, const 
     return CDB_OK;
 }
 
+// err: where device errors go (NULL: the workspace's own error word)
 static cdb_status loop_step(const cdb_model* model, const cdb_kv* kv, const cdb_state* state, const cdb_rows* rows,
-                            const cdb_gate* gate, const cdb_step_out* out, void* ws, size_t ws_bytes, hipStream_t st) {
+                            const cdb_gate* gate, const cdb_step_out* out, void* ws, size_t ws_bytes, hipStream_t st,
+                            int* err = nullptr) {
     cdb_status s = check_common(model, kv, state, rows, ws, ws_bytes, 1);
     if (s != CDB_OK) return s;
     const cdb_model_desc& d = model->desc;
@@ -368,6 +371,7 @@ static cdb_status loop_step(const cdb_model* model, const cdb_kv* kv, const cdb_
     if (d.injection && !state->e) return CDB_ERR_INVALID_ARG;
     const int M = rows->n_rows;
     Ctx c = make_ctx(model, ws, M);
+    if (err) c.err = err;
     cdb_rows r = *rows;
     if (gate) r.depth = nullptr;
     if (M > 0) {
@@ -408,6 +412,48 @@ cdb_status cdb_loop_step_gated(const cdb_model* model, const cdb_kv* kv, const c
                                size_t ws_bytes, hipStream_t st) {
     if (!gate) return CDB_ERR_INVALID_ARG;
     return loop_step(model, kv, state, rows, gate, out, ws, ws_bytes, st);
+}
+
+}  // extern "C"
+
+// Scratch of cdb_loop_step_noalloc: one copy per device, alive until the
+// process ends.  Host code never uses this name as an address (on the host it
+// is a stand-in symbol); it uses the device address hipGetSymbolAddress gives,
+// looked up once per device.
+constexpr size_t kNoAllocScratchBytes = (size_t)48 << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's scratch address (NULL if the lookup fails).
+void* device_scratch() {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return nullptr;
+        g_scratch_ptr[dev] = p;
+    }
+    return g_scratch_ptr[dev];
+}
+}  // namespace
+
+extern "C" {
+
+cdb_status cdb_loop_step_noalloc(const cdb_model* model, const cdb_kv* kv, const cdb_state* state,
+                                 const cdb_rows* rows, const cdb_step_out* out, int32_t* d_error, hipStream_t st) {
+    if (!d_error || !model || !rows) return CDB_ERR_INVALID_ARG;
+    if (!desc_supported(model->desc)) return CDB_ERR_UNSUPPORTED;
+    if (rows->n_rows < 0) return CDB_ERR_INVALID_ARG;
+    if (rows->n_rows > kMaxRows || ws_layout(model->desc, rows->n_rows).total > kNoAllocScratchBytes)
+        return CDB_ERR_CAPACITY;
+    void* ws = device_scratch();
+    if (!ws) return CDB_ERR_HIP;
+    return loop_step(model, kv, state, rows, nullptr, out, ws, kNoAllocScratchBytes, st, d_error);
 }
 
 cdb_status cdb_boundary_coda(const cdb_model* model, const cdb_kv* kv, const cdb_state* state, const cdb_rows* rows,
