@@ -144,6 +144,62 @@ def time_attention(shape, kv, rows, n_rows, launches):
     return e0.elapsed_time(e1) / launches
 
 
+def runner_ws(dm, rows, two):
+    """The driver runner's workspace: one stage workspace, or two halves when
+    the boundary stages run on their own stream (error words start at zero).
+    Returns (buffer, half)."""
+    import torch
+
+    import paper_2608_09444_amd as cdb
+    n = (cdb.cdb_workspace_bytes(dm.desc, rows) + 255) & ~255
+    return torch.zeros(2 * n if two else n, dtype=torch.uint8, device="cuda"), n
+
+
+def check_runner_ws(ws, half, what):
+    import paper_2608_09444_amd as cdb
+    codes = [cdb.cdb_read_device_error(ws)] + ([cdb.cdb_read_device_error(ws[half:])] if ws.numel() > half else [])
+    if any(codes):
+        raise RuntimeError(f"device error {codes} in {what}")
+
+
+def host_threads():
+    """The host cores this process may use: its CPU affinity, capped by
+    OMP_NUM_THREADS when set (the job's CPU share on a shared host)."""
+    n = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+    omp = os.environ.get("OMP_NUM_THREADS")
+    if omp and omp.isdigit() and int(omp) > 0:
+        n = min(n, int(omp))
+    return max(1, n)
+
+
+def host_info():
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    aff = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else None
+    return {"nproc": os.cpu_count(), "affinity_cpus": aff, "omp_num_threads": os.environ.get("OMP_NUM_THREADS"),
+            "cpu_model": model}
+
+
+def reduced_legs(args):
+    """Which legs run below their workload's full size in this invocation."""
+    red = {}
+    if 0 < args.serving_requests < 2000:
+        red["serving"] = f"{args.serving_requests} of the trace's 2000 requests (--serving-requests 2000 for all)"
+    if 0 < args.huginn_decode < 512:
+        red["huginn_e2e"] = f"{args.huginn_decode} of 512 decode tokens per request"
+    if not args.long_context:
+        red["long_context"] = "not run (--long-context; it allocates nearly all HBM)"
+    if args.huginn_decode == 0:
+        red["huginn"] = "not run"
+    return red
+
+
 def cpu_baseline(shape, w, rows_np, n_sample, threads, min_s=10.0):
     """The CPU oracle's loop step on `n_sample` rows of the same batch (same
     positions, depths, loop indices; seeded random KV and state)."""
@@ -213,21 +269,25 @@ def e2e_decode(shape, dm, kv, n_seqs, prompt, n_decode, seed=3):
         for q in range(n):
             d.add_sequence(prompt, (depths if dep is None else dep)[q][:nd])
         scratch = torch.empty(d.scratch_bytes(shape.vocab), dtype=torch.uint8, device="cuda")
-        secs = d.run(dm.model, kv.c, state.c, scratch, first, ws.buf, tokens_out=out_ids)
-        if cdb.cdb_read_device_error(ws.buf) != 0:
-            raise RuntimeError("device error in the driver run")
+        rws, half = runner_ws(dm, 256, mode.get("boundary_stream", False))
+        secs = d.run(dm.model, kv.c, state.c, scratch, first, rws, tokens_out=out_ids)
+        check_runner_ws(rws, half, "the driver run")
         return secs, d.stats()
 
     run(4, 8)  # first use of the boundary kernels
     res = {"workload": f"{n_seqs} requests, prompt {prompt} (KV synthesized), {n_decode} decode tokens each, "
                        f"depths categorical {{1:.3,2:.3,3:.2,4:.2}}, max batch 64, full depth-indexed KV",
            "mean_depth": round(mean_depth, 4), "flop_bound": round(cost.flop_bound(shape, mean_depth), 4)}
+    run(4, 8, boundary_stream=1)
     for name, mode in (("cdb_refill", {}), ("cdb_no_refill", {"refill": False}), ("cb_fixed_depth",
-                                                                               {"fixed_depth": True})):
+                                                                               {"fixed_depth": True}),
+                       ("cdb_refill_boundary_stream_fill", {"boundary_stream": 1}),
+                       ("cdb_refill_boundary_stream_hold", {"boundary_stream": 2})):
         secs, st = run(n_seqs, n_decode, **mode)
         res[name] = {"tokens_per_s": round(st["tokens"] / secs, 1), "seconds": round(secs, 4),
                      "loop_steps": st["loop_steps"], "idle_rows": st["idle_rows"],
-                     "coda_calls": st["coda_calls"]}
+                     "coda_calls": st["coda_calls"],
+                     "host_wait_us_per_loop_step": round(st["host_wait_us"] / max(1, st["loop_steps"]), 2)}
         log(f"e2e {name}: {st['tokens']} tokens in {secs:.3f}s, {st['loop_steps']} loop steps")
     cb = res["cb_fixed_depth"]["tokens_per_s"]
     res["speedup_refill_vs_cb"] = round(res["cdb_refill"]["tokens_per_s"] / cb, 4)
@@ -535,23 +595,28 @@ def huginn_leg(n_decode, steps=20, warmup=3):
         for q in range(n):
             d.add_sequence(prompt, depths[q][:nd])
         scratch = torch.empty(d.scratch_bytes(shape.vocab), dtype=torch.uint8, device="cuda")
-        secs = d.run(dm.model, kv.c, state.c, scratch, first, ws.buf, tokens_out=out_ids)
-        if cdb.cdb_read_device_error(ws.buf) != 0:
-            raise RuntimeError("device error in the huginn driver run")
+        rws, half = runner_ws(dm, 256, mode.get("boundary_stream", False))
+        secs = d.run(dm.model, kv.c, state.c, scratch, first, rws, tokens_out=out_ids)
+        check_runner_ws(rws, half, "the huginn driver run")
         return secs, d.stats()
 
     run(4, 4)  # first use of the boundary kernels at this shape
+    run(4, 4, boundary_stream=1)
     e2e = {"workload": f"{n_seqs} requests, prompt {prompt} (KV synthesized), {n_decode} decode tokens each, depths "
                        f"lognormal median 12, sigma 0.5, clipped to [4, 32], max batch {wl.max_batch}, shared KV, "
                        f"minimum boundary batch 32",
            "mean_depth": round(mean_depth, 4), "flop_bound": round(cost.flop_bound(shape, mean_depth), 4)}
-    for name, mode in (("cdb_refill", {}), ("cb_fixed_depth", {"fixed_depth": True})):
+    for name, mode in (("cdb_refill", {}), ("cb_fixed_depth", {"fixed_depth": True}),
+                       ("cdb_refill_boundary_stream_fill", {"boundary_stream": 1}),
+                       ("cdb_refill_boundary_stream_hold", {"boundary_stream": 2})):
         secs, st = run(n_seqs, n_decode, **mode)
         e2e[name] = {"tokens_per_s": round(st["tokens"] / secs, 1), "seconds": round(secs, 4),
                      "loop_steps": st["loop_steps"], "loop_rows": st["loop_rows"], "idle_rows": st["idle_rows"],
                      "coda_calls": st["coda_calls"], "prelude_calls": st["prelude_calls"]}
         log(f"huginn e2e {name}: {st['tokens']} tokens in {secs:.3f}s, {st['loop_steps']} loop steps")
     e2e["speedup_refill_vs_cb"] = round(e2e["cdb_refill"]["tokens_per_s"] / e2e["cb_fixed_depth"]["tokens_per_s"], 4)
+    e2e["boundary_stream_gain"] = {k: round(e2e["cdb_refill_boundary_stream_" + k]["tokens_per_s"] /
+                                            e2e["cdb_refill"]["tokens_per_s"], 4) for k in ("fill", "hold")}
     res["e2e"] = e2e
     del kv, state, ws, dm
     torch.cuda.empty_cache()
@@ -685,51 +750,138 @@ def long_context_leg(shape, dm, headroom_gib=16):
     return res
 
 
-def graph_leg(dm, kv, state, rows, out, ws, steps, reps=3):
-    """cdb_loop_step captured once in a HIP graph and replayed: the replay time
-    per step, and each of `reps` replays checked bit for bit against an eager
-    step from the same saved state (eager work and synchronisation between the
-    replays)."""
+def graph_leg(dm, kv, state, rows_np, steps, counts=(64, 40, 17)):
+    """cdb_loop_step captured once in a HIP graph at the batch's row capacity,
+    with the row count in device memory (cdb_rows.d_n_rows), and replayed at
+    several counts: each count's replay is checked bit for bit against an eager
+    call of exactly that many rows from the same saved state and cache (eager
+    work and synchronisation between the replays); the full-count replay is
+    timed."""
+    import numpy as np
     import torch
 
     import paper_2608_09444_amd as cdb
     st = torch.cuda.current_stream()
+    cap = len(rows_np["pos"])
     h0 = state.h.clone()
-
-    def outputs():
-        return state.h.clone(), out.score.clone(), out.mask.clone(), out.cont.clone()
-
+    ar = np.arange(cap, dtype=np.int32)
+    d_n = torch.full((1,), cap, dtype=torch.int32, device="cuda")
+    rows_g = cdb.Rows(ar, ar, rows_np["pos"], rows_np["c"], rows_np["depth"], d_n_rows=d_n)
+    out_g = cdb.StepOut(cap)
+    ws_g = cdb.Workspace(dm.desc, cap)
+    ws_e = cdb.Workspace(dm.desc, cap)
+    cdb.cdb_loop_step(dm.model, kv.c, state.c, rows_g.c, out_g.c, ws_g.buf)
+    torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
     side = torch.cuda.Stream()
     side.wait_stream(st)
     with torch.cuda.stream(side):
         with torch.cuda.graph(g, stream=side):
-            cdb.cdb_loop_step(dm.model, kv.c, state.c, rows.c, out.c, ws.buf)
+            cdb.cdb_loop_step(dm.model, kv.c, state.c, rows_g.c, out_g.c, ws_g.buf, stream=side)
     st.wait_stream(side)
     torch.cuda.synchronize()
-    ok = True
-    for _ in range(reps):
+    checked = {}
+    for n in counts:
+        # K/V written by a step at its own positions is rewritten identically by
+        # the next call from the same state, so only the state is restored
         state.h.copy_(h0)
-        cdb.cdb_loop_step(dm.model, kv.c, state.c, rows.c, out.c, ws.buf)
+        sl = slice(0, n)
+        rows_e = cdb.Rows(ar[sl], ar[sl], rows_np["pos"][sl], rows_np["c"][sl], rows_np["depth"][sl])
+        out_e = cdb.StepOut(n)
+        cdb.cdb_loop_step(dm.model, kv.c, state.c, rows_e.c, out_e.c, ws_e.buf)
         torch.cuda.synchronize()
-        ref = outputs()
+        ref = (state.h.clone(), out_e.score[:n].clone(), out_e.mask[:n].clone(), out_e.counts.clone())
         state.h.copy_(h0)
+        d_n.fill_(n)
         torch.cuda.synchronize()
         g.replay()
         torch.cuda.synchronize()
-        got = outputs()
-        ok &= all(torch.equal(a, b) for a, b in zip(ref, got))
+        got = (state.h.clone(), out_g.score[:n].clone(), out_g.mask[:n].clone(), out_g.counts.clone())
+        checked[str(n)] = all(torch.equal(a, b) for a, b in zip(ref, got))
+    d_n.fill_(cap)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(st)
     for _ in range(steps):
         g.replay()
     e1.record(st)
     e1.synchronize()
-    if cdb.cdb_read_device_error(ws.buf) != 0:
+    if cdb.cdb_read_device_error(ws_g.buf) != 0 or cdb.cdb_read_device_error(ws_e.buf) != 0:
         raise RuntimeError("device error in the graph replays")
+    state.h.copy_(h0)
     ms = e0.elapsed_time(e1) / steps
-    log(f"graph replay: {ms:.3f} ms/step, replays {'identical to' if ok else 'DIFFERENT from'} eager steps")
-    return {"ms_per_step": round(ms, 4), "replays_match_eager": bool(ok)}
+    log(f"graph replay at {cap} rows: {ms:.3f} ms/step; replays at counts {list(checked)} identical to eager "
+        f"calls: {checked}")
+    return {"ms_per_step": round(ms, 4), "capacity": cap, "replays_match_eager": checked}
+
+
+def idle_ablation(shape_name, n_decode=48, pause_s=1.0):
+    """Whole decodes under the scheduler variants of Section 4.3, one after the
+    other with `pause_s` of device silence between them, for a kernel trace to
+    split into one segment per variant (GPU idle = the share of each segment
+    with no kernel running): the synchronous scheduler (the host waits for every
+    loop step), the asynchronous one, asynchronous with device-decided exits and
+    the lookahead gate, and asynchronous with the boundary stages on a second
+    stream.  Ouro-shaped: 64 requests, prompt 512 (KV synthesized), full
+    depth-indexed KV, max batch 64; Huginn-shaped (no gate variant: its
+    convergence criterion has no threshold these random-init states straddle
+    usefully): 128 requests, prompt 256, shared KV, max batch 128, minimum
+    boundary batch 32."""
+    import numpy as np
+    import torch
+
+    import cdbgen
+    import paper_2608_09444_amd as cdb
+    from paper_2608_09444_amd import driver as drv
+    if shape_name == "ouro":
+        shape, n_seqs, prompt, batch, layout, depth_spec = cdbgen.OURO, 64, 512, 64, drv.KV_FULL, cdbgen.OURO_DEPTHS
+        extra = {}
+    else:
+        wl = cdbgen.WORKLOADS[3]
+        shape, n_seqs, prompt, batch, layout, depth_spec = cdbgen.HUGINN, wl.n_seqs, wl.prompt, wl.max_batch, \
+            drv.KV_SHARED, wl.depth
+        extra = {"min_coda_batch": 32}
+    R = shape.r_max
+    dm = cdb.DeviceModel(shape, cdbgen.model_weights(shape))
+    max_pages = cdbgen.pages_for(prompt + n_decode)
+    per = R if layout == drv.KV_FULL else 1
+    pages = n_seqs * max_pages
+    kv = cdb.PagedKV(shape, n_seqs, max_pages, pages if shape.n_prelude else 0, pages * per,
+                     pages if shape.n_coda else 0, fill="random")
+    for pool in (kv.pre, kv.core, kv.coda):
+        pool.normal_(0.0, 1.0)
+    state = cdb.State(shape, n_seqs)
+    depths = [cdbgen.draw_depths(depth_spec, n_decode, R, seed=3, stream=q) for q in range(n_seqs)]
+    first = cdbgen.prompt_ids(shape.vocab, 1, n_seqs, seed=4)[0]
+    order = [("synchronous", {"sync_steps": True}), ("asynchronous", {})]
+    if shape.exit_kind == 0:  # the learned-gate form: a threshold of 0.5 on the random-init gate
+        order.append(("asynchronous_lookahead_gate", {"gated": True, "lookahead": True, "threshold": 0.5}))
+    order.append(("asynchronous_boundary_stream_fill", {"boundary_stream": 1}))
+    order.append(("asynchronous_boundary_stream_hold", {"boundary_stream": 2}))
+    res = {"order": [n for n, _ in order]}
+    for k, (name, mode) in enumerate([("warmup", {})] + order):
+        d = drv.Driver(max_batch=batch, max_active=n_seqs, r_max=R, max_seqs=n_seqs, max_pages=max_pages,
+                       core_pages=pages * per, pre_pages=pages, coda_pages=pages, has_prelude=shape.n_prelude > 0,
+                       has_coda=shape.n_coda > 0, kv_layout=layout, **extra, **mode)
+        nd = 4 if name == "warmup" else n_decode
+        for q in range(n_seqs):
+            d.add_sequence(prompt, None if mode.get("gated") else depths[q][:nd], n_decode=nd)
+        scratch = torch.empty(d.scratch_bytes(shape.vocab), dtype=torch.uint8, device="cuda")
+        ws, half = runner_ws(dm, 256, mode.get("boundary_stream", False))
+        torch.cuda.synchronize()
+        time.sleep(pause_s)
+        secs = d.run(dm.model, kv.c, state.c, scratch, first, ws)
+        torch.cuda.synchronize()
+        check_runner_ws(ws, half, f"the {name} run")
+        st = d.stats()
+        if name != "warmup":
+            res[name] = {"seconds": round(secs, 4), "tokens_per_s": round(st["tokens"] / secs, 1),
+                         "loop_steps": st["loop_steps"], "ms_per_loop_step": round(secs * 1e3 / st["loop_steps"], 4),
+                         "host_wait_us_per_loop_step": round(st["host_wait_us"] / st["loop_steps"], 2)}
+            log(f"idle ablation {shape_name} {name}: {res[name]}")
+    time.sleep(pause_s)
+    del kv, state, dm
+    torch.cuda.empty_cache()
+    return res
 
 
 def copy_peak(gib=4, reps=5):
@@ -754,7 +906,8 @@ def copy_peak(gib=4, reps=5):
     return round(gbs, 1)
 
 
-def serving_leg(shape, dm, n_req, rate=20.0, max_batch=64, chunk=512, core_pages=24576, fixed_depth=False):
+def serving_leg(shape, dm, n_req, rate=20.0, max_batch=64, chunk=512, core_pages=24576, fixed_depth=False,
+                boundary_stream=0):
     """A serving trace of the ouro-shaped model: Poisson arrivals at `rate`
     requests/s, prompt lengths lognormal (median 300, sigma 1, [16, 4096]),
     output lengths lognormal (median 400, sigma 1, [16, 2048]), categorical
@@ -775,19 +928,19 @@ def serving_leg(shape, dm, n_req, rate=20.0, max_batch=64, chunk=512, core_pages
     arrivals = cdbgen.poisson_arrivals(n_req, rate)
     max_pages = cdbgen.pages_for(int(plen.max() + olen.max()))
     d = drv.Driver(max_batch=max_batch, max_active=max_batch, r_max=R, max_seqs=n_req, max_pages=max_pages,
-                   core_pages=core_pages, prefill_chunk=chunk, fixed_depth=fixed_depth)
+                   core_pages=core_pages, prefill_chunk=chunk, fixed_depth=fixed_depth,
+                   boundary_stream=boundary_stream)
     for q in range(n_req):
         d.add_request(cdbgen.prompt_ids(shape.vocab, 1, int(plen[q]), stream=q)[0],
                       cdbgen.draw_depths(wl.depth, int(olen[q]), R, stream=1000 + q), arrival=float(arrivals[q]))
     kv = cdb.PagedKV(shape, n_req, max_pages, 0, core_pages, 0)
     state = cdb.State(shape, n_req)
-    ws = cdb.Workspace(dm.desc, chunk)
+    ws, half = runner_ws(dm, chunk, boundary_stream)
     scratch = torch.empty(d.scratch_bytes(shape.vocab), dtype=torch.uint8, device="cuda")
-    log(f"serving{' (fixed depth)' if fixed_depth else ''}: {n_req} requests at {rate}/s, {int(plen.sum())} prompt + "
-        f"{int(olen.sum())} output tokens")
-    secs = d.run(dm.model, kv.c, state.c, scratch, None, ws.buf)
-    if cdb.cdb_read_device_error(ws.buf) != 0:
-        raise RuntimeError("device error in the serving run")
+    log(f"serving{' (fixed depth)' if fixed_depth else ''}{' (boundary stream)' if boundary_stream else ''}: "
+        f"{n_req} requests at {rate}/s, {int(plen.sum())} prompt + {int(olen.sum())} output tokens")
+    secs = d.run(dm.model, kv.c, state.c, scratch, None, ws)
+    check_runner_ws(ws, half, "the serving run")
     st = d.stats()
     lat = d.latencies(n_req)
     lat = lat[lat >= 0]
@@ -799,7 +952,9 @@ def serving_leg(shape, dm, n_req, rate=20.0, max_batch=64, chunk=512, core_pages
            "normalized_latency_s": {"p50": round(float(np.percentile(lat, 50)), 5),
                                     "p99": round(float(np.percentile(lat, 99)), 5)},
            "finished": int(len(lat)), "loop_steps": st["loop_steps"], "idle_rows": st["idle_rows"],
-           "prefill_calls": st["prefill_calls"], "coda_calls": st["coda_calls"]}
+           "prefill_calls": st["prefill_calls"], "coda_calls": st["coda_calls"],
+           "host_wait_us_per_loop_step": round(st["host_wait_us"] / max(1, st["loop_steps"]), 2),
+           "page_table_uploads": st["pt_uploads"], "page_table_upload_bytes": st["pt_upload_bytes"]}
     log(f"serving: {st['tokens']} tokens in {secs:.2f}s, p50/p99 normalized latency "
         f"{res['normalized_latency_s']['p50'] * 1e3:.1f}/{res['normalized_latency_s']['p99'] * 1e3:.1f} ms")
     del kv, state, ws, scratch
@@ -862,13 +1017,15 @@ def main():
     ap.add_argument("--no-sweep", action="store_true", help="skip the loop-step batch-size sweep and the latency-model grid")
     ap.add_argument("--serving-requests", type=int, default=200,
                     help="requests in the serving-trace run (0 = skip; 2000 is the full trace)")
-    ap.add_argument("--huginn-decode", type=int, default=64,
+    ap.add_argument("--huginn-decode", type=int, default=512,
                     help="decode tokens per request in the Huginn-shaped whole-decode runs (0 = skip the Huginn leg; "
                          "512 is the full workload)")
     ap.add_argument("--long-context", action="store_true",
                     help="also run config 4's long-context decodes (about 250 GB of KV pools, ≈ 3 minutes)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="run one plain device copy of this many MiB first (a known-size reference for HBM counters)")
+    ap.add_argument("--idle-ablation", action="store_true",
+                    help="only the scheduler-variant decodes for a kernel trace (GPU idle per variant)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the loop step shards by sequence with no exchange between GPUs, "
@@ -880,6 +1037,10 @@ def main():
 
     import cdbgen
     import paper_2608_09444_amd as cdb
+    if args.idle_ablation:
+        print(json.dumps({"idle_ablation": {"ouro": idle_ablation("ouro"), "huginn": idle_ablation("huginn")}}),
+              flush=True)
+        return
     shape = cdbgen.OURO
     n_rows, pos_lo, pos_hi = 64, 512, 767
     log("setup")
@@ -920,7 +1081,7 @@ def main():
     log(f"{ms:.3f} ms/step, {value:.0f} rows/s, step bytes {sb / 1e9:.2f} GB -> {sb / (ms * 1e-3) / 1e9:.0f} GB/s")
 
     try:
-        graph = graph_leg(dm, kv, state, rows, out, ws, args.steps)
+        graph = graph_leg(dm, kv, state, rows_np, args.steps)
     except RuntimeError as e:  # a capture the runtime refuses is reported, not fatal
         graph = {"error": str(e)}
     copy_gbs = copy_peak()
@@ -947,7 +1108,9 @@ def main():
     serving = None
     if args.serving_requests > 0:
         serving = {"cdb_refill": serving_leg(shape, dm, args.serving_requests),
-                   "cb_fixed_depth": serving_leg(shape, dm, args.serving_requests, fixed_depth=True)}
+                   "cb_fixed_depth": serving_leg(shape, dm, args.serving_requests, fixed_depth=True),
+                   "cdb_refill_boundary_stream_fill": serving_leg(shape, dm, args.serving_requests,
+                                                                  boundary_stream=1)}
         a, b = serving["cdb_refill"], serving["cb_fixed_depth"]
         serving["throughput_ratio"] = round(a["tokens_per_s"] / b["tokens_per_s"], 4)
         serving["p50_latency_reduction"] = round(1 - a["normalized_latency_s"]["p50"] /
@@ -967,12 +1130,14 @@ def main():
 
     cpu = None
     if args.cpu_sample > 0:
-        threads = min(16, os.cpu_count() or 1)
+        info = host_info()
+        threads = host_threads()
         log(f"cpu baseline on {args.cpu_sample} rows, {threads} threads")
         cpu = cpu_baseline(shape, w, rows_np, args.cpu_sample, threads)
         log("cpu baseline on 1 row, 1 thread")
         one = cpu_baseline(shape, w, rows_np, 1, 1, min_s=8.0)
         cpu["single_core"] = {"value": one["value"], "cores": 1, "sample": one["sample"]}
+        cpu.update(info)
 
     res = {
         "metric": "mixed-depth loop-step tokens/s (Ouro-1.4B-shaped, bs=64); % HBM/MFMA roofline",
@@ -1010,6 +1175,7 @@ def main():
         "serving": serving,
         "huginn": huginn,
         "long_context": long_ctx,
+        "reduced_legs": reduced_legs(args),
     }
     print(json.dumps(res), flush=True)
 

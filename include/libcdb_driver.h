@@ -55,6 +55,15 @@ typedef struct {
                                        through cdb_prefill in chunks of at most this many tokens */
     int32_t sync_steps;             /* 1: the runner waits for every loop step before planning the next
                                        (the synchronous scheduler, for comparison); 0: never waits */
+    int32_t boundary_stream;        /* 0: every call on one stream.  1, 2: prelude, coda and prefill calls
+                                       run on a second stream with their own workspace, ordered with the
+                                       loop steps by events (Section 4.3).  In refill mode the tokens whose
+                                       prelude was planned since the last loop step are held back from
+                                       the next step, which so does not wait for that boundary work:
+                                       with 1 they still fill rows the loop queue leaves free (no row
+                                       idles; the step then waits for their prelude), with 2 they always
+                                       join the step after next (the boundary work of step k overlaps
+                                       step k + 1 whole, at the cost of rows idling one step) */
 } cdb_driver_config;
 
 /* Core KV layouts (Section 4.2, App. C.1, Table 1), all by page-table aliasing:
@@ -84,6 +93,10 @@ typedef struct {
     int64_t coda_calls, coda_rows, prelude_calls, prelude_rows;
     int64_t tokens;                            /* decode tokens finished (coda rows) */
     int64_t prefill_calls, prefill_tokens;     /* prompt chunks run by the driver */
+    int64_t host_wait_us;                      /* cdb_driver_run: time the host spent waiting on the device
+                                                  (staging-buffer reuse, page-table uploads, gated
+                                                  decisions, sync_steps), microseconds */
+    int64_t pt_uploads, pt_upload_bytes;       /* page-table uploads and the bytes they copied */
 } cdb_driver_stats;
 
 cdb_driver* cdb_driver_create(const cdb_driver_config* cfg);
@@ -155,8 +168,15 @@ size_t cdb_driver_scratch_bytes(const cdb_driver* d, int32_t vocab);
  * id the coda produced after decode input k (tokens_stride >= every
  * sequence's n_decode, else CDB_ERR_INVALID_ARG).  Gated mode: the device's
  * exit decisions are copied back after every loop step and fed to the
- * scheduler (one step late with lookahead); CDB_ERR_INVALID_ARG if they ever
- * disagree with the exits applied.  Returns a cdb_status; *seconds = wall
+ * scheduler (one step late with lookahead, the last step's after the run);
+ * CDB_ERR_INVALID_ARG if they ever disagree with the exits applied.
+ * boundary_stream: the loop steps run on `stream`, the prelude, coda and
+ * prefill calls on a second stream the runner creates (default priority) and
+ * destroys before returning; ws then holds two workspaces, ws_bytes / 2 each
+ * (rounded down to 256 bytes; the second starts there), the first for loop
+ * steps, the second for boundary stages (its device error word covers those).
+ * Page-table changes after the first upload copy only the blocks of
+ * sequences admitted or released.  Returns a cdb_status; *seconds = wall
  * time including the final synchronisation.  With the environment variable
  * CDB_DRIVER_PROGRESS set, a progress line goes to stderr every 10 s. */
 int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, const cdb_state* state, void* scratch,

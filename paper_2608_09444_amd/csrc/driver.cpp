@@ -98,12 +98,32 @@ struct cdb_driver {
     bool round_open = false;      // no-refill: a round is running
     cdb_driver_stats stats;
     double now = 0.0;  // seconds, advanced by the runner (or by tests)
-    bool table_dirty = true;
+    bool table_all_dirty = true;         // the whole page table must be uploaded (first run)
+    std::vector<int32_t> dirty_seqs;     // sequences whose page-table block changed since the last upload
+    std::vector<uint8_t> seq_dirty;      // per sequence: listed in dirty_seqs
+    std::deque<int32_t> loop_hold;       // boundary stream: tokens prelude'd since the last loop tick
     std::vector<uint8_t> last_plan;  // gated: exits applied to the last completed loop tick, in row order
     bool result_pending = false;     // gated lookahead: the last completed loop tick's result is still due
 };
 
 static int32_t planes(const cdb_driver* d) { return d->cfg.r_max + 2; }
+
+static void mark_dirty(cdb_driver* d, int32_t q) {
+    if (!d->seq_dirty[q]) {
+        d->seq_dirty[q] = 1;
+        d->dirty_seqs.push_back(q);
+    }
+}
+
+// Tokens whose prelude was just planned: with boundary stages on their own
+// stream they join the loop step after next, so the next loop step does not
+// wait for that prelude (refill mode); otherwise the loop queue directly.
+static void to_loop_queue(cdb_driver* d, int32_t q) {
+    if (d->cfg.boundary_stream && d->cfg.refill)
+        d->loop_hold.push_back(q);
+    else
+        d->loopq.push_back(q);
+}
 
 static int32_t depth_of(const cdb_driver* d, const Seq& s) {
     if (d->cfg.fixed_depth) return d->cfg.r_max;
@@ -166,7 +186,7 @@ static bool try_admit(cdb_driver* d, int32_t q) {
         s.state = PRELUDE;
         d->fresh.push_back(q);
     }
-    d->table_dirty = true;
+    mark_dirty(d, q);
     return true;
 }
 
@@ -188,7 +208,7 @@ static void release(cdb_driver* d, int32_t q) {
         }
     }
     d->active--;
-    d->table_dirty = true;
+    mark_dirty(d, q);
 }
 
 static void admit(cdb_driver* d) {
@@ -217,11 +237,13 @@ extern "C" {
 cdb_driver* cdb_driver_create(const cdb_driver_config* cfg) {
     if (!cfg || cfg->max_batch < 1 || cfg->max_batch > 256 || cfg->r_max < 1 || cfg->max_seqs < 1 ||
         cfg->max_pages < 1 || cfg->max_active < 1 || cfg->min_coda_batch < 1 || cfg->kv_layout < 0 ||
-        cfg->kv_layout > 2 || (cfg->gated && cfg->fixed_depth) || cfg->prefill_chunk < 0 || cfg->prefill_chunk > 512)
+        cfg->kv_layout > 2 || (cfg->gated && cfg->fixed_depth) || cfg->prefill_chunk < 0 || cfg->prefill_chunk > 512 ||
+        cfg->boundary_stream < 0 || cfg->boundary_stream > 2)
         return nullptr;
     cdb_driver* d = new cdb_driver();
     d->cfg = *cfg;
     d->page_table.assign((size_t)cfg->max_seqs * (cfg->r_max + 2) * cfg->max_pages, -1);
+    d->seq_dirty.assign(cfg->max_seqs, 0);
     d->pre = Allocator(cfg->has_prelude ? cfg->pre_pages : 0);
     d->core = Allocator(cfg->core_pages);
     d->coda = Allocator(cfg->has_coda ? cfg->coda_pages : 0);
@@ -313,6 +335,12 @@ int32_t cdb_driver_next(cdb_driver* d, cdb_driver_tick* t) {
         return 1;
     };
     if (d->cfg.refill) {
+        // held tokens join now when nothing else is left to run in the core
+        if (d->loopq.empty() && d->batch.empty())
+            while (!d->loop_hold.empty()) {
+                d->loopq.push_back(d->loop_hold.front());
+                d->loop_hold.pop_front();
+            }
         const bool loop_left = !d->loopq.empty() || !d->batch.empty();
         const int32_t n_exit = (int32_t)d->exited.size();
         if (n_exit > 0 && (n_exit >= d->cfg.min_coda_batch || !loop_left)) return coda_tick();
@@ -323,6 +351,18 @@ int32_t cdb_driver_next(cdb_driver* d, cdb_driver_tick* t) {
             while ((int32_t)d->batch.size() < d->cfg.max_batch && !d->loopq.empty()) {
                 d->batch.push_back(d->loopq.front());
                 d->loopq.pop_front();
+            }
+            // boundary_stream 1: held tokens still take rows the queue left free
+            // (this step then waits for their prelude); 2: they join the next step
+            if (d->cfg.boundary_stream == 1)
+                while ((int32_t)d->batch.size() < d->cfg.max_batch && !d->loop_hold.empty()) {
+                    d->batch.push_back(d->loop_hold.front());
+                    d->loop_hold.pop_front();
+                }
+            // tokens held back from this step join the next one
+            while (!d->loop_hold.empty()) {
+                d->loopq.push_back(d->loop_hold.front());
+                d->loop_hold.pop_front();
             }
             return loop_tick();
         }
@@ -380,7 +420,7 @@ int32_t cdb_driver_complete(cdb_driver* d, const cdb_driver_tick* t) {
         // the prelude of the continuing sequences' next inputs runs right after
         d->stats.prelude_calls += cont.empty() ? 0 : 1;
         d->stats.prelude_rows += (int64_t)cont.size();
-        for (int32_t q : cont) d->loopq.push_back(q);
+        for (int32_t q : cont) to_loop_queue(d, q);
         if (!d->cfg.refill && d->exited.empty() && d->batch.empty()) d->round_open = false;  // round over
     } else if (t->stage == CDB_TICK_PREFILL) {
         const int32_t q = t->seq[0];
@@ -400,7 +440,7 @@ int32_t cdb_driver_complete(cdb_driver* d, const cdb_driver_tick* t) {
             const int32_t q = t->seq[i];
             d->fresh.erase(std::find(d->fresh.begin(), d->fresh.end(), q));
             d->seqs[q].state = LOOP;
-            d->loopq.push_back(q);
+            to_loop_queue(d, q);
         }
         d->stats.prelude_calls++;
         d->stats.prelude_rows += t->n_rows;
@@ -476,7 +516,8 @@ int32_t cdb_driver_latencies(const cdb_driver* d, double* normalized, int32_t n)
 
 // ------------------------------------------------------------------ runner
 
-// Device scratch: two row sets (6 x 256 int32 each), next ids (256), loop-step
+// Device scratch: three row sets (6 x 256 int32 each: the loop step's, the
+// boundary stage's, the prelude's after a coda), next ids (256), loop-step
 // outputs (scores, mask, cont, exited, counts, exit_next), the gate's pending
 // flags (max_seqs), each sequence's first decode input (max_seqs int32),
 // logits (256 x vocab fp32).
@@ -488,7 +529,7 @@ static ScratchLayout scratch_layout(int32_t max_seqs, int32_t vocab) {
     ScratchLayout L;
     size_t off = 0;
     L.rows = off;
-    off += 2 * 6 * 256 * 4;
+    off += 3 * 6 * 256 * 4;
     L.ids = off;
     off += 256 * 4;
     L.step = off;
@@ -508,6 +549,46 @@ size_t cdb_driver_scratch_bytes(const cdb_driver* d, int32_t vocab) {
     return d && vocab > 0 ? scratch_layout(d->cfg.max_seqs, vocab).total : 0;
 }
 
+namespace {
+
+// Host-side waits on the device, timed for the driver's statistics.
+struct Waits {
+    std::chrono::steady_clock::duration total{};
+    void on(hipEvent_t e) {
+        const auto t0 = std::chrono::steady_clock::now();
+        hipEventSynchronize(e);
+        total += std::chrono::steady_clock::now() - t0;
+    }
+    hipError_t on(hipStream_t s) {
+        const auto t0 = std::chrono::steady_clock::now();
+        const hipError_t r = hipStreamSynchronize(s);
+        total += std::chrono::steady_clock::now() - t0;
+        return r;
+    }
+};
+
+// A ring of events recorded on one stream, numbered by a running count, so
+// another stream can wait for "the n-th record" (a later record of the same
+// slot orders at least as late, which keeps such waits correct).
+struct EventRing {
+    static constexpr int N = 64;
+    hipEvent_t ev[N];
+    int64_t count = 0;  // records so far; record k (1-based) sits in slot (k - 1) % N
+    EventRing() {
+        for (int i = 0; i < N; ++i) hipEventCreateWithFlags(&ev[i], hipEventDisableTiming);
+    }
+    ~EventRing() {
+        for (int i = 0; i < N; ++i) hipEventDestroy(ev[i]);
+    }
+    int64_t record(hipStream_t s) {
+        hipEventRecord(ev[count % N], s);
+        return ++count;
+    }
+    hipEvent_t at(int64_t k) const { return ev[(k - 1) % N]; }
+};
+
+}  // namespace
+
 int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, const cdb_state* state, void* scratch,
                        size_t scratch_bytes, const int32_t* first_tokens, int32_t* tokens_out,
                        int32_t tokens_stride, void* ws, size_t ws_bytes, hipStream_t stream, double* seconds) {
@@ -522,9 +603,21 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
     if (scratch_bytes < SL.total) return CDB_ERR_CAPACITY;
     if (kv->max_seqs != d->cfg.max_seqs || kv->max_pages != d->cfg.max_pages) return CDB_ERR_INVALID_ARG;
     if (state->n_slots < d->cfg.max_seqs) return CDB_ERR_INVALID_ARG;
+    const bool two = d->cfg.boundary_stream != 0;
+    // the loop steps' stream and workspace (A), the boundary stages' (B)
+    hipStream_t sA = stream, sB = stream;
+    unsigned char* wsA = static_cast<unsigned char*>(ws);
+    unsigned char* wsB = wsA;
+    size_t wsA_bytes = ws_bytes, wsB_bytes = ws_bytes;
+    if (two) {
+        wsA_bytes = wsB_bytes = (ws_bytes / 2) & ~(size_t)255;
+        wsB = wsA + wsA_bytes;
+        if (hipStreamCreateWithFlags(&sB, hipStreamNonBlocking) != hipSuccess) return CDB_ERR_HIP;
+    }
     unsigned char* base = static_cast<unsigned char*>(scratch);
-    int32_t* drows = reinterpret_cast<int32_t*>(base + SL.rows);  // main rows
-    int32_t* drows2 = drows + 6 * 256;                            // prelude rows after a coda
+    int32_t* drowsA = reinterpret_cast<int32_t*>(base + SL.rows);  // loop-step rows
+    int32_t* drowsB = drowsA + 6 * 256;                            // coda / prelude / prefill rows
+    int32_t* drows2 = drowsB + 6 * 256;                            // prelude rows after a coda
     int32_t* dids = reinterpret_cast<int32_t*>(base + SL.ids);
     int32_t* dfirst = reinterpret_cast<int32_t*>(base + SL.first);  // first decode input per sequence
     float* dlogits = reinterpret_cast<float*>(base + SL.logits);
@@ -535,55 +628,56 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
     out.exited = out.cont + 256;
     out.counts = out.exited + 256;
     out.exit_next = reinterpret_cast<uint8_t*>(out.counts + 2);
-    int32_t status0 = CDB_OK;
+    int32_t status = CDB_OK;
     cdb_gate gate;
     gate.threshold = d->cfg.threshold;
     gate.lookahead = d->cfg.lookahead;
     gate.pending = base + SL.pending;
     const bool gated = d->cfg.gated != 0;
-    if (gated && hipMemsetAsync(gate.pending, 0, d->cfg.max_seqs, stream) != hipSuccess) return CDB_ERR_HIP;
+    Waits waits;
+    if (gated && hipMemsetAsync(gate.pending, 0, d->cfg.max_seqs, sA) != hipSuccess) status = CDB_ERR_HIP;
 
-    // pinned host staging: a ring of row buffers, each reused only after the
-    // copy that last read it has completed (device buffers are reused in
-    // stream order); a second ring receives the gated steps' decisions
-    const int RING = 8;
+    // pinned host staging: a ring of row buffers and one of page-table blocks,
+    // each slot reused only after the copy that last read it has completed; a
+    // third ring receives the gated steps' decisions
+    const int RING = 8, PT_RING = 64;
     const size_t slot_ints = 6 * 256;
-    int32_t* pinned = nullptr;
-    int32_t* pinned_pt = nullptr;
-    uint8_t* pinned_rb = nullptr;
+    const size_t block_ints = (size_t)planes(d) * d->cfg.max_pages;  // one sequence's page-table block
     const size_t pt_bytes = d->page_table.size() * 4;
-    if (hipHostMalloc(reinterpret_cast<void**>(&pinned), RING * slot_ints * 4) != hipSuccess) return CDB_ERR_HIP;
-    if (hipHostMalloc(reinterpret_cast<void**>(&pinned_pt), pt_bytes) != hipSuccess) {
-        hipHostFree(pinned);
-        return CDB_ERR_HIP;
-    }
-    if (hipHostMalloc(reinterpret_cast<void**>(&pinned_rb), RING * 512) != hipSuccess) {
-        hipHostFree(pinned);
-        hipHostFree(pinned_pt);
-        return CDB_ERR_HIP;
-    }
-    hipEvent_t ev[RING], rb_ev[RING], pt_ev;
+    int32_t* pinned = nullptr;
+    int32_t* pinned_pt = nullptr;  // the whole table (first upload) and the caller's first inputs
+    int32_t* pinned_blk = nullptr;
+    uint8_t* pinned_rb = nullptr;
+    bool alloc_ok = hipHostMalloc(reinterpret_cast<void**>(&pinned), RING * slot_ints * 4) == hipSuccess;
+    alloc_ok = alloc_ok && hipHostMalloc(reinterpret_cast<void**>(&pinned_pt),
+                                         std::max(pt_bytes, d->seqs.size() * 4 + 4)) == hipSuccess;
+    alloc_ok = alloc_ok && hipHostMalloc(reinterpret_cast<void**>(&pinned_blk), PT_RING * block_ints * 4) == hipSuccess;
+    alloc_ok = alloc_ok && hipHostMalloc(reinterpret_cast<void**>(&pinned_rb), RING * 512) == hipSuccess;
+    hipEvent_t ev[RING], rb_ev[RING], blk_ev[PT_RING], pt_ev;
     for (int i = 0; i < RING; ++i) {
         hipEventCreateWithFlags(&ev[i], hipEventDisableTiming);
         hipEventCreateWithFlags(&rb_ev[i], hipEventDisableTiming);
     }
+    for (int i = 0; i < PT_RING; ++i) hipEventCreateWithFlags(&blk_ev[i], hipEventDisableTiming);
     hipEventCreateWithFlags(&pt_ev, hipEventDisableTiming);
+    EventRing evA, evB;          // after loop steps (A); after boundary calls and uploads (B)
+    int64_t waitedA = 0, waitedB = 0;  // latest record of the other stream each stream already waits for
+    std::vector<int64_t> ready(d->cfg.max_seqs, 0);  // B record after each sequence's latest boundary call
     bool pt_used = false;
-    // the caller's first inputs (prefilled prompts) to the device; the page-table
-    // staging buffer carries them, and its next upload waits for this copy
-    if (first_tokens) {
+    if (!alloc_ok) status = CDB_ERR_HIP;
+    // the caller's first inputs (prefilled prompts) to the device
+    if (status == CDB_OK && first_tokens) {
         const size_t nb = d->seqs.size() * 4;  // one entry per added sequence
         memcpy(pinned_pt, first_tokens, nb);
-        if (nb && hipMemcpyAsync(dfirst, pinned_pt, nb, hipMemcpyHostToDevice, stream) !=
-            hipSuccess)
-            status0 = CDB_ERR_HIP;
-        hipEventRecord(pt_ev, stream);
+        if (nb && hipMemcpyAsync(dfirst, pinned_pt, nb, hipMemcpyHostToDevice, sA) != hipSuccess)
+            status = CDB_ERR_HIP;
+        hipEventRecord(pt_ev, sA);
         pt_used = true;
     }
-    int ring = 0, rb_ring = 0;
+    int ring = 0, rb_ring = 0, blk_ring = 0;
     auto stage = [&](const int32_t* slot, const int32_t* seq, const int32_t* pos, const int32_t* c,
-                     const int32_t* dep, const int32_t* tok, int32_t n, int32_t* dst) -> hipError_t {
-        hipEventSynchronize(ev[ring]);
+                     const int32_t* dep, const int32_t* tok, int32_t n, int32_t* dst, hipStream_t s) -> hipError_t {
+        waits.on(ev[ring]);
         int32_t* h = pinned + ring * slot_ints;
         memcpy(h, slot, n * 4);
         memcpy(h + 256, seq, n * 4);
@@ -591,18 +685,68 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
         if (c) memcpy(h + 768, c, n * 4);
         if (dep) memcpy(h + 1024, dep, n * 4);
         if (tok) memcpy(h + 1280, tok, n * 4);
-        hipError_t e = hipMemcpyAsync(dst, h, slot_ints * 4, hipMemcpyHostToDevice, stream);
-        hipEventRecord(ev[ring], stream);
+        hipError_t e = hipMemcpyAsync(dst, h, slot_ints * 4, hipMemcpyHostToDevice, s);
+        hipEventRecord(ev[ring], s);
         ring = (ring + 1) % RING;
         return e;
     };
-    auto stage_ids = [&](const int32_t* ids, int32_t n, int32_t* dst) -> hipError_t {
-        hipEventSynchronize(ev[ring]);
+    auto stage_ids = [&](const int32_t* ids, int32_t n, int32_t* dst, hipStream_t s) -> hipError_t {
+        waits.on(ev[ring]);
         int32_t* h = pinned + ring * slot_ints;
         memcpy(h, ids, (size_t)n * 4);
-        hipError_t e = hipMemcpyAsync(dst, h, (size_t)n * 4, hipMemcpyHostToDevice, stream);
-        hipEventRecord(ev[ring], stream);
+        hipError_t e = hipMemcpyAsync(dst, h, (size_t)n * 4, hipMemcpyHostToDevice, s);
+        hipEventRecord(ev[ring], s);
         ring = (ring + 1) % RING;
+        return e;
+    };
+    // cross-stream ordering (no-ops with one stream)
+    auto b_waits_for_a = [&]() {
+        if (two && evA.count > waitedB) {
+            hipStreamWaitEvent(sB, evA.at(evA.count), 0);
+            waitedB = evA.count;
+        }
+    };
+    auto a_waits_for_b = [&](int64_t k) {
+        if (two && k > waitedA) {
+            hipStreamWaitEvent(sA, evB.at(k), 0);
+            waitedA = k;
+        }
+    };
+    // page-table changes to the device: the whole table once, then only the
+    // blocks of sequences admitted or released since, each through its own
+    // pinned slot; they go on the boundary stream, which runs every new
+    // sequence's first call (the loop steps reach a new sequence only after
+    // waiting for that call)
+    auto upload_table = [&]() -> hipError_t {
+        hipError_t e = hipSuccess;
+        int32_t* dpt = const_cast<int32_t*>(kv->page_table);
+        if (d->table_all_dirty) {
+            if (pt_used) waits.on(pt_ev);
+            memcpy(pinned_pt, d->page_table.data(), pt_bytes);
+            e = hipMemcpyAsync(dpt, pinned_pt, pt_bytes, hipMemcpyHostToDevice, sA);
+            hipEventRecord(pt_ev, sA);
+            pt_used = true;
+            if (two) {
+                hipStreamWaitEvent(sB, pt_ev, 0);
+            }
+            d->stats.pt_uploads++;
+            d->stats.pt_upload_bytes += (int64_t)pt_bytes;
+            d->table_all_dirty = false;
+        } else {
+            for (int32_t q : d->dirty_seqs) {
+                if (e != hipSuccess) break;
+                waits.on(blk_ev[blk_ring]);
+                int32_t* hb = pinned_blk + blk_ring * block_ints;
+                memcpy(hb, d->page_table.data() + (size_t)q * block_ints, block_ints * 4);
+                e = hipMemcpyAsync(dpt + (size_t)q * block_ints, hb, block_ints * 4, hipMemcpyHostToDevice, sB);
+                hipEventRecord(blk_ev[blk_ring], sB);
+                blk_ring = (blk_ring + 1) % PT_RING;
+                d->stats.pt_uploads++;
+                d->stats.pt_upload_bytes += (int64_t)block_ints * 4;
+            }
+        }
+        for (int32_t q : d->dirty_seqs) d->seq_dirty[q] = 0;
+        d->dirty_seqs.clear();
         return e;
     };
     // gated: the previous loop tick and the ring slot of its decisions
@@ -610,7 +754,6 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
     int prev_rb = -1;
 
     cdb_driver_tick t;
-    int32_t status = status0;
     std::vector<int32_t> toks(256), npos(256);
     // CDB_DRIVER_PROGRESS set: a line on stderr every 10 s of a long run
     const bool progress = getenv("CDB_DRIVER_PROGRESS") != nullptr;
@@ -627,17 +770,11 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
         const int32_t r = cdb_driver_next(d, &t);
         if (r == 0) break;
         if (r < 0) continue;  // the next request has not arrived yet
-        if (d->table_dirty) {
-            if (pt_used) hipEventSynchronize(pt_ev);
-            memcpy(pinned_pt, d->page_table.data(), pt_bytes);
-            if (hipMemcpyAsync(const_cast<int32_t*>(kv->page_table), pinned_pt, pt_bytes, hipMemcpyHostToDevice,
-                               stream) != hipSuccess) {
+        if (d->table_all_dirty || !d->dirty_seqs.empty()) {
+            if (upload_table() != hipSuccess) {
                 status = CDB_ERR_HIP;
                 break;
             }
-            hipEventRecord(pt_ev, stream);
-            pt_used = true;
-            d->table_dirty = false;
         }
         const int32_t n = t.n_rows;
         cdb_status s = CDB_OK;
@@ -645,15 +782,16 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
             // the chunk's prompt ids through the staging ring; the chunk's last
             // greedy id lands in the sequence's first-input entry
             const int32_t q = t.seq[0];
-            if (stage_ids(d->seqs[q].prompt.data() + t.pos[0], n, drows) != hipSuccess) {
+            if (stage_ids(d->seqs[q].prompt.data() + t.pos[0], n, drowsB, sB) != hipSuccess) {
                 status = CDB_ERR_HIP;
                 break;
             }
-            s = cdb_prefill(model, kv, q, t.pos[0], n, drows, nullptr, dfirst + q, ws, ws_bytes, stream);
+            s = cdb_prefill(model, kv, q, t.pos[0], n, drowsB, nullptr, dfirst + q, wsB, wsB_bytes, sB);
             if (s != CDB_OK) {
                 status = s;
                 break;
             }
+            ready[q] = two ? evB.record(sB) : 0;
             if (cdb_driver_complete(d, &t) != 0) {
                 status = CDB_ERR_INVALID_ARG;
                 break;
@@ -663,43 +801,55 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
         // sixth row array: the decode index (coda); the prelude of first inputs
         // gathers its tokens from the first-input entries on the device
         for (int32_t i = 0; i < n; ++i) toks[i] = t.stage == CDB_TICK_CODA ? t.decode_index[i] : 0;
-        if (stage(t.slot, t.seq, t.pos, t.c, t.depth, toks.data(), n, drows) != hipSuccess) {
+        const bool on_b = t.stage != CDB_TICK_LOOP;
+        int32_t* drows = on_b ? drowsB : drowsA;
+        if (t.stage == CDB_TICK_CODA) b_waits_for_a();  // its rows exited in loop steps already enqueued
+        if (t.stage == CDB_TICK_LOOP) {
+            int64_t need = 0;
+            for (int32_t i = 0; i < n; ++i) need = std::max(need, ready[t.seq[i]]);
+            a_waits_for_b(need);
+        }
+        if (stage(t.slot, t.seq, t.pos, t.c, t.depth, toks.data(), n, drows, on_b ? sB : sA) != hipSuccess) {
             status = CDB_ERR_HIP;
             break;
         }
         cdb_rows rows{n, drows, drows + 256, drows + 512, drows + 768, drows + 1024, nullptr};
         if (t.stage == CDB_TICK_PRELUDE_FIRST) {
-            if (cdb::launch_gather_ids(n, drows + 256, dfirst, d->cfg.max_seqs, drows + 1280, stream) != hipSuccess) {
+            if (cdb::launch_gather_ids(n, drows + 256, dfirst, d->cfg.max_seqs, drows + 1280, sB) != hipSuccess) {
                 status = CDB_ERR_HIP;
                 break;
             }
-            s = cdb_boundary_prelude(model, kv, state, &rows, drows + 1280, ws, ws_bytes, stream);
+            s = cdb_boundary_prelude(model, kv, state, &rows, drows + 1280, wsB, wsB_bytes, sB);
+            if (s == CDB_OK && two) {
+                const int64_t k = evB.record(sB);
+                for (int32_t i = 0; i < n; ++i) ready[t.seq[i]] = k;
+            }
         } else if (t.stage == CDB_TICK_LOOP) {
             if (!gated) {
-                s = cdb_loop_step(model, kv, state, &rows, &out, ws, ws_bytes, stream);
+                s = cdb_loop_step(model, kv, state, &rows, &out, wsA, wsA_bytes, sA);
             } else {
                 rows.depth = nullptr;
-                s = cdb_loop_step_gated(model, kv, state, &rows, &gate, &out, ws, ws_bytes, stream);
+                s = cdb_loop_step_gated(model, kv, state, &rows, &gate, &out, wsA, wsA_bytes, sA);
                 if (s == CDB_OK) {
                     // this step's decisions to the host
                     const int rs = rb_ring;
                     rb_ring = (rb_ring + 1) % RING;
-                    hipEventSynchronize(rb_ev[rs]);
+                    waits.on(rb_ev[rs]);
                     uint8_t* hb = pinned_rb + rs * 512;
-                    if (hipMemcpyAsync(hb, out.exit_mask, n, hipMemcpyDeviceToHost, stream) != hipSuccess ||
-                        hipMemcpyAsync(hb + 256, out.exit_next, n, hipMemcpyDeviceToHost, stream) != hipSuccess) {
+                    if (hipMemcpyAsync(hb, out.exit_mask, n, hipMemcpyDeviceToHost, sA) != hipSuccess ||
+                        hipMemcpyAsync(hb + 256, out.exit_next, n, hipMemcpyDeviceToHost, sA) != hipSuccess) {
                         status = CDB_ERR_HIP;
                         break;
                     }
-                    hipEventRecord(rb_ev[rs], stream);
+                    hipEventRecord(rb_ev[rs], sA);
                     if (!d->cfg.lookahead) {
                         // the step's own exits are needed before it completes
-                        hipEventSynchronize(rb_ev[rs]);
+                        waits.on(rb_ev[rs]);
                         cdb_driver_loop_result(d, &t, hb, hb + 256);
                     } else {
                         // lookahead: the previous step's decisions complete this one
                         if (prev_rb >= 0) {
-                            hipEventSynchronize(rb_ev[prev_rb]);
+                            waits.on(rb_ev[prev_rb]);
                             const uint8_t* pb = pinned_rb + prev_rb * 512;
                             if (cdb_driver_loop_result(d, &prev, pb, pb + 256) != 0) s = CDB_ERR_INVALID_ARG;
                         }
@@ -708,23 +858,28 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
                     }
                 }
             }
+            if (s == CDB_OK && two) evA.record(sA);
         } else if (t.stage == CDB_TICK_CODA) {
-            s = cdb_boundary_coda(model, kv, state, &rows, dlogits, dids, ws, ws_bytes, stream);
+            s = cdb_boundary_coda(model, kv, state, &rows, dlogits, dids, wsB, wsB_bytes, sB);
             if (s == CDB_OK && tokens_out &&
                 cdb::launch_scatter_ids(n, dids, drows + 256, drows + 1280, d->cfg.max_seqs, tokens_stride, tokens_out,
-                                        stream) != hipSuccess)
+                                        sB) != hipSuccess)
                 s = CDB_ERR_HIP;
             if (s == CDB_OK && t.n_continue > 0) {
                 // the continuing sequences are the coda batch's first rows: the
                 // coda's ids are the prelude's tokens, one position further
                 for (int32_t i = 0; i < t.n_continue; ++i) npos[i] = t.pos[i] + 1;
-                if (stage(t.slot, t.seq, npos.data(), nullptr, nullptr, nullptr, t.n_continue, drows2) !=
+                if (stage(t.slot, t.seq, npos.data(), nullptr, nullptr, nullptr, t.n_continue, drows2, sB) !=
                     hipSuccess) {
                     status = CDB_ERR_HIP;
                     break;
                 }
                 cdb_rows prow{t.n_continue, drows2, drows2 + 256, drows2 + 512, nullptr, nullptr, nullptr};
-                s = cdb_boundary_prelude(model, kv, state, &prow, dids, ws, ws_bytes, stream);
+                s = cdb_boundary_prelude(model, kv, state, &prow, dids, wsB, wsB_bytes, sB);
+            }
+            if (s == CDB_OK && two) {
+                const int64_t k = evB.record(sB);
+                for (int32_t i = 0; i < t.n_continue; ++i) ready[t.seq[i]] = k;
             }
         }
         if (s != CDB_OK) {
@@ -735,23 +890,37 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
             status = CDB_ERR_INVALID_ARG;
             break;
         }
-        if (d->cfg.sync_steps && t.stage == CDB_TICK_LOOP && hipStreamSynchronize(stream) != hipSuccess) {
+        if (d->cfg.sync_steps && t.stage == CDB_TICK_LOOP && waits.on(sA) != hipSuccess) {
             status = CDB_ERR_HIP;
             break;
         }
     }
-    if (hipStreamSynchronize(stream) != hipSuccess && status == CDB_OK) status = CDB_ERR_HIP;
+    // gated lookahead: the last loop step's decisions are still due; a device
+    // decision the scheduler did not apply is an error, as for every earlier step
+    if (status == CDB_OK && gated && d->cfg.lookahead && d->result_pending && prev_rb >= 0) {
+        waits.on(rb_ev[prev_rb]);
+        const uint8_t* pb = pinned_rb + prev_rb * 512;
+        if (cdb_driver_loop_result(d, &prev, pb, pb + 256) != 0) status = CDB_ERR_INVALID_ARG;
+    }
+    if (waits.on(sA) != hipSuccess && status == CDB_OK) status = CDB_ERR_HIP;
+    if (two) {
+        if (waits.on(sB) != hipSuccess && status == CDB_OK) status = CDB_ERR_HIP;
+        hipStreamDestroy(sB);
+    }
     const double secs = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
     d->now = secs;
+    d->stats.host_wait_us += (int64_t)std::chrono::duration_cast<std::chrono::microseconds>(waits.total).count();
     if (seconds) *seconds = secs;
     for (int i = 0; i < RING; ++i) {
         hipEventDestroy(ev[i]);
         hipEventDestroy(rb_ev[i]);
     }
+    for (int i = 0; i < PT_RING; ++i) hipEventDestroy(blk_ev[i]);
     hipEventDestroy(pt_ev);
-    hipHostFree(pinned);
-    hipHostFree(pinned_pt);
-    hipHostFree(pinned_rb);
+    if (pinned) hipHostFree(pinned);
+    if (pinned_pt) hipHostFree(pinned_pt);
+    if (pinned_blk) hipHostFree(pinned_blk);
+    if (pinned_rb) hipHostFree(pinned_rb);
     return status;
 }
 

@@ -341,3 +341,73 @@ def test_add_sequence_rejects_what_could_never_run():
     two.add_sequence(4, [1], arrival=1.0)
     with pytest.raises(ValueError):
         two.add_sequence(4, [1], arrival=0.5)  # before the previous arrival
+
+
+def test_boundary_stream_holds_new_tokens_back_one_loop_step():
+    """With boundary stages on their own stream (refill), tokens whose prelude
+    was just planned are held back from the next loop step.  Mode 2: they join
+    the step after next, so a step holds such tokens only when it holds nothing
+    else.  Mode 1: they still fill rows the loop queue leaves free, so no row
+    idles while loop work waits.  Every token still runs exactly its depth,
+    loops in order."""
+    rng = np.random.default_rng(7)
+    tables = [rng.integers(1, 5, size=int(rng.integers(2, 7))) for _ in range(10)]
+    totals = {}
+    for bs in (0, 1, 2):
+        d = Driver(max_batch=4, max_active=6, r_max=4, max_seqs=10, max_pages=1, core_pages=6 * 4,
+                   boundary_stream=bs)
+        for tb in tables:
+            d.add_sequence(3, tb)
+        prelude_at = {}  # token -> index of the tick that ran its prelude
+        last_loop = -1
+        in_core = {}
+        mixed = 0  # loop steps holding both just-prelude'd tokens and others
+        for k, t in enumerate(d.step()):
+            if t.stage == TICK_PRELUDE_FIRST:
+                for i in range(t.n_rows):
+                    prelude_at[(t.seq[i], 0)] = k
+            elif t.stage == TICK_CODA:
+                for i in range(t.n_continue):
+                    prelude_at[(t.seq[i], t.decode_index[i] + 1)] = k
+            elif t.stage == TICK_LOOP:
+                keys = [(t.seq[i], t.decode_index[i]) for i in range(t.n_rows)]
+                # tokens whose prelude ran and which have not exited
+                live = {x for x in prelude_at if in_core.get(x, 0) < tables[x[0]][x[1]]}
+                if bs == 1:  # no row idles while such tokens wait
+                    assert len(keys) == min(4, len(live)), (k, keys, live)
+                fresh = [x for x in keys if in_core.get(x, 0) == 0 and prelude_at[x] > last_loop]
+                mixed += 0 < len(fresh) < len(keys)
+                for i, x in enumerate(keys):
+                    assert in_core.get(x, 0) == t.c[i]
+                    in_core[x] = t.c[i] + 1
+                last_loop = k
+        st = d.stats()
+        assert st["loop_rows"] == sum(int(x.sum()) for x in tables)
+        assert st["tokens"] == sum(len(x) for x in tables)
+        totals[bs] = st["loop_steps"]
+        assert (mixed == 0) == (bs == 2) or bs == 1
+    assert totals[2] >= totals[1] >= totals[0] - 1
+
+
+def test_gated_lookahead_last_decisions_are_checked():
+    """Gated mode with the lookahead: the last loop step's device decisions,
+    given after the run, must match the exits the scheduler applied."""
+    for mask, want in (([1], 0), ([0], -1)):
+        d = Driver(max_batch=2, max_active=1, r_max=2, max_seqs=1, max_pages=1, core_pages=2, gated=True,
+                   lookahead=True, threshold=0.5)
+        d.add_sequence(1, None, n_decode=1)
+        t = d.next()
+        assert t.stage == TICK_PRELUDE_FIRST
+        d.complete(t)
+        first = d.next()
+        assert first.stage == TICK_LOOP and first.c[0] == 0
+        assert d.complete(first) == 0
+        second = d.next()
+        assert second.stage == TICK_LOOP and second.c[0] == 1
+        assert d.loop_result(first, [0], [1]) == 0  # loop 1 did not end the token
+        assert d.complete(second) == 0  # loop r_max ends it
+        coda = d.next()
+        assert coda.stage == TICK_CODA
+        d.complete(coda)
+        assert d.next() is None
+        assert d.loop_result(second, mask, [0]) == want

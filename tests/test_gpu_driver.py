@@ -39,6 +39,26 @@ def _requests(shape, seed=40):
     return prompts, ndec, depths
 
 
+def _driver_ws(gm, rows, cfg):
+    """The runner's workspace: one stage workspace, or two (halves) when the
+    boundary stages have their own stream; error words start at zero."""
+    n = cdb.cdb_workspace_bytes(gm.desc, rows)
+    n = (n + 255) & ~255
+    return torch.zeros(2 * n if cfg.get("boundary_stream") else n, dtype=torch.uint8, device="cuda"), n
+
+
+def _ws_errors(ws, half):
+    return [cdb.cdb_read_device_error(ws), cdb.cdb_read_device_error(ws[half:])] if ws.numel() > half else \
+        [cdb.cdb_read_device_error(ws)]
+
+
+def _check_table_uploads(st, n_seqs, shape, max_pages):
+    """After the first whole-table upload, only changed sequences' blocks travel."""
+    full = n_seqs * (shape.r_max + 2) * max_pages * 4
+    assert st["pt_uploads"] >= 1
+    assert st["pt_upload_bytes"] == full + (st["pt_uploads"] - 1) * full // n_seqs
+
+
 def _decode_on_gpu(shape, gm, prompts, ndec, depths, kv_layout=drv.KV_FULL, **cfg):
     """depths[q] is None in gated mode."""
     """Prefill every prompt through the stage calls (one block per sequence),
@@ -81,10 +101,14 @@ def _decode_on_gpu(shape, gm, prompts, ndec, depths, kv_layout=drv.KV_FULL, **cf
     state = cdb.State(shape, n)
     scratch = torch.empty(d.scratch_bytes(shape.vocab), dtype=torch.uint8, device="cuda")
     out_ids = torch.full((n, max(ndec)), -1, dtype=torch.int32, device="cuda")
-    secs = d.run(gm.model, kv.c, state.c, scratch, first, ws.buf, tokens_out=out_ids)
-    torch.cuda.synchronize()
     assert cdb.cdb_read_device_error(ws.buf) == 0
-    return first, out_ids.cpu().numpy(), d.stats(), secs
+    rws, half = _driver_ws(gm, 256, cfg)
+    secs = d.run(gm.model, kv.c, state.c, scratch, first, rws, tokens_out=out_ids)
+    torch.cuda.synchronize()
+    assert _ws_errors(rws, half) == [0] * (2 if cfg.get("boundary_stream") else 1)
+    st = d.stats()
+    _check_table_uploads(st, n, shape, max_pages)
+    return first, out_ids.cpu().numpy(), st, secs
 
 
 def _check_against_oracle(shape, w, prompts, ndec, depths, first, ids, kv_layout):
@@ -121,7 +145,9 @@ def test_driver_decode_is_schedule_invariant_and_follows_oracle(kv_layout):
     runs = {}
     for name, cfg in (("refill", dict(max_batch=4, max_active=n)),
                       ("no-refill", dict(max_batch=3, max_active=n, refill=False)),
-                      ("refill-coda3", dict(max_batch=6, max_active=n, min_coda_batch=3))):
+                      ("refill-coda3", dict(max_batch=6, max_active=n, min_coda_batch=3)),
+                      ("refill-boundary-stream-1", dict(max_batch=4, max_active=n, boundary_stream=1)),
+                      ("refill-boundary-stream-2", dict(max_batch=4, max_active=n, boundary_stream=2))):
         first, ids, st, secs = _decode_on_gpu(s, gm, prompts, ndec, depths, kv_layout, **cfg)
         _say(f"[gpu]   {name}: {st} in {secs * 1e3:.1f} ms")
         assert st["tokens"] == sum(ndec)
@@ -151,14 +177,17 @@ def test_driver_decode_with_injection_is_schedule_invariant_and_follows_oracle(k
     n = len(prompts)
     runs = {}
     for name, cfg in (("refill", dict(max_batch=4, max_active=n)),
-                      ("no-refill", dict(max_batch=5, max_active=n, refill=False))):
+                      ("no-refill", dict(max_batch=5, max_active=n, refill=False)),
+                      ("refill-boundary-stream", dict(max_batch=4, max_active=n, min_coda_batch=2,
+                                                      boundary_stream=2))):
         first, ids, st, secs = _decode_on_gpu(s, gm, prompts, ndec, depths, kv_layout, **cfg)
         _say(f"[gpu]   {name}: {st} in {secs * 1e3:.1f} ms")
         assert st["tokens"] == sum(ndec)
         assert st["loop_rows"] == sum(int(x.sum()) for x in depths)
         runs[name] = (first, ids)
-    assert np.array_equal(runs["refill"][0], runs["no-refill"][0])
-    assert np.array_equal(runs["refill"][1], runs["no-refill"][1])
+    for name in runs:
+        assert np.array_equal(runs["refill"][0], runs[name][0]), name
+        assert np.array_equal(runs["refill"][1], runs[name][1]), name
     checked = _check_against_oracle(s, w, prompts, ndec, depths, *runs["refill"], kv_layout)
     _say(f"[gpu]   {checked} greedy ids checked against the oracle")
     assert checked >= 0.3 * (sum(ndec) + n)
@@ -235,14 +264,16 @@ def test_gated_driver_decode_is_schedule_invariant(lookahead):
     _say(f"[gpu] gated driver decode {s.name}, lookahead {lookahead}, threshold {thr:.4f}")
     runs = {}
     for name, cfg in (("refill", dict(max_batch=4, max_active=n)),
-                      ("no-refill", dict(max_batch=3, max_active=n, refill=False))):
+                      ("no-refill", dict(max_batch=3, max_active=n, refill=False)),
+                      ("refill-boundary-stream", dict(max_batch=4, max_active=n, boundary_stream=1))):
         first, ids, st, secs = _decode_on_gpu(s, gm, prompts, ndec, [None] * n, gated=True, lookahead=lookahead,
                                               threshold=thr, **cfg)
         _say(f"[gpu]   {name}: {st} in {secs * 1e3:.1f} ms")
         assert st["tokens"] == sum(ndec)
         runs[name] = (first, ids, st["loop_rows"])
-    a, b = runs["refill"], runs["no-refill"]
-    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1]) and a[2] == b[2]
+    a = runs["refill"]
+    for name, b in runs.items():
+        assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1]) and a[2] == b[2], name
     lo = sum(ndec) * (2 if lookahead else 1)
     assert lo <= a[2] < sum(ndec) * s.r_max  # some tokens exit early, none before the minimum depth
 
@@ -291,13 +322,13 @@ def _decode_with_driver_prefill(shape, gm, prompts, ndec, depths, chunk, **cfg):
     for q in range(n):
         d.add_request(prompts[q], depths[q])
     kv = cdb.PagedKV(shape, n, max_pages, tot, tot * R, tot)
-    ws = cdb.Workspace(gm.desc, max(256, chunk))
+    ws, half = _driver_ws(gm, max(256, chunk), cfg)
     state = cdb.State(shape, n)
     scratch = torch.empty(d.scratch_bytes(shape.vocab), dtype=torch.uint8, device="cuda")
     out_ids = torch.full((n, max(ndec)), -1, dtype=torch.int32, device="cuda")
-    secs = d.run(gm.model, kv.c, state.c, scratch, None, ws.buf, tokens_out=out_ids)
+    secs = d.run(gm.model, kv.c, state.c, scratch, None, ws, tokens_out=out_ids)
     torch.cuda.synchronize()
-    assert cdb.cdb_read_device_error(ws.buf) == 0
+    assert _ws_errors(ws, half) == [0] * (2 if cfg.get("boundary_stream") else 1)
     return out_ids.cpu().numpy(), d.stats(), secs
 
 
@@ -313,7 +344,8 @@ def test_driver_prefill_chunks_decode_like_the_oracle():
     runs = {}
     for name, cfg in (("refill", dict(max_batch=4, max_active=n)),
                       ("no-refill", dict(max_batch=3, max_active=n, refill=False)),
-                      ("two-at-a-time", dict(max_batch=2, max_active=2))):
+                      ("two-at-a-time", dict(max_batch=2, max_active=2)),
+                      ("boundary-stream", dict(max_batch=4, max_active=3, boundary_stream=2))):
         ids, st, secs = _decode_with_driver_prefill(s, gm, prompts, ndec, depths, chunk, **cfg)
         _say(f"[gpu]   {name}: {st} in {secs * 1e3:.1f} ms")
         assert st["tokens"] == sum(ndec)
@@ -339,14 +371,16 @@ def test_driver_decode_at_ouro_width_follows_oracle():
     prompts = [cdbgen.prompt_ids(s.vocab, 1, p, seed=46, stream=q)[0] for q, p in enumerate(plens)]
     depths = [cdbgen.draw_depths(cdbgen.OURO_DEPTHS, n, s.r_max, seed=47, stream=q) for q, n in enumerate(ndec)]
     runs = {}
-    for name, cfg in (("refill", dict(max_batch=3, max_active=4)), ("no-refill", dict(max_batch=4, max_active=4,
-                                                                                        refill=False))):
+    for name, cfg in (("refill", dict(max_batch=3, max_active=4)),
+                      ("no-refill", dict(max_batch=4, max_active=4, refill=False)),
+                      ("refill-boundary-stream", dict(max_batch=3, max_active=4, boundary_stream=1))):
         first, ids, st, secs = _decode_on_gpu(s, gm, prompts, ndec, depths, drv.KV_FULL, **cfg)
         _say(f"[gpu]   {name}: {st} in {secs * 1e3:.1f} ms")
         assert st["tokens"] == sum(ndec)
         runs[name] = (first, ids)
-    assert np.array_equal(runs["refill"][0], runs["no-refill"][0])
-    assert np.array_equal(runs["refill"][1], runs["no-refill"][1])
+    for name in runs:
+        assert np.array_equal(runs["refill"][0], runs[name][0]), name
+        assert np.array_equal(runs["refill"][1], runs[name][1]), name
     checked = _check_against_oracle(s, w, prompts, ndec, depths, *runs["refill"], drv.KV_FULL)
     _say(f"[gpu]   {checked} greedy ids checked against the oracle")
     assert checked >= 0.3 * (sum(ndec) + len(plens))
