@@ -103,6 +103,61 @@ def test_captured_loop_step_replays_for_any_row_count():
     torch.cuda.empty_cache()
 
 
+def test_device_row_count_in_eager_loop_step():
+    """An eager (uncaptured) loop step of 64 rows of capacity with a device row
+    count: for live counts below and at a 32-row tile and up to the capacity,
+    every row's results equal those of a call of exactly that many rows, and
+    outputs past the count are left alone."""
+    s = cdbgen.shrink(cdbgen.OURO, n_core=2)
+    w = cdbgen.model_weights(cdbgen.OURO)
+    w = dict(w, layers=w["layers"][:2])
+    cap = 64
+    rows_np = cdbgen.decode_snapshot(cap, cdbgen.OURO_DEPTHS, s.r_max, 512, 767, stream=91)
+    gm = cdb.DeviceModel(s, w)
+    pt, max_pages, n_pages = _own_pages(s, rows_np)
+    kv = cdb.PagedKV(s, cap, max_pages, 0, n_pages, 0, fill="random")
+    g = torch.Generator(device="cuda")
+    g.manual_seed(33)
+    kv.core.normal_(0.0, 1.0, generator=g)
+    kv.page_table.copy_(torch.from_numpy(pt))
+    state = cdb.State(s, cap)
+    state.h.normal_(0.0, 1.0, generator=g)
+    h0, kv0 = state.h.clone(), kv.core.clone()
+    ar = np.arange(cap, dtype=np.int32)
+    d_n = torch.full((1,), cap, dtype=torch.int32, device="cuda")
+    rows_d = cdb.Rows(ar, ar, rows_np["pos"], rows_np["c"], rows_np["depth"], d_n_rows=d_n)
+    out_d = cdb.StepOut(cap)
+    ws_d = cdb.Workspace(gm.desc, cap)
+    ws_e = cdb.Workspace(gm.desc, cap)
+    for n in (20, 32, 56, 64):
+        _say(f"[gpu] eager loop step at {cap} rows of capacity with {n} live rows, against a call of {n} rows")
+        state.h.copy_(h0)
+        kv.core.copy_(kv0)
+        sl = slice(0, n)
+        rows_e = cdb.Rows(ar[sl], ar[sl], rows_np["pos"][sl], rows_np["c"][sl], rows_np["depth"][sl])
+        out_e = cdb.StepOut(n)
+        cdb.cdb_loop_step(gm.model, kv.c, state.c, rows_e.c, out_e.c, ws_e.buf)
+        torch.cuda.synchronize()
+        assert cdb.cdb_read_device_error(ws_e.buf) == 0
+        want = (state.h.clone(), kv.core.clone())
+        state.h.copy_(h0)
+        kv.core.copy_(kv0)
+        d_n.fill_(n)
+        out_d.score.fill_(-1.0)
+        cdb.cdb_loop_step(gm.model, kv.c, state.c, rows_d.c, out_d.c, ws_d.buf)
+        torch.cuda.synchronize()
+        assert cdb.cdb_read_device_error(ws_d.buf) == 0
+        assert torch.equal(state.h, want[0])
+        assert torch.equal(kv.core, want[1])
+        cnt = out_e.counts.cpu().tolist()
+        assert out_d.counts.cpu().tolist() == cnt
+        for a, b in ((out_d.score, out_e.score), (out_d.mask, out_e.mask), (out_d.exit_next, out_e.exit_next)):
+            assert torch.equal(a[:n], b[:n])
+        assert bool((out_d.score[n:] == -1.0).all())
+        assert torch.equal(out_d.cont[:cnt[0]], out_e.cont[:cnt[0]])
+        assert torch.equal(out_d.exited[:cnt[1]], out_e.exited[:cnt[1]])
+
+
 def test_device_row_count_in_boundary_calls():
     """Prelude and coda with a device row count: the first n rows' states,
     logits and greedy ids equal an eager call of n rows; the other rows'
