@@ -486,17 +486,39 @@ __device__ __forceinline__ void qkv_block_epilogue(const QkvBlockInputs& in, con
 // the caches), double-buffered in registers.  Each wave owns its outputs, so
 // the epilogue runs from the accumulators: column n's RoPE / SwiGLU partner
 // n ^ 16 is element j ^ 8 of the same lane.
+//
+// Tile order (xcd_order): the grid is one-dimensional, padded to a multiple of
+// 8, and the dispatcher hands workgroup b to XCD b % 8.  With xcd_order 0 the
+// tasks run column group first (every row tile of a column group lands on a
+// different XCD); with 1 each XCD takes a contiguous range of tasks ordered
+// row tile first, so the row tiles that read one weight tile run together on
+// one XCD and share its L2.
 template <int EPI, bool LDS, int WM>
-__global__ __launch_bounds__(256) void k_gemm_mn(GemmArgs ga, EpiArgs ea) {
+__global__ __launch_bounds__(256) void k_gemm_mn(GemmArgs ga, EpiArgs ea, int xcd_order) {
     static_assert(WM == 1 || WM == 2, "one or two m-tiles per wave");
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int KS = ga.K >> 4;
     const int stripes = ga.N >> 5;
     const int mtiles = (gemm_rows(ga.M) + 31) >> 5;  // m-tiles the activation buffer holds
-    const int s = blockIdx.z;
+    const int gx = (stripes + 3) / 4, gy = (ga.M + 64 * WM - 1) / (64 * WM), tasks = gx * gy * ga.S;
+    int bx, by, s;
+    if (xcd_order) {
+        const int per = (tasks + 7) / 8;
+        const int t = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
+        if (t >= tasks) return;
+        by = t % gy;
+        s = (t / gy) % ga.S;
+        bx = t / (gy * ga.S);
+    } else {
+        const int t = blockIdx.x;
+        if (t >= tasks) return;
+        bx = t % gx;
+        by = (t / gx) % gy;
+        s = t / (gx * gy);
+    }
     const int k0 = (int)(((long)s * KS) / ga.S), k1 = (int)(((long)(s + 1) * KS) / ga.S);
-    const int nt0 = blockIdx.x * 4 + (wave & 1) * 2;   // first stripe of this wave
-    const int mt0 = blockIdx.y * 2 * WM + (wave >> 1) * WM;  // first m-tile of this wave
+    const int nt0 = bx * 4 + (wave & 1) * 2;   // first stripe of this wave
+    const int mt0 = by * 2 * WM + (wave >> 1) * WM;  // first m-tile of this wave
 
     floatx16 acc[2][WM];
 #pragma unroll
@@ -563,7 +585,7 @@ __global__ __launch_bounds__(256) void k_gemm_mn(GemmArgs ga, EpiArgs ea) {
         constexpr int LPW = TPS / 4;     // loads per wave per stage
         static_assert(TPS % 4 == 0, "a stage's tiles split evenly over the 4 waves");
         extern __shared__ __align__(16) unsigned char lds_ring[];
-        const int ntb = blockIdx.x * 4, mtb = blockIdx.y * 2 * WM;
+        const int ntb = bx * 4, mtb = by * 2 * WM;
         const u32x4* Wg = reinterpret_cast<const u32x4*>(ga.Wp);
         const u32x4* Xg = reinterpret_cast<const u32x4*>(ga.X);
         const int nst = (k1 - k0 + CH - 1) / CH;
@@ -646,8 +668,16 @@ __global__ __launch_bounds__(256) void k_gemm_mn(GemmArgs ga, EpiArgs ea) {
 
 // Which tile-kernel path a projection takes: the LDS-staged one pays off for
 // the wide projections (gate/up and a full-width LM head: 20% faster at 512
-// rows); q/k/v, O and down are faster with direct loads.
-static bool mn_lds(int epi, int N) { return epi == EPI_SWIGLU || (epi == EPI_STORE && N >= 8192); }
+// rows) and for split-K projections whose splits run long k loops (Huginn-
+// shaped O and down, 165 and 560 k steps per split at 512 rows: 64 -> 52 and
+// 218 -> 174 us); q/k/v and the short-split O and down (Ouro-shaped: 32 and 88
+// k steps) are faster with direct loads.
+static int mn_splits(int N, int K, int M, int rows_per_tile);
+static int lds_wave_mtiles(int M) { return ((M + 63) / 64) % 2 ? 1 : 2; }
+static bool mn_lds(int epi, int N, int K, int M) {
+    if (epi == EPI_SWIGLU || (epi == EPI_STORE && N >= 8192)) return true;
+    return epi == EPI_PARTIAL && (K / 16) / mn_splits(N, K, M, 64 * lds_wave_mtiles(M)) >= 128;
+}
 
 // m-tiles per wave of the tile kernel: 2 (128-row workgroup tiles) or 1 (64-row
 // tiles; the sums are the same either way).  Direct loads: 1 for q/k/v when
@@ -658,22 +688,33 @@ static bool mn_lds(int epi, int N) { return epi == EPI_SWIGLU || (epi == EPI_STO
 // every size from 272 to 512 rows but 480-512.  LDS-staged: 1 when the rows
 // span an odd number of 64-row tiles, which 128-row tiles would pad by 64 rows
 // (gate/up at 300 rows: 36.0 -> 30.1 us; at 512 rows 64-row tiles gain nothing).
-static int mn_wave_mtiles(int epi, int N, int M) {
-    if (mn_lds(epi, N)) return ((M + 63) / 64) % 2 ? 1 : 2;
+static int mn_wave_mtiles(int epi, int N, int K, int M) {
+    if (mn_lds(epi, N, K, M)) return lds_wave_mtiles(M);
     return epi == EPI_QKV && ((M + 63) / 64) * ((N / 32 + 3) / 4) <= 256 ? 1 : 2;
 }
 
-// Launch shape for M > kMaxRows rows (k_gemm_mn): K split only for the
-// split-K partial epilogue, until the grid covers the chip.
-GemmShape gemm_shape_mn(int N, int K, int M, int epi) {
-    const int rows_per_tile = 64 * mn_wave_mtiles(epi, N, M);
+// K splits of the split-K partial epilogue: doubled until the grid covers the
+// chip, keeping at least 32 k steps per split.
+static int mn_splits(int N, int K, int M, int rows_per_tile) {
     const int tiles = ((N / 32 + 3) / 4) * ((M + rows_per_tile - 1) / rows_per_tile);
     const int KS = K / 16;
     int S = 1;
-    if (epi == EPI_PARTIAL)
-        while (tiles * S < 256 && KS / (S * 2) >= 32) S *= 2;
+    while (tiles * S < 256 && KS / (S * 2) >= 32) S *= 2;
+    return S;
+}
+
+// Launch shape for M > kMaxRows rows (k_gemm_mn): K split only for the
+// split-K partial epilogue.
+GemmShape gemm_shape_mn(int N, int K, int M, int epi) {
+    const int S = epi == EPI_PARTIAL ? mn_splits(N, K, M, 64 * mn_wave_mtiles(epi, N, K, M)) : 1;
     return GemmShape{N, K, S, 4, 4};
 }
+
+// XCD-aware tile order (see k_gemm_mn) for grids of more than two workgroups
+// per CU (LM heads and Huginn-shaped gate/up at 512 rows: 615 -> 485 and
+// 325 -> 292 us) and for LDS-staged split-K grids; the others keep the plain
+// order, which is as fast or up to 5% faster for them.
+static int mn_xcd_order(bool lds, int tasks, int S) { return tasks > 512 || (lds && S > 1) ? 1 : 0; }
 
 GemmShape gemm_shape(int N, int K, int epi, int M) {
     // S and KW fix every wave's K range and so the summation order of each
@@ -742,7 +783,8 @@ static hipError_t launch_epi(const GemmArgs& ga, const EpiArgs& ea, int ns, hipS
 
 template <int EPI, bool LDS, int WM>
 static hipError_t launch_mn_wm(const GemmArgs& ga, const EpiArgs& ea, hipStream_t st) {
-    dim3 grid((ga.N / 32 + 3) / 4, (ga.M + 64 * WM - 1) / (64 * WM), ga.S);
+    const int tasks = (ga.N / 32 + 3) / 4 * ((ga.M + 64 * WM - 1) / (64 * WM)) * ga.S;
+    const dim3 grid((tasks + 7) / 8 * 8);
     // dynamic LDS: the ring of the LDS path, the q/k/v epilogue's staging blocks
     constexpr size_t ring = LDS ? 2 * 4 * (4 + 2 * WM) * 1024 : 0;
     constexpr size_t stage = EPI == EPI_QKV ? 4 * 64 * (32 * WM + 1) * 4 : 0;
@@ -756,16 +798,16 @@ static hipError_t launch_mn_wm(const GemmArgs& ga, const EpiArgs& ea, hipStream_
             attr_set = true;
         }
     }
-    k_gemm_mn<EPI, LDS, WM><<<grid, 256, smem, st>>>(ga, ea);
+    k_gemm_mn<EPI, LDS, WM><<<grid, 256, smem, st>>>(ga, ea, mn_xcd_order(LDS, tasks, ga.S));
     return hipGetLastError();
 }
 
 template <int EPI>
 static hipError_t launch_mn(const GemmArgs& ga, const EpiArgs& ea, hipStream_t st) {
-    if (mn_lds(EPI, ga.N))
-        return mn_wave_mtiles(EPI, ga.N, ga.M) == 1 ? launch_mn_wm<EPI, true, 1>(ga, ea, st)
-                                                    : launch_mn_wm<EPI, true, 2>(ga, ea, st);
-    if (mn_wave_mtiles(EPI, ga.N, ga.M) == 1) return launch_mn_wm<EPI, false, 1>(ga, ea, st);
+    const int wm = mn_wave_mtiles(EPI, ga.N, ga.K, ga.M);
+    if (mn_lds(EPI, ga.N, ga.K, ga.M))
+        return wm == 1 ? launch_mn_wm<EPI, true, 1>(ga, ea, st) : launch_mn_wm<EPI, true, 2>(ga, ea, st);
+    if (wm == 1) return launch_mn_wm<EPI, false, 1>(ga, ea, st);
     return launch_mn_wm<EPI, false, 2>(ga, ea, st);
 }
 
