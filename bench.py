@@ -1015,6 +1015,8 @@ def main():
     ap.add_argument("--no-e2e", action="store_true", help="skip the whole-decode driver runs")
     ap.add_argument("--no-prefill", action="store_true", help="skip the chunked-prefill timing")
     ap.add_argument("--no-sweep", action="store_true", help="skip the loop-step batch-size sweep and the latency-model grid")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="skip the graph-replay leg (its replays at fewer live rows would mix into per-kernel profiles)")
     ap.add_argument("--serving-requests", type=int, default=200,
                     help="requests in the serving-trace run (0 = skip; 2000 is the full trace)")
     ap.add_argument("--huginn-decode", type=int, default=512,
@@ -1080,10 +1082,12 @@ def main():
     sb = step_bytes(shape, rows_np)
     log(f"{ms:.3f} ms/step, {value:.0f} rows/s, step bytes {sb / 1e9:.2f} GB -> {sb / (ms * 1e-3) / 1e9:.0f} GB/s")
 
-    try:
-        graph = graph_leg(dm, kv, state, rows_np, args.steps)
-    except RuntimeError as e:  # a capture the runtime refuses is reported, not fatal
-        graph = {"error": str(e)}
+    graph = None
+    if not args.no_graph:
+        try:
+            graph = graph_leg(dm, kv, state, rows_np, args.steps)
+        except RuntimeError as e:  # a capture the runtime refuses is reported, not fatal
+            graph = {"error": str(e)}
     copy_gbs = copy_peak()
 
     attn_ms = time_attention(shape, kv, rows, n_rows, args.steps * shape.n_core)
