@@ -384,13 +384,19 @@ __global__ __launch_bounds__(256) void k_compact(int M, const uint8_t* __restric
 }
 
 // Last-exited cache: for each exiting row (depth < r_max), copy its K/V at pos
-// from plane depth to planes depth+1..r_max, for the core layer blockIdx.y;
-// depth is the row's exit depth, 0 for a continuing row.  Workgroup (0, 0)
-// also runs the step's stable compaction (the copy needs none of its output).
-// The destination page ids are read into LDS first and each chunk of the
-// source entry (up to 8 16-byte vectors per thread) is loaded once, before
-// any store: source and destinations share the pool, so a load left after a
-// store would wait for it, one round trip per vector and plane.
+// from plane depth to planes depth+1..r_max.  blockIdx.y = core layer * parts +
+// part: a workgroup takes the destination planes depth+1+4*part .. +3 of one
+// layer, so deep loops (31 destinations at r_max 32) spread over several
+// workgroups.  depth is the row's exit depth, 0 for a continuing row.
+// Workgroup (0, 0) also runs the step's stable compaction (the copy needs none
+// of its output).  The destination page ids are read into LDS first and each
+// chunk of the source entry (up to 8 16-byte vectors per thread) is loaded
+// once, before any store: source and destinations share the pool, so a load
+// left after a store would wait for it, one round trip per vector and plane.
+// Planes that share a page (shared layouts) are written once, by the lowest
+// plane that maps to it, and not at all when it is the source page.
+constexpr int kCopyPlanesPerWg = 4;
+
 __global__ __launch_bounds__(256) void k_copy_on_exit(int H, int hd, int r_max, KvTarget kv,
                                                       const int32_t* __restrict__ seq, const int32_t* __restrict__ pos,
                                                       const int32_t* __restrict__ depth,
@@ -404,23 +410,26 @@ __global__ __launch_bounds__(256) void k_copy_on_exit(int H, int hd, int r_max, 
     if (i >= n) return;
     const int dep = depth[i];
     if (dep >= r_max || dep < 1) return;
+    const int parts = max(1, (r_max - 1 + kCopyPlanesPerWg - 1) / kCopyPlanesPerWg);
+    const int l = blockIdx.y / parts, part = blockIdx.y - l * parts;
+    const int n_dst = r_max - dep;
+    const int k0 = part * kCopyPlanesPerWg, k1 = min(n_dst, k0 + kCopyPlanesPerWg);
+    if (k0 >= k1) return;
     const int sq = seq[i], ps = pos[i], pg = ps / kPage;
-    const int l = blockIdx.y;
     if (sq < 0 || sq >= kv.max_seqs || pg < 0 || pg >= kv.max_pages) {
-        if (threadIdx.x == 0) set_err(err, CDB_DEV_BAD_INDEX);
+        if (threadIdx.x == 0 && part == 0) set_err(err, CDB_DEV_BAD_INDEX);
         return;
     }
     const int32_t* pt = kv.page_table + (size_t)sq * kv.n_planes * kv.max_pages;
     const int src = pt[(size_t)dep * kv.max_pages + pg];
     if (src < 0 || src >= kv.n_pages) {
-        if (threadIdx.x == 0) set_err(err, CDB_DEV_UNMAPPED_PAGE);
+        if (threadIdx.x == 0 && part == 0) set_err(err, CDB_DEV_UNMAPPED_PAGE);
         return;
     }
-    const int n_dst = r_max - dep;
     if (threadIdx.x < n_dst) {
         const int dst = pt[(size_t)(dep + 1 + threadIdx.x) * kv.max_pages + pg];
         const bool ok = dst >= 0 && dst < kv.n_pages;
-        if (!ok) set_err(err, CDB_DEV_UNMAPPED_PAGE);
+        if (!ok && threadIdx.x >= k0 && threadIdx.x < k1) set_err(err, CDB_DEV_UNMAPPED_PAGE);
         s_dst[threadIdx.x] = ok ? dst : -1;
     }
     __syncthreads();
@@ -433,6 +442,14 @@ __global__ __launch_bounds__(256) void k_copy_on_exit(int H, int hd, int r_max, 
         const int kvh = v / vec_per_head, e = v - kvh * vec_per_head;
         return ((size_t)kvh * kPage + tok) * hd + e * 8;
     };
+    // this workgroup's planes that receive a copy
+    auto writes = [&](int k) {
+        const int dst = s_dst[k];
+        if (dst < 0 || dst == src) return false;
+        for (int j = 0; j < k; ++j)
+            if (s_dst[j] == dst) return false;
+        return true;
+    };
     const uint16_t* src_base = kv.pool + kv_offset(l, src, kv.n_pages, 0, 0, H, 0, hd);
     constexpr int VPT = 8;  // vectors per thread per chunk
     for (int base = 0; base < nvec; base += VPT * 256) {
@@ -444,12 +461,9 @@ __global__ __launch_bounds__(256) void k_copy_on_exit(int H, int hd, int r_max, 
             off[u] = v < nvec ? in_page(v) : 0;
             if (v < nvec) buf[u] = *reinterpret_cast<const uint4*>(src_base + off[u]);
         }
-        int prev = src;  // aliased planes (shared layouts) map one page: copy it once
-        for (int k = 0; k < n_dst; ++k) {
-            const int dst = s_dst[k];
-            if (dst < 0 || dst == src || dst == prev) continue;
-            prev = dst;
-            uint16_t* dst_base = kv.pool + kv_offset(l, dst, kv.n_pages, 0, 0, H, 0, hd);
+        for (int k = k0; k < k1; ++k) {
+            if (!writes(k)) continue;
+            uint16_t* dst_base = kv.pool + kv_offset(l, s_dst[k], kv.n_pages, 0, 0, H, 0, hd);
 #pragma unroll
             for (int u = 0; u < VPT; ++u) {
                 const int v = base + threadIdx.x + u * 256;
@@ -627,7 +641,8 @@ hipError_t launch_copy_on_exit(const cdb_model_desc& md, const cdb_kv& kv, const
     t.max_seqs = kv.max_seqs;
     t.max_pages = kv.max_pages;
     t.n_planes = md.r_max + 2;
-    dim3 grid(r.n_rows, md.n_core);
+    const int parts = (md.r_max - 1 + kCopyPlanesPerWg - 1) / kCopyPlanesPerWg;
+    dim3 grid(r.n_rows, md.n_core * std::max(parts, 1));
     k_copy_on_exit<<<grid, 256, 0, st>>>(md.n_heads, md.head_dim, md.r_max, t, r.seq, r.pos, deff, mask, cont, exited,
                                          counts, err, r.d_n_rows);
     return hipGetLastError();
