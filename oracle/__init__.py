@@ -16,6 +16,10 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "liboracle.so")
 LIB32_PATH = os.path.join(_HERE, "liboracle_acc32.so")
+# fp32-accumulator builds that sum the projections' dot products in another
+# order (reverse, blocks of 32): further fp32 realizations for tolerance sizing
+LIB32_ORDER_PATHS = {1: os.path.join(_HERE, "liboracle_acc32_rev.so"),
+                     2: os.path.join(_HERE, "liboracle_acc32_blk32.so")}
 _SRC = os.path.join(_HERE, "cdb_oracle.c")
 
 ORC_OK, ORC_ERR_ARG, ORC_ERR_UNMAPPED = 0, 1, 2
@@ -25,7 +29,9 @@ def build(force: bool = True) -> str:
     """Compile the oracle with gcc (plain C, OpenMP over independent rows): the
     fp64 oracle, and the same source with fp32 accumulators (used only to size
     tolerances)."""
-    for path, extra in ((LIB_PATH, []), (LIB32_PATH, ["-DORC_ACC=float"])):
+    builds = [(LIB_PATH, []), (LIB32_PATH, ["-DORC_ACC=float"])] + \
+        [(p, ["-DORC_ACC=float", f"-DORC_SUM_ORDER={k}"]) for k, p in LIB32_ORDER_PATHS.items()]
+    for path, extra in builds:
         if force or not os.path.exists(path):
             tmp = path + ".tmp"
             subprocess.check_call(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-Wall", *extra, "-o", tmp, _SRC,
@@ -37,10 +43,14 @@ def build(force: bool = True) -> str:
 _libs = {}
 
 
-def lib(acc32: bool = False):
-    key = bool(acc32)
+def lib(acc32: bool = False, sum_order: int = 0):
+    """The fp64 oracle, or with acc32 an fp32-accumulator build summing in
+    sum_order (0 index order, 1 reverse, 2 blocks of 32)."""
+    if sum_order and not acc32:
+        raise ValueError("other summation orders exist only as fp32 builds")
+    key = (bool(acc32), int(sum_order))
     if key not in _libs:
-        path = LIB32_PATH if acc32 else LIB_PATH
+        path = LIB32_ORDER_PATHS[sum_order] if sum_order else (LIB32_PATH if acc32 else LIB_PATH)
         if not os.path.exists(path) or os.path.getmtime(path) < os.path.getmtime(_SRC):
             build()
         L = C.CDLL(path)
@@ -110,12 +120,13 @@ class Model:
     storage mode (bf16_storage=True rounds what the model keeps in bf16)."""
 
     def __init__(self, shape, weights: Dict[str, object], bf16_storage: bool = True, acc32: bool = False,
-                 kv_layout: int = KV_FULL):
-        """acc32: run the same steps with fp32 accumulators (tolerance sizing only).
+                 kv_layout: int = KV_FULL, sum_order: int = 0):
+        """acc32: run the same steps with fp32 accumulators (tolerance sizing
+        only), summing the projections in sum_order (0, 1 reverse, 2 blocks of 32).
         kv_layout: the core KV layout the dense references follow (the paged
         operators follow whatever the page table maps)."""
         self.shape = shape
-        self.L = lib(acc32)
+        self.L = lib(acc32, sum_order)
         self.desc = OrcDesc(shape.d, shape.n_heads, shape.head_dim, shape.d_ff, shape.vocab, shape.n_prelude,
                             shape.n_core, shape.n_coda, shape.r_max, shape.injection, shape.exit_kind,
                             1 if bf16_storage else 0, shape.rms_eps, shape.rope_base, kv_layout)

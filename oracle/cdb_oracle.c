@@ -64,6 +64,14 @@
 #define ORC_ACC double
 #endif
 typedef ORC_ACC acc_t;
+/* Summation order of the projections' dot products: 0 in index order (the
+ * oracle), 1 in reverse index order, 2 in blocks of 32 terms whose partial sums
+ * are then added in order.  Orders 1 and 2 are built only with fp32
+ * accumulators, as further samples of how far an fp32 implementation that sums
+ * in another order drifts from fp64. */
+#ifndef ORC_SUM_ORDER
+#define ORC_SUM_ORDER 0
+#endif
 
 /* ------------------------------------------------------------------ layouts */
 
@@ -124,7 +132,17 @@ static void matvec(const uint16_t* W, int n_out, int n_in, const double* x, doub
     for (int o = 0; o < n_out; ++o) {
         const uint16_t* w = W + (size_t)o * n_in;
         acc_t acc = 0.0;
+#if ORC_SUM_ORDER == 1
+        for (int i = n_in - 1; i >= 0; --i) acc += (acc_t)bf(w[i]) * (acc_t)x[i];
+#elif ORC_SUM_ORDER == 2
+        for (int b = 0; b < n_in; b += 32) {
+            acc_t part = 0.0;
+            for (int i = b; i < n_in && i < b + 32; ++i) part += (acc_t)bf(w[i]) * (acc_t)x[i];
+            acc += part;
+        }
+#else
         for (int i = 0; i < n_in; ++i) acc += (acc_t)bf(w[i]) * (acc_t)x[i];
+#endif
         y[o] = acc;
     }
 }

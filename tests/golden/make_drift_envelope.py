@@ -13,6 +13,27 @@ sys.path[:0] = [os.path.dirname(HERE), os.path.dirname(os.path.dirname(HERE))]
 from oracle_side import DriftRun, free_run_case, run_schedule  # noqa: E402
 
 
+def spread(calls, key):
+    """How far one realization exceeds the largest of the others (leave-one-out),
+    at most over the run, among the realizations that have drifted at that call
+    (at least a tenth of the call's largest distance; a call with fewer than two
+    such is skipped): the device, one more fp32 implementation, may exceed the
+    realizations' largest distance by as much."""
+    worst = 1.0
+    for c in calls:
+        each = c.get(key + "_each")
+        if not each:
+            continue
+        top = max(each)
+        drifted = [v for v in each if top > 0 and v >= 0.1 * top]
+        if len(drifted) < 2:
+            continue
+        for r, v in enumerate(drifted):
+            others = max(drifted[:r] + drifted[r + 1:])
+            worst = max(worst, v / others)
+    return worst
+
+
 def main(name):
     s, w, prompts, depths, n_dec, max_batch = free_run_case(name)
     t0 = time.time()
@@ -25,6 +46,7 @@ def main(name):
     for key in ("h_max", "h_mean", "h_rel", "logit_max", "logit_mean", "logit_rel", "score_max"):
         vals = [c[key] for c in dr.calls if key in c]
         out["run_" + key] = max(vals) if vals else 0.0
+    out["spread"] = {key: spread(dr.calls, key) for key in ("h_max", "logit_max", "score_max")}
     path = os.path.join(HERE, f"drift_{name}.json")
     with open(path, "w") as f:
         json.dump(out, f, indent=1)

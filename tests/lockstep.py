@@ -55,7 +55,15 @@ class Lockstep:
         self.resync = resync
         self.sensitivity = sensitivity
         self.envelope = envelope["calls"] if envelope else None
+        # free-running envelopes: how far one of the oracle's realizations exceeds
+        # the largest of the others (per output kind), for the report
+        self.spread = envelope.get("spread", {}) if envelope else {}
+        self.rec = None  # this call's envelope record (free-running runs)
+        self.single_row = {"calls": 0, "max_ratio": 0.0}
         self.tol = (TOL_MAX, TOL_MEAN)
+        self.score_tol = TOL_MAX
+        self.w_exit = (np.asarray(weights["w_exit"], np.uint16).astype(np.uint32) << 16).view(np.float32).astype(
+            np.float64)
         self.self_diff = {"max": 0.0, "mean": 0.0}
         self.s = s = shape
         self.R = s.r_max
@@ -93,13 +101,27 @@ class Lockstep:
     def _cmp(self, key_max, key_mean, got, want, what, key_rel=None):
         """max-abs is checked per call; mean-abs is a statistic of the whole
         result, checked over the run by check_means() (a call of two rows is
-        dominated by single bf16 rounding flips)."""
+        dominated by single bf16 rounding flips).  In a free-running run a call
+        of one row is bounded instead by the row's relative L2 error and its
+        mean-abs error, each at DRIFT_FACTOR times the realizations': the largest
+        of one row's d errors is too heavy-tailed a statistic for a sample of
+        realizations to bound (its ratio to that bound is reported)."""
         d = np.abs(np.asarray(got, np.float64) - want)
         mx, mn = float(d.max()) if d.size else 0.0, float(d.mean()) if d.size else 0.0
         self.errors[key_max] = max(self.errors[key_max], mx)
-        self.ratio[key_max] = max(self.ratio.get(key_max, 0.0), mx / self.tol[0])
+        rel = row_rel(got, want) if key_rel else 0.0
         if key_rel:
-            self.errors[key_rel] = max(self.errors[key_rel], row_rel(got, want))
+            self.errors[key_rel] = max(self.errors[key_rel], rel)
+        one_row = self.rec is not None and np.atleast_2d(want).shape[0] == 1 and key_rel is not None
+        if one_row:
+            self.single_row["calls"] += 1
+            self.single_row["max_ratio"] = max(self.single_row["max_ratio"], mx / self.tol[0])
+            rb = max(DRIFT_FACTOR * self.rec[key_rel], 1e-12)
+            self.ratio[key_rel] = max(self.ratio.get(key_rel, 0.0), rel / rb)
+            assert rel <= rb and mn <= self.tol[1], \
+                f"{what} (one row): rel {rel:.3e} (bound {rb:.3e}), mean abs {mn:.3e} (bound {self.tol[1]:.3e})"
+        else:
+            self.ratio[key_max] = max(self.ratio.get(key_max, 0.0), mx / self.tol[0])
         if key_mean:
             self.errors[key_mean] = max(self.errors[key_mean], mn)
             acc = self.run_sums.setdefault(key_mean, [0.0, 0, 0.0])
@@ -107,7 +129,7 @@ class Lockstep:
             acc[1] += d.size
             acc[2] += self.tol[1] * d.size
         tmax = self.tol[0]
-        assert mx <= tmax, f"{what}: max abs {mx:.3e}, mean abs {mn:.3e} (max bound {tmax:.3e})"
+        assert one_row or mx <= tmax, f"{what}: max abs {mx:.3e}, mean abs {mn:.3e} (max bound {tmax:.3e})"
 
     def check_means(self):
         """Mean-abs error of each output kind over the run against the
@@ -160,11 +182,14 @@ class Lockstep:
         if variants is not None:
             mx = max(float(np.abs(v - got64).max()) for v in variants)
             mn = max(float(np.abs(v - got64).mean()) for v in variants)
-        elif self.envelope is not None:
-            rec = self.envelope[k]
+        self.rec = None
+        if variants is None and self.envelope is not None:
+            rec = self.rec = self.envelope[k]
             assert rec["stage"] == stage and rec["rows"] == len(got64), (k, rec, stage, len(got64))
             key = "logit" if stage == "coda" else "h"
             mx, mn = rec[key + "_max"], rec[key + "_mean"]
+            if stage == "loop":
+                self.score_tol = max(TOL_MAX, DRIFT_FACTOR * rec["score_max"])
         if mx is None:
             return
         self.self_diff["max"] = max(self.self_diff["max"], mx)
@@ -227,9 +252,21 @@ class Lockstep:
             pend = self.opending[slots].copy()
             exit_now = (pend != 0) | (cs + 1 == self.R)
             deps = np.where(exit_now, cs + 1, self.R).astype(np.int32)
+        # states before the call on both sides (the exit score of the
+        # convergence criterion is a distance from them)
+        idx = torch.as_tensor(slots, dtype=torch.long, device="cuda")
+        o_in = self.oh[slots].copy()
+        g_in = self.gstate.h[idx].double().cpu().numpy()
+        # each realization gives its states and its exit scores: the score takes
+        # its own bound from the realizations' scores
         g32 = self._oracle_bound(lambda m: oracle.loop_step(m, self.op, self.oh, self.oe, slots, seqs, poss, cs, deps),
-                                 lambda _: self.oh[slots].copy())
+                                 lambda r: (self.oh[slots].copy(), np.array(r["score"], np.float64)))
         o = self.o.loop(seqs, poss, cs, deps)
+        self.score_tol = TOL_MAX
+        if g32 is not None:
+            dscore = max(float(np.abs(sc - o["score"]).max()) for _, sc in g32)
+            self.score_tol = max(TOL_MAX, DRIFT_FACTOR * dscore)
+            g32 = [h for h, _ in g32]
         self._set_bound(g32, self.oh[slots], "loop")
         rows = cdb.Rows(slots, seqs, poss, cs, None if gated else deps)
         out = cdb.StepOut(len(seqs))
@@ -246,11 +283,26 @@ class Lockstep:
         assert out.mask[:n].cpu().numpy().tolist() == o["exit_mask"].tolist()
         assert out.cont[:cnt[0]].cpu().numpy().tolist() == o["cont"].tolist()
         assert out.exited[:cnt[1]].cpu().numpy().tolist() == o["exited"].tolist()
+        g_out = self.gstate.h[idx].double().cpu().numpy()
+        o_out = self.oh[slots].copy()
         self._cmp_state(slots, "loop-step state")
-        sc = out.score[:n].cpu().numpy()
+        sc = out.score[:n].cpu().numpy().astype(np.float64)
+        # the device's score is the exit signal of the device's own states
+        own = self._exit_signal(g_out, g_in)
+        assert (np.abs(sc - own) <= 1e-4 + 1e-5 * np.abs(own)).all(), \
+            f"exit score against the device's own states: {np.abs(sc - own).max():.3e}"
+        # against the oracle: the realizations' score drift; for the convergence
+        # distance ||h - h_in||_2 also what the state differences on both sides
+        # allow (triangle inequality), which the state bounds above already limit
         d = np.abs(sc - o["score"])
+        bound = np.full(n, self.score_tol)
+        if self.s.exit_kind == 1:
+            derived = np.linalg.norm((g_out - o_out) - (g_in - o_in), axis=1)
+            bound = np.maximum(bound, derived * (1 + 1e-6) + 1e-4 + 1e-5 * np.abs(o["score"]))
+        self.score_bound = bound
         self.errors["score_max"] = max(self.errors["score_max"], float(d.max()))
-        assert float(d.max()) <= self.tol[0], f"exit score max abs {d.max():.3e}"
+        self.ratio["score_max"] = max(self.ratio.get("score_max", 0.0), float((d / bound).max()))
+        assert (d <= bound).all(), f"exit score max abs {d.max():.3e} (bound {bound[np.argmax(d / bound)]:.3e})"
         dev_next = out.exit_next[:n].cpu().numpy()
         if not gated:
             # replayed depths: the next loop is the last one exactly when c + 2 == depth
@@ -266,6 +318,14 @@ class Lockstep:
             print(f"[lockstep] {self.calls} max errors {self.errors}", flush=True)
         return o
 
+    def _exit_signal(self, h, h_in):
+        """The exit signal of states h (rows) after a loop from h_in, in fp64:
+        ||h - h_in||_2, or sigmoid(w_exit . RMSNorm(h)) (Section 4.3; App. C.2)."""
+        if self.s.exit_kind == 1:
+            return np.linalg.norm(h - h_in, axis=1)
+        nrm = h / np.sqrt(np.mean(h * h, axis=1, keepdims=True) + self.s.rms_eps)
+        return 1.0 / (1.0 + np.exp(-(nrm @ self.w_exit)))
+
     def _gate_next(self, cs, slots, o, dev_next, pend):
         """The oracle's decisions for the next loop from its own scores; a
         device decision may differ only where the oracle's score lies within
@@ -275,7 +335,7 @@ class Lockstep:
         exited = o["exit_mask"] != 0
         self.gate_stats["decisions"] += int((~exited).sum())
         self.gate_stats["exits_before_r_max"] += int((exited & (cs + 1 < self.R)).sum())
-        near = np.abs(o["score"] - thr) <= self.tol[0]
+        near = np.abs(o["score"] - thr) <= self.score_bound
         self.gate_stats["near_threshold"] += int((near & ~exited).sum())
         diff = (dev_next != o_next) & ~exited
         assert not (diff & ~near).any(), f"exit decisions differ away from the threshold: {o['score'][diff]}"

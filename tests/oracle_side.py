@@ -31,10 +31,10 @@ class OracleSide:
     drift realizations perturb or round the state there)."""
 
     def __init__(self, shape, weights, seq_lens: List[int], kv_layout: int = 0, extra_pages: int = 0,
-                 bf16_storage: bool = True, acc32: bool = False, state_hook=None):
+                 bf16_storage: bool = True, acc32: bool = False, state_hook=None, sum_order: int = 0):
         s = self.s = shape
         self.R = s.r_max
-        self.om = oracle.Model(s, weights, bf16_storage=bf16_storage, acc32=acc32)
+        self.om = oracle.Model(s, weights, bf16_storage=bf16_storage, acc32=acc32, sum_order=sum_order)
         n_seq = len(seq_lens)
         self.max_pages = max(cdbgen.pages_for(t) for t in seq_lens)
         tot = sum(cdbgen.pages_for(t) for t in seq_lens) + extra_pages
@@ -155,7 +155,20 @@ def free_run_case(name: str):
     """Inputs of a free-running lockstep run (no resync): the model, its
     weights, prompts, per-token depths, decode lengths and batch size.
     ouro24: the Ouro-shaped model at full depth (24 core layers, r_max 4),
-    2 sequences, prompt 16, decode 6, config 2's depth distribution."""
+    2 sequences, prompt 16, decode 6, config 2's depth distribution.
+    huginn4: the Huginn-shaped model whole (2 prelude, 4 recurrent layers with
+    the injection adapter looped up to 32 times, 2 coda), 2 sequences, prompt
+    3, decode 3, config 3's depth distribution."""
+    if name == "huginn4":
+        s = cdbgen.HUGINN
+        P, N, n_seqs, stream = 3, 3, 2, 20
+        depth_spec = cdbgen.WORKLOADS[3].depth
+        w = cdbgen.model_weights(s)
+        prompts = [cdbgen.prompt_ids(s.vocab, 1, P, stream=stream + q)[0] for q in range(n_seqs)]
+        depths = [np.concatenate([np.full(P, s.r_max, np.int32),
+                                  cdbgen.draw_depths(depth_spec, N, s.r_max, stream=stream + q)])
+                  for q in range(n_seqs)]
+        return s, w, prompts, depths, [N] * n_seqs, n_seqs
     if name == "ouro24":
         s = cdbgen.OURO
         P, N, n_seqs, stream = 16, 6, 2, 20
@@ -179,18 +192,23 @@ def free_run_case(name: str):
 class DriftRun:
     """The fp64 oracle run alongside fp32-level realizations of its own
     arithmetic, each free-running on its own state and pools: the same source
-    with fp32 accumulators; the fp64 steps with the state rounded to fp32 after
+    with fp32 accumulators, summing the projections in index order, in reverse
+    and in blocks of 32; the fp64 steps with the state rounded to fp32 after
     every call (as a device keeps it); and the fp64 steps with fp32-sized
-    relative noise (2^-24 N(0, 1)) on the state after every call, two draws.
+    relative noise (2^-24 N(0, 1)) on the state after every call, six draws.
     Every call records, per output, the largest distance of any realization
     from the fp64 run: how far an fp32 implementation of the same arithmetic
-    can sit from the oracle after this many calls."""
+    can sit from the oracle after this many calls.  Decode calls hold one to a
+    few rows, whose largest deviation a handful of realizations samples poorly;
+    hence ten."""
 
-    def __init__(self, shape, weights, seq_lens, threads: int = 5):
+    N_NOISE = 6
+
+    def __init__(self, shape, weights, seq_lens, threads: int = 6):
         from concurrent.futures import ThreadPoolExecutor
 
         self.ref = OracleSide(shape, weights, seq_lens)
-        rngs = [np.random.default_rng(7000 + k) for k in range(2)]
+        rngs = [np.random.default_rng(7000 + k) for k in range(self.N_NOISE)]
 
         def to_fp32(side, slots):
             for a in (side.oh, side.oe):
@@ -204,10 +222,9 @@ class DriftRun:
                         a[slots] *= 1.0 + 2.0 ** -24 * rngs[k].standard_normal(a[slots].shape)
             return hook
 
-        self.real = [OracleSide(shape, weights, seq_lens, acc32=True),
-                     OracleSide(shape, weights, seq_lens, state_hook=to_fp32),
-                     OracleSide(shape, weights, seq_lens, state_hook=noise(0)),
-                     OracleSide(shape, weights, seq_lens, state_hook=noise(1))]
+        self.real = [OracleSide(shape, weights, seq_lens, acc32=True, sum_order=k) for k in (0, 1, 2)] + \
+                    [OracleSide(shape, weights, seq_lens, state_hook=to_fp32)] + \
+                    [OracleSide(shape, weights, seq_lens, state_hook=noise(k)) for k in range(self.N_NOISE)]
         self.pool = ThreadPoolExecutor(max_workers=threads)  # the oracle's ctypes calls release the GIL
         self.calls = []
 
@@ -218,8 +235,9 @@ class DriftRun:
     def _states(self, slots, outs):
         want = self.ref.oh[slots]
         d = [np.abs(side.oh[slots] - want) for side in self.real]
-        return {"h_max": max(float(x.max()) for x in d), "h_mean": max(float(x.mean()) for x in d),
-                "h_rel": max(row_rel(side.oh[slots], want) for side in self.real)}
+        each = [float(x.max()) for x in d]
+        return {"h_max": max(each), "h_mean": max(float(x.mean()) for x in d),
+                "h_rel": max(row_rel(side.oh[slots], want) for side in self.real), "h_max_each": each}
 
     def prelude(self, seqs, poss, toks):
         self._all(lambda side: side.prelude(seqs, poss, toks))
@@ -231,7 +249,8 @@ class DriftRun:
         outs = self._all(lambda side: side.loop(seqs, poss, cs, deps))
         rec = {"stage": "loop", "rows": len(seqs)}
         rec.update(self._states(self.ref.slots(seqs, poss), outs))
-        rec["score_max"] = max(float(np.abs(o["score"] - outs[0]["score"]).max()) for o in outs[1:])
+        rec["score_max_each"] = [float(np.abs(o["score"] - outs[0]["score"]).max()) for o in outs[1:]]
+        rec["score_max"] = max(rec["score_max_each"])
         for o in outs[1:]:
             assert o["exit_mask"].tolist() == outs[0]["exit_mask"].tolist()
         self.calls.append(rec)
@@ -242,6 +261,7 @@ class DriftRun:
         ol = outs[0][0]
         d = [np.abs(o[0] - ol) for o in outs[1:]]
         self.calls.append({"stage": "coda", "rows": len(seqs), "logit_max": max(float(x.max()) for x in d),
+                           "logit_max_each": [float(x.max()) for x in d],
                            "logit_mean": max(float(x.mean()) for x in d),
                            "logit_rel": max(row_rel(o[0], ol) for o in outs[1:])})
         return outs[0]

@@ -164,6 +164,20 @@ def test_config2_free_running_decode_at_full_depth(case):
     the oracle's own fp32-level realizations run free over the same decode
     (tests/golden/drift_<case>.json, written by make_drift_envelope.py from the
     oracle alone)."""
+    _free_run(case)
+
+
+def test_config3_free_running_decode_at_full_depth():
+    """The Huginn-shaped model whole (2 prelude layers, 4 recurrent layers with
+    the injection adapter looped up to 32 times, 2 coda layers, vocab 65536)
+    decoding with no resync: 2 sequences, prompt 3 (32 loops each), decode 3
+    at config 3's lognormal depths, rows of both sequences sharing loop steps
+    at different loop indices.  Bounded call by call by the stored envelope of
+    the oracle's own fp32-level realizations (tests/golden/drift_huginn4.json)."""
+    _free_run("huginn4")
+
+
+def _free_run(case):
     import json
     import os
     from lockstep import Lockstep
@@ -171,11 +185,13 @@ def test_config2_free_running_decode_at_full_depth(case):
     s, w, prompts, depths, n_dec, max_batch = free_run_case(case)
     env = json.load(open(os.path.join(os.path.dirname(__file__), "golden", f"drift_{case}.json")))
     assert env["depths"] == [d.tolist() for d in depths]
-    _say(f"[gpu] free-running {case}: {s.n_core} core layers, depths {[d[16:].tolist() for d in depths]}")
+    n_prompt = len(prompts[0])
+    _say(f"[gpu] free-running {case}: {s.n_core} core layers, depths {[d[n_prompt:].tolist() for d in depths]}")
     ls = Lockstep(s, w, [len(p) + n for p, n in zip(prompts, n_dec)], max_batch=max_batch, envelope=env)
     toks = ls.run(prompts, n_dec, depths)
     assert [t.tolist() for t in toks] == env["tokens"]
     _say(f"[gpu] free-running {case} errors {ls.errors} ratio to bound {ls.ratio} calls {ls.calls} "
+         f"one-row calls {ls.single_row} realizations' own spread {env.get('spread')} "
          f"argmax checked {ls.argmax_checked}; oracle fp32 realizations: h {env['run_h_max']:.4g} / "
          f"{env['run_h_mean']:.4g} rel {env['run_h_rel']:.4g}, logits {env['run_logit_max']:.4g} / "
          f"{env['run_logit_mean']:.4g}")
