@@ -225,6 +225,31 @@ def test_fixed_depth_bf16_storage_stays_near_exact():
     assert 0 < diff.max() < 5e-2  # rounding happens, and stays at bf16 scale
 
 
+@pytest.mark.parametrize("shape", [SMALL, SMALL_INJ], ids=lambda s: s.name)
+def test_fp32_realizations_are_distinct_fp32_implementations(shape):
+    """The fp32-accumulator builds that size tolerances (projection sums in
+    index order, in reverse, in blocks of 32) each stay within fp32 rounding of
+    the fp64 oracle and differ from one another: three distinct fp32
+    implementations of the same arithmetic.  The fp64 oracle exists in one
+    summation order only."""
+    w = weights(shape)
+    T = 9
+    tokens = cdbgen.prompt_ids(shape.vocab, 1, T, seed=7)[0]
+    depth = np.full(T, shape.r_max, dtype=np.int32)
+    ref = oracle.Model(shape, w, bf16_storage=False).ref_sequence(tokens, depth)["logits"]
+    scale = float(np.abs(ref).max())
+    outs = [oracle.Model(shape, w, bf16_storage=False, acc32=True, sum_order=k).ref_sequence(tokens, depth)["logits"]
+            for k in (0, 1, 2)]
+    for o in outs:
+        d = float(np.abs(o - ref).max())
+        assert 0 < d < 1e-4 * scale
+    for a in range(3):
+        for b in range(a + 1, 3):
+            assert not np.array_equal(outs[a], outs[b])
+    with pytest.raises(ValueError):
+        oracle.Model(shape, w, sum_order=1)
+
+
 # ----------------------------------------------------- brute force (no cache)
 
 @pytest.mark.parametrize("bf16", [False, True])
