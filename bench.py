@@ -279,10 +279,12 @@ def e2e_decode(shape, dm, kv, n_seqs, prompt, n_decode, seed=3):
                        f"depths categorical {{1:.3,2:.3,3:.2,4:.2}}, max batch 64, full depth-indexed KV",
            "mean_depth": round(mean_depth, 4), "flop_bound": round(cost.flop_bound(shape, mean_depth), 4)}
     run(4, 8, boundary_stream=1)
+    run(4, 8, graph_loop=True)
     for name, mode in (("cdb_refill", {}), ("cdb_no_refill", {"refill": False}), ("cb_fixed_depth",
                                                                                {"fixed_depth": True}),
                        ("cdb_refill_boundary_stream_fill", {"boundary_stream": 1}),
-                       ("cdb_refill_boundary_stream_hold", {"boundary_stream": 2})):
+                       ("cdb_refill_boundary_stream_hold", {"boundary_stream": 2}),
+                       ("cdb_refill_graph", {"graph_loop": True})):
         secs, st = run(n_seqs, n_decode, **mode)
         res[name] = {"tokens_per_s": round(st["tokens"] / secs, 1), "seconds": round(secs, 4),
                      "loop_steps": st["loop_steps"], "idle_rows": st["idle_rows"],
@@ -291,6 +293,7 @@ def e2e_decode(shape, dm, kv, n_seqs, prompt, n_decode, seed=3):
         log(f"e2e {name}: {st['tokens']} tokens in {secs:.3f}s, {st['loop_steps']} loop steps")
     cb = res["cb_fixed_depth"]["tokens_per_s"]
     res["speedup_refill_vs_cb"] = round(res["cdb_refill"]["tokens_per_s"] / cb, 4)
+    res["graph_gain"] = round(res["cdb_refill_graph"]["tokens_per_s"] / res["cdb_refill"]["tokens_per_s"], 4)
     res["speedup_no_refill_vs_cb"] = round(res["cdb_no_refill"]["tokens_per_s"] / cb, 4)
     # no early exits (every token at r_max): CDB can gain nothing, so its ratio
     # to fixed depth is the scheduler's own overhead (Section 6.2)
@@ -602,13 +605,15 @@ def huginn_leg(n_decode, steps=20, warmup=3):
 
     run(4, 4)  # first use of the boundary kernels at this shape
     run(4, 4, boundary_stream=1)
+    run(4, 4, graph_loop=True)
     e2e = {"workload": f"{n_seqs} requests, prompt {prompt} (KV synthesized), {n_decode} decode tokens each, depths "
                        f"lognormal median 12, sigma 0.5, clipped to [4, 32], max batch {wl.max_batch}, shared KV, "
                        f"minimum boundary batch 32",
            "mean_depth": round(mean_depth, 4), "flop_bound": round(cost.flop_bound(shape, mean_depth), 4)}
     for name, mode in (("cdb_refill", {}), ("cb_fixed_depth", {"fixed_depth": True}),
                        ("cdb_refill_boundary_stream_fill", {"boundary_stream": 1}),
-                       ("cdb_refill_boundary_stream_hold", {"boundary_stream": 2})):
+                       ("cdb_refill_boundary_stream_hold", {"boundary_stream": 2}),
+                       ("cdb_refill_graph", {"graph_loop": True})):
         secs, st = run(n_seqs, n_decode, **mode)
         e2e[name] = {"tokens_per_s": round(st["tokens"] / secs, 1), "seconds": round(secs, 4),
                      "loop_steps": st["loop_steps"], "loop_rows": st["loop_rows"], "idle_rows": st["idle_rows"],
@@ -617,6 +622,7 @@ def huginn_leg(n_decode, steps=20, warmup=3):
     e2e["speedup_refill_vs_cb"] = round(e2e["cdb_refill"]["tokens_per_s"] / e2e["cb_fixed_depth"]["tokens_per_s"], 4)
     e2e["boundary_stream_gain"] = {k: round(e2e["cdb_refill_boundary_stream_" + k]["tokens_per_s"] /
                                             e2e["cdb_refill"]["tokens_per_s"], 4) for k in ("fill", "hold")}
+    e2e["graph_gain"] = round(e2e["cdb_refill_graph"]["tokens_per_s"] / e2e["cdb_refill"]["tokens_per_s"], 4)
     res["e2e"] = e2e
     del kv, state, ws, dm
     torch.cuda.empty_cache()
@@ -907,7 +913,7 @@ def copy_peak(gib=4, reps=5):
 
 
 def serving_leg(shape, dm, n_req, rate=20.0, max_batch=64, chunk=512, core_pages=24576, fixed_depth=False,
-                boundary_stream=0):
+                boundary_stream=0, graph_loop=False):
     """A serving trace of the ouro-shaped model: Poisson arrivals at `rate`
     requests/s, prompt lengths lognormal (median 300, sigma 1, [16, 4096]),
     output lengths lognormal (median 400, sigma 1, [16, 2048]), categorical
@@ -929,7 +935,7 @@ def serving_leg(shape, dm, n_req, rate=20.0, max_batch=64, chunk=512, core_pages
     max_pages = cdbgen.pages_for(int(plen.max() + olen.max()))
     d = drv.Driver(max_batch=max_batch, max_active=max_batch, r_max=R, max_seqs=n_req, max_pages=max_pages,
                    core_pages=core_pages, prefill_chunk=chunk, fixed_depth=fixed_depth,
-                   boundary_stream=boundary_stream)
+                   boundary_stream=boundary_stream, graph_loop=graph_loop)
     for q in range(n_req):
         d.add_request(cdbgen.prompt_ids(shape.vocab, 1, int(plen[q]), stream=q)[0],
                       cdbgen.draw_depths(wl.depth, int(olen[q]), R, stream=1000 + q), arrival=float(arrivals[q]))
@@ -937,7 +943,8 @@ def serving_leg(shape, dm, n_req, rate=20.0, max_batch=64, chunk=512, core_pages
     state = cdb.State(shape, n_req)
     ws, half = runner_ws(dm, chunk, boundary_stream)
     scratch = torch.empty(d.scratch_bytes(shape.vocab), dtype=torch.uint8, device="cuda")
-    log(f"serving{' (fixed depth)' if fixed_depth else ''}{' (boundary stream)' if boundary_stream else ''}: "
+    log(f"serving{' (fixed depth)' if fixed_depth else ''}{' (boundary stream)' if boundary_stream else ''}"
+        f"{' (graph replay)' if graph_loop else ''}: "
         f"{n_req} requests at {rate}/s, {int(plen.sum())} prompt + {int(olen.sum())} output tokens")
     secs = d.run(dm.model, kv.c, state.c, scratch, None, ws)
     check_runner_ws(ws, half, "the serving run")

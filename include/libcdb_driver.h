@@ -64,6 +64,10 @@ typedef struct {
                                        idles; the step then waits for their prelude), with 2 they always
                                        join the step after next (the boundary work of step k overlaps
                                        step k + 1 whole, at the cost of rows idling one step) */
+    int32_t graph_loop;             /* 1: the loop step is captured once in a HIP graph at max_batch rows with
+                                       the row count in device memory (cdb_rows.d_n_rows) and each loop tick
+                                       replays it: one launch instead of the step's kernels (Section 4.3,
+                                       static shapes and graphs).  Results are those of the direct calls. */
 } cdb_driver_config;
 
 /* Core KV layouts (Section 4.2, App. C.1, Table 1), all by page-table aliasing:
@@ -97,6 +101,7 @@ typedef struct {
                                                   (staging-buffer reuse, page-table uploads, gated
                                                   decisions, sync_steps), microseconds */
     int64_t pt_uploads, pt_upload_bytes;       /* page-table uploads and the bytes they copied */
+    int64_t graph_launches;                    /* loop steps run as graph replays (graph_loop) */
 } cdb_driver_stats;
 
 cdb_driver* cdb_driver_create(const cdb_driver_config* cfg);

@@ -238,7 +238,7 @@ cdb_driver* cdb_driver_create(const cdb_driver_config* cfg) {
     if (!cfg || cfg->max_batch < 1 || cfg->max_batch > 256 || cfg->r_max < 1 || cfg->max_seqs < 1 ||
         cfg->max_pages < 1 || cfg->max_active < 1 || cfg->min_coda_batch < 1 || cfg->kv_layout < 0 ||
         cfg->kv_layout > 2 || (cfg->gated && cfg->fixed_depth) || cfg->prefill_chunk < 0 || cfg->prefill_chunk > 512 ||
-        cfg->boundary_stream < 0 || cfg->boundary_stream > 2)
+        cfg->boundary_stream < 0 || cfg->boundary_stream > 2 || cfg->graph_loop < 0 || cfg->graph_loop > 1)
         return nullptr;
     cdb_driver* d = new cdb_driver();
     d->cfg = *cfg;
@@ -524,12 +524,17 @@ int32_t cdb_driver_latencies(const cdb_driver* d, double* normalized, int32_t n)
 struct ScratchLayout {
     size_t rows, ids, step, pending, first, logits, total;
 };
+// one set of stage rows on the device: slot, seq, pos, c, depth and a sixth
+// array (decode index or token) of 256 entries each, then the live row count
+// a captured loop step reads (cdb_rows.d_n_rows)
+constexpr int kRowSetInts = 6 * 256 + 64;
+constexpr int kRowCount = 6 * 256;
 
 static ScratchLayout scratch_layout(int32_t max_seqs, int32_t vocab) {
     ScratchLayout L;
     size_t off = 0;
     L.rows = off;
-    off += 3 * 6 * 256 * 4;
+    off += 3 * (size_t)kRowSetInts * 4;
     L.ids = off;
     off += 256 * 4;
     L.step = off;
@@ -616,8 +621,8 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
     }
     unsigned char* base = static_cast<unsigned char*>(scratch);
     int32_t* drowsA = reinterpret_cast<int32_t*>(base + SL.rows);  // loop-step rows
-    int32_t* drowsB = drowsA + 6 * 256;                            // coda / prelude / prefill rows
-    int32_t* drows2 = drowsB + 6 * 256;                            // prelude rows after a coda
+    int32_t* drowsB = drowsA + kRowSetInts;                        // coda / prelude / prefill rows
+    int32_t* drows2 = drowsB + kRowSetInts;                        // prelude rows after a coda
     int32_t* dids = reinterpret_cast<int32_t*>(base + SL.ids);
     int32_t* dfirst = reinterpret_cast<int32_t*>(base + SL.first);  // first decode input per sequence
     float* dlogits = reinterpret_cast<float*>(base + SL.logits);
@@ -641,7 +646,7 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
     // each slot reused only after the copy that last read it has completed; a
     // third ring receives the gated steps' decisions
     const int RING = 8, PT_RING = 64;
-    const size_t slot_ints = 6 * 256;
+    const size_t slot_ints = kRowSetInts;
     const size_t block_ints = (size_t)planes(d) * d->cfg.max_pages;  // one sequence's page-table block
     const size_t pt_bytes = d->page_table.size() * 4;
     int32_t* pinned = nullptr;
@@ -675,8 +680,10 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
         pt_used = true;
     }
     int ring = 0, rb_ring = 0, blk_ring = 0;
+    // live: the row count written after the arrays (read by a captured loop step)
     auto stage = [&](const int32_t* slot, const int32_t* seq, const int32_t* pos, const int32_t* c,
-                     const int32_t* dep, const int32_t* tok, int32_t n, int32_t* dst, hipStream_t s) -> hipError_t {
+                     const int32_t* dep, const int32_t* tok, int32_t n, int32_t* dst, hipStream_t s,
+                     int32_t live = -1) -> hipError_t {
         waits.on(ev[ring]);
         int32_t* h = pinned + ring * slot_ints;
         memcpy(h, slot, n * 4);
@@ -685,6 +692,7 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
         if (c) memcpy(h + 768, c, n * 4);
         if (dep) memcpy(h + 1024, dep, n * 4);
         if (tok) memcpy(h + 1280, tok, n * 4);
+        h[kRowCount] = live < 0 ? n : live;
         hipError_t e = hipMemcpyAsync(dst, h, slot_ints * 4, hipMemcpyHostToDevice, s);
         hipEventRecord(ev[ring], s);
         ring = (ring + 1) % RING;
@@ -753,6 +761,38 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
     cdb_driver_tick prev;
     int prev_rb = -1;
 
+    // graph_loop: the loop step captured once at max_batch rows, the live count
+    // read from the row set's count entry; replayed on the loop-step stream
+    const bool use_graph = d->cfg.graph_loop != 0;
+    hipGraphExec_t gexec = nullptr;
+    const cdb_rows rows_cap{d->cfg.max_batch, drowsA, drowsA + 256, drowsA + 512, drowsA + 768,
+                            gated ? nullptr : drowsA + 1024, drowsA + kRowCount};
+    auto loop_call = [&](const cdb_rows* r, hipStream_t st) -> cdb_status {
+        return gated ? cdb_loop_step_gated(model, kv, state, r, &gate, &out, wsA, wsA_bytes, st)
+                     : cdb_loop_step(model, kv, state, r, &out, wsA, wsA_bytes, st);
+    };
+    // capture on a private stream (the caller's may be the null stream); the
+    // captured launches run only when the graph is launched
+    auto capture = [&]() -> cdb_status {
+        hipStream_t cs = nullptr;
+        if (hipStreamCreateWithFlags(&cs, hipStreamNonBlocking) != hipSuccess) return CDB_ERR_HIP;
+        cdb_status cst = CDB_ERR_HIP;
+        if (hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal) == hipSuccess) {
+            cst = loop_call(&rows_cap, cs);
+            hipGraph_t g = nullptr;
+            const hipError_t e = hipStreamEndCapture(cs, &g);  // ends the capture whatever the call returned
+            if (cst == CDB_OK && (e != hipSuccess || !g)) cst = CDB_ERR_HIP;
+            if (cst == CDB_OK && hipGraphInstantiate(&gexec, g, nullptr, nullptr, 0) != hipSuccess) {
+                gexec = nullptr;
+                cst = CDB_ERR_HIP;
+            }
+            if (g) hipGraphDestroy(g);  // the executable graph keeps what it needs
+        }
+        hipStreamDestroy(cs);
+        (void)hipGetLastError();
+        return cst;
+    };
+
     cdb_driver_tick t;
     std::vector<int32_t> toks(256), npos(256);
     // CDB_DRIVER_PROGRESS set: a line on stderr every 10 s of a long run
@@ -808,6 +848,21 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
             int64_t need = 0;
             for (int32_t i = 0; i < n; ++i) need = std::max(need, ready[t.seq[i]]);
             a_waits_for_b(need);
+            if (use_graph && !gexec) {
+                // one direct call at capacity with a live count of zero (no rows
+                // are touched; every kernel of the capacity's launch shapes has then
+                // run once, which sets their first-use attributes outside capture)
+                if (stage(t.slot, t.seq, t.pos, t.c, t.depth, toks.data(), n, drowsA, sA, 0) != hipSuccess) {
+                    status = CDB_ERR_HIP;
+                    break;
+                }
+                s = loop_call(&rows_cap, sA);
+                if (s == CDB_OK) s = capture();
+                if (s != CDB_OK) {
+                    status = s;
+                    break;
+                }
+            }
         }
         if (stage(t.slot, t.seq, t.pos, t.c, t.depth, toks.data(), n, drows, on_b ? sB : sA) != hipSuccess) {
             status = CDB_ERR_HIP;
@@ -825,11 +880,14 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
                 for (int32_t i = 0; i < n; ++i) ready[t.seq[i]] = k;
             }
         } else if (t.stage == CDB_TICK_LOOP) {
-            if (!gated) {
-                s = cdb_loop_step(model, kv, state, &rows, &out, wsA, wsA_bytes, sA);
+            if (gated) rows.depth = nullptr;
+            if (use_graph) {
+                s = hipGraphLaunch(gexec, sA) == hipSuccess ? CDB_OK : CDB_ERR_HIP;
+                if (s == CDB_OK) d->stats.graph_launches++;
             } else {
-                rows.depth = nullptr;
-                s = cdb_loop_step_gated(model, kv, state, &rows, &gate, &out, wsA, wsA_bytes, sA);
+                s = loop_call(&rows, sA);
+            }
+            if (gated) {
                 if (s == CDB_OK) {
                     // this step's decisions to the host
                     const int rs = rb_ring;
@@ -907,6 +965,7 @@ int32_t cdb_driver_run(cdb_driver* d, const cdb_model* model, const cdb_kv* kv, 
         if (waits.on(sB) != hipSuccess && status == CDB_OK) status = CDB_ERR_HIP;
         hipStreamDestroy(sB);
     }
+    if (gexec) hipGraphExecDestroy(gexec);
     const double secs = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
     d->now = secs;
     d->stats.host_wait_us += (int64_t)std::chrono::duration_cast<std::chrono::microseconds>(waits.total).count();

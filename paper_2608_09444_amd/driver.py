@@ -29,7 +29,8 @@ class cdb_driver_config(C.Structure):
                                           "r_max", "has_prelude", "has_coda", "max_seqs", "max_pages",
                                           "pre_pages", "core_pages", "coda_pages", "kv_layout", "gated",
                                           "lookahead")] + [("threshold", C.c_float), ("prefill_chunk", C.c_int32),
-                                                           ("sync_steps", C.c_int32), ("boundary_stream", C.c_int32)]
+                                                           ("sync_steps", C.c_int32), ("boundary_stream", C.c_int32),
+                                                           ("graph_loop", C.c_int32)]
 
 
 class cdb_driver_tick(C.Structure):
@@ -41,7 +42,8 @@ class cdb_driver_tick(C.Structure):
 class cdb_driver_stats(C.Structure):
     _fields_ = [(n, C.c_int64) for n in ("loop_steps", "loop_rows", "idle_rows", "coda_calls", "coda_rows",
                                           "prelude_calls", "prelude_rows", "tokens", "prefill_calls",
-                                          "prefill_tokens", "host_wait_us", "pt_uploads", "pt_upload_bytes")]
+                                          "prefill_tokens", "host_wait_us", "pt_uploads", "pt_upload_bytes",
+                                          "graph_launches")]
 
 
 _bound = False
@@ -89,14 +91,15 @@ class Driver:
                  core_pages: int, pre_pages: int = 0, coda_pages: int = 0, has_prelude: bool = False,
                  has_coda: bool = False, refill: bool = True, fixed_depth: bool = False, min_coda_batch: int = 1,
                  kv_layout: int = KV_FULL, gated: bool = False, lookahead: bool = False, threshold: float = 0.0,
-                 prefill_chunk: int = 0, sync_steps: bool = False, boundary_stream: int = 0):
+                 prefill_chunk: int = 0, sync_steps: bool = False, boundary_stream: int = 0,
+                 graph_loop: bool = False):
         """boundary_stream: 1 or 2 puts prelude, coda and prefill on a second
         stream (libcdb_driver.h); run() then needs a workspace holding two
-        (each half of ws)."""
+        (each half of ws).  graph_loop: loop steps replay one captured graph."""
         self.cfg = cdb_driver_config(max_batch, max_active, int(refill), int(fixed_depth), min_coda_batch, r_max,
                                      int(has_prelude), int(has_coda), max_seqs, max_pages, pre_pages, core_pages,
                                      coda_pages, kv_layout, int(gated), int(lookahead), threshold, prefill_chunk,
-                                     int(sync_steps), int(boundary_stream))
+                                     int(sync_steps), int(boundary_stream), int(graph_loop))
         self.h = lib().cdb_driver_create(C.byref(self.cfg))
         if not self.h:
             raise ValueError("cdb_driver_create: invalid configuration")

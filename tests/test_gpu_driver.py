@@ -147,10 +147,14 @@ def test_driver_decode_is_schedule_invariant_and_follows_oracle(kv_layout):
                       ("no-refill", dict(max_batch=3, max_active=n, refill=False)),
                       ("refill-coda3", dict(max_batch=6, max_active=n, min_coda_batch=3)),
                       ("refill-boundary-stream-1", dict(max_batch=4, max_active=n, boundary_stream=1)),
-                      ("refill-boundary-stream-2", dict(max_batch=4, max_active=n, boundary_stream=2))):
+                      ("refill-boundary-stream-2", dict(max_batch=4, max_active=n, boundary_stream=2)),
+                      ("refill-graph", dict(max_batch=4, max_active=n, graph_loop=True)),
+                      ("no-refill-graph-boundary-stream", dict(max_batch=3, max_active=n, refill=False,
+                                                               boundary_stream=1, graph_loop=True))):
         first, ids, st, secs = _decode_on_gpu(s, gm, prompts, ndec, depths, kv_layout, **cfg)
         _say(f"[gpu]   {name}: {st} in {secs * 1e3:.1f} ms")
         assert st["tokens"] == sum(ndec)
+        assert st["graph_launches"] == (st["loop_steps"] if cfg.get("graph_loop") else 0)
         assert st["loop_rows"] == sum(int(x.sum()) for x in depths)
         runs[name] = (first, ids)
     base = runs["refill"]
@@ -179,7 +183,8 @@ def test_driver_decode_with_injection_is_schedule_invariant_and_follows_oracle(k
     for name, cfg in (("refill", dict(max_batch=4, max_active=n)),
                       ("no-refill", dict(max_batch=5, max_active=n, refill=False)),
                       ("refill-boundary-stream", dict(max_batch=4, max_active=n, min_coda_batch=2,
-                                                      boundary_stream=2))):
+                                                      boundary_stream=2)),
+                      ("refill-graph", dict(max_batch=4, max_active=n, graph_loop=True))):
         first, ids, st, secs = _decode_on_gpu(s, gm, prompts, ndec, depths, kv_layout, **cfg)
         _say(f"[gpu]   {name}: {st} in {secs * 1e3:.1f} ms")
         assert st["tokens"] == sum(ndec)
@@ -265,7 +270,8 @@ def test_gated_driver_decode_is_schedule_invariant(lookahead):
     runs = {}
     for name, cfg in (("refill", dict(max_batch=4, max_active=n)),
                       ("no-refill", dict(max_batch=3, max_active=n, refill=False)),
-                      ("refill-boundary-stream", dict(max_batch=4, max_active=n, boundary_stream=1))):
+                      ("refill-boundary-stream", dict(max_batch=4, max_active=n, boundary_stream=1)),
+                      ("refill-graph", dict(max_batch=4, max_active=n, graph_loop=True))):
         first, ids, st, secs = _decode_on_gpu(s, gm, prompts, ndec, [None] * n, gated=True, lookahead=lookahead,
                                               threshold=thr, **cfg)
         _say(f"[gpu]   {name}: {st} in {secs * 1e3:.1f} ms")
@@ -345,7 +351,8 @@ def test_driver_prefill_chunks_decode_like_the_oracle():
     for name, cfg in (("refill", dict(max_batch=4, max_active=n)),
                       ("no-refill", dict(max_batch=3, max_active=n, refill=False)),
                       ("two-at-a-time", dict(max_batch=2, max_active=2)),
-                      ("boundary-stream", dict(max_batch=4, max_active=3, boundary_stream=2))):
+                      ("boundary-stream", dict(max_batch=4, max_active=3, boundary_stream=2)),
+                      ("graph", dict(max_batch=4, max_active=n, graph_loop=True))):
         ids, st, secs = _decode_with_driver_prefill(s, gm, prompts, ndec, depths, chunk, **cfg)
         _say(f"[gpu]   {name}: {st} in {secs * 1e3:.1f} ms")
         assert st["tokens"] == sum(ndec)
@@ -373,7 +380,8 @@ def test_driver_decode_at_ouro_width_follows_oracle():
     runs = {}
     for name, cfg in (("refill", dict(max_batch=3, max_active=4)),
                       ("no-refill", dict(max_batch=4, max_active=4, refill=False)),
-                      ("refill-boundary-stream", dict(max_batch=3, max_active=4, boundary_stream=1))):
+                      ("refill-boundary-stream", dict(max_batch=3, max_active=4, boundary_stream=1)),
+                      ("refill-graph", dict(max_batch=3, max_active=4, graph_loop=True))):
         first, ids, st, secs = _decode_on_gpu(s, gm, prompts, ndec, depths, drv.KV_FULL, **cfg)
         _say(f"[gpu]   {name}: {st} in {secs * 1e3:.1f} ms")
         assert st["tokens"] == sum(ndec)
