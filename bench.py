@@ -826,8 +826,9 @@ def idle_ablation(shape_name, n_decode=48, pause_s=1.0):
     split into one segment per variant (GPU idle = the share of each segment
     with no kernel running): the synchronous scheduler (the host waits for every
     loop step), the asynchronous one, asynchronous with device-decided exits and
-    the lookahead gate, and asynchronous with the boundary stages on a second
-    stream.  Ouro-shaped: 64 requests, prompt 512 (KV synthesized), full
+    the lookahead gate, asynchronous with the boundary stages on a second
+    stream, and asynchronous with loop steps replayed from a graph.
+    Ouro-shaped: 64 requests, prompt 512 (KV synthesized), full
     depth-indexed KV, max batch 64; Huginn-shaped (no gate variant: its
     convergence criterion has no threshold these random-init states straddle
     usefully): 128 requests, prompt 256, shared KV, max batch 128, minimum
@@ -863,6 +864,7 @@ def idle_ablation(shape_name, n_decode=48, pause_s=1.0):
         order.append(("asynchronous_lookahead_gate", {"gated": True, "lookahead": True, "threshold": 0.5}))
     order.append(("asynchronous_boundary_stream_fill", {"boundary_stream": 1}))
     order.append(("asynchronous_boundary_stream_hold", {"boundary_stream": 2}))
+    order.append(("asynchronous_graph_replay", {"graph_loop": True}))
     res = {"order": [n for n, _ in order]}
     for k, (name, mode) in enumerate([("warmup", {})] + order):
         d = drv.Driver(max_batch=batch, max_active=n_seqs, r_max=R, max_seqs=n_seqs, max_pages=max_pages,
@@ -888,6 +890,43 @@ def idle_ablation(shape_name, n_decode=48, pause_s=1.0):
     del kv, state, dm
     torch.cuda.empty_cache()
     return res
+
+
+def idle_segments(csv_path, silence_ns=300_000_000):
+    """Reads a rocprofv3 kernel trace (CSV) of an `--idle-ablation` run and
+    splits it into one segment per decode at gaps longer than `silence_ns`.
+    Per segment: span (first kernel start to last kernel end), busy (the union
+    of the kernel intervals), idle = 1 - busy / span, and the largest gaps
+    between kernels.  Host-side only; no device is touched."""
+    import csv
+    with open(csv_path, newline="") as f:
+        iv = sorted((int(r["Start_Timestamp"]), int(r["End_Timestamp"])) for r in csv.DictReader(f))
+    if not iv:
+        raise SystemExit(f"{csv_path}: no kernels in the trace")
+    segs, cur, cur_end = [], [iv[0]], iv[0][1]
+    for a in iv[1:]:
+        if a[0] - cur_end > silence_ns:
+            segs.append(cur)
+            cur, cur_end = [a], a[1]
+        else:
+            cur.append(a)
+            cur_end = max(cur_end, a[1])
+    segs.append(cur)
+    out = []
+    for seg in segs:
+        t0, t1 = seg[0][0], max(e for _, e in seg)
+        busy, end, gaps = 0, t0, []
+        for s0, e0 in seg:
+            if s0 > end and end > t0:
+                gaps.append(s0 - end)
+            if e0 > end:
+                busy += e0 - max(s0, end)
+                end = e0
+        span = max(t1 - t0, 1)
+        out.append({"kernels": len(seg), "span_ms": round(span / 1e6, 2), "busy_ms": round(busy / 1e6, 2),
+                    "idle_pct": round((1 - busy / span) * 100, 2),
+                    "largest_gaps_us": [round(g / 1e3, 1) for g in sorted(gaps)[-3:]]})
+    return out
 
 
 def copy_peak(gib=4, reps=5):
@@ -1035,7 +1074,14 @@ def main():
                     help="run one plain device copy of this many MiB first (a known-size reference for HBM counters)")
     ap.add_argument("--idle-ablation", action="store_true",
                     help="only the scheduler-variant decodes for a kernel trace (GPU idle per variant)")
+    ap.add_argument("--idle-trace", metavar="CSV",
+                    help="only analyse a kernel trace of an --idle-ablation run: GPU idle per decode segment "
+                         "(host-side, no device)")
     args = ap.parse_args()
+    if args.idle_trace:
+        for k, seg in enumerate(idle_segments(args.idle_trace)):
+            print(json.dumps({"segment": k, **seg}), flush=True)
+        return
     if args.gpus != 1:
         print("bench.py measures one GPU only: the loop step shards by sequence with no exchange between GPUs, "
               "and this benchmark runs and reports the single-GPU path (use --gpus 1).", file=sys.stderr)
