@@ -193,12 +193,21 @@ __device__ __forceinline__ void stripe_epilogue(const float* fin, int fld, int n
     }
 }
 
+// k steps per register load batch of the decode kernel (register budget: two
+// batches of NS weight + MT activation operands)
+__host__ __device__ constexpr int decode_batch_steps(int MT, int NS) {
+    return NS == 1 ? (MT <= 2 ? 8 : (MT == 4 ? 4 : 1)) : (MT <= 2 ? 4 : (MT == 4 ? 2 : 1));
+}
+
 // MT = 32-row tiles of M covered by one pass (M <= 32 * MT); NS = adjacent
-// 32-column stripes per workgroup (they share every activation load).
-template <int EPI, int MT, int NS>
+// 32-column stripes per workgroup (they share every activation load); TAIL:
+// some wave's K range is not a whole number of load batches (decode_batch_steps).
+template <int EPI, int MT, int NS, bool TAIL>
 __global__ __launch_bounds__(512) void k_gemm(GemmArgs ga, EpiArgs ea) {
     extern __shared__ __align__(16) float smem[];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    // the wave index as a scalar, so each wave's K range and its batch tests
+    // below are wave-uniform branches
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int KW = ga.KW;
     const int KS = ga.K >> 4;  // 16-wide k steps
     const int s = blockIdx.y;
@@ -225,16 +234,17 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs ga, EpiArgs ea) {
         wsrc[ns] = reinterpret_cast<const u32x4*>(ga.Wp) + (size_t)min(nt + ns, stripes - 1) * KS * 64 + lane;
     // X is in fragment layout: the operand of m-tile t at k step k is the 1 KiB tile (t, k)
     const u32x4* xsrc = reinterpret_cast<const u32x4*>(ga.X) + lane;
-    // k steps per load batch (register budget: two batches of NS + MT operands)
-    constexpr int CH = NS == 1 ? (MT <= 2 ? 8 : (MT == 4 ? 4 : 1)) : (MT <= 2 ? 4 : (MT == 4 ? 2 : 1));
+    constexpr int CH = decode_batch_steps(MT, NS);
 
     // Two register sets: the next batch's loads are in flight while the
     // current batch feeds the MFMAs.
     u32x4 wa[CH][NS], wb[CH][NS];
     u32x4 xa[CH][MT], xb[CH][MT];
     // Loads are unconditional (steps past the wave's range re-read its last
-    // step, whose weight tile is then zeroed) so that the compiler keeps each
-    // batch's loads in flight across the other batch's MFMAs.
+    // step) so that the compiler keeps each batch's loads in flight across the
+    // other batch's MFMAs.  With TAIL, the wave's last batch skips the MFMAs of
+    // the steps past its range (a wave-uniform branch); without it every batch
+    // is whole and no step is tested.
     auto load = [&](u32x4 (&w)[CH][NS], u32x4 (&x)[CH][MT], int c0) {
 #pragma unroll
         for (int i = 0; i < CH; ++i) {
@@ -245,20 +255,20 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs ga, EpiArgs ea) {
             for (int t = 0; t < MT; ++t) x[i][t] = xsrc[((size_t)t * KS + ks) * 64];
         }
     };
+    auto step = [&](const u32x4 (&w)[NS], const u32x4 (&x)[MT]) {
+#pragma unroll
+        for (int ns = 0; ns < NS; ++ns) {
+            const bf16x8 a = __builtin_bit_cast(bf16x8, w[ns]);
+#pragma unroll
+            for (int t = 0; t < MT; ++t)
+                acc[ns][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, __builtin_bit_cast(bf16x8, x[t]), acc[ns][t],
+                                                                     0, 0, 0);
+        }
+    };
     auto compute = [&](const u32x4 (&w)[CH][NS], const u32x4 (&x)[CH][MT], int c0) {
 #pragma unroll
-        for (int i = 0; i < CH; ++i) {
-            const uint32_t keep = c0 + i < ks1 ? 0xffffffffu : 0u;
-#pragma unroll
-            for (int ns = 0; ns < NS; ++ns) {
-                const u32x4 wm = w[i][ns] & keep;
-                const bf16x8 a = __builtin_bit_cast(bf16x8, wm);
-#pragma unroll
-                for (int t = 0; t < MT; ++t)
-                    acc[ns][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, __builtin_bit_cast(bf16x8, x[i][t]),
-                                                                         acc[ns][t], 0, 0, 0);
-            }
-        }
+        for (int i = 0; i < CH; ++i)
+            if (!TAIL || c0 + i < ks1) step(w[i], x[i]);
     };
     if (ks0 < ks1) load(wa, xa, ks0);
 
@@ -752,11 +762,25 @@ GemmShape gemm_shape(int N, int K, int epi, int M) {
     return GemmShape{N, K, S, KW, NS};
 }
 
-template <int EPI, int MT, int NS>
-static hipError_t launch_mt(const GemmArgs& ga, const EpiArgs& ea, hipStream_t st) {
+// Whether some wave's K range in k_gemm (the same proportional split of each
+// workgroup's split over its KW waves) is not a whole number of batches.
+static bool decode_has_tail(int K, int S, int KW, int ch) {
+    const int KS = K / 16;
+    for (int s = 0; s < S; ++s) {
+        const int a0 = (int)(((long)s * KS) / S), a1 = (int)(((long)(s + 1) * KS) / S);
+        for (int w = 0; w < KW; ++w) {
+            const int n = (int)(((long)(w + 1) * (a1 - a0)) / KW) - (int)(((long)w * (a1 - a0)) / KW);
+            if (n % ch) return true;
+        }
+    }
+    return false;
+}
+
+template <int EPI, int MT, int NS, bool TAIL>
+static hipError_t launch_tail(const GemmArgs& ga, const EpiArgs& ea, hipStream_t st) {
     static bool attr_set = false;
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm<EPI, MT, NS>),
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm<EPI, MT, NS, TAIL>),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
         if (e != hipSuccess) return e;
         attr_set = true;
@@ -764,8 +788,14 @@ static hipError_t launch_mt(const GemmArgs& ga, const EpiArgs& ea, hipStream_t s
     size_t lds = ((size_t)ga.KW * 1024 + (size_t)NS * 32 * (MT * 32 + 1)) * 4;
     if (EPI == EPI_QKV) lds += (size_t)NS * MT * 32 * 16 * 8 + (size_t)MT * 32 * 2 * 4;
     dim3 grid((ga.N / 32 + NS - 1) / NS, ga.S);
-    k_gemm<EPI, MT, NS><<<grid, ga.KW * 64, lds, st>>>(ga, ea);
+    k_gemm<EPI, MT, NS, TAIL><<<grid, ga.KW * 64, lds, st>>>(ga, ea);
     return hipGetLastError();
+}
+
+template <int EPI, int MT, int NS>
+static hipError_t launch_mt(const GemmArgs& ga, const EpiArgs& ea, hipStream_t st) {
+    return decode_has_tail(ga.K, ga.S, ga.KW, decode_batch_steps(MT, NS)) ? launch_tail<EPI, MT, NS, true>(ga, ea, st)
+                                                                          : launch_tail<EPI, MT, NS, false>(ga, ea, st);
 }
 
 template <int EPI, int NS>
