@@ -317,7 +317,7 @@ def _first_ids_by_prefill(shape, gm, prompts, chunk):
     return first
 
 
-def _decode_with_driver_prefill(shape, gm, prompts, ndec, depths, chunk, **cfg):
+def _decode_with_driver_prefill(shape, gm, prompts, ndec, depths, chunk, arrivals=None, **cfg):
     R = shape.r_max
     n = len(prompts)
     T = [len(p) + k for p, k in zip(prompts, ndec)]
@@ -326,7 +326,7 @@ def _decode_with_driver_prefill(shape, gm, prompts, ndec, depths, chunk, **cfg):
     d = drv.Driver(max_seqs=n, max_pages=max_pages, core_pages=tot * R, pre_pages=tot, coda_pages=tot,
                    has_prelude=shape.n_prelude > 0, has_coda=shape.n_coda > 0, r_max=R, prefill_chunk=chunk, **cfg)
     for q in range(n):
-        d.add_request(prompts[q], depths[q])
+        d.add_request(prompts[q], depths[q], arrival=0.0 if arrivals is None else arrivals[q])
     kv = cdb.PagedKV(shape, n, max_pages, tot, tot * R, tot)
     ws, half = _driver_ws(gm, max(256, chunk), cfg)
     state = cdb.State(shape, n)
@@ -335,6 +335,10 @@ def _decode_with_driver_prefill(shape, gm, prompts, ndec, depths, chunk, **cfg):
     secs = d.run(gm.model, kv.c, state.c, scratch, None, ws, tokens_out=out_ids)
     torch.cuda.synchronize()
     assert _ws_errors(ws, half) == [0] * (2 if cfg.get("boundary_stream") else 1)
+    if arrivals is not None:
+        # every request finished after it arrived, and the run lasted past the last arrival
+        lat = d.latencies(n)
+        assert len(lat) == n and (lat > 0).all() and secs >= max(arrivals)
     return out_ids.cpu().numpy(), d.stats(), secs
 
 
@@ -352,7 +356,10 @@ def test_driver_prefill_chunks_decode_like_the_oracle():
                       ("no-refill", dict(max_batch=3, max_active=n, refill=False)),
                       ("two-at-a-time", dict(max_batch=2, max_active=2)),
                       ("boundary-stream", dict(max_batch=4, max_active=3, boundary_stream=2)),
-                      ("graph", dict(max_batch=4, max_active=n, graph_loop=True))):
+                      ("graph", dict(max_batch=4, max_active=n, graph_loop=True)),
+                      # requests arriving while others decode (wall-clock seconds from the run's start):
+                      # admissions mid-run and waits for the next arrival, as in the serving trace
+                      ("arrivals", dict(max_batch=4, max_active=n, arrivals=[0.0, 0.0, 0.004, 0.008, 0.016, 0.03]))):
         ids, st, secs = _decode_with_driver_prefill(s, gm, prompts, ndec, depths, chunk, **cfg)
         _say(f"[gpu]   {name}: {st} in {secs * 1e3:.1f} ms")
         assert st["tokens"] == sum(ndec)
