@@ -44,3 +44,20 @@ def test_huginn_core_weights_include_the_adapter():
     h = cdbgen.HUGINN
     per_layer = 4 * h.d * h.d + 3 * h.d * h.d_ff
     assert cdbgen.param_counts(h)["core"] * 2 == (h.n_core * per_layer + h.d * 2 * h.d) * 2 == 3_274_444_800
+
+
+def test_idle_segments_of_a_synthetic_kernel_trace(tmp_path):
+    # two decodes separated by 1 s of silence; the first has two overlapping
+    # kernels (busy is their union), a 10 us gap and a nested kernel
+    us = 1000
+    kernels = [(0, 40 * us), (30 * us, 60 * us), (70 * us, 100 * us), (80 * us, 90 * us),
+               (1_000_100 * us, 1_000_110 * us), (1_000_130 * us, 1_000_150 * us)]
+    p = tmp_path / "run_kernel_trace.csv"
+    p.write_text("Kernel_Name,Start_Timestamp,End_Timestamp\n" +
+                 "".join(f"k{i},{a},{b}\n" for i, (a, b) in enumerate(kernels)))
+    segs = bench.idle_segments(str(p))
+    assert len(segs) == 2
+    assert segs[0]["kernels"] == 4 and segs[0]["span_ms"] == 0.1 and segs[0]["busy_ms"] == 0.09
+    assert segs[0]["idle_pct"] == 10.0 and segs[0]["largest_gaps_us"] == [10.0]
+    assert segs[1]["kernels"] == 2 and segs[1]["span_ms"] == 0.05 and segs[1]["busy_ms"] == 0.03
+    assert segs[1]["idle_pct"] == 40.0 and segs[1]["largest_gaps_us"] == [20.0]
