@@ -129,6 +129,10 @@ static void rmsnorm(const double* x, int n, double eps, double* y) {
 
 /* y[o] = sum_i W[o][i] x[i] for a row-major bf16 matrix W [n_out][n_in]. */
 static void matvec(const uint16_t* W, int n_out, int n_in, const double* x, double* y) {
+    /* outputs are independent: for a large product called outside a parallel region (calls
+     * with fewer rows than threads), they are shared among the threads; each output's sum is
+     * the same either way */
+#pragma omp parallel for schedule(static) if (!omp_in_parallel() && (long)n_out * n_in >= (1L << 20))
     for (int o = 0; o < n_out; ++o) {
         const uint16_t* w = W + (size_t)o * n_in;
         acc_t acc = 0.0;
@@ -655,7 +659,9 @@ static double* kv_at(const orc_paged* p, const orc_desc* m, int plane, int seq, 
 
 /* Run stage layers [first, first + nl) for all rows, layer by layer: every row
  * writes its K/V for a layer before any row attends at that layer, so rows of
- * one sequence at consecutive positions see each other causally. */
+ * one sequence at consecutive positions see each other causally.  Rows run in
+ * parallel when there are at least as many as threads; fewer run one after the
+ * other, with each product's outputs shared among the threads (matvec). */
 static int stage_layers(const orc_desc* m, const orc_weights* w, const orc_paged* p, int plane, int first,
                         int nl, int n, const int32_t* seq, const int32_t* pos, double* hs) {
     int d = m->d, H = m->n_heads, hd = m->head_dim;
@@ -663,7 +669,7 @@ static int stage_layers(const orc_desc* m, const orc_weights* w, const orc_paged
     int err = ORC_OK;
     for (int l = 0; l < nl && err == ORC_OK; ++l) {
         /* each row writes only its own K/V slot, so rows run independently */
-#pragma omp parallel for schedule(dynamic, 1)
+#pragma omp parallel for schedule(dynamic, 1) if (n >= omp_get_max_threads())
         for (int i = 0; i < n; ++i) {
             double* k = (double*)malloc(sizeof(double) * (size_t)d);
             double* v = (double*)malloc(sizeof(double) * (size_t)d);
@@ -687,7 +693,7 @@ static int stage_layers(const orc_desc* m, const orc_weights* w, const orc_paged
             free(v);
         }
         if (err != ORC_OK) break;
-#pragma omp parallel for schedule(dynamic, 1)
+#pragma omp parallel for schedule(dynamic, 1) if (n >= omp_get_max_threads())
         for (int i = 0; i < n; ++i) {
             int ctx = pos[i] + 1;
             double* kbuf = (double*)malloc(sizeof(double) * (size_t)ctx * d);
@@ -843,7 +849,7 @@ int orc_coda(const orc_desc* m, const orc_weights* w, const orc_paged* p, const 
         memcpy(hs + (size_t)i * d, state_h + (size_t)slot[i] * d, sizeof(double) * (size_t)d);
     int err = stage_layers(m, w, p, m->r_max + 1, m->n_prelude + m->n_core, m->n_coda, n, seq, pos, hs);
     if (err == ORC_OK) {
-#pragma omp parallel for schedule(dynamic, 1)
+#pragma omp parallel for schedule(dynamic, 1) if (n >= omp_get_max_threads())
         for (int i = 0; i < n; ++i)
             next_ids[i] = lm_head(m, w, hs + (size_t)i * d, logits + (size_t)i * m->vocab);
     }
