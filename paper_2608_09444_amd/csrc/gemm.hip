@@ -199,6 +199,14 @@ __host__ __device__ constexpr int decode_batch_steps(int MT, int NS) {
     return NS == 1 ? (MT <= 2 ? 8 : (MT == 4 ? 4 : 1)) : (MT <= 2 ? 4 : (MT == 4 ? 2 : 1));
 }
 
+// 32x32 tiles the decode kernel's wave reduction sums per round: all NS x MT
+// of them when 8 waves' copies, the reduced block and the q/k/v staging fit in
+// 160 KB of LDS, else one
+__host__ __device__ constexpr int decode_red_tiles(bool qkv, int MT, int NS) {
+    return (8 * NS * MT * 1024 + NS * 32 * (MT * 32 + 1) + (qkv ? NS * MT * 32 * 32 + MT * 64 : 0)) * 4 <= 160 * 1024
+               ? NS * MT : 1;
+}
+
 // MT = 32-row tiles of M covered by one pass (M <= 32 * MT); NS = adjacent
 // 32-column stripes per workgroup (they share every activation load); TAIL:
 // some wave's K range is not a whole number of load batches (decode_batch_steps).
@@ -307,11 +315,16 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs ga, EpiArgs ea) {
         if (c0 + CH < ks1) compute(wb, xb, c0 + CH);
     }
 
-    // Sum the KW wave tiles in wave order, one 32x32 m-tile at a time.
+    // Sum the KW wave tiles in wave order: with 8 waves (a grid of one
+    // workgroup per CU at most) all NS x MT 32x32 tiles in one round where they
+    // fit in LDS (decode_red_tiles), else one tile at a time, which keeps the
+    // LDS of wider grids small enough for several workgroups per CU.
     // acc[ns][t][j] holds D[n = (j/4)*8 + (lane/32)*4 + j%4][m = t*32 + lane%32]
     // of stripe nt + ns.
-    float* red = smem;                    // [KW][32 n][32 m]
-    float* fin = smem + KW * 1024;        // [NS][32 n][MT*32 m + 1]
+    constexpr int RT = decode_red_tiles(EPI == EPI_QKV, MT, NS);
+    const bool one_round = RT > 1 && KW == 8;
+    float* red = smem;                                   // [KW][RT or 1][32 n][32 m]
+    float* fin = smem + KW * (one_round ? RT : 1) * 1024;  // [NS][32 n][MT*32 m + 1]
     const int fld = MT * 32 + 1;
     QkvStage qs{};
     if constexpr (EPI == EPI_QKV) {
@@ -343,22 +356,42 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs ga, EpiArgs ea) {
         }
         qs = QkvStage{s_rope, s_pid, s_tok};  // visible after the reduction's barriers
     }
+    if (RT > 1 && one_round) {
 #pragma unroll
-    for (int ns = 0; ns < NS; ++ns) {
+        for (int ns = 0; ns < NS; ++ns)
 #pragma unroll
-        for (int t = 0; t < MT; ++t) {
+            for (int t = 0; t < MT; ++t)
 #pragma unroll
-            for (int j = 0; j < 16; ++j) {
-                const int nn = (j >> 2) * 8 + (lane >> 5) * 4 + (j & 3);
-                red[wave * 1024 + nn * 32 + (lane & 31)] = acc[ns][t][j];
+                for (int j = 0; j < 16; ++j) {
+                    const int nn = (j >> 2) * 8 + (lane >> 5) * 4 + (j & 3);
+                    red[(wave * RT + ns * MT + t) * 1024 + nn * 32 + (lane & 31)] = acc[ns][t][j];
+                }
+        __syncthreads();
+        for (int e = tid; e < RT * 1024; e += nthr) {
+            const int tile = e >> 10, r = e & 1023, ns = tile / MT, t = tile - ns * MT;
+            float sum = 0.f;
+            for (int w = 0; w < KW; ++w) sum += red[(w * RT + tile) * 1024 + r];
+            fin[ns * 32 * fld + (r >> 5) * fld + t * 32 + (r & 31)] = sum;
+        }
+        __syncthreads();
+    } else {
+#pragma unroll
+        for (int ns = 0; ns < NS; ++ns) {
+#pragma unroll
+            for (int t = 0; t < MT; ++t) {
+#pragma unroll
+                for (int j = 0; j < 16; ++j) {
+                    const int nn = (j >> 2) * 8 + (lane >> 5) * 4 + (j & 3);
+                    red[wave * 1024 + nn * 32 + (lane & 31)] = acc[ns][t][j];
+                }
+                __syncthreads();
+                for (int e = tid; e < 1024; e += nthr) {
+                    float sum = 0.f;
+                    for (int w = 0; w < KW; ++w) sum += red[w * 1024 + e];
+                    fin[ns * 32 * fld + (e >> 5) * fld + t * 32 + (e & 31)] = sum;
+                }
+                __syncthreads();
             }
-            __syncthreads();
-            for (int e = tid; e < 1024; e += nthr) {
-                float sum = 0.f;
-                for (int w = 0; w < KW; ++w) sum += red[w * 1024 + e];
-                fin[ns * 32 * fld + (e >> 5) * fld + t * 32 + (e & 31)] = sum;
-            }
-            __syncthreads();
         }
     }
 
@@ -785,7 +818,8 @@ static hipError_t launch_tail(const GemmArgs& ga, const EpiArgs& ea, hipStream_t
         if (e != hipSuccess) return e;
         attr_set = true;
     }
-    size_t lds = ((size_t)ga.KW * 1024 + (size_t)NS * 32 * (MT * 32 + 1)) * 4;
+    const int rt = decode_red_tiles(EPI == EPI_QKV, MT, NS);
+    size_t lds = ((size_t)ga.KW * (rt > 1 && ga.KW == 8 ? rt : 1) * 1024 + (size_t)NS * 32 * (MT * 32 + 1)) * 4;
     if (EPI == EPI_QKV) lds += (size_t)NS * MT * 32 * 16 * 8 + (size_t)MT * 32 * 2 * 4;
     dim3 grid((ga.N / 32 + NS - 1) / NS, ga.S);
     k_gemm<EPI, MT, NS, TAIL><<<grid, ga.KW * 64, lds, st>>>(ga, ea);
