@@ -676,7 +676,9 @@ __global__ __launch_bounds__(256) void k_gemm_mn(GemmArgs ga, EpiArgs ea, int xc
         }
     }
     if constexpr (EPI == EPI_QKV) {
-        // the wave's block through its own LDS region (64 columns x (32 WM + 1)-float rows)
+        // the wave's block through its own LDS region (64 columns x (32 WM + 1)-float rows);
+        // on the LDS path the region overlaps the ring, which the other waves may still be reading
+        if constexpr (LDS) __syncthreads();
         extern __shared__ __align__(16) unsigned char lds_ring[];
         constexpr int fld = 32 * WM + 1;
         float* fin = reinterpret_cast<float*>(lds_ring) + wave * 64 * fld;
