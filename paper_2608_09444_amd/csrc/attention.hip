@@ -199,7 +199,7 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(const float* __restric
         }
     };
 
-    // (a one-page register prefetch costs more occupancy than it gains here)
+    // (a one-page register prefetch of the next item measured no faster)
     for (int item = wave; item < total; item += kAttnWaves) {
         const uint16_t* base = page_ptr(item);
         if (!base) {
