@@ -298,3 +298,54 @@ def test_loop_step_is_deterministic_as_benched():
         assert torch.equal(a, b)
     del runs
     torch.cuda.empty_cache()
+
+
+def test_coda_argmax_takes_the_lowest_index_on_exact_ties():
+    """Greedy ties on the device (reading 9: the lowest index wins).  Two
+    identical LM-head rows at the same position of their 32-column stripes go
+    through the same arithmetic and give bit-identical logits; copying the
+    winning row r to a lower such index must move the winner there, and
+    copying it to a higher one must leave r."""
+    s = cdbgen.TINY
+    w = cdbgen.model_weights(s)
+    n, R, V = 6, s.r_max, s.vocab
+    pos = np.arange(n, dtype=np.int32) * 5 + 3
+    ar = np.arange(n, dtype=np.int32)
+    max_pages = cdbgen.pages_for(int(pos.max()) + 1)
+    pt = np.full((n, R + 2, max_pages), -1, np.int32)
+    pt[:, R + 1, :] = np.arange(n * max_pages).reshape(n, max_pages)
+    kv = cdb.PagedKV(s, n, max_pages, 1, 1, n * max_pages, fill="random")
+    g = torch.Generator(device="cuda")
+    g.manual_seed(91)
+    kv.coda.normal_(0.0, 1.0, generator=g)
+    kv.page_table.copy_(torch.from_numpy(pt))
+    coda0 = kv.coda.clone()
+    state = cdb.State(s, n)
+    state.h.normal_(0.0, 1.0, generator=g)
+    rows = cdb.Rows(ar, ar, pos)
+    gm = cdb.DeviceModel(s, w)
+    ws = cdb.Workspace(gm.desc, n)
+
+    def coda(model):
+        kv.coda.copy_(coda0)  # the coda rewrites its own K/V entries; start each call from the same cache
+        logits = torch.empty((n, V), dtype=torch.float32, device="cuda")
+        ids = torch.empty(n, dtype=torch.int32, device="cuda")
+        cdb.cdb_boundary_coda(model.model, kv.c, state.c, rows.c, logits, ids, ws.buf)
+        torch.cuda.synchronize()
+        assert cdb.cdb_read_device_error(ws.buf) == 0
+        return logits.cpu().numpy(), ids.cpu().numpy()
+
+    lg, ids = coda(gm)
+    assert (ids == lg.argmax(axis=1)).all()  # random logits, no ties: the plain argmax
+    # a row whose winner has a lower and a higher index at the same stripe position
+    row = next(i for i in range(n) if 32 <= int(ids[i]) < V - 32)
+    r = int(ids[row])
+    head = np.asarray(w["lm_head"])
+    h2d = head.reshape(V, s.d)
+    for j in (r % 32, r + 32 * max(1, (V - 1 - r) // 64)):
+        h2 = h2d.copy()
+        h2[j] = h2d[r]
+        lg2, ids2 = coda(cdb.DeviceModel(s, dict(w, lm_head=h2.reshape(head.shape))))
+        _say(f"[gpu] LM-head row {r} copied to row {j}: greedy id {int(ids2[row])}")
+        assert np.array_equal(lg2[:, j], lg2[:, r])  # an exact tie in every row
+        assert int(ids2[row]) == min(j, r)
