@@ -483,11 +483,25 @@ __global__ __launch_bounds__(256) void k_argmax(int V, const float* __restrict__
     const float* x = logits + (size_t)i * V;
     float bv = -INFINITY;
     int bi = 0x7fffffff;
-    for (int k = threadIdx.x; k < V; k += 256) {
-        const float v = x[k];
-        if (v > bv) {  // k increases, so ties keep the lower index
-            bv = v;
-            bi = k;
+    // each thread visits its values in increasing k, so a strict > keeps the
+    // lower index on ties; 16-byte loads where the row allows them
+    if ((V & 3) == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0) {
+        const float4* x4 = reinterpret_cast<const float4*>(x);
+        for (int k4 = threadIdx.x; k4 < (V >> 2); k4 += 256) {
+            const float4 v = x4[k4];
+            const int k = k4 * 4;
+            if (v.x > bv) { bv = v.x; bi = k; }
+            if (v.y > bv) { bv = v.y; bi = k + 1; }
+            if (v.z > bv) { bv = v.z; bi = k + 2; }
+            if (v.w > bv) { bv = v.w; bi = k + 3; }
+        }
+    } else {
+        for (int k = threadIdx.x; k < V; k += 256) {
+            const float v = x[k];
+            if (v > bv) {
+                bv = v;
+                bi = k;
+            }
         }
     }
     sv[threadIdx.x] = bv;
